@@ -1,0 +1,260 @@
+/*
+ * bitsmoe.h -- C ABI of the MI355X (gfx950) BitsMoE spectral quantizer.
+ *
+ * BitsMoE (arXiv 2606.00079) quantizes the experts of an MoE projection
+ * through a shared basis: the E expert weights of one projection type share
+ * an output space (Sec. 3.2), so the left singular vectors of the
+ * concatenation W_cat = [W_1 ... W_E] (App. B.1, Eqs. app_down_w_cat and
+ * app_down_cat_svd_absorbed) are kept unquantized, and each expert keeps its
+ * coordinates in that basis, C_e = U^T W_e, whose rows ("spectral units") are
+ * quantized at a width chosen per unit.  The width comes from an integer
+ * program over an activation-aware loss (Sec. 3.3, Eq.
+ * ilp_piecewise_projection), here the exact loss
+ * delta H delta^T of App. B.2 (Eq. app_down_exact_metric).
+ *
+ * One projection runs, in order:
+ *   bitsmoe_gram          H = X^T X / n                      (device)
+ *   bitsmoe_gram_experts  M = sum_e W_e W_e^T                (device)
+ *   bitsmoe_shared_basis  U = top-r eigenvectors of M        (host LAPACK)
+ *   bitsmoe_project       C_e = U^T W_e                      (device)
+ *   bitsmoe_score         L[u][j] = delta H delta^T          (device)
+ *   bitsmoe_allocate      widths per unit under a budget     (host, exact)
+ *   bitsmoe_pack_layout   word offsets of the packed units   (host)
+ *   bitsmoe_pack          bit-plane codes + fp16 params      (device)
+ *
+ * Conventions shared by every call:
+ *  - Pointers named *_dev are device memory on the current HIP device;
+ *    *_host are host memory.  The caller allocates and owns every input and
+ *    output; the library never frees caller memory.
+ *  - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *    Device calls only enqueue work on it and return without waiting, unless
+ *    stated otherwise.  The library keeps per-device scratch memory that is
+ *    reused by every call on that device, so calls on one device must be
+ *    ordered (one stream, or synchronized by the caller); calls that overlap
+ *    on one device race on the scratch.
+ *  - Every call returns a status.  Arguments are checked before any work is
+ *    enqueued; on a non-OK status nothing has been enqueued unless the status
+ *    is BITSMOE_ERR_DEVICE, and the outputs are unspecified.
+ *    bitsmoe_last_error() gives a text for the last non-OK status of the
+ *    calling thread.
+ *  - Matrices are row-major and densely packed unless a stride is given.
+ *  - Shape rules that are not met give BITSMOE_ERR_SHAPE; null pointers and
+ *    non-positive sizes give BITSMOE_ERR_ARG.
+ */
+#ifndef BITSMOE_H
+#define BITSMOE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  BITSMOE_OK = 0,
+  BITSMOE_ERR_ARG = 1,          /* null pointer, non-positive size, bad enum   */
+  BITSMOE_ERR_SHAPE = 2,        /* size outside the supported shape rules       */
+  BITSMOE_ERR_DTYPE = 3,        /* unsupported element type                     */
+  BITSMOE_ERR_DEVICE = 4,       /* a HIP call or kernel launch failed           */
+  BITSMOE_ERR_NOMEM = 5,        /* scratch or host memory could not be had      */
+  BITSMOE_ERR_NUMERIC = 6,      /* non-finite input, or the eigensolver failed  */
+  BITSMOE_ERR_INFEASIBLE = 7,   /* budget below min(bits) * units               */
+  BITSMOE_ERR_UNAVAILABLE = 8   /* no LAPACK library could be loaded            */
+} bitsmoe_status;
+
+typedef enum {
+  BITSMOE_F32 = 0,   /* IEEE fp32                                   */
+  BITSMOE_BF16 = 1   /* bfloat16, read as exact values              */
+} bitsmoe_dtype;
+
+/* Largest candidate width and group sizes accepted by score and pack. */
+#define BITSMOE_MAX_BITS 8
+#define BITSMOE_MAX_NBITS 8
+
+/*
+ * Step 1a -- calibration Gram.
+ * H = X^T X / n, the token-averaged outer product of the calibration rows.
+ * The paper weights tokens by routing affinity, H = X Diag(g) X^T
+ * (App. B.2, Eq. app_affinity_gram); this call uses g_t = 1/n for every row.
+ *   X_dev  [n][d] of type xt (bf16, or fp32 which is split into two bf16
+ *          terms so that the result keeps fp32 accuracy)
+ *   H_dev  [d][d] fp32 output, full symmetric matrix.
+ * Shape rules: n >= 1, d >= 64 and d % 64 == 0.
+ */
+bitsmoe_status bitsmoe_gram(const void* X_dev, bitsmoe_dtype xt, int64_t n, int64_t d,
+                            float* H_dev, void* stream);
+
+/*
+ * Step 1b -- cross-expert Gram.
+ * M = sum_e W_e W_e^T = W_cat W_cat^T, whose eigenvectors are the left
+ * singular vectors of W_cat = [W_1 ... W_E] (App. B.1, Eqs. app_down_w_cat,
+ * app_down_cat_svd_absorbed).  Partial sums over K chunks of at most 4096
+ * terms are formed in fp32 and added in fp64 in a fixed order, so the result
+ * is deterministic.
+ *   W_dev  [E][d_out][d_in] of type wt
+ *   M_dev  [d_out][d_out] fp64 output, full symmetric.
+ * Shape rules: E >= 1, d_out % 64 == 0, d_in % 64 == 0.
+ */
+bitsmoe_status bitsmoe_gram_experts(const void* W_dev, bitsmoe_dtype wt, int64_t E,
+                                    int64_t d_out, int64_t d_in, double* M_dev, void* stream);
+
+/*
+ * Step 2 -- shared basis (host).
+ * Copies M to the host, computes its eigendecomposition with LAPACK (dsyevd)
+ * and keeps the r eigenvectors of largest eigenvalue: the retained left
+ * singular vectors Phi of W_cat (App. B.1).  Eigenvalues are returned in
+ * descending order and each eigenvector is signed so that its entry of
+ * largest magnitude is positive (lowest index on ties).
+ *   M_dev         [d_out][d_out] fp64 symmetric (read)
+ *   Ut_dev        [r][d_out] fp32 output; row k = eigenvector k
+ *   eigvals_host  [r] fp64 output (may be NULL)
+ *   host_ms       wall time of the whole call in ms (may be NULL)
+ * Synchronous: waits for `stream`, and returns after Ut_dev is written.
+ * 1 <= r <= d_out.  ERR_UNAVAILABLE if no LAPACK can be loaded (see
+ * bitsmoe_set_lapack), ERR_NUMERIC if M is not finite or LAPACK fails.
+ */
+bitsmoe_status bitsmoe_shared_basis(const double* M_dev, int64_t d_out, int64_t r,
+                                    float* Ut_dev, double* eigvals_host, double* host_ms,
+                                    void* stream);
+
+/*
+ * Step 3 -- expert spectral factors.
+ * C_e = U^T W_e for every expert: with W_e = Phi P~_e^T and Phi orthonormal
+ * (App. B.1, Eq. app_down_p_tilde_partition), row k of C_e is the spectral
+ * component of expert e along basis vector k.  U is split into two bf16
+ * terms (and fp32 W into two as well) so the product keeps fp32 accuracy.
+ *   Ut_dev  [r][d_out] fp32
+ *   W_dev   [E][d_out][d_in] of type wt
+ *   C_dev   [E][r][d_in] fp32 output; unit u = e*r + k is row u.
+ * Shape rules: d_out % 64 == 0, d_in % 64 == 0, 1 <= r <= d_out.
+ */
+bitsmoe_status bitsmoe_project(const float* Ut_dev, const void* W_dev, bitsmoe_dtype wt,
+                               int64_t E, int64_t d_out, int64_t d_in, int64_t r,
+                               float* C_dev, void* stream);
+
+/*
+ * Step 4 -- activation-aware loss table.
+ * For every unit row c (length d) and every candidate width b = bits[j]:
+ * the row is fake-quantized group-wise (groups of `group` consecutive
+ * entries, asymmetric min/max round-to-nearest: s = fp16(fl32(max-min) /
+ * (2^b-1)), m = fp16(min), q = clamp(rint((c-m)/s), 0, 2^b-1), x = m + q s),
+ * delta = c - x, and
+ *     L[u][j] = delta H delta^T,
+ * the per-component term of the exact output-space loss
+ * sum_k alpha_k^2 eps_k^T H eps_k (App. B.2, Eq. app_down_exact_metric).
+ *   C_dev      [units][d] fp32
+ *   H_dev      [d][d] fp32 symmetric positive semidefinite
+ *   bits_host  [nbits] widths, strictly ascending, each in 1..8
+ *   L_dev      [units][nbits] fp32 output
+ * Shape rules: d % 64 == 0, group in {32, 64, 128, 256}, d % group == 0,
+ * 1 <= nbits <= 8.
+ * Accuracy: the off-diagonal part of H enters through bf16 matrix-core
+ * products with fp32 accumulation; the diagonal part is added in fp32.
+ */
+bitsmoe_status bitsmoe_score(const float* C_dev, int64_t units, int64_t d, const float* H_dev,
+                             const int* bits_host, int nbits, int group, float* L_dev,
+                             void* stream);
+
+/*
+ * ILP (host) -- per-projection bit allocation (Sec. 3.3, Eq.
+ * ilp_piecewise_projection; App. B.4, Eq. ilp_piecewise_eps):
+ *     minimize sum_u L[u][j_u]  subject to  sum_u bits[j_u] <= budget_bits.
+ * Solved exactly: costs are first mapped to int64 as
+ * rint(L * 2^K / max|L|), K = 62 - ceil(log2(units + 1)), so every sum is
+ * exact; among all optima the lexicographically smallest width vector (in
+ * unit order) is returned.
+ *   L_host         [units][nbits] fp32 (finite)
+ *   bits_host      [nbits] strictly ascending widths, each in 1..8
+ *   bits_out_host  [units] output: the chosen width of each unit
+ *   objective_out  sum of the chosen L in fp64 (may be NULL)
+ * ERR_INFEASIBLE if budget_bits < bits[0] * units; ERR_NUMERIC for a
+ * non-finite cost; ERR_NOMEM if the exact search does not fit in memory.
+ */
+bitsmoe_status bitsmoe_allocate(const float* L_host, int64_t units, const int* bits_host,
+                                int nbits, int64_t budget_bits, uint8_t* bits_out_host,
+                                double* objective_out);
+
+/*
+ * Same as bitsmoe_allocate, with solver controls for testing and reporting:
+ *   full_dp_limit  instances with units * (capacity + 1) <= this use a plain
+ *                  dynamic program over all units; larger ones first fix
+ *                  every unit whose reduced cost at the LP-relaxation
+ *                  multiplier exceeds the LP gap (such a unit takes the same
+ *                  width in every optimum) and run the exact program on the
+ *                  rest.  < 0 selects the default (2^26).
+ *   core_units_out number of units left to the exact program (may be NULL).
+ */
+bitsmoe_status bitsmoe_allocate_ex(const float* L_host, int64_t units, const int* bits_host,
+                                   int nbits, int64_t budget_bits, uint8_t* bits_out_host,
+                                   double* objective_out, int64_t full_dp_limit,
+                                   int64_t* core_units_out);
+
+/*
+ * Packed layout (host): unit u occupies bits[u] * d/64 uint64 words starting
+ * at word_offsets_host[u]; word_offsets_host has units + 1 entries and the
+ * last one is the total.  d % 64 == 0; each width in 1..8.
+ */
+bitsmoe_status bitsmoe_pack_layout(const uint8_t* bits_host, int64_t units, int64_t d,
+                                   int64_t* word_offsets_host);
+
+/*
+ * Step 5 -- pack the factors at the chosen widths.
+ * Each unit row is quantized by the same group rule as bitsmoe_score, with
+ * the quotient (c - m)/s taken in fp64, and stored as bit planes: plane t
+ * (0 = least significant) of unit u is the word range
+ * [off[u] + t*d/64, off[u] + (t+1)*d/64), and bit j of word w of a plane is
+ * bit t of the code of entry 64*w + j.  params_dev[u][g] holds the fp16 bit
+ * patterns {scale, min} of group g.
+ *   C_dev             [units][d] fp32
+ *   bits_dev          [units] widths (device)
+ *   word_offsets_dev  [units + 1] from bitsmoe_pack_layout (device)
+ *   codes_dev         [total_words] uint64 output
+ *   params_dev        [units][d/group][2] uint16 output
+ * A unit whose width is outside 1..8, or whose offsets do not match its
+ * width or exceed total_words, is left unwritten.
+ */
+bitsmoe_status bitsmoe_pack(const float* C_dev, int64_t units, int64_t d, int group,
+                            const uint8_t* bits_dev, const int64_t* word_offsets_dev,
+                            int64_t total_words, uint64_t* codes_dev, uint16_t* params_dev,
+                            void* stream);
+
+/*
+ * Inverse of bitsmoe_pack: x = m + q * s per entry, fp32 [units][d].  This
+ * is the dequantized factor a decoder would use; it equals the fake-quant
+ * value of bitsmoe_score's rule.
+ */
+bitsmoe_status bitsmoe_unpack(const uint64_t* codes_dev, const uint16_t* params_dev,
+                              const uint8_t* bits_dev, const int64_t* word_offsets_dev,
+                              int64_t total_words, int64_t units, int64_t d, int group,
+                              float* Chat_dev, void* stream);
+
+/* Path of a LAPACK shared library for bitsmoe_shared_basis (LP64 or ILP64
+ * dsyevd; both plain and "64_"-suffixed symbol names are tried).  When never
+ * set, the environment variable BITSMOE_LAPACK is used, then liblapack.so.3. */
+bitsmoe_status bitsmoe_set_lapack(const char* path);
+
+/* Kernel timing for measurement.  While enabled, every device call records a
+ * pair of HIP events on its stream around each of its main kernels, under
+ * the names "gram", "gram_experts", "project", "score_dgen", "score_gemm",
+ * "pack".  bitsmoe_kernel_time waits for the recorded events of `name`,
+ * returns their summed duration in ms and the number of launches, and
+ * forgets them.  Enabling costs two event records per kernel and no
+ * synchronization. */
+bitsmoe_status bitsmoe_timing(int enable);
+bitsmoe_status bitsmoe_kernel_time(const char* name, double* total_ms, int64_t* launches);
+
+/* Text of the last non-OK status on the calling thread ("" if none). */
+const char* bitsmoe_last_error(void);
+
+/* Frees the scratch memory the library holds on every device.  Must not
+ * race with calls in flight. */
+void bitsmoe_release(void);
+
+/* Library version string. */
+const char* bitsmoe_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* BITSMOE_H */

@@ -1,0 +1,286 @@
+"""MI355X (gfx950) BitsMoE spectral quantizer: Python binding of libbitsmoe.
+
+Thin ctypes marshalling over the C ABI declared in ``include/bitsmoe.h``.
+Every step runs in the library (HIP kernels on the device, LAPACK and the
+exact ILP on the host); torch is used only to allocate device memory and to
+name the current stream.  There is no fallback: if the library is not built,
+importing the functions raises.
+
+Steps, in order (one projection type of one MoE layer):
+
+    H      = gram(X)                         # X^T X / n
+    M      = gram_experts(W)                 # sum_e W_e W_e^T (fp64)
+    Ut, ev = shared_basis(M, r)              # top-r eigenvectors (host)
+    C      = project(Ut, W)                  # C_e = U^T W_e, [E*r][d_in]
+    L      = score(C, H, bits, group)        # delta H delta^T per (unit, width)
+    b, obj = allocate(L, bits, budget)       # exact ILP (host)
+    off    = pack_layout(b, d)
+    codes, params = pack(C, b, off, group)
+"""
+from __future__ import annotations
+
+import ctypes
+import glob
+import os
+from typing import Optional, Sequence, Tuple
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libbitsmoe.so")
+
+OK = 0
+_STATUS = {0: "OK", 1: "ERR_ARG", 2: "ERR_SHAPE", 3: "ERR_DTYPE", 4: "ERR_DEVICE",
+           5: "ERR_NOMEM", 6: "ERR_NUMERIC", 7: "ERR_INFEASIBLE", 8: "ERR_UNAVAILABLE"}
+F32, BF16 = 0, 1
+
+EXPORTS = [
+    "bitsmoe_gram", "bitsmoe_gram_experts", "bitsmoe_shared_basis", "bitsmoe_project",
+    "bitsmoe_score", "bitsmoe_allocate", "bitsmoe_allocate_ex", "bitsmoe_pack_layout",
+    "bitsmoe_pack", "bitsmoe_unpack", "bitsmoe_set_lapack", "bitsmoe_last_error",
+    "bitsmoe_release", "bitsmoe_version", "bitsmoe_timing", "bitsmoe_kernel_time",
+]
+
+
+class BitsmoeError(RuntimeError):
+    def __init__(self, status: int, where: str, msg: str):
+        self.status = status
+        self.code = _STATUS.get(status, str(status))
+        super().__init__(f"{where}: {self.code}: {msg}")
+
+
+_lib = None
+
+
+def _find_lapack() -> Optional[str]:
+    """A LAPACK shared library for the host eigensolve: the one bundled with
+    numpy/scipy (OpenBLAS), else the system one."""
+    import numpy
+    cands = []
+    for mod_dir in (os.path.dirname(numpy.__file__),):
+        parent = os.path.dirname(mod_dir)
+        cands += sorted(glob.glob(os.path.join(parent, "numpy.libs", "libscipy_openblas*.so")))
+        cands += sorted(glob.glob(os.path.join(parent, "scipy.libs", "libscipy_openblas*.so")))
+    cands += ["liblapack.so.3"]
+    return cands[0] if cands else None
+
+
+def lib() -> ctypes.CDLL:
+    """Loads libbitsmoe.so (built by ``paper_2606_00079_amd.build``)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2606_00079_amd.build`")
+    L = ctypes.CDLL(LIB_PATH)
+    vp, i64, i32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int
+    L.bitsmoe_gram.argtypes = [vp, i32, i64, i64, vp, vp]
+    L.bitsmoe_gram_experts.argtypes = [vp, i32, i64, i64, i64, vp, vp]
+    L.bitsmoe_shared_basis.argtypes = [vp, i64, i64, vp, vp, vp, vp]
+    L.bitsmoe_project.argtypes = [vp, vp, i32, i64, i64, i64, i64, vp, vp]
+    L.bitsmoe_score.argtypes = [vp, i64, i64, vp, vp, i32, i32, vp, vp]
+    L.bitsmoe_allocate.argtypes = [vp, i64, vp, i32, i64, vp, vp]
+    L.bitsmoe_allocate_ex.argtypes = [vp, i64, vp, i32, i64, vp, vp, i64, vp]
+    L.bitsmoe_pack_layout.argtypes = [vp, i64, i64, vp]
+    L.bitsmoe_pack.argtypes = [vp, i64, i64, i32, vp, vp, i64, vp, vp, vp]
+    L.bitsmoe_unpack.argtypes = [vp, vp, vp, vp, i64, i64, i64, i32, vp, vp]
+    L.bitsmoe_set_lapack.argtypes = [ctypes.c_char_p]
+    L.bitsmoe_timing.argtypes = [i32]
+    L.bitsmoe_kernel_time.argtypes = [ctypes.c_char_p, vp, vp]
+    L.bitsmoe_last_error.restype = ctypes.c_char_p
+    L.bitsmoe_version.restype = ctypes.c_char_p
+    for name in EXPORTS:
+        if name not in ("bitsmoe_last_error", "bitsmoe_version", "bitsmoe_release"):
+            getattr(L, name).restype = ctypes.c_int
+    L.bitsmoe_release.restype = None
+    lp = _find_lapack()
+    if lp and os.environ.get("BITSMOE_LAPACK") is None:
+        L.bitsmoe_set_lapack(lp.encode())
+    _lib = L
+    return L
+
+
+def _check(st: int, where: str) -> None:
+    if st != OK:
+        raise BitsmoeError(st, where, lib().bitsmoe_last_error().decode())
+
+
+# ---------------------------------------------------------------------------
+# torch glue (device memory and streams only)
+# ---------------------------------------------------------------------------
+def _torch():
+    import torch
+    return torch
+
+
+def _stream():
+    return ctypes.c_void_p(_torch().cuda.current_stream().cuda_stream)
+
+
+def _dev(t, name: str):
+    torch = _torch()
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError(f"{name} must be a CUDA (HIP) tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _dtype_code(t, name: str) -> int:
+    torch = _torch()
+    if t.dtype == torch.bfloat16:
+        return BF16
+    if t.dtype == torch.float32:
+        return F32
+    raise TypeError(f"{name} must be bfloat16 or float32")
+
+
+def _bits_arr(bits: Sequence[int]):
+    a = np.ascontiguousarray(np.asarray(bits, dtype=np.int32))
+    return a, a.ctypes.data_as(ctypes.c_void_p)
+
+
+def gram(X, out=None):
+    """H = X^T X / n for calibration rows X [n][d] (bf16 or fp32) -> fp32 [d][d]."""
+    torch = _torch()
+    n, d = X.shape
+    if out is None:
+        out = torch.empty((d, d), dtype=torch.float32, device=X.device)
+    _check(lib().bitsmoe_gram(_dev(X, "X"), _dtype_code(X, "X"), n, d, _dev(out, "H"), _stream()),
+           "gram")
+    return out
+
+
+def gram_experts(W, out=None):
+    """M = sum_e W_e W_e^T for W [E][d_out][d_in] -> fp64 [d_out][d_out]."""
+    torch = _torch()
+    E, d_out, d_in = W.shape
+    if out is None:
+        out = torch.empty((d_out, d_out), dtype=torch.float64, device=W.device)
+    _check(lib().bitsmoe_gram_experts(_dev(W, "W"), _dtype_code(W, "W"), E, d_out, d_in,
+                                      _dev(out, "M"), _stream()), "gram_experts")
+    return out
+
+
+def shared_basis(M, r: int, out=None) -> Tuple[object, np.ndarray, float]:
+    """Top-r eigenvectors of M (host LAPACK). Returns (Ut [r][d_out] fp32, eigvals, host_ms)."""
+    torch = _torch()
+    d = M.shape[0]
+    if M.dtype != torch.float64:
+        raise TypeError("M must be float64")
+    if out is None:
+        out = torch.empty((r, d), dtype=torch.float32, device=M.device)
+    ev = np.zeros(r, dtype=np.float64)
+    ms = ctypes.c_double(0.0)
+    _check(lib().bitsmoe_shared_basis(_dev(M, "M"), d, r, _dev(out, "Ut"),
+                                      ev.ctypes.data_as(ctypes.c_void_p), ctypes.byref(ms),
+                                      _stream()), "shared_basis")
+    return out, ev, ms.value
+
+
+def project(Ut, W, out=None):
+    """C_e = U^T W_e -> fp32 [E*r][d_in] (unit u = e*r + k)."""
+    torch = _torch()
+    r, d_out = Ut.shape
+    E, d_out2, d_in = W.shape
+    if d_out2 != d_out:
+        raise ValueError("Ut and W disagree on d_out")
+    if Ut.dtype != torch.float32:
+        raise TypeError("Ut must be float32")
+    if out is None:
+        out = torch.empty((E * r, d_in), dtype=torch.float32, device=W.device)
+    _check(lib().bitsmoe_project(_dev(Ut, "Ut"), _dev(W, "W"), _dtype_code(W, "W"), E, d_out, d_in,
+                                 r, _dev(out, "C"), _stream()), "project")
+    return out
+
+
+def score(C, H, bits: Sequence[int], group: int, out=None):
+    """L[u][j] = delta H delta^T for every unit and width -> fp32 [units][len(bits)]."""
+    torch = _torch()
+    units, d = C.shape
+    if C.dtype != torch.float32 or H.dtype != torch.float32:
+        raise TypeError("C and H must be float32")
+    if tuple(H.shape) != (d, d):
+        raise ValueError("H must be [d][d]")
+    b, bp = _bits_arr(bits)
+    if out is None:
+        out = torch.empty((units, len(b)), dtype=torch.float32, device=C.device)
+    _check(lib().bitsmoe_score(_dev(C, "C"), units, d, _dev(H, "H"), bp, len(b), group,
+                               _dev(out, "L"), _stream()), "score")
+    return out
+
+
+def allocate(L, bits: Sequence[int], budget: int, full_dp_limit: int = -1,
+             return_core: bool = False):
+    """Exact ILP on the host. L: host array [units][len(bits)] fp32."""
+    Lh = np.ascontiguousarray(np.asarray(L, dtype=np.float32))
+    units = Lh.shape[0]
+    b, bp = _bits_arr(bits)
+    out = np.zeros(units, dtype=np.uint8)
+    obj = ctypes.c_double(0.0)
+    core = ctypes.c_int64(0)
+    _check(lib().bitsmoe_allocate_ex(Lh.ctypes.data_as(ctypes.c_void_p), units, bp, len(b),
+                                     int(budget), out.ctypes.data_as(ctypes.c_void_p),
+                                     ctypes.byref(obj), int(full_dp_limit), ctypes.byref(core)),
+           "allocate")
+    if return_core:
+        return out, obj.value, core.value
+    return out, obj.value
+
+
+def pack_layout(bits_u, d: int) -> np.ndarray:
+    bu = np.ascontiguousarray(np.asarray(bits_u, dtype=np.uint8))
+    off = np.zeros(bu.shape[0] + 1, dtype=np.int64)
+    _check(lib().bitsmoe_pack_layout(bu.ctypes.data_as(ctypes.c_void_p), bu.shape[0], d,
+                                     off.ctypes.data_as(ctypes.c_void_p)), "pack_layout")
+    return off
+
+
+def pack(C, bits_dev, offsets_dev, group: int, total_words: int, codes=None, params=None):
+    """Bit-plane codes (uint64 words, as int64 tensor) and fp16 params (as int16 [units][d/G][2])."""
+    torch = _torch()
+    units, d = C.shape
+    if codes is None:
+        codes = torch.empty((max(int(total_words), 1),), dtype=torch.int64, device=C.device)
+    if params is None:
+        params = torch.empty((units, d // group, 2), dtype=torch.int16, device=C.device)
+    _check(lib().bitsmoe_pack(_dev(C, "C"), units, d, group, _dev(bits_dev, "bits"),
+                              _dev(offsets_dev, "offsets"), int(total_words), _dev(codes, "codes"),
+                              _dev(params, "params"), _stream()), "pack")
+    return codes, params
+
+
+def unpack(codes, params, bits_dev, offsets_dev, units: int, d: int, group: int,
+           total_words: int, out=None):
+    torch = _torch()
+    if out is None:
+        out = torch.empty((units, d), dtype=torch.float32, device=codes.device)
+    _check(lib().bitsmoe_unpack(_dev(codes, "codes"), _dev(params, "params"), _dev(bits_dev, "bits"),
+                                _dev(offsets_dev, "offsets"), int(total_words), units, d, group,
+                                _dev(out, "Chat"), _stream()), "unpack")
+    return out
+
+
+def timing(enable: bool) -> None:
+    """Records HIP events around every main kernel while enabled."""
+    _check(lib().bitsmoe_timing(1 if enable else 0), "timing")
+
+
+def kernel_time(name: str) -> Tuple[float, int]:
+    """(summed ms, launches) of the kernel ``name`` since it was last read."""
+    ms = ctypes.c_double(0.0)
+    n = ctypes.c_int64(0)
+    _check(lib().bitsmoe_kernel_time(name.encode(), ctypes.byref(ms), ctypes.byref(n)), "kernel_time")
+    return ms.value, n.value
+
+
+def release() -> None:
+    lib().bitsmoe_release()
+
+
+def version() -> str:
+    return lib().bitsmoe_version().decode()
+
+
+def last_error() -> str:
+    return lib().bitsmoe_last_error().decode()

@@ -1,0 +1,228 @@
+// Step 1: the calibration Gram H = X^T X / n and the cross-expert Gram
+// M = sum_e W_e W_e^T, both as symmetric split-K matrix-core GEMMs whose fp32
+// partial tiles are added in fp64 in a fixed order (deterministic).
+#include <algorithm>
+#include <cstdio>
+
+#include "bitsmoe.h"
+#include "common.hpp"
+#include "gemm.hpp"
+#include "internal.hpp"
+
+namespace bitsmoe {
+namespace {
+
+constexpr int GT = 128;  // tile edge of the symmetric GEMMs
+using gemm::BK;
+
+// X [n][d] -> Xt [d][npad] (bf16), rows beyond n zero.  For fp32 input the
+// value is split x = hi + lo with hi = bf16(x), lo = bf16(x - hi).
+template <bool F32>
+__global__ __launch_bounds__(256) void transpose_split_kernel(const void* __restrict__ X, int64_t n,
+                                                              int64_t d, int64_t npad,
+                                                              uint16_t* __restrict__ hi,
+                                                              uint16_t* __restrict__ lo) {
+  __shared__ float tile[64][65];
+  const int64_t t0 = static_cast<int64_t>(blockIdx.x) * 64;  // token block
+  const int64_t c0 = static_cast<int64_t>(blockIdx.y) * 64;  // channel block
+  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;     // 64 x 4
+  for (int i = ty; i < 64; i += 4) {
+    const int64_t t = t0 + i, c = c0 + tx;
+    float v = 0.0f;
+    if (t < n && c < d) {
+      if (F32)
+        v = static_cast<const float*>(X)[t * d + c];
+      else
+        v = bf16_to_f32(static_cast<const uint16_t*>(X)[t * d + c]);
+    }
+    tile[i][tx] = v;
+  }
+  __syncthreads();
+  for (int i = ty; i < 64; i += 4) {
+    const int64_t c = c0 + i, t = t0 + tx;
+    if (c < d && t < npad) {
+      const float v = tile[tx][i];
+      const uint16_t h = f32_to_bf16(v);
+      hi[c * npad + t] = h;
+      if (F32) lo[c * npad + t] = f32_to_bf16(v - bf16_to_f32(h));
+    }
+  }
+}
+
+// fp32 W -> (hi, lo) bf16 with the same layout.
+__global__ __launch_bounds__(256) void split_kernel(const float* __restrict__ W, int64_t count,
+                                                    uint16_t* __restrict__ hi,
+                                                    uint16_t* __restrict__ lo) {
+  for (int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; i < count;
+       i += static_cast<int64_t>(gridDim.x) * 256) {
+    const float v = W[i];
+    const uint16_t h = f32_to_bf16(v);
+    hi[i] = h;
+    lo[i] = f32_to_bf16(v - bf16_to_f32(h));
+  }
+}
+
+// Stores each wave's fp32 accumulators into partials[split][tile][GT][GT].
+struct PartialStore {
+  float* part;
+  int64_t ntiles;     // tiles in the upper triangle
+  int ntiles_side;    // tiles per side
+  template <class F>
+  __device__ void operator()(F& f) const {
+    const int64_t t = (static_cast<int64_t>(f.tm) * (2 * ntiles_side - f.tm + 1)) / 2 + (f.tn - f.tm);
+    float* base = part + (static_cast<int64_t>(f.ks) * ntiles + t) * GT * GT;
+#pragma unroll
+    for (int mi = 0; mi < F::FM; ++mi)
+#pragma unroll
+      for (int ni = 0; ni < F::FN; ++ni)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int lr = f.row(mi, r) - f.tm * GT;
+          const int lc = f.col(ni) - f.tn * GT;
+          base[lr * GT + lc] = f.acc[mi][ni][r];
+        }
+  }
+};
+
+// out[i][j] = scale * sum_s partial (fp64, splits in order), mirrored.
+template <typename OutT>
+__global__ __launch_bounds__(256) void sym_reduce_kernel(const float* __restrict__ part, int splits,
+                                                         int64_t ntiles, int T, int64_t d,
+                                                         double scale, OutT* __restrict__ out) {
+  const int64_t idx = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (idx >= d * d) return;
+  int64_t i = idx / d, j = idx % d;
+  int64_t ti = i / GT, tj = j / GT;
+  if (ti > tj) {
+    int64_t tmp = i; i = j; j = tmp;
+    tmp = ti; ti = tj; tj = tmp;
+  }
+  const int64_t t = (ti * (2 * T - ti + 1)) / 2 + (tj - ti);
+  const int64_t off = t * GT * GT + (i % GT) * GT + (j % GT);
+  double s = 0.0;
+  for (int k = 0; k < splits; ++k) s += static_cast<double>(part[k * ntiles * GT * GT + off]);
+  out[idx] = static_cast<OutT>(s * scale);
+}
+
+// Launches the symmetric split-K GEMM of p (tiles/splits already set) and
+// reduces it into out.
+template <typename OutT>
+bitsmoe_status run_symmetric(gemm::Problem p, int64_t d, double scale, OutT* out, void* stream,
+                             const char* name) {
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int T = static_cast<int>((d + GT - 1) / GT);
+  const int64_t ntiles = static_cast<int64_t>(T) * (T + 1) / 2;
+  p.tiles_m = p.tiles_n = T;
+  p.symmetric = 1;
+  // K chunks of at most 4096 terms; at least ~2 workgroups per CU.
+  int64_t splits = (p.ktiles * BK + 4095) / 4096;
+  while (splits * ntiles < 512 && splits < p.ktiles) splits *= 2;
+  splits = std::min<int64_t>(splits, p.ktiles);
+  splits = std::max<int64_t>(splits, 1);
+  p.splits = static_cast<int>(splits);
+  bitsmoe_status st;
+  float* part = static_cast<float*>(
+      scratch(kScratchPart, static_cast<size_t>(splits) * ntiles * GT * GT * sizeof(float), stream, &st));
+  if (!part) return st;
+  PartialStore epi{part, ntiles, T};
+  dim3 grid(static_cast<unsigned>(ntiles), static_cast<unsigned>(splits), 1);
+  {
+    KernelTimer timer(name, stream);
+    hipLaunchKernelGGL((gemm::gemm_nt_kernel<GT, GT, 2, 2, PartialStore>), grid,
+                       dim3(gemm::kThreads), 0, s, p, epi);
+  }
+  BITSMOE_LAUNCH_CHECK("gram: gemm launch");
+  const int64_t total = d * d;
+  hipLaunchKernelGGL((sym_reduce_kernel<OutT>), dim3(static_cast<unsigned>((total + 255) / 256)),
+                     dim3(256), 0, s, part, p.splits, ntiles, T, d, scale, out);
+  BITSMOE_LAUNCH_CHECK("gram: reduce launch");
+  return BITSMOE_OK;
+}
+
+}  // namespace
+}  // namespace bitsmoe
+
+using namespace bitsmoe;
+
+extern "C" bitsmoe_status bitsmoe_gram(const void* X_dev, bitsmoe_dtype xt, int64_t n, int64_t d,
+                                       float* H_dev, void* stream) {
+  if (!X_dev || !H_dev) return fail(BITSMOE_ERR_ARG, "gram: null pointer");
+  if (n <= 0 || d <= 0) return fail(BITSMOE_ERR_ARG, "gram: non-positive size");
+  if (xt != BITSMOE_F32 && xt != BITSMOE_BF16) return fail(BITSMOE_ERR_DTYPE, "gram: dtype");
+  if (d % 64 != 0) return fail(BITSMOE_ERR_SHAPE, "gram: d must be a multiple of 64");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int64_t npad = (n + BK - 1) / BK * BK;
+  const bool f32 = xt == BITSMOE_F32;
+  bitsmoe_status st;
+  uint16_t* hi = static_cast<uint16_t*>(scratch(kScratchA, d * npad * 2, stream, &st));
+  if (!hi) return st;
+  uint16_t* lo = nullptr;
+  if (f32) {
+    lo = static_cast<uint16_t*>(scratch(kScratchB, d * npad * 2, stream, &st));
+    if (!lo) return st;
+  }
+  dim3 tg(static_cast<unsigned>((npad + 63) / 64), static_cast<unsigned>((d + 63) / 64));
+  if (f32)
+    hipLaunchKernelGGL(transpose_split_kernel<true>, tg, dim3(256), 0, s, X_dev, n, d, npad, hi, lo);
+  else
+    hipLaunchKernelGGL(transpose_split_kernel<false>, tg, dim3(256), 0, s, X_dev, n, d, npad, hi, lo);
+  BITSMOE_LAUNCH_CHECK("gram: transpose launch");
+  gemm::Problem p{};
+  p.a.ld = p.b.ld = npad;
+  p.a.rows = p.b.rows = d;
+  p.segs = 1;
+  p.kseg = npad;
+  if (f32) {
+    p.passes = 3;  // hi*hi + hi*lo + lo*hi
+    p.a.pass[0] = hi; p.b.pass[0] = hi;
+    p.a.pass[1] = hi; p.b.pass[1] = lo;
+    p.a.pass[2] = lo; p.b.pass[2] = hi;
+  } else {
+    p.passes = 1;
+    p.a.pass[0] = p.b.pass[0] = hi;
+  }
+  p.ktiles = p.passes * npad / BK;
+  st = run_symmetric<float>(p, d, 1.0 / static_cast<double>(n), H_dev, stream, "gram");
+  if (st != BITSMOE_OK) return st;
+  return ok();
+}
+
+extern "C" bitsmoe_status bitsmoe_gram_experts(const void* W_dev, bitsmoe_dtype wt, int64_t E,
+                                               int64_t d_out, int64_t d_in, double* M_dev,
+                                               void* stream) {
+  if (!W_dev || !M_dev) return fail(BITSMOE_ERR_ARG, "gram_experts: null pointer");
+  if (E <= 0 || d_out <= 0 || d_in <= 0) return fail(BITSMOE_ERR_ARG, "gram_experts: non-positive size");
+  if (wt != BITSMOE_F32 && wt != BITSMOE_BF16) return fail(BITSMOE_ERR_DTYPE, "gram_experts: dtype");
+  if (d_out % 64 != 0 || d_in % 64 != 0)
+    return fail(BITSMOE_ERR_SHAPE, "gram_experts: d_out and d_in must be multiples of 64");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  gemm::Problem p{};
+  p.a.ld = p.b.ld = d_in;
+  p.a.estride = p.b.estride = d_out * d_in;
+  p.a.rows = p.b.rows = d_out;
+  p.segs = static_cast<int>(E);
+  p.kseg = d_in;
+  if (wt == BITSMOE_F32) {
+    const int64_t count = E * d_out * d_in;
+    bitsmoe_status st;
+    uint16_t* hi = static_cast<uint16_t*>(scratch(kScratchA, count * 2, stream, &st));
+    if (!hi) return st;
+    uint16_t* lo = static_cast<uint16_t*>(scratch(kScratchB, count * 2, stream, &st));
+    if (!lo) return st;
+    const unsigned blocks = static_cast<unsigned>(std::min<int64_t>((count + 255) / 256, 65536));
+    hipLaunchKernelGGL(split_kernel, dim3(blocks), dim3(256), 0, s,
+                       static_cast<const float*>(W_dev), count, hi, lo);
+    BITSMOE_LAUNCH_CHECK("gram_experts: split launch");
+    p.passes = 3;
+    p.a.pass[0] = hi; p.b.pass[0] = hi;
+    p.a.pass[1] = hi; p.b.pass[1] = lo;
+    p.a.pass[2] = lo; p.b.pass[2] = hi;
+  } else {
+    p.passes = 1;
+    p.a.pass[0] = p.b.pass[0] = static_cast<const uint16_t*>(W_dev);
+  }
+  p.ktiles = static_cast<int64_t>(p.passes) * E * d_in / BK;
+  bitsmoe_status st = run_symmetric<double>(p, d_out, 1.0, M_dev, stream, "gram_experts");
+  if (st != BITSMOE_OK) return st;
+  return ok();
+}

@@ -1,0 +1,173 @@
+// Step 5: pack every spectral unit at its assigned width as bit planes with
+// fp16 (scale, min) per group, and the inverse (dequantize) for checking.
+//
+// One wave per unit.  Word w of the row holds entries 64 w .. 64 w + 63, one
+// per lane, so the plane-t word of w is the wave ballot of bit t of the lane
+// codes.  Words are gathered in LDS and written out contiguously.  Codes use
+// the fp64 quotient rule of the quantizer, so they match an fp64 reference
+// bit for bit given the same fp32 row.
+#include <algorithm>
+
+#include "bitsmoe.h"
+#include "common.hpp"
+#include "internal.hpp"
+
+namespace bitsmoe {
+namespace {
+
+template <int G>
+__global__ __launch_bounds__(64) void pack_kernel(const float* __restrict__ C, int64_t units,
+                                                  int64_t d, const uint8_t* __restrict__ bits,
+                                                  const int64_t* __restrict__ off,
+                                                  int64_t total_words,
+                                                  uint64_t* __restrict__ codes,
+                                                  uint32_t* __restrict__ params) {
+  extern __shared__ uint64_t smem[];  // [8 * nw] plane words, then [d/G] params
+  constexpr int WPB = G >= 64 ? G / 64 : 1;  // words per group batch
+  constexpr int RED = G >= 64 ? 64 : G;      // lanes sharing a group within a word
+  const int lane = threadIdx.x;
+  const int64_t u = blockIdx.x;
+  if (u >= units) return;
+  const int b = bits[u];
+  const int64_t nw = d / 64;
+  const int64_t o0 = off[u], o1 = off[u + 1];
+  if (b < 1 || b > BITSMOE_MAX_BITS || o1 - o0 != b * nw || o0 < 0 || o1 > total_words) return;
+  uint64_t* wbuf = smem;
+  uint32_t* pbuf = reinterpret_cast<uint32_t*>(smem + 8 * nw);
+  const double qmax = static_cast<double>((1 << b) - 1);
+  const float qmaxf = static_cast<float>((1 << b) - 1);
+  const float* crow = C + u * d;
+  for (int64_t w0 = 0; w0 < nw; w0 += WPB) {
+    float c[WPB];
+#pragma unroll
+    for (int i = 0; i < WPB; ++i) c[i] = crow[64 * (w0 + i) + lane];
+    float mn = c[0], mx = c[0];
+#pragma unroll
+    for (int i = 1; i < WPB; ++i) {
+      mn = fminf(mn, c[i]);
+      mx = fmaxf(mx, c[i]);
+    }
+#pragma unroll
+    for (int o = RED / 2; o > 0; o >>= 1) {
+      mn = fminf(mn, __shfl_xor(mn, o, 64));
+      mx = fmaxf(mx, __shfl_xor(mx, o, 64));
+    }
+    const uint16_t m16 = f32_to_f16_bits(mn);
+    const uint16_t s16 = f32_to_f16_bits((mx - mn) / qmaxf);
+    const double md = f16_bits_to_f64(m16);
+    const double sd = f16_bits_to_f64(s16);
+#pragma unroll
+    for (int i = 0; i < WPB; ++i) {
+      int q = 0;
+      if (sd > 0.0) {
+        const double t = (static_cast<double>(c[i]) - md) / sd;
+        q = static_cast<int>(fmin(fmax(rint(t), 0.0), qmax));
+      }
+      for (int t = 0; t < b; ++t) {
+        const uint64_t word = __ballot((q >> t) & 1);
+        if (lane == 0) wbuf[t * nw + w0 + i] = word;
+      }
+    }
+    if ((lane % RED) == 0) {
+      const int64_t g = (64 * w0 + lane) / G;
+      pbuf[g] = static_cast<uint32_t>(s16) | (static_cast<uint32_t>(m16) << 16);
+    }
+  }
+  __syncthreads();
+  for (int64_t i = lane; i < b * nw; i += 64) codes[o0 + i] = wbuf[i];
+  const int64_t ng = d / G;
+  for (int64_t g = lane; g < ng; g += 64) params[u * ng + g] = pbuf[g];
+}
+
+__global__ __launch_bounds__(64) void unpack_kernel(const uint64_t* __restrict__ codes,
+                                                    const uint32_t* __restrict__ params,
+                                                    const uint8_t* __restrict__ bits,
+                                                    const int64_t* __restrict__ off,
+                                                    int64_t total_words, int64_t units, int64_t d,
+                                                    int G, float* __restrict__ out) {
+  const int lane = threadIdx.x;
+  const int64_t u = blockIdx.x;
+  if (u >= units) return;
+  const int b = bits[u];
+  const int64_t nw = d / 64;
+  const int64_t o0 = off[u], o1 = off[u + 1];
+  if (b < 1 || b > BITSMOE_MAX_BITS || o1 - o0 != b * nw || o0 < 0 || o1 > total_words) return;
+  const int64_t ng = d / G;
+  for (int64_t w = 0; w < nw; ++w) {
+    uint32_t q = 0;
+    for (int t = 0; t < b; ++t) q |= static_cast<uint32_t>((codes[o0 + t * nw + w] >> lane) & 1u) << t;
+    const int64_t k = 64 * w + lane;
+    const uint32_t pr = params[u * ng + k / G];
+    const float s = f16_bits_to_f32(static_cast<uint16_t>(pr & 0xffffu));
+    const float m = f16_bits_to_f32(static_cast<uint16_t>(pr >> 16));
+    out[u * d + k] = fmaf(static_cast<float>(q), s, m);
+  }
+}
+
+bitsmoe_status check_pack_args(int64_t units, int64_t d, int group) {
+  if (units <= 0 || d <= 0) return fail(BITSMOE_ERR_ARG, "pack: non-positive size");
+  if (!(group == 32 || group == 64 || group == 128 || group == 256))
+    return fail(BITSMOE_ERR_SHAPE, "pack: group must be 32, 64, 128 or 256");
+  if (d % 64 != 0 || d % group != 0)
+    return fail(BITSMOE_ERR_SHAPE, "pack: d must be a multiple of 64 and of the group");
+  if (units > INT32_MAX) return fail(BITSMOE_ERR_SHAPE, "pack: too many units");
+  return BITSMOE_OK;
+}
+
+}  // namespace
+}  // namespace bitsmoe
+
+using namespace bitsmoe;
+
+extern "C" bitsmoe_status bitsmoe_pack(const float* C_dev, int64_t units, int64_t d, int group,
+                                       const uint8_t* bits_dev, const int64_t* word_offsets_dev,
+                                       int64_t total_words, uint64_t* codes_dev,
+                                       uint16_t* params_dev, void* stream) {
+  if (!C_dev || !bits_dev || !word_offsets_dev || !codes_dev || !params_dev)
+    return fail(BITSMOE_ERR_ARG, "pack: null pointer");
+  bitsmoe_status st = check_pack_args(units, d, group);
+  if (st != BITSMOE_OK) return st;
+  if (total_words < 0) return fail(BITSMOE_ERR_ARG, "pack: negative total_words");
+  const size_t lds = static_cast<size_t>(8 * (d / 64)) * 8 + static_cast<size_t>(d / group) * 4;
+  if (lds > 160 * 1024) return fail(BITSMOE_ERR_SHAPE, "pack: row too long");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  uint32_t* pr = reinterpret_cast<uint32_t*>(params_dev);
+  dim3 grid(static_cast<unsigned>(units));
+  KernelTimer timer("pack", stream);
+  switch (group) {
+    case 32:
+      hipLaunchKernelGGL(pack_kernel<32>, grid, dim3(64), lds, s, C_dev, units, d, bits_dev,
+                         word_offsets_dev, total_words, codes_dev, pr);
+      break;
+    case 64:
+      hipLaunchKernelGGL(pack_kernel<64>, grid, dim3(64), lds, s, C_dev, units, d, bits_dev,
+                         word_offsets_dev, total_words, codes_dev, pr);
+      break;
+    case 128:
+      hipLaunchKernelGGL(pack_kernel<128>, grid, dim3(64), lds, s, C_dev, units, d, bits_dev,
+                         word_offsets_dev, total_words, codes_dev, pr);
+      break;
+    default:
+      hipLaunchKernelGGL(pack_kernel<256>, grid, dim3(64), lds, s, C_dev, units, d, bits_dev,
+                         word_offsets_dev, total_words, codes_dev, pr);
+      break;
+  }
+  BITSMOE_LAUNCH_CHECK("pack: launch");
+  return ok();
+}
+
+extern "C" bitsmoe_status bitsmoe_unpack(const uint64_t* codes_dev, const uint16_t* params_dev,
+                                         const uint8_t* bits_dev, const int64_t* word_offsets_dev,
+                                         int64_t total_words, int64_t units, int64_t d, int group,
+                                         float* Chat_dev, void* stream) {
+  if (!codes_dev || !params_dev || !bits_dev || !word_offsets_dev || !Chat_dev)
+    return fail(BITSMOE_ERR_ARG, "unpack: null pointer");
+  bitsmoe_status st = check_pack_args(units, d, group);
+  if (st != BITSMOE_OK) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipLaunchKernelGGL(unpack_kernel, dim3(static_cast<unsigned>(units)), dim3(64), 0, s, codes_dev,
+                     reinterpret_cast<const uint32_t*>(params_dev), bits_dev, word_offsets_dev,
+                     total_words, units, d, group, Chat_dev);
+  BITSMOE_LAUNCH_CHECK("unpack: launch");
+  return ok();
+}

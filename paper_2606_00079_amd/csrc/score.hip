@@ -1,0 +1,287 @@
+// Step 4: the activation-aware loss table L[u][j] = delta H delta^T.
+//
+// For unit row c and width b = bits[j], delta = c - Q_b(c) with the group-wise
+// asymmetric round-to-nearest quantizer, and the loss is the exact
+// output-space term eps^T H eps of App. B.2 (Eq. app_down_exact_metric),
+// written for the unnormalized row.  Split as
+//     delta H delta^T = sum_k H_kk delta_k^2  +  delta H_off delta^T,
+// the diagonal part is summed in fp32 from the fp32 error, and the
+// off-diagonal part, a GEMM of the error rows with H_off, runs on the matrix
+// cores in bf16 with fp32 accumulation:
+//   1. hoff_kernel   H -> bf16 H_off (zero diagonal) and fp32 diag(H)
+//   2. dgen_kernel   one wave per unit: group min/max, fake-quant at every
+//                    width, bf16 error rows D[u*nb + j][:] and the diagonal
+//                    term of each (u, j)
+//   3. gemm          acc[i][row] = sum_k H_off[i][k] D[row][k], epilogue
+//                    sum_i D[row][i] acc[i][row] per 128-wide i tile
+//   4. finalize      L = diagonal term + the tile partials, in a fixed order.
+#include <algorithm>
+
+#include "bitsmoe.h"
+#include "common.hpp"
+#include "gemm.hpp"
+#include "internal.hpp"
+
+namespace bitsmoe {
+namespace {
+
+constexpr int SBM = 128;  // i (H row) tile
+constexpr int SBN = 128;  // D row tile
+using gemm::BK;
+
+__global__ __launch_bounds__(256) void hoff_kernel(const float* __restrict__ H, int64_t d,
+                                                   uint16_t* __restrict__ Hoff,
+                                                   float* __restrict__ hdiag) {
+  const int64_t total = d * d;
+  for (int64_t idx = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; idx < total;
+       idx += static_cast<int64_t>(gridDim.x) * 256) {
+    const int64_t i = idx / d, k = idx - i * d;
+    const float v = H[idx];
+    Hoff[idx] = (i == k) ? uint16_t(0) : f32_to_bf16(v);
+    if (i == k) hdiag[i] = v;
+  }
+}
+
+struct QuantBits {
+  int nb;
+  int b[BITSMOE_MAX_NBITS];
+};
+
+// Group-wise fake quantization of one unit per wave.  Lane l covers entries
+// [512 c + 8 l, 512 c + 8 l + 8) of chunk c; a group of G entries spans G/8
+// consecutive lanes.  Codes follow the fp64 rule exactly: the fp32 quotient
+// is used unless it lies within 1e-4 of a rounding boundary (its error is
+// below 5e-5 for codes up to 255), in which case fp64 decides.
+template <int NB>
+__global__ __launch_bounds__(256) void dgen_kernel(const float* __restrict__ C, int64_t units,
+                                                   int64_t d, int G, QuantBits qb,
+                                                   const float* __restrict__ hdiag,
+                                                   uint16_t* __restrict__ D,
+                                                   float* __restrict__ diag) {
+  const int lane = threadIdx.x & 63;
+  const int64_t u = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
+  if (u >= units) return;  // whole wave exits together
+  constexpr int nb = NB;
+  const int glanes = G / 8;
+  float dacc[NB];
+#pragma unroll
+  for (int j = 0; j < NB; ++j) dacc[j] = 0.0f;
+  const float* crow = C + u * d;
+  for (int64_t k0 = 0; k0 < d; k0 += 512) {
+    const int64_t k = k0 + 8 * lane;
+    const bool active = k < d;
+    float c[8];
+    float hd[8];
+    if (active) {
+      const float4 v0 = *reinterpret_cast<const float4*>(crow + k);
+      const float4 v1 = *reinterpret_cast<const float4*>(crow + k + 4);
+      c[0] = v0.x; c[1] = v0.y; c[2] = v0.z; c[3] = v0.w;
+      c[4] = v1.x; c[5] = v1.y; c[6] = v1.z; c[7] = v1.w;
+      const float4 h0 = *reinterpret_cast<const float4*>(hdiag + k);
+      const float4 h1 = *reinterpret_cast<const float4*>(hdiag + k + 4);
+      hd[0] = h0.x; hd[1] = h0.y; hd[2] = h0.z; hd[3] = h0.w;
+      hd[4] = h1.x; hd[5] = h1.y; hd[6] = h1.z; hd[7] = h1.w;
+    } else {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) c[i] = hd[i] = 0.0f;
+    }
+    float mn = c[0], mx = c[0];
+#pragma unroll
+    for (int i = 1; i < 8; ++i) {
+      mn = fminf(mn, c[i]);
+      mx = fmaxf(mx, c[i]);
+    }
+    for (int o = 1; o < glanes; o <<= 1) {
+      mn = fminf(mn, __shfl_xor(mn, o, 64));
+      mx = fmaxf(mx, __shfl_xor(mx, o, 64));
+    }
+    if (!active) continue;
+    const float mf = f16_bits_to_f32(f32_to_f16_bits(mn));
+    const float range = mx - mn;
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+      const int b = qb.b[j];
+      const float qmax = static_cast<float>((1 << b) - 1);
+      const float s32 = range / qmax;
+      const float sf = f16_bits_to_f32(f32_to_f16_bits(s32));
+      const float inv = sf > 0.0f ? 1.0f / sf : 0.0f;
+      uint16_t out[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        float q = 0.0f;
+        if (sf > 0.0f) {
+          const float t = (c[i] - mf) * inv;
+          const float fl = floorf(t);
+          if (fabsf(t - fl - 0.5f) < 1e-4f) {
+            const double td = (static_cast<double>(c[i]) - static_cast<double>(mf)) /
+                              static_cast<double>(sf);
+            q = static_cast<float>(fmin(fmax(rint(td), 0.0), static_cast<double>(qmax)));
+          } else {
+            q = fminf(fmaxf(rintf(t), 0.0f), qmax);
+          }
+        }
+        const float xh = fmaf(q, sf, mf);
+        const float dl = c[i] - xh;
+        out[i] = f32_to_bf16(dl);
+        dacc[j] = fmaf(hd[i] * dl, dl, dacc[j]);
+      }
+      uint4 pk;
+      pk.x = static_cast<uint32_t>(out[0]) | (static_cast<uint32_t>(out[1]) << 16);
+      pk.y = static_cast<uint32_t>(out[2]) | (static_cast<uint32_t>(out[3]) << 16);
+      pk.z = static_cast<uint32_t>(out[4]) | (static_cast<uint32_t>(out[5]) << 16);
+      pk.w = static_cast<uint32_t>(out[6]) | (static_cast<uint32_t>(out[7]) << 16);
+      *reinterpret_cast<uint4*>(D + (u * nb + j) * d + k) = pk;
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < NB; ++j) {
+    const float v = wave_sum(dacc[j]);
+    if (lane == 0) diag[u * nb + j] = v;
+  }
+}
+
+// part[row][tm] = sum over this tile's i of D[row][i] * acc[i][row].
+struct RowDot {
+  const uint16_t* D;
+  float* part;
+  int64_t R, d;
+  int tiles_m;
+  template <class F>
+  __device__ void operator()(F& f) const {
+    __shared__ float red[2][SBN];
+    float s[F::FN];
+#pragma unroll
+    for (int ni = 0; ni < F::FN; ++ni) {
+      s[ni] = 0.0f;
+      const int64_t row = f.col(ni);
+      if (row < R) {
+        const uint16_t* drow = D + row * d;
+#pragma unroll
+        for (int mi = 0; mi < F::FM; ++mi)
+#pragma unroll
+          for (int g = 0; g < 4; ++g) {
+            const int i = f.row(mi, 4 * g);
+            if (i < d) {
+              const uint2 v = *reinterpret_cast<const uint2*>(drow + i);
+              s[ni] += bf16_to_f32(static_cast<uint16_t>(v.x & 0xffff)) * f.acc[mi][ni][4 * g + 0] +
+                       bf16_to_f32(static_cast<uint16_t>(v.x >> 16)) * f.acc[mi][ni][4 * g + 1] +
+                       bf16_to_f32(static_cast<uint16_t>(v.y & 0xffff)) * f.acc[mi][ni][4 * g + 2] +
+                       bf16_to_f32(static_cast<uint16_t>(v.y >> 16)) * f.acc[mi][ni][4 * g + 3];
+            }
+          }
+      }
+      s[ni] += __shfl_xor(s[ni], 32, 64);
+    }
+    // combine the waves that share these rows (wm = 0, 1)
+    if ((f.lane >> 5) == 0) {
+#pragma unroll
+      for (int ni = 0; ni < F::FN; ++ni) red[f.wm][f.wn * (SBN / 2) + 32 * ni + f.lane] = s[ni];
+    }
+    __syncthreads();
+    const int t = threadIdx.x;
+    if (t < SBN) {
+      const int64_t row = static_cast<int64_t>(f.tn) * SBN + t;
+      if (row < R) part[row * tiles_m + f.tm] = red[0][t] + red[1][t];
+    }
+  }
+};
+
+__global__ __launch_bounds__(256) void finalize_kernel(const float* __restrict__ diag,
+                                                       const float* __restrict__ part, int64_t R,
+                                                       int tiles_m, float* __restrict__ L) {
+  const int64_t row = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (row >= R) return;
+  float s = diag[row];
+  const float* p = part + row * tiles_m;
+  for (int t = 0; t < tiles_m; ++t) s += p[t];
+  L[row] = s;
+}
+
+}  // namespace
+}  // namespace bitsmoe
+
+using namespace bitsmoe;
+
+extern "C" bitsmoe_status bitsmoe_score(const float* C_dev, int64_t units, int64_t d,
+                                        const float* H_dev, const int* bits_host, int nbits,
+                                        int group, float* L_dev, void* stream) {
+  if (!C_dev || !H_dev || !bits_host || !L_dev) return fail(BITSMOE_ERR_ARG, "score: null pointer");
+  if (units <= 0 || d <= 0) return fail(BITSMOE_ERR_ARG, "score: non-positive size");
+  if (nbits < 1 || nbits > BITSMOE_MAX_NBITS) return fail(BITSMOE_ERR_ARG, "score: nbits outside 1..8");
+  QuantBits qb{};
+  qb.nb = nbits;
+  for (int j = 0; j < nbits; ++j) {
+    if (bits_host[j] < 1 || bits_host[j] > BITSMOE_MAX_BITS)
+      return fail(BITSMOE_ERR_ARG, "score: width outside 1..8");
+    if (j > 0 && bits_host[j] <= bits_host[j - 1])
+      return fail(BITSMOE_ERR_ARG, "score: widths must be strictly ascending");
+    qb.b[j] = bits_host[j];
+  }
+  if (!(group == 32 || group == 64 || group == 128 || group == 256))
+    return fail(BITSMOE_ERR_SHAPE, "score: group must be 32, 64, 128 or 256");
+  if (d % 64 != 0 || d % group != 0)
+    return fail(BITSMOE_ERR_SHAPE, "score: d must be a multiple of 64 and of the group");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int64_t R = units * nbits;
+  const int tiles_m = static_cast<int>((d + SBM - 1) / SBM);
+  const int64_t tiles_n = (R + SBN - 1) / SBN;
+  if (tiles_n * tiles_m > INT32_MAX) return fail(BITSMOE_ERR_SHAPE, "score: too many units");
+  bitsmoe_status st;
+  uint16_t* Hoff = static_cast<uint16_t*>(scratch(kScratchA, d * d * 2, stream, &st));
+  if (!Hoff) return st;
+  float* small = static_cast<float*>(scratch(kScratchMisc, (d + R) * sizeof(float), stream, &st));
+  if (!small) return st;
+  float* hdiag = small;
+  float* diag = small + d;
+  uint16_t* D = static_cast<uint16_t*>(scratch(kScratchD, R * d * 2, stream, &st));
+  if (!D) return st;
+  float* part = static_cast<float*>(scratch(kScratchPart, R * tiles_m * sizeof(float), stream, &st));
+  if (!part) return st;
+
+  const unsigned hb = static_cast<unsigned>(std::min<int64_t>((d * d + 255) / 256, 16384));
+  hipLaunchKernelGGL(hoff_kernel, dim3(hb), dim3(256), 0, s, H_dev, d, Hoff, hdiag);
+  BITSMOE_LAUNCH_CHECK("score: hoff launch");
+  const unsigned db = static_cast<unsigned>((units + 3) / 4);
+  {
+  KernelTimer dgen_timer("score_dgen", stream);
+  switch (nbits) {
+#define BITSMOE_DGEN(NB)                                                                       \
+  case NB:                                                                                     \
+    hipLaunchKernelGGL(dgen_kernel<NB>, dim3(db), dim3(256), 0, s, C_dev, units, d, group, qb, \
+                       hdiag, D, diag);                                                        \
+    break;
+    BITSMOE_DGEN(1) BITSMOE_DGEN(2) BITSMOE_DGEN(3) BITSMOE_DGEN(4)
+    BITSMOE_DGEN(5) BITSMOE_DGEN(6) BITSMOE_DGEN(7) BITSMOE_DGEN(8)
+#undef BITSMOE_DGEN
+  }
+  }
+  BITSMOE_LAUNCH_CHECK("score: dgen launch");
+
+  gemm::Problem p{};
+  p.a.pass[0] = Hoff;
+  p.a.ld = d;
+  p.a.rows = d;
+  p.b.pass[0] = D;
+  p.b.ld = d;
+  p.b.rows = R;
+  p.passes = 1;
+  p.segs = 1;
+  p.kseg = d;
+  p.ktiles = d / BK;
+  p.splits = 1;
+  p.tiles_m = tiles_m;
+  p.tiles_n = static_cast<int>(tiles_n);
+  p.symmetric = 0;
+  RowDot epi{D, part, R, d, tiles_m};
+  dim3 grid(static_cast<unsigned>(tiles_m * tiles_n), 1, 1);
+  {
+    KernelTimer timer("score_gemm", stream);
+    hipLaunchKernelGGL((gemm::gemm_nt_kernel<SBM, SBN, 2, 2, RowDot>), grid, dim3(gemm::kThreads),
+                       0, s, p, epi);
+  }
+  BITSMOE_LAUNCH_CHECK("score: gemm launch");
+  hipLaunchKernelGGL(finalize_kernel, dim3(static_cast<unsigned>((R + 255) / 256)), dim3(256), 0, s,
+                     diag, part, R, tiles_m, L_dev);
+  BITSMOE_LAUNCH_CHECK("score: finalize launch");
+  return ok();
+}

@@ -1,0 +1,106 @@
+"""End-to-end driver: one projection, or a whole MoE layer, through the C ABI.
+
+A projection runs three device segments separated by the two host steps:
+
+    device:  gram (H), gram_experts (M)
+    host:    shared_basis (LAPACK eigensolve of M)
+    device:  project (C), score (L)
+    host:    allocate (exact ILP over L)
+    device:  pack (codes, params)
+
+Device segments are timed with HIP events on the current stream; the host
+steps with a wall clock.  Gate and up projections of a layer read the same
+calibration input, so their H is computed once.
+"""
+from __future__ import annotations
+
+import dataclasses
+import time
+from typing import Dict, List, Optional, Sequence
+
+import numpy as np
+
+from . import (allocate, gram, gram_experts, pack, pack_layout, project, score, shared_basis)
+
+
+@dataclasses.dataclass
+class ProjectionResult:
+    H: object
+    M: object
+    Ut: object
+    eigvals: np.ndarray
+    C: object
+    L: object
+    bits_u: np.ndarray
+    objective: float
+    offsets: np.ndarray
+    codes: object
+    params: object
+    times: Dict[str, float]
+
+
+class _Seg:
+    """HIP-event timer for one device segment on the current stream."""
+
+    def __init__(self):
+        import torch
+        self.t = torch
+        self.a = torch.cuda.Event(enable_timing=True)
+        self.b = torch.cuda.Event(enable_timing=True)
+
+    def __enter__(self):
+        self.a.record()
+        return self
+
+    def __exit__(self, *exc):
+        self.b.record()
+
+    def ms(self) -> float:
+        self.b.synchronize()
+        return float(self.a.elapsed_time(self.b))
+
+
+def quantize_projection(W, X, r: int, bits: Sequence[int], group: int, budget: int,
+                        H=None) -> ProjectionResult:
+    import torch
+    times: Dict[str, float] = {}
+    s1 = _Seg()
+    with s1:
+        if H is None:
+            H = gram(X)
+        M = gram_experts(W)
+    Ut, ev, eig_ms = shared_basis(M, r)      # synchronizes the stream first
+    times["gpu_gram_ms"] = s1.ms()
+    times["host_eig_ms"] = eig_ms
+    s2 = _Seg()
+    with s2:
+        C = project(Ut, W)
+        L = score(C, H, bits, group)
+    t0 = time.perf_counter()
+    Lh = L.cpu().numpy()                     # waits for the score
+    bits_u, obj = allocate(Lh, bits, budget)
+    off = pack_layout(bits_u, C.shape[1])
+    times["gpu_score_ms"] = s2.ms()
+    bits_d = torch.from_numpy(bits_u).to(C.device, non_blocking=False)
+    off_d = torch.from_numpy(off).to(C.device, non_blocking=False)
+    times["host_ilp_ms"] = (time.perf_counter() - t0) * 1e3
+    s3 = _Seg()
+    with s3:
+        codes, params = pack(C, bits_d, off_d, group, int(off[-1]))
+    times["gpu_pack_ms"] = s3.ms()
+    times["gpu_ms"] = times["gpu_gram_ms"] + times["gpu_score_ms"] + times["gpu_pack_ms"]
+    return ProjectionResult(H, M, Ut, ev, C, L, bits_u, obj, off, codes, params, times)
+
+
+def quantize_layer(projs: List[dict]) -> List[ProjectionResult]:
+    """projs: dicts with W, X, r, bits, group, budget.  X objects that are the
+    same tensor share one H."""
+    cache = {}
+    out = []
+    for p in projs:
+        key = id(p["X"])
+        res = quantize_projection(p["W"], p["X"], p["r"], p["bits"], p["group"], p["budget"],
+                                  H=cache.get(key))
+        cache[key] = res.H
+        out.append(res)
+    return out

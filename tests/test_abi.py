@@ -1,0 +1,161 @@
+"""CPU tests of the C ABI: symbols, host-side solvers, argument checking.
+
+No device work runs here: the device entry points are only called with
+arguments that are rejected before anything is enqueued.
+"""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+from oracle.ilp import Infeasible
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "bitsmoe.h")
+
+pkg = pytest.importorskip("paper_2606_00079_amd")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(pkg.LIB_PATH):
+        pytest.skip("libbitsmoe.so not built")
+    return pkg.lib()
+
+
+def _declared():
+    txt = open(HEADER).read()
+    return sorted(set(re.findall(r"\b(bitsmoe_[a-z_0-9]+)\s*\(", txt)))
+
+
+def test_header_declares_and_library_exports_everything(lib):
+    names = _declared()
+    assert "bitsmoe_score" in names and "bitsmoe_pack" in names
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(names) == set(pkg.EXPORTS)
+
+
+def test_version(lib):
+    assert "gfx950" in pkg.version()
+
+
+# ------------------------------------------------------------------ allocate
+def _rand_L(g, U, nb, ties=False):
+    L = g.gamma(2.0, 1.0, size=(U, nb)) * np.logspace(0, -3, nb)[None, :] * g.uniform(0.1, 10, (U, 1))
+    if ties:
+        L = np.round(L * 8) / 8
+        for _ in range(max(1, U // 10)):
+            L[g.integers(0, U)] = L[g.integers(0, U)]
+        L[g.integers(0, U)] = 0.0
+    return L.astype(np.float32)
+
+
+@pytest.mark.parametrize("seed", range(10))
+@pytest.mark.parametrize("force_core", [False, True])
+def test_allocate_matches_oracle_dp(lib, seed, force_core):
+    g = np.random.default_rng(500 + seed)
+    U = int(g.integers(1, 300))
+    bits = [[1, 2, 3, 4], [1, 2, 3, 4, 8], [2, 3], [1]][seed % 4]
+    L = _rand_L(g, U, len(bits), ties=seed % 2 == 1)
+    for frac in (0.0, 0.3, 0.5, 0.77, 1.0):
+        budget = int(U * bits[0] + frac * U * (bits[-1] - bits[0]))
+        ref, _ = oracle.allocate_dp(L, bits, budget)
+        got, obj, core = pkg.allocate(L, bits, budget, full_dp_limit=0 if force_core else -1,
+                                      return_core=True)
+        assert np.array_equal(got, ref), (U, bits, budget)
+        assert np.isclose(obj, oracle.objective(L, bits, ref), rtol=1e-12)
+        assert int(got.astype(np.int64).sum()) <= budget
+
+
+def test_allocate_matches_exhaustive_tiny(lib):
+    g = np.random.default_rng(9)
+    for _ in range(30):
+        U = int(g.integers(1, 7))
+        bits = [1, 2, 3, 4]
+        L = _rand_L(g, U, 4, ties=True)
+        budget = int(g.integers(U, 4 * U + 1))
+        ref, _ = oracle.allocate_exhaustive(L, bits, budget)
+        for lim in (-1, 0):
+            got, _ = pkg.allocate(L, bits, budget, full_dp_limit=lim)
+            assert np.array_equal(got, ref)
+
+
+def test_allocate_core_path_mid_size(lib):
+    # Large enough that the default solver reduces to a core; checked against
+    # the oracle's full dynamic program.
+    g = np.random.default_rng(21)
+    U = 6000
+    bits = [1, 2, 3, 4]
+    L = _rand_L(g, U, 4)
+    budget = 2 * U
+    ref, _ = oracle.allocate_dp(L, bits, budget)
+    got, obj, core = pkg.allocate(L, bits, budget, full_dp_limit=0, return_core=True)
+    assert np.array_equal(got, ref)
+    assert core < U // 4
+
+
+def test_allocate_errors(lib):
+    L = np.ones((4, 2), dtype=np.float32)
+    with pytest.raises(pkg.BitsmoeError) as e:
+        pkg.allocate(L, [1, 2], 3)
+    assert e.value.code == "ERR_INFEASIBLE"
+    with pytest.raises(Infeasible):
+        oracle.allocate_dp(L, [1, 2], 3)
+    L2 = L.copy()
+    L2[1, 1] = np.nan
+    with pytest.raises(pkg.BitsmoeError) as e:
+        pkg.allocate(L2, [1, 2], 6)
+    assert e.value.code == "ERR_NUMERIC"
+    with pytest.raises(pkg.BitsmoeError) as e:
+        pkg.allocate(L, [2, 1], 6)
+    assert e.value.code == "ERR_ARG"
+    with pytest.raises(pkg.BitsmoeError) as e:
+        pkg.allocate(L, [1, 9], 6)
+    assert e.value.code == "ERR_ARG"
+
+
+def test_pack_layout_matches_oracle(lib):
+    g = np.random.default_rng(3)
+    bits_u = g.choice([1, 2, 3, 4, 8], size=77).astype(np.uint8)
+    for d in (64, 256, 2048):
+        assert np.array_equal(pkg.pack_layout(bits_u, d), oracle.pack_layout(bits_u, d))
+    with pytest.raises(pkg.BitsmoeError) as e:
+        pkg.pack_layout(bits_u, 100)
+    assert e.value.code == "ERR_SHAPE"
+    bad = bits_u.copy()
+    bad[5] = 0
+    with pytest.raises(pkg.BitsmoeError):
+        pkg.pack_layout(bad, 64)
+
+
+# ------------------------------------------------- device calls, rejected early
+def test_device_entry_points_validate_before_launch(lib):
+    fake = ctypes.c_void_p(0x1000)   # never dereferenced: every call below is rejected first
+    null = ctypes.c_void_p(0)
+    s = ctypes.c_void_p(0)
+    bits = (ctypes.c_int * 4)(1, 2, 3, 4)
+    bad_bits = (ctypes.c_int * 2)(3, 2)
+    assert lib.bitsmoe_gram(null, 1, 10, 64, fake, s) == 1
+    assert lib.bitsmoe_gram(fake, 1, 10, 100, fake, s) == 2
+    assert lib.bitsmoe_gram(fake, 7, 10, 64, fake, s) == 3
+    assert lib.bitsmoe_gram(fake, 1, 0, 64, fake, s) == 1
+    assert lib.bitsmoe_gram_experts(fake, 1, 2, 96, 64, fake, s) == 2
+    assert lib.bitsmoe_gram_experts(fake, 1, 0, 64, 64, fake, s) == 1
+    assert lib.bitsmoe_project(fake, fake, 1, 2, 64, 64, 65, fake, s) == 2
+    assert lib.bitsmoe_project(fake, fake, 1, 2, 64, 100, 8, fake, s) == 2
+    assert lib.bitsmoe_score(fake, 10, 256, fake, bits, 4, 48, fake, s) == 2
+    assert lib.bitsmoe_score(fake, 10, 320, fake, bits, 4, 128, fake, s) == 2
+    assert lib.bitsmoe_score(fake, 10, 256, fake, bad_bits, 2, 64, fake, s) == 1
+    assert lib.bitsmoe_score(fake, 10, 256, fake, bits, 0, 64, fake, s) == 1
+    assert lib.bitsmoe_score(fake, 0, 256, fake, bits, 4, 64, fake, s) == 1
+    assert lib.bitsmoe_pack(fake, 10, 256, 48, fake, fake, 10, fake, fake, s) == 2
+    assert lib.bitsmoe_pack(null, 10, 256, 64, fake, fake, 10, fake, fake, s) == 1
+    assert lib.bitsmoe_unpack(fake, fake, fake, fake, 10, 10, 200, 64, fake, s) == 2
+    assert lib.bitsmoe_shared_basis(fake, 64, 65, fake, null, null, s) == 2
+    assert "r > d_out" in pkg.last_error()
+    assert lib.bitsmoe_shared_basis(null, 64, 4, fake, null, null, s) == 1
+    assert lib.bitsmoe_set_lapack(b"/nonexistent/liblapack.so") == 8

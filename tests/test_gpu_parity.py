@@ -1,0 +1,335 @@
+"""GPU parity: every step of the HIP path against the fp64 oracle.
+
+Stage-wise: each device step is fed the same inputs as the oracle step it is
+compared with (the device's own upstream outputs, copied to the host), so
+errors do not compound and near-degenerate eigenvectors cannot make two
+correct results look different.
+
+Bars (written in each test): H, M, C and U within 1e-3 relative Frobenius;
+L within 1e-3 relative per entry; ILP widths, codes and scale/min parameters
+bit-exact.
+"""
+import math
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from conftest import gpu_available
+
+pytestmark = pytest.mark.gpu
+
+if not gpu_available():  # pragma: no cover - collected on CPU but skipped
+    pytest.skip("no GPU", allow_module_level=True)
+
+import torch  # noqa: E402
+
+import paper_2606_00079_amd as bm  # noqa: E402
+from paper_2606_00079_amd import pipeline  # noqa: E402
+
+DEV = "cuda:0"
+REL = 1e-3
+
+
+def say(*a):
+    print("[gpu-parity]", *a, flush=True)
+    sys.stdout.flush()
+
+
+def dev(a: np.ndarray, dtype: str):
+    if dtype == "bf16":
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).to(DEV)
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(DEV)
+
+
+def f64(a: np.ndarray, dtype: str) -> np.ndarray:
+    return synth.as_f64(a, dtype)
+
+
+def relfro(a, b) -> float:
+    a = np.asarray(a, np.float64)
+    b = np.asarray(b, np.float64)
+    return float(np.linalg.norm(a - b) / max(np.linalg.norm(b), 1e-300))
+
+
+def l_rel(got, ref) -> float:
+    got = np.asarray(got, np.float64)
+    ref = np.asarray(ref, np.float64)
+    den = np.maximum(np.abs(ref), 1e-30)
+    return float(np.max(np.abs(got - ref) / den))
+
+
+# ------------------------------------------------------------------------- H
+@pytest.mark.parametrize("case", ["tiny_f32", "ragged_bf16", "ragged_f32", "qwen_bf16"])
+def test_gram(case):
+    say("gram", case)
+    if case == "tiny_f32":
+        X = synth.calibration_input(synth.CONFIGS["tiny"], "gate")
+        dt = "f32"
+    elif case == "ragged_bf16":
+        X = synth.f32_to_bf16_bits(synth.random_rows(1001, 320, seed=1, scale=1.0, heavy=True))
+        dt = "bf16"
+    elif case == "ragged_f32":
+        X = synth.random_rows(77, 192, seed=2, scale=3.0)
+        dt = "f32"
+    else:
+        X = synth.calibration_input(synth.CONFIGS["qwen_gate"], "gate")
+        dt = "bf16"
+    H = bm.gram(dev(X, dt)).cpu().numpy()
+    ref = oracle.gram(f64(X, dt))
+    err = relfro(H, ref)
+    say("gram", case, "rel fro", err)
+    assert err <= REL
+    assert np.array_equal(H, H.T)
+    # per-entry: diagonal to fp32 accuracy
+    assert l_rel(np.diag(H), np.diag(ref)) < 1e-5
+
+
+# ------------------------------------------------------------------------- M
+@pytest.mark.parametrize("case", ["tiny_f32", "ragged_bf16", "qwen_gate_bf16"])
+def test_gram_experts(case):
+    say("gram_experts", case)
+    if case == "tiny_f32":
+        W = synth.expert_weights(synth.CONFIGS["tiny"], "gate")
+        dt = "f32"
+    elif case == "ragged_bf16":
+        W = synth.f32_to_bf16_bits(synth.random_rows(3 * 192, 320, seed=3).reshape(3, 192, 320))
+        dt = "bf16"
+    else:
+        W = synth.expert_weights(synth.CONFIGS["qwen_gate"], "gate")
+        dt = "bf16"
+    M = bm.gram_experts(dev(W, dt)).cpu().numpy()
+    ref = oracle.gram_experts(f64(W, dt))
+    err = relfro(M, ref)
+    say("gram_experts", case, "rel fro", err)
+    assert err <= REL
+    assert np.array_equal(M, M.T)
+    assert abs(np.trace(M) - np.trace(ref)) <= 1e-5 * np.trace(ref)
+
+
+def test_gram_experts_deterministic():
+    say("gram_experts determinism")
+    W = dev(synth.expert_weights(synth.CONFIGS["qwen_gate"], "gate", experts=range(16)), "bf16")
+    a = bm.gram_experts(W).cpu().numpy()
+    b = bm.gram_experts(W).cpu().numpy()
+    assert np.array_equal(a, b)
+
+
+# ------------------------------------------------------------------------- U
+@pytest.mark.parametrize("case", ["planted", "tiny", "qwen_gate"])
+def test_shared_basis(case):
+    say("shared_basis", case)
+    if case == "planted":
+        g = np.random.default_rng(4)
+        Q = np.linalg.qr(g.standard_normal((128, 128)))[0]
+        lam = np.linspace(100.0, 1.0, 128)
+        M = (Q * lam) @ Q.T
+        r = 20
+    elif case == "tiny":
+        W = synth.expert_weights(synth.CONFIGS["tiny"], "gate").astype(np.float64)
+        M = oracle.gram_experts(W)
+        r = 64
+    else:
+        Wb = synth.expert_weights(synth.CONFIGS["qwen_gate"], "gate", experts=range(32))
+        M = oracle.gram_experts(f64(Wb, "bf16"))
+        r = 384
+    Md = torch.from_numpy(M).to(DEV)
+    Ut, ev, ms = bm.shared_basis(Md, r)
+    Ut = Ut.cpu().numpy().astype(np.float64)
+    Uo, evo = oracle.shared_basis(M, r)
+    say("shared_basis", case, "host ms", ms)
+    assert np.allclose(ev, evo, rtol=1e-9, atol=1e-12 * evo[0])
+    U = Ut.T
+    res = np.linalg.norm(M @ U - U * ev) / np.linalg.norm(M)
+    orth = np.abs(Ut @ U - np.eye(r)).max()
+    say("shared_basis", case, "residual", res, "orth", orth)
+    assert res <= 1e-6
+    assert orth <= 1e-6
+    for k in range(r):
+        i = int(np.argmax(np.abs(Ut[k])))
+        assert Ut[k, i] > 0
+    # eigenvectors with a clear gap must agree with the oracle's
+    gaps = np.minimum(np.abs(np.diff(np.r_[np.inf, evo])), np.abs(np.diff(np.r_[evo, -np.inf])))
+    clear = gaps > 1e-6 * evo[0]
+    if case != "qwen_gate":
+        assert clear.sum() > 0
+    for k in np.nonzero(clear)[0]:
+        assert np.abs(Ut[k] - Uo[k]).max() < 1e-5
+
+
+# ------------------------------------------------------------------------- C
+@pytest.mark.parametrize("case", ["tiny_f32", "ragged_bf16", "qwen_gate_bf16"])
+def test_project(case):
+    say("project", case)
+    g = np.random.default_rng(5)
+    if case == "tiny_f32":
+        W = synth.expert_weights(synth.CONFIGS["tiny"], "gate")
+        dt, r = "f32", 64
+    elif case == "ragged_bf16":
+        W = synth.f32_to_bf16_bits(synth.random_rows(3 * 192, 320, seed=6).reshape(3, 192, 320))
+        dt, r = "bf16", 100
+    else:
+        W = synth.expert_weights(synth.CONFIGS["qwen_gate"], "gate")
+        dt, r = "bf16", 384
+    d_out = W.shape[1]
+    Ut = np.linalg.qr(g.standard_normal((d_out, r)))[0].T.astype(np.float32)
+    C = bm.project(dev(Ut, "f32"), dev(W, dt)).cpu().numpy()
+    ref = oracle.project(Ut.astype(np.float64), f64(W, dt))
+    err = relfro(C, ref)
+    say("project", case, "rel fro", err)
+    assert err <= REL
+    # per row as well: every unit's factor row within the bar
+    rows = np.linalg.norm(C - ref, axis=1) / np.linalg.norm(ref, axis=1)
+    assert rows.max() <= REL
+
+
+# ------------------------------------------------------------------------- L
+SCORE_CASES = [
+    # (name, units, d, group, bits, heavy)
+    ("tiny", None, None, None, None, None),
+    ("ragged_units", 257, 256, 64, (1, 2, 3, 4), False),
+    ("ragged_tile_d", 130, 192, 64, (1, 2, 3, 4), True),
+    ("group32_bits8", 70, 256, 32, (1, 2, 3, 4, 8), False),
+    ("group256", 40, 512, 256, (2, 4), True),
+    ("one_width", 33, 128, 128, (3,), False),
+]
+
+
+def _score_inputs(case):
+    name, units, d, group, bits, heavy = case
+    if name == "tiny":
+        cfg = synth.CONFIGS["tiny"]
+        W = synth.expert_weights(cfg, "gate").astype(np.float64)
+        X = synth.calibration_input(cfg, "gate")
+        Ut, _ = oracle.shared_basis(oracle.gram_experts(W), 64)
+        C = oracle.project(Ut, W).astype(np.float32)
+        H = oracle.gram(X.astype(np.float64)).astype(np.float32)
+        return C, H, cfg.group, cfg.bits
+    C = synth.random_rows(units, d, seed=units + d, scale=0.05, heavy=heavy)
+    X = synth.random_rows(2 * d, d, seed=d, scale=1.0, heavy=heavy)
+    X[:, ::17] *= 10.0
+    H = oracle.gram(X.astype(np.float64)).astype(np.float32)
+    return C, H, group, bits
+
+
+@pytest.mark.parametrize("case", SCORE_CASES, ids=lambda c: c[0])
+def test_score(case):
+    say("score", case[0])
+    C, H, group, bits = _score_inputs(case)
+    L = bm.score(dev(C, "f32"), dev(H, "f32"), bits, group).cpu().numpy()
+    ref = oracle.score(C, H.astype(np.float64), bits, group)
+    err = l_rel(L, ref)
+    say("score", case[0], "max rel", err)
+    assert np.all(L >= 0)
+    assert err <= REL
+
+
+def test_score_deterministic_and_degenerate_rows():
+    say("score degenerate")
+    C = synth.random_rows(64, 256, seed=9)
+    C[0] = 0.0                      # all-zero unit: L = 0 at every width
+    C[1] = 0.125                    # constant unit, fp16-exact: L = 0
+    C[2, ::2] = 0.9375              # two-level unit whose range / (2^b - 1) is
+    C[2, 1::2] = 0.0                # fp16-exact at b = 1, 2, 4: reproduced exactly
+    g = np.random.default_rng(1)
+    X = g.standard_normal((300, 256)).astype(np.float32)
+    H = oracle.gram(X.astype(np.float64)).astype(np.float32)
+    Cd, Hd = dev(C, "f32"), dev(H, "f32")
+    a = bm.score(Cd, Hd, [1, 2, 4], 64).cpu().numpy()
+    b = bm.score(Cd, Hd, [1, 2, 4], 64).cpu().numpy()
+    assert np.array_equal(a, b)
+    assert np.all(a[:3] == 0)
+    ref = oracle.score(C, H.astype(np.float64), [1, 2, 4], 64)
+    assert l_rel(a[3:], ref[3:]) <= REL
+
+
+# ---------------------------------------------------------------------- pack
+@pytest.mark.parametrize("group,d,units", [(64, 256, 300), (128, 2048, 97), (32, 192, 65),
+                                           (256, 768, 40)])
+def test_pack_bit_exact(group, d, units):
+    say("pack", group, d, units)
+    g = np.random.default_rng(group + d)
+    C = synth.random_rows(units, d, seed=units, scale=0.04, heavy=True)
+    C[0] = 0.0
+    C[1] = 0.3
+    bits_u = g.choice([1, 2, 3, 4, 8], size=units).astype(np.uint8)
+    off = bm.pack_layout(bits_u, d)
+    bd = torch.from_numpy(bits_u).to(DEV)
+    od = torch.from_numpy(off).to(DEV)
+    codes, params = bm.pack(dev(C, "f32"), bd, od, group, int(off[-1]))
+    rc, rp, roff = oracle.pack(C, bits_u, group)
+    assert np.array_equal(off, roff)
+    assert np.array_equal(codes.cpu().numpy().view(np.uint64), rc)
+    assert np.array_equal(params.cpu().numpy().view(np.uint16), rp)
+    xh = bm.unpack(codes, params, bd, od, units, d, group, int(off[-1])).cpu().numpy()
+    ref = oracle.unpack(rc, rp, bits_u, d, group)
+    assert np.array_equal(xh.astype(np.float64), ref)
+
+
+# -------------------------------------------------------------- end to end
+def _stagewise(proj, sample_rows=None, check_ilp=True):
+    """Run the pipeline and check each stage on the device's own inputs."""
+    W, X = proj.W, proj.X
+    Wd, Xd = dev(W, proj.dtype), dev(X, proj.dtype)
+    res = pipeline.quantize_projection(Wd, Xd, proj.r, proj.bits, proj.group, proj.budget_bits)
+    say("pipeline times", res.times)
+    W64, X64 = f64(W, proj.dtype), f64(X, proj.dtype)
+    # H and M against the oracle from the inputs
+    assert relfro(res.H.cpu().numpy(), oracle.gram(X64)) <= REL
+    M = res.M.cpu().numpy()
+    assert relfro(M, oracle.gram_experts(W64)) <= REL
+    # U: invariants on the device's own M
+    Ut = res.Ut.cpu().numpy().astype(np.float64)
+    U = Ut.T
+    assert np.linalg.norm(M @ U - U * res.eigvals) / np.linalg.norm(M) <= 1e-6
+    # C from the device's U
+    C = res.C.cpu().numpy()
+    Cref = oracle.project(res.Ut.cpu().numpy().astype(np.float64), W64)
+    assert relfro(C, Cref) <= REL
+    # L from the device's C and H
+    H = res.H.cpu().numpy().astype(np.float64)
+    L = res.L.cpu().numpy()
+    rows = np.arange(C.shape[0]) if sample_rows is None else sample_rows
+    Lref = oracle.score_rows(C, H, proj.bits, proj.group, rows=rows)
+    err = l_rel(L[rows], Lref)
+    say("L max rel", err)
+    assert err <= REL
+    # ILP from the device's L: bit-exact
+    if check_ilp:
+        bref, _ = oracle.allocate_dp(L, proj.bits, proj.budget_bits)
+        assert np.array_equal(res.bits_u, bref)
+    # codes and params from the device's C and widths: bit-exact
+    sub = rows[: min(len(rows), 512)]
+    rc, rp, _ = oracle.pack(C[sub], res.bits_u[sub], proj.group)
+    codes = res.codes.cpu().numpy().view(np.uint64)
+    params = res.params.cpu().numpy().view(np.uint16)
+    for i, u in enumerate(sub):
+        o0, o1 = res.offsets[u], res.offsets[u + 1]
+        ro = oracle.pack_layout(res.bits_u[sub], C.shape[1])
+        assert np.array_equal(codes[o0:o1], rc[ro[i]:ro[i + 1]])
+    assert np.array_equal(params[sub], rp)
+    assert int(res.bits_u.astype(np.int64).sum()) <= proj.budget_bits
+    return res
+
+
+def test_end_to_end_tiny():
+    say("end-to-end tiny")
+    proj = synth.make_projection("tiny")
+    a = _stagewise(proj)
+    # determinism of the whole path
+    b = pipeline.quantize_projection(dev(proj.W, "f32"), dev(proj.X, "f32"), proj.r, proj.bits,
+                                     proj.group, proj.budget_bits)
+    assert np.array_equal(a.L.cpu().numpy(), b.L.cpu().numpy())
+    assert np.array_equal(a.bits_u, b.bits_u)
+    assert np.array_equal(a.codes.cpu().numpy(), b.codes.cpu().numpy())
+
+
+def test_end_to_end_qwen_gate_full_size():
+    say("end-to-end qwen gate (E=128, 768x2048, r=384)")
+    proj = synth.make_projection("qwen_gate")
+    g = np.random.default_rng(0)
+    units = proj.E * proj.r
+    rows = np.sort(g.choice(units, size=384, replace=False))
+    _stagewise(proj, sample_rows=rows, check_ilp=True)
