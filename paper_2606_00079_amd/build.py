@@ -75,6 +75,13 @@ def build(verbose: bool = False, jobs: int = 8) -> str:
     tmp = LIB + ".tmp"
     _run([_hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs,
           f"-L{ROCM}/lib", "-lamdhip64", "-ldl"])
+    # A kernel whose host stub was dropped links fine but fails at load time.
+    nm = shutil.which("nm")
+    if nm:
+        undef = _run([nm, "-u", tmp])
+        missing = [l for l in undef.splitlines() if "__device_stub__" in l]
+        if missing:
+            raise RuntimeError("kernel host stubs missing from the library:\n" + "\n".join(missing))
     os.replace(tmp, LIB)
     return LIB
 

@@ -35,6 +35,14 @@ __device__ __forceinline__ double f16_bits_to_f64(uint16_t b) {
   return static_cast<double>(static_cast<float>(__builtin_bit_cast(_Float16, b)));
 }
 
+// Returns v unchanged but opaque to the optimizer: computations that depend
+// on the result cannot be hoisted above this point (used so that epilogue
+// address arithmetic is not moved before a long loop and kept live there).
+__device__ __forceinline__ int opaque(int v) {
+  asm volatile("" : "+v"(v));
+  return v;
+}
+
 template <typename T>
 __device__ __forceinline__ T wave_sum(T v) {
 #pragma unroll

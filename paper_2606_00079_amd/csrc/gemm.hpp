@@ -6,10 +6,19 @@
 // calibration Gram (A = B = X^T), the cross-expert Gram (A = B = the expert
 // rows, k running over experts and input channels), the spectral factors
 // (A = U^T, B = W_e^T) and the loss table (A = off-diagonal H, B = error
-// rows).  The engine takes a workgroup tile of BM x BN outputs, 4 waves of
-// 64 lanes, stages K in steps of 32 through double-buffered LDS and issues
-// v_mfma_f32_32x32x16_bf16.  What happens to the fp32 accumulators is left to
-// an epilogue functor.
+// rows).  What happens to the fp32 accumulators is left to an epilogue
+// functor.
+//
+// Kernel shape: a BM x BN workgroup tile, 4 waves of 64 lanes in a 2 x 2
+// grid, each wave owning a (BM/2) x (BN/2) block of v_mfma_f32_32x32x16_bf16
+// accumulators.  K advances 32 at a time through four LDS stages filled by
+// direct global->LDS loads (global_load_lds_dwordx4), so three stages are in
+// flight while one is multiplied; the stages are distinct LDS arrays and the
+// K loop is unrolled by four, which lets the compiler see that reading one
+// stage does not wait for the loads into the others.  LDS rows are 64 bytes
+// and the four 16-byte chunks of row r are stored XOR-swizzled by
+// (r / 4) mod 4, so the fragment reads of the matrix-core operands are free
+// of bank conflicts.
 //
 // The K index is a flattened (pass, segment, k) triple:
 //   * passes   let one launch add up to 4 products A_p B_p^T into the same
@@ -18,16 +27,28 @@
 //              stride apart in memory (the experts of W for M = sum W_e W_e^T).
 // gridDim.y splits K (split-K); gridDim.z is a batch index with its own
 // operand strides.
+//
+// Tile order.  Workgroups are dispatched round-robin over the 8 XCDs, each
+// with its own L2.  The linear workgroup id is first remapped so that every
+// XCD receives a contiguous range of logical ids, and logical ids walk the
+// tiles in groups of `group_n` column tiles, rows fastest: the workgroups
+// resident on one XCD then share both their A row-slabs and B column-slabs
+// through that XCD's L2.
 #pragma once
+
+#include <type_traits>
 
 #include "common.hpp"
 
 namespace bitsmoe {
 namespace gemm {
 
-constexpr int BK = 32;             // K elements per LDS stage
-constexpr int LDK = BK + 8;        // padded LDS row (80 bytes: conflict-free 16-byte reads)
+constexpr int BK = 32;             // K elements per LDS stage (one 64-byte row)
+constexpr int KC = BK / 8;         // 16-byte chunks per LDS row
+constexpr int RPB = 512 / BK;      // rows per 1 KiB block (one wave-wide direct load)
+constexpr int kStages = 4;         // LDS stages; kStages - 1 are in flight
 constexpr int kThreads = 256;
+constexpr int kXcds = 8;
 
 struct Side {
   const uint16_t* pass[4];  // base pointer of each pass
@@ -46,21 +67,35 @@ struct Problem {
   int splits;        // gridDim.y
   int tiles_m, tiles_n;
   int symmetric;     // 1: only tiles with tm <= tn are launched (gridDim.x = T(T+1)/2)
+  int group_n;       // column tiles per ordering group (non-symmetric)
 };
 
-__device__ __forceinline__ void tile_coords(const Problem& p, int t, int* tm, int* tn) {
-  if (!p.symmetric) {
-    *tm = t / p.tiles_n;
-    *tn = t % p.tiles_n;
+// XCD-contiguous logical id of the linear workgroup id t (of n in total).
+__device__ __forceinline__ int xcd_remap(int t, int n) {
+  const int x = t % kXcds, i = t / kXcds;
+  const int q = n / kXcds, rem = n % kXcds;
+  return (x < rem) ? x * (q + 1) + i : rem * (q + 1) + (x - rem) * q + i;
+}
+
+__device__ __forceinline__ void tile_coords(const Problem& p, int t, int n, int* tm, int* tn) {
+  t = xcd_remap(t, n);
+  if (p.symmetric) {
+    int r = 0;
+    while (t >= p.tiles_m - r) {
+      t -= p.tiles_m - r;
+      ++r;
+    }
+    *tm = r;
+    *tn = r + t;
     return;
   }
-  int r = 0;
-  while (t >= p.tiles_m - r) {
-    t -= p.tiles_m - r;
-    ++r;
-  }
-  *tm = r;
-  *tn = r + t;
+  const int per_group = p.group_n * p.tiles_m;
+  const int g = t / per_group, w = t - g * per_group;
+  const int first_n = g * p.group_n;
+  // the grid holds tiles_m * tiles_n workgroups, so the last (possibly
+  // narrower) group still has w / tiles_m < its width
+  *tm = w % p.tiles_m;
+  *tn = first_n + w / p.tiles_m;
 }
 
 __device__ __forceinline__ const uint16_t* pass_ptr(const Side& s, int pass) {
@@ -72,23 +107,92 @@ __device__ __forceinline__ const uint16_t* pass_ptr(const Side& s, int pass) {
   }
 }
 
-// Address of element (row, k0) of K tile `kt` for operand side `s`.
-__device__ __forceinline__ const uint16_t* tile_ptr(const Problem& p, const Side& s, int64_t kt,
-                                                    int64_t row, int64_t z) {
-  const int64_t tiles_seg = p.kseg / BK;
-  const int64_t per_pass = static_cast<int64_t>(p.segs) * tiles_seg;
-  const int pass = static_cast<int>(kt / per_pass);
-  const int64_t rem = kt - static_cast<int64_t>(pass) * per_pass;
-  const int64_t seg = rem / tiles_seg;
-  const int64_t k0 = (rem - seg * tiles_seg) * BK;
-  return pass_ptr(s, pass) + z * s.bstride + seg * s.estride + row * s.ld + k0;
+// Position of a K tile in the flattened (pass, segment, k) index.  Advanced
+// incrementally inside the K loop so that no division runs there.
+struct KPos {
+  int pass;
+  int64_t seg, k0;
+  __device__ __forceinline__ void init(const Problem& p, int64_t kt) {
+    const int64_t tiles_seg = p.kseg / BK;
+    const int64_t per_pass = static_cast<int64_t>(p.segs) * tiles_seg;
+    pass = static_cast<int>(kt / per_pass);
+    const int64_t rem = kt - static_cast<int64_t>(pass) * per_pass;
+    seg = rem / tiles_seg;
+    k0 = (rem - seg * tiles_seg) * BK;
+  }
+  __device__ __forceinline__ void next(const Problem& p) {
+    k0 += BK;
+    if (k0 == p.kseg) {
+      k0 = 0;
+      if (++seg == p.segs) {
+        seg = 0;
+        ++pass;
+      }
+    }
+  }
+  // first element of this K tile in row 0 of batch z for side s
+  __device__ __forceinline__ const uint16_t* base(const Side& s, int64_t z) const {
+    return pass_ptr(s, pass) + z * s.bstride + seg * s.estride + k0;
+  }
+};
+
+// One wave-wide direct global->LDS load of 16 bytes per lane: lane l reads
+// base + voff_l bytes and its 16 bytes land at LDS byte address lds + 16 l.
+// `base` and `lds` are wave-uniform.  Issued through inline assembly so that
+// the compiler neither tracks the LDS write nor inserts waits for it: every
+// caller waits explicitly (s_waitcnt vmcnt) and synchronizes the workgroup
+// before the data is read.  M0 carries the LDS address; nothing else in the
+// kernels that use this helper uses M0.
+__device__ __forceinline__ void dma16(const void* base, uint32_t voff, const void* lds) {
+  const uint32_t l = __builtin_amdgcn_readfirstlane(
+      static_cast<uint32_t>(reinterpret_cast<uintptr_t>(lds)));
+  // readfirstlane returns a signed int: both halves are zero-extended
+  // explicitly, or a low word with bit 31 set would smear into the high word.
+  const uint64_t b = reinterpret_cast<uint64_t>(base);
+  const uint32_t hi = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<uint32_t>(b >> 32)));
+  const uint32_t lo = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<uint32_t>(b)));
+  const uint64_t bu = (static_cast<uint64_t>(hi) << 32) | static_cast<uint64_t>(lo);
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1"
+               :
+               : "v"(voff), "s"(bu), "s"(l)
+               : "memory");
 }
 
+// Swizzle: the LDS serves a 16-byte read for 16 lanes per cycle out of 64
+// four-byte banks (256 bytes, four 64-byte rows), so chunk j of row r is
+// stored in slot j ^ ((r / 4) mod 4): sixteen consecutive rows read at the
+// same chunk then cover all 64 banks once.
+__device__ __forceinline__ int swz(int r, int j) { return j ^ ((r >> 2) & 3); }
+// LDS element offset of chunk j (8 bf16) of row r.
+__device__ __forceinline__ int lds_off(int r, int j) { return r * BK + (swz(r, j) << 3); }
+
+// s_waitcnt on the vector-memory counter only (expcnt and lgkmcnt left at
+// their maxima), in the gfx9 encoding: vmcnt[3:0] in bits 3:0, vmcnt[5:4] in
+// bits 15:14.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// The K-loop stage buffers, free once the loop is done; epilogues may use
+// them as scratch: kStages A buffers then kStages B buffers.
+struct StageLds {
+  uint16_t* a;        // A stage buffers, a_elems bf16 each, contiguous
+  uint16_t* b;        // B stage buffers, b_elems bf16 each, contiguous
+  int a_elems, b_elems;
+  // buffer k of the 2 * kStages (arithmetic, so no indexed pointer table)
+  __device__ __forceinline__ uint16_t* buf(int k) const {
+    return k < kStages ? a + k * a_elems : b + (k - kStages) * b_elems;
+  }
+};
+
 // Accumulator fragment bookkeeping handed to epilogues.
-template <int BM, int BN, int WM, int WN>
+template <int BM, int BN>
 struct Frag {
-  static constexpr int FM = BM / WM / 32;
-  static constexpr int FN = BN / WN / 32;
+  static constexpr int WM = BM / 2, WN = BN / 2;
+  static constexpr int FM = WM / 32;
+  static constexpr int FN = WN / 32;
   f32x16 acc[FM][FN];
   int tm, tn;        // tile coordinates
   int row0, col0;    // first row / column of this wave's sub-tile (global)
@@ -103,29 +207,33 @@ struct Frag {
   __device__ __forceinline__ int col(int ni) const { return col0 + 32 * ni + (lane & 31); }
 };
 
-template <int BM, int BN, int WM, int WN, class Epi>
-__global__ __launch_bounds__(kThreads) void gemm_nt_kernel(Problem p, Epi epi) {
-  static_assert(WM * WN == 4, "four waves");
-  static_assert(BM % (32 * WM) == 0 && BN % (32 * WN) == 0, "wave tile");
-  constexpr int ACH = BM * BK / 8 / kThreads;  // 16-byte chunks per thread
-  constexpr int BCH = BN * BK / 8 / kThreads;
-  static_assert(ACH >= 1 && BCH >= 1, "tile too small");
-  using F = Frag<BM, BN, WM, WN>;
+template <int BM, int BN, class Epi>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
+void gemm_nt_kernel(Problem p, Epi epi) {
+  static_assert(BM % 64 == 0 && BN % 64 == 0, "tile");
+  constexpr int AW = BM / RPB / 4;  // direct 1 KiB loads per wave per stage
+  constexpr int BW = BN / RPB / 4;
+  constexpr int LPS = AW + BW;      // vector-memory instructions per wave per stage
+  constexpr int ASZ = BM * BK, BSZ = BN * BK;  // elements per stage
+  static_assert(AW >= 1 && BW >= 1, "tile too small");
+  static_assert(kStages == 4, "the K loop below is unrolled for four stages");
+  using F = Frag<BM, BN>;
 
-  __shared__ __align__(16) uint16_t As[2][BM * LDK];
-  __shared__ __align__(16) uint16_t Bs[2][BN * LDK];
+  __shared__ __align__(1024) uint16_t As[kStages * ASZ];
+  __shared__ __align__(1024) uint16_t Bs[kStages * BSZ];
 
   const int tid = threadIdx.x;
   F f;
   f.lane = tid & 63;
-  f.wave = tid >> 6;
-  f.wm = f.wave / WN;
-  f.wn = f.wave % WN;
-  tile_coords(p, blockIdx.x, &f.tm, &f.tn);
+  // wave-uniform: keeps everything derived from it in scalar registers
+  f.wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  f.wm = f.wave >> 1;
+  f.wn = f.wave & 1;
+  tile_coords(p, blockIdx.x, gridDim.x, &f.tm, &f.tn);
   f.ks = blockIdx.y;
   f.z = blockIdx.z;
-  f.row0 = f.tm * BM + f.wm * (BM / WM);
-  f.col0 = f.tn * BN + f.wn * (BN / WN);
+  f.row0 = f.tm * BM + f.wm * F::WM;
+  f.col0 = f.tn * BN + f.wn * F::WN;
 #pragma unroll
   for (int mi = 0; mi < F::FM; ++mi)
 #pragma unroll
@@ -136,71 +244,115 @@ __global__ __launch_bounds__(kThreads) void gemm_nt_kernel(Problem p, Epi epi) {
   const int64_t kt0 = p.ktiles * f.ks / p.splits;
   const int64_t kt1 = p.ktiles * (f.ks + 1) / p.splits;
 
-  uint4 ra[ACH], rb[BCH];
-  auto load = [&](int64_t kt) {
+  // Direct global->LDS loads.  Wave instruction i of this wave fills the
+  // 1 KiB LDS block b = wave + 4 i (rows b*RPB .. b*RPB+RPB-1); lane l lands
+  // at byte 16 l of the block, i.e. row b*RPB + l/KC, slot l%KC, so it fetches
+  // the global chunk that the swizzle stores in that slot.  Rows past the end
+  // are clamped to the last row: their accumulators are never stored.
+  const int64_t a_row0 = static_cast<int64_t>(f.tm) * BM;
+  const int64_t b_row0 = static_cast<int64_t>(f.tn) * BN;
+  uint32_t oa[AW], ob[BW];  // byte offsets from the tile's first row
 #pragma unroll
-    for (int i = 0; i < ACH; ++i) {
-      const int c = tid + kThreads * i;
-      const int r = c >> 2, k8 = (c & 3) * 8;
-      const int64_t gr = static_cast<int64_t>(f.tm) * BM + r;
-      ra[i] = (gr < p.a.rows) ? *reinterpret_cast<const uint4*>(tile_ptr(p, p.a, kt, gr, f.z) + k8)
-                              : make_uint4(0, 0, 0, 0);
-    }
+  for (int i = 0; i < AW; ++i) {
+    const int r = (f.wave + 4 * i) * RPB + f.lane / KC;
+    const int j = swz(r, f.lane % KC);
+    const int64_t gr = (a_row0 + r < p.a.rows) ? a_row0 + r : p.a.rows - 1;
+    oa[i] = static_cast<uint32_t>(((gr - a_row0) * p.a.ld + 8 * j) * 2);
+  }
 #pragma unroll
-    for (int i = 0; i < BCH; ++i) {
-      const int c = tid + kThreads * i;
-      const int r = c >> 2, k8 = (c & 3) * 8;
-      const int64_t gr = static_cast<int64_t>(f.tn) * BN + r;
-      rb[i] = (gr < p.b.rows) ? *reinterpret_cast<const uint4*>(tile_ptr(p, p.b, kt, gr, f.z) + k8)
-                              : make_uint4(0, 0, 0, 0);
-    }
-  };
-  auto store = [&](int buf) {
+  for (int i = 0; i < BW; ++i) {
+    const int r = (f.wave + 4 * i) * RPB + f.lane / KC;
+    const int j = swz(r, f.lane % KC);
+    const int64_t gr = (b_row0 + r < p.b.rows) ? b_row0 + r : p.b.rows - 1;
+    ob[i] = static_cast<uint32_t>(((gr - b_row0) * p.b.ld + 8 * j) * 2);
+  }
+  KPos kp;
+  auto issue = [&](int s) {
+    const uint16_t* pa = kp.base(p.a, f.z) + a_row0 * p.a.ld;
+    const uint16_t* pb = kp.base(p.b, f.z) + b_row0 * p.b.ld;
 #pragma unroll
-    for (int i = 0; i < ACH; ++i) {
-      const int c = tid + kThreads * i;
-      *reinterpret_cast<uint4*>(&As[buf][(c >> 2) * LDK + (c & 3) * 8]) = ra[i];
-    }
+    for (int i = 0; i < AW; ++i) dma16(pa, oa[i], As + s * ASZ + (f.wave + 4 * i) * (RPB * BK));
 #pragma unroll
-    for (int i = 0; i < BCH; ++i) {
-      const int c = tid + kThreads * i;
-      *reinterpret_cast<uint4*>(&Bs[buf][(c >> 2) * LDK + (c & 3) * 8]) = rb[i];
-    }
+    for (int i = 0; i < BW; ++i) dma16(pb, ob[i], Bs + s * BSZ + (f.wave + 4 * i) * (RPB * BK));
+    kp.next(p);
   };
 
-  if (kt0 < kt1) {
-    load(kt0);
-    store(0);
-    __syncthreads();
-    int buf = 0;
-    const int arow = f.wm * (BM / WM) + (f.lane & 31);
-    const int brow = f.wn * (BN / WN) + (f.lane & 31);
-    const int kq = 8 * (f.lane >> 5);
-    for (int64_t kt = kt0; kt < kt1; ++kt) {
-      const bool more = kt + 1 < kt1;
-      if (more) load(kt + 1);
+  const int arow = f.wm * F::WM + (f.lane & 31);
+  const int brow = f.wn * F::WN + (f.lane & 31);
+  const int jq = f.lane >> 5;
+  // one K=16 step: operand fragments from LDS, then FM x FN matrix-core ops
+  auto kstep = [&](const uint16_t* la, const uint16_t* lb, int kk) {
+    const int j = 2 * kk + jq;
+    bf16x8 fa[F::FM], fb[F::FN];
 #pragma unroll
-      for (int kk = 0; kk < BK; kk += 16) {
-        bf16x8 af[F::FM], bfr[F::FN];
+    for (int mi = 0; mi < F::FM; ++mi)
+      fa[mi] = *reinterpret_cast<const bf16x8*>(&la[lds_off(arow + 32 * mi, j)]);
 #pragma unroll
-        for (int mi = 0; mi < F::FM; ++mi)
-          af[mi] = *reinterpret_cast<const bf16x8*>(&As[buf][(arow + 32 * mi) * LDK + kk + kq]);
+    for (int ni = 0; ni < F::FN; ++ni)
+      fb[ni] = *reinterpret_cast<const bf16x8*>(&lb[lds_off(brow + 32 * ni, j)]);
 #pragma unroll
-        for (int ni = 0; ni < F::FN; ++ni)
-          bfr[ni] = *reinterpret_cast<const bf16x8*>(&Bs[buf][(brow + 32 * ni) * LDK + kk + kq]);
+    for (int mi = 0; mi < F::FM; ++mi)
 #pragma unroll
-        for (int mi = 0; mi < F::FM; ++mi)
+      for (int ni = 0; ni < F::FN; ++ni)
+        f.acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[mi], fb[ni], f.acc[mi][ni], 0, 0, 0);
+  };
+
+  const int64_t nk = kt1 - kt0;
+  int64_t issued = 0;
+  // One K stage: wait until stage i has landed in every wave (the stages
+  // issued after it may stay in flight), refill the buffer freed by stage
+  // i - 1, and multiply stage i.
+  auto step = [&](auto s, int64_t i) {
+    constexpr int S = decltype(s)::value;
+    const int64_t after = issued - 1 - i;  // stages in flight behind stage i
+    if (after >= 2)
+      wait_vmcnt<2 * LPS>();
+    else if (after == 1)
+      wait_vmcnt<LPS>();
+    else
+      wait_vmcnt<0>();
+    // Bare barrier: __syncthreads() would also wait for every load in flight.
+    // This wave's part of stage i has landed (the wait above), and the LDS
+    // reads of stage i - 1 were consumed by its matrix-core instructions.
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+    if (issued < nk) {
+      issue((S + kStages - 1) % kStages);
+      ++issued;
+    }
 #pragma unroll
-          for (int ni = 0; ni < F::FN; ++ni)
-            f.acc[mi][ni] =
-                __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[mi], bfr[ni], f.acc[mi][ni], 0, 0, 0);
-      }
-      if (more) store(buf ^ 1);
-      __syncthreads();
-      buf ^= 1;
+    for (int kk = 0; kk < BK / 16; ++kk) kstep(As + S * ASZ, Bs + S * BSZ, kk);
+  };
+
+  if (nk > 0) {
+    kp.init(p, kt0);
+    for (int s = 0; s < kStages - 1 && issued < nk; ++s) {
+      issue(s);
+      ++issued;
+    }
+    for (int64_t it = 0; it < nk; it += kStages) {
+      step(std::integral_constant<int, 0>(), it);
+      if (it + 1 < nk) step(std::integral_constant<int, 1>(), it + 1);
+      if (it + 2 < nk) step(std::integral_constant<int, 2>(), it + 2);
+      if (it + 3 < nk) step(std::integral_constant<int, 3>(), it + 3);
     }
   }
-  epi(f);
+  // Pin the accumulators to AGPRs across the loop: otherwise an epilogue
+  // that feeds them to VALU instructions can pull part of them into VGPRs,
+  // which the loop then runs out of.
+#pragma unroll
+  for (int mi = 0; mi < F::FM; ++mi)
+#pragma unroll
+    for (int ni = 0; ni < F::FN; ++ni) asm volatile("" : "+a"(f.acc[mi][ni]));
+  wait_vmcnt<0>();
+  __syncthreads();  // epilogues may reuse the stage buffers
+  StageLds lds;
+  lds.a = As;
+  lds.b = Bs;
+  lds.a_elems = ASZ;
+  lds.b_elems = BSZ;
+  epi(f, lds);
 }
 
 }  // namespace gemm

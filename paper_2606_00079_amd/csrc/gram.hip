@@ -12,7 +12,7 @@
 namespace bitsmoe {
 namespace {
 
-constexpr int GT = 128;  // tile edge of the symmetric GEMMs
+constexpr int GT = 256;  // tile edge of the symmetric GEMMs
 using gemm::BK;
 
 // X [n][d] -> Xt [d][npad] (bf16), rows beyond n zero.  For fp32 input the
@@ -68,7 +68,7 @@ struct PartialStore {
   int64_t ntiles;     // tiles in the upper triangle
   int ntiles_side;    // tiles per side
   template <class F>
-  __device__ void operator()(F& f) const {
+  __device__ void operator()(F& f, const gemm::StageLds&) const {
     const int64_t t = (static_cast<int64_t>(f.tm) * (2 * ntiles_side - f.tm + 1)) / 2 + (f.tn - f.tm);
     float* base = part + (static_cast<int64_t>(f.ks) * ntiles + t) * GT * GT;
 #pragma unroll
@@ -128,7 +128,7 @@ bitsmoe_status run_symmetric(gemm::Problem p, int64_t d, double scale, OutT* out
   dim3 grid(static_cast<unsigned>(ntiles), static_cast<unsigned>(splits), 1);
   {
     KernelTimer timer(name, stream);
-    hipLaunchKernelGGL((gemm::gemm_nt_kernel<GT, GT, 2, 2, PartialStore>), grid,
+    hipLaunchKernelGGL((gemm::gemm_nt_kernel<GT, GT, PartialStore>), grid,
                        dim3(gemm::kThreads), 0, s, p, epi);
   }
   BITSMOE_LAUNCH_CHECK("gram: gemm launch");
@@ -151,7 +151,7 @@ extern "C" bitsmoe_status bitsmoe_gram(const void* X_dev, bitsmoe_dtype xt, int6
   if (xt != BITSMOE_F32 && xt != BITSMOE_BF16) return fail(BITSMOE_ERR_DTYPE, "gram: dtype");
   if (d % 64 != 0) return fail(BITSMOE_ERR_SHAPE, "gram: d must be a multiple of 64");
   hipStream_t s = static_cast<hipStream_t>(stream);
-  const int64_t npad = (n + BK - 1) / BK * BK;
+  const int64_t npad = (n + BK - 1) / BK * BK;  // K padded with zero rows to the K step
   const bool f32 = xt == BITSMOE_F32;
   bitsmoe_status st;
   uint16_t* hi = static_cast<uint16_t*>(scratch(kScratchA, d * npad * 2, stream, &st));

@@ -12,7 +12,8 @@
 namespace bitsmoe {
 namespace {
 
-constexpr int PT = 128;
+constexpr int PM = 128;  // basis-vector tile
+constexpr int PN = 256;  // input-channel tile
 using gemm::BK;
 
 // fp32 -> (hi, lo) bf16, same layout.
@@ -68,7 +69,7 @@ struct FactorStore {
   float* C;
   int64_t r, d_in;
   template <class F>
-  __device__ void operator()(F& f) const {
+  __device__ void operator()(F& f, const gemm::StageLds&) const {
     float* base = C + f.z * r * d_in;
 #pragma unroll
     for (int mi = 0; mi < F::FM; ++mi)
@@ -147,14 +148,15 @@ extern "C" bitsmoe_status bitsmoe_project(const float* Ut_dev, const void* W_dev
   }
   p.ktiles = static_cast<int64_t>(p.passes) * d_out / BK;
   p.splits = 1;
-  p.tiles_m = static_cast<int>((r + PT - 1) / PT);
-  p.tiles_n = static_cast<int>((d_in + PT - 1) / PT);
+  p.tiles_m = static_cast<int>((r + PM - 1) / PM);
+  p.tiles_n = static_cast<int>((d_in + PN - 1) / PN);
   p.symmetric = 0;
+  p.group_n = p.tiles_n;
   FactorStore epi{C_dev, r, d_in};
   dim3 grid(static_cast<unsigned>(p.tiles_m * p.tiles_n), 1, static_cast<unsigned>(E));
   {
     KernelTimer timer("project", stream);
-    hipLaunchKernelGGL((gemm::gemm_nt_kernel<PT, PT, 2, 2, FactorStore>), grid,
+    hipLaunchKernelGGL((gemm::gemm_nt_kernel<PM, PN, FactorStore>), grid,
                        dim3(gemm::kThreads), 0, s, p, epi);
   }
   BITSMOE_LAUNCH_CHECK("project: gemm launch");

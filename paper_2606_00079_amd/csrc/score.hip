@@ -25,8 +25,8 @@
 namespace bitsmoe {
 namespace {
 
-constexpr int SBM = 128;  // i (H row) tile
-constexpr int SBN = 128;  // D row tile
+constexpr int SBM = 256;  // i (H row) tile
+constexpr int SBN = 256;  // D row tile
 using gemm::BK;
 
 __global__ __launch_bounds__(256) void hoff_kernel(const float* __restrict__ H, int64_t d,
@@ -141,46 +141,74 @@ __global__ __launch_bounds__(256) void dgen_kernel(const float* __restrict__ C, 
 }
 
 // part[row][tm] = sum over this tile's i of D[row][i] * acc[i][row].
+//
+// The tile's 256 x 256 block of D (rows tn*256.., columns tm*256..) is first
+// brought into the free stage buffers by direct global->LDS loads: 512 bytes
+// per row, 32 rows per 16 KiB buffer, the 16-byte chunk c of row j stored in
+// slot c ^ (j mod 32) so that 32 lanes reading 32 rows at one chunk spread
+// over the banks.  Each lane then reads its D values (one row per column
+// fragment, four 8-byte runs per row fragment) from LDS.  Rows and columns
+// past the end are clamped on load and weighted by zero.
 struct RowDot {
   const uint16_t* D;
   float* part;
   int64_t R, d;
   int tiles_m;
   template <class F>
-  __device__ void operator()(F& f) const {
+  __device__ void operator()(F& f, const gemm::StageLds& lds) const {
+    static_assert(SBM == 256 && SBN == 256, "layout below assumes 256 x 256 tiles");
     __shared__ float red[2][SBN];
+    const int lane = opaque(f.lane);
+    const int wave = lane >= 0 ? f.wave : 0;  // ties wave to the opaque lane
+    const int64_t i_base = static_cast<int64_t>(f.tm) * SBM;
+    const int64_t j_base = static_cast<int64_t>(f.tn) * SBN;
+    // 1 KiB block b holds rows 2b, 2b+1; wave w loads blocks w, w+4, ...
+#pragma unroll 4
+    for (int b = wave; b < 128; b += 4) {
+      const int j = 2 * b + (lane >> 5);
+      const int c = (lane & 31) ^ (j & 31);
+      // uniform base row of this block; the lane's row is it or the next one
+      const int64_t row0 = min(j_base + 2 * b, R - 1);
+      const int64_t row = min(j_base + j, R - 1);
+      const int64_t col = min(i_base + 8 * c, d - 8);
+      uint16_t* dst = lds.buf(b >> 4) + (b & 15) * 512;
+      gemm::dma16(D + row0 * d, static_cast<uint32_t>(((row - row0) * d + col) * 2), dst);
+    }
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
     float s[F::FN];
 #pragma unroll
     for (int ni = 0; ni < F::FN; ++ni) {
-      s[ni] = 0.0f;
-      const int64_t row = f.col(ni);
-      if (row < R) {
-        const uint16_t* drow = D + row * d;
+      // one column fragment at a time: keeps the LDS reads from being hoisted
+      // next to all 256 accumulators
+      __builtin_amdgcn_sched_barrier(0);
+      const int jl = f.wn * F::WN + 32 * ni + (lane & 31);
+      const uint16_t* rowp = lds.buf(jl >> 5) + (jl & 31) * 256;
+      float acc = 0.0f;
 #pragma unroll
-        for (int mi = 0; mi < F::FM; ++mi)
+      for (int mi = 0; mi < F::FM; ++mi)
 #pragma unroll
-          for (int g = 0; g < 4; ++g) {
-            const int i = f.row(mi, 4 * g);
-            if (i < d) {
-              const uint2 v = *reinterpret_cast<const uint2*>(drow + i);
-              s[ni] += bf16_to_f32(static_cast<uint16_t>(v.x & 0xffff)) * f.acc[mi][ni][4 * g + 0] +
-                       bf16_to_f32(static_cast<uint16_t>(v.x >> 16)) * f.acc[mi][ni][4 * g + 1] +
-                       bf16_to_f32(static_cast<uint16_t>(v.y & 0xffff)) * f.acc[mi][ni][4 * g + 2] +
-                       bf16_to_f32(static_cast<uint16_t>(v.y >> 16)) * f.acc[mi][ni][4 * g + 3];
-            }
-          }
-      }
-      s[ni] += __shfl_xor(s[ni], 32, 64);
+        for (int g = 0; g < 4; ++g) {
+          const int il = f.wm * F::WM + 32 * mi + 8 * g;      // first i of the chunk
+          const int c = il >> 3;
+          const uint2 v = *reinterpret_cast<const uint2*>(rowp + ((c ^ (jl & 31)) << 3) +
+                                                          4 * (lane >> 5));
+          const float w = (i_base + il + 4 * (lane >> 5) < d) ? 1.0f : 0.0f;
+          acc += w * (bf16_to_f32(static_cast<uint16_t>(v.x & 0xffff)) * f.acc[mi][ni][4 * g + 0] +
+                      bf16_to_f32(static_cast<uint16_t>(v.x >> 16)) * f.acc[mi][ni][4 * g + 1] +
+                      bf16_to_f32(static_cast<uint16_t>(v.y & 0xffff)) * f.acc[mi][ni][4 * g + 2] +
+                      bf16_to_f32(static_cast<uint16_t>(v.y >> 16)) * f.acc[mi][ni][4 * g + 3]);
+        }
+      s[ni] = acc + __shfl_xor(acc, 32, 64);
     }
     // combine the waves that share these rows (wm = 0, 1)
-    if ((f.lane >> 5) == 0) {
+    if ((lane >> 5) == 0) {
 #pragma unroll
-      for (int ni = 0; ni < F::FN; ++ni) red[f.wm][f.wn * (SBN / 2) + 32 * ni + f.lane] = s[ni];
+      for (int ni = 0; ni < F::FN; ++ni) red[f.wm][f.wn * F::WN + 32 * ni + lane] = s[ni];
     }
     __syncthreads();
-    const int t = threadIdx.x;
-    if (t < SBN) {
-      const int64_t row = static_cast<int64_t>(f.tn) * SBN + t;
+    for (int t = threadIdx.x; t < SBN; t += gemm::kThreads) {
+      const int64_t row = j_base + t;
       if (row < R) part[row * tiles_m + f.tm] = red[0][t] + red[1][t];
     }
   }
@@ -272,11 +300,12 @@ extern "C" bitsmoe_status bitsmoe_score(const float* C_dev, int64_t units, int64
   p.tiles_m = tiles_m;
   p.tiles_n = static_cast<int>(tiles_n);
   p.symmetric = 0;
+  p.group_n = std::max(1, 32 / tiles_m);  // ~one XCD's worth of workgroups per group
   RowDot epi{D, part, R, d, tiles_m};
   dim3 grid(static_cast<unsigned>(tiles_m * tiles_n), 1, 1);
   {
     KernelTimer timer("score_gemm", stream);
-    hipLaunchKernelGGL((gemm::gemm_nt_kernel<SBM, SBN, 2, 2, RowDot>), grid, dim3(gemm::kThreads),
+    hipLaunchKernelGGL((gemm::gemm_nt_kernel<SBM, SBN, RowDot>), grid, dim3(gemm::kThreads),
                        0, s, p, epi);
   }
   BITSMOE_LAUNCH_CHECK("score: gemm launch");
