@@ -43,11 +43,24 @@
 namespace bitsmoe {
 namespace gemm {
 
-constexpr int BK = 32;             // K elements per LDS stage (one 64-byte row)
-constexpr int KC = BK / 8;         // 16-byte chunks per LDS row
-constexpr int RPB = 512 / BK;      // rows per 1 KiB block (one wave-wide direct load)
-constexpr int kStages = 4;         // LDS stages; kStages - 1 are in flight
+constexpr int BK = 32;             // unit in which Problem::ktiles counts K
+constexpr int kKAlign = 64;        // every K segment (Problem::kseg) is a multiple of this
 constexpr int kThreads = 256;
+
+// Compile-time loop: calls f(std::integral_constant<int, I>) for I = 0..N-1.
+template <int I, int N>
+struct StaticFor {
+  template <class Fn>
+  __device__ __forceinline__ static void run(Fn&& fn) {
+    fn(std::integral_constant<int, I>());
+    StaticFor<I + 1, N>::run(fn);
+  }
+};
+template <int N>
+struct StaticFor<N, N> {
+  template <class Fn>
+  __device__ __forceinline__ static void run(Fn&&) {}
+};
 constexpr int kXcds = 8;
 
 struct Side {
@@ -109,19 +122,20 @@ __device__ __forceinline__ const uint16_t* pass_ptr(const Side& s, int pass) {
 
 // Position of a K tile in the flattened (pass, segment, k) index.  Advanced
 // incrementally inside the K loop so that no division runs there.
+template <int KB>
 struct KPos {
   int pass;
   int64_t seg, k0;
   __device__ __forceinline__ void init(const Problem& p, int64_t kt) {
-    const int64_t tiles_seg = p.kseg / BK;
+    const int64_t tiles_seg = p.kseg / KB;
     const int64_t per_pass = static_cast<int64_t>(p.segs) * tiles_seg;
     pass = static_cast<int>(kt / per_pass);
     const int64_t rem = kt - static_cast<int64_t>(pass) * per_pass;
     seg = rem / tiles_seg;
-    k0 = (rem - seg * tiles_seg) * BK;
+    k0 = (rem - seg * tiles_seg) * KB;
   }
   __device__ __forceinline__ void next(const Problem& p) {
-    k0 += BK;
+    k0 += KB;
     if (k0 == p.kseg) {
       k0 = 0;
       if (++seg == p.segs) {
@@ -159,12 +173,18 @@ __device__ __forceinline__ void dma16(const void* base, uint32_t voff, const voi
 }
 
 // Swizzle: the LDS serves a 16-byte read for 16 lanes per cycle out of 64
-// four-byte banks (256 bytes, four 64-byte rows), so chunk j of row r is
-// stored in slot j ^ ((r / 4) mod 4): sixteen consecutive rows read at the
-// same chunk then cover all 64 banks once.
-__device__ __forceinline__ int swz(int r, int j) { return j ^ ((r >> 2) & 3); }
+// four-byte banks (256 bytes), so with KB-element rows (KB/8 chunks) chunk j
+// of row r is stored in slot j ^ ((r / (16 / (KB/8))) mod (KB/8)): sixteen
+// consecutive rows read at the same chunk then cover all 64 banks once
+// (KB = 64: key (r/2) mod 8; KB = 32: key (r/4) mod 4).
+template <int KB>
+__device__ __forceinline__ int swz(int r, int j) {
+  constexpr int KC = KB / 8;
+  return j ^ ((r / (16 / KC)) & (KC - 1));
+}
 // LDS element offset of chunk j (8 bf16) of row r.
-__device__ __forceinline__ int lds_off(int r, int j) { return r * BK + (swz(r, j) << 3); }
+template <int KB>
+__device__ __forceinline__ int lds_off(int r, int j) { return r * KB + (swz<KB>(r, j) << 3); }
 
 // s_waitcnt on the vector-memory counter only (expcnt and lgkmcnt left at
 // their maxima), in the gfx9 encoding: vmcnt[3:0] in bits 3:0, vmcnt[5:4] in
@@ -178,12 +198,13 @@ __device__ __forceinline__ void wait_vmcnt() {
 // The K-loop stage buffers, free once the loop is done; epilogues may use
 // them as scratch: kStages A buffers then kStages B buffers.
 struct StageLds {
-  uint16_t* a;        // A stage buffers, a_elems bf16 each, contiguous
-  uint16_t* b;        // B stage buffers, b_elems bf16 each, contiguous
+  uint16_t* a;        // A stage buffers, a_elems bf16 in all, contiguous
+  uint16_t* b;        // B stage buffers, b_elems bf16 in all, contiguous
   int a_elems, b_elems;
-  // buffer k of the 2 * kStages (arithmetic, so no indexed pointer table)
-  __device__ __forceinline__ uint16_t* buf(int k) const {
-    return k < kStages ? a + k * a_elems : b + (k - kStages) * b_elems;
+  // 16 KiB piece k of the A buffers followed by the B buffers
+  __device__ __forceinline__ uint16_t* piece(int k) const {
+    const int per_a = a_elems / 8192;
+    return k < per_a ? a + k * 8192 : b + (k - per_a) * 8192;
   }
 };
 
@@ -207,20 +228,23 @@ struct Frag {
   __device__ __forceinline__ int col(int ni) const { return col0 + 32 * ni + (lane & 31); }
 };
 
-template <int BM, int BN, class Epi>
+template <int BM, int BN, int KB, int STAGES, class Epi>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void gemm_nt_kernel(Problem p, Epi epi) {
   static_assert(BM % 64 == 0 && BN % 64 == 0, "tile");
+  static_assert(KB == 32 || KB == 64, "K step");
+  static_assert(STAGES >= 2 && STAGES <= 6, "stages");
+  constexpr int KC = KB / 8;        // 16-byte chunks per LDS row
+  constexpr int RPB = 512 / KB;     // rows per 1 KiB block (one wave-wide direct load)
   constexpr int AW = BM / RPB / 4;  // direct 1 KiB loads per wave per stage
   constexpr int BW = BN / RPB / 4;
   constexpr int LPS = AW + BW;      // vector-memory instructions per wave per stage
-  constexpr int ASZ = BM * BK, BSZ = BN * BK;  // elements per stage
+  constexpr int ASZ = BM * KB, BSZ = BN * KB;  // elements per stage
   static_assert(AW >= 1 && BW >= 1, "tile too small");
-  static_assert(kStages == 4, "the K loop below is unrolled for four stages");
   using F = Frag<BM, BN>;
 
-  __shared__ __align__(1024) uint16_t As[kStages * ASZ];
-  __shared__ __align__(1024) uint16_t Bs[kStages * BSZ];
+  __shared__ __align__(1024) uint16_t As[STAGES * ASZ];
+  __shared__ __align__(1024) uint16_t Bs[STAGES * BSZ];
 
   const int tid = threadIdx.x;
   F f;
@@ -241,8 +265,9 @@ void gemm_nt_kernel(Problem p, Epi epi) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) f.acc[mi][ni][r] = 0.0f;
 
-  const int64_t kt0 = p.ktiles * f.ks / p.splits;
-  const int64_t kt1 = p.ktiles * (f.ks + 1) / p.splits;
+  const int64_t ktiles = p.ktiles * BK / KB;  // K tiles of this kernel's step
+  const int64_t kt0 = ktiles * f.ks / p.splits;
+  const int64_t kt1 = ktiles * (f.ks + 1) / p.splits;
 
   // Direct global->LDS loads.  Wave instruction i of this wave fills the
   // 1 KiB LDS block b = wave + 4 i (rows b*RPB .. b*RPB+RPB-1); lane l lands
@@ -255,25 +280,25 @@ void gemm_nt_kernel(Problem p, Epi epi) {
 #pragma unroll
   for (int i = 0; i < AW; ++i) {
     const int r = (f.wave + 4 * i) * RPB + f.lane / KC;
-    const int j = swz(r, f.lane % KC);
+    const int j = swz<KB>(r, f.lane % KC);
     const int64_t gr = (a_row0 + r < p.a.rows) ? a_row0 + r : p.a.rows - 1;
     oa[i] = static_cast<uint32_t>(((gr - a_row0) * p.a.ld + 8 * j) * 2);
   }
 #pragma unroll
   for (int i = 0; i < BW; ++i) {
     const int r = (f.wave + 4 * i) * RPB + f.lane / KC;
-    const int j = swz(r, f.lane % KC);
+    const int j = swz<KB>(r, f.lane % KC);
     const int64_t gr = (b_row0 + r < p.b.rows) ? b_row0 + r : p.b.rows - 1;
     ob[i] = static_cast<uint32_t>(((gr - b_row0) * p.b.ld + 8 * j) * 2);
   }
-  KPos kp;
+  KPos<KB> kp;
   auto issue = [&](int s) {
     const uint16_t* pa = kp.base(p.a, f.z) + a_row0 * p.a.ld;
     const uint16_t* pb = kp.base(p.b, f.z) + b_row0 * p.b.ld;
 #pragma unroll
-    for (int i = 0; i < AW; ++i) dma16(pa, oa[i], As + s * ASZ + (f.wave + 4 * i) * (RPB * BK));
+    for (int i = 0; i < AW; ++i) dma16(pa, oa[i], As + s * ASZ + (f.wave + 4 * i) * (RPB * KB));
 #pragma unroll
-    for (int i = 0; i < BW; ++i) dma16(pb, ob[i], Bs + s * BSZ + (f.wave + 4 * i) * (RPB * BK));
+    for (int i = 0; i < BW; ++i) dma16(pb, ob[i], Bs + s * BSZ + (f.wave + 4 * i) * (RPB * KB));
     kp.next(p);
   };
 
@@ -286,10 +311,10 @@ void gemm_nt_kernel(Problem p, Epi epi) {
     bf16x8 fa[F::FM], fb[F::FN];
 #pragma unroll
     for (int mi = 0; mi < F::FM; ++mi)
-      fa[mi] = *reinterpret_cast<const bf16x8*>(&la[lds_off(arow + 32 * mi, j)]);
+      fa[mi] = *reinterpret_cast<const bf16x8*>(&la[lds_off<KB>(arow + 32 * mi, j)]);
 #pragma unroll
     for (int ni = 0; ni < F::FN; ++ni)
-      fb[ni] = *reinterpret_cast<const bf16x8*>(&lb[lds_off(brow + 32 * ni, j)]);
+      fb[ni] = *reinterpret_cast<const bf16x8*>(&lb[lds_off<KB>(brow + 32 * ni, j)]);
 #pragma unroll
     for (int mi = 0; mi < F::FM; ++mi)
 #pragma unroll
@@ -305,12 +330,12 @@ void gemm_nt_kernel(Problem p, Epi epi) {
   auto step = [&](auto s, int64_t i) {
     constexpr int S = decltype(s)::value;
     const int64_t after = issued - 1 - i;  // stages in flight behind stage i
-    if (after >= 2)
-      wait_vmcnt<2 * LPS>();
-    else if (after == 1)
-      wait_vmcnt<LPS>();
-    else
-      wait_vmcnt<0>();
+    static_assert((STAGES - 1) * LPS < 64, "vmcnt holds at most 63 outstanding loads");
+    StaticFor<0, STAGES>::run([&](auto q) {
+      // wait_vmcnt<N> for the largest N = n * LPS with n <= after
+      constexpr int n = STAGES - 1 - decltype(q)::value;
+      if (after == n || (n == STAGES - 1 && after > n)) wait_vmcnt<n * LPS>();
+    });
     // Bare barrier: __syncthreads() would also wait for every load in flight.
     // This wave's part of stage i has landed (the wait above), and the LDS
     // reads of stage i - 1 were consumed by its matrix-core instructions.
@@ -318,24 +343,24 @@ void gemm_nt_kernel(Problem p, Epi epi) {
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
     if (issued < nk) {
-      issue((S + kStages - 1) % kStages);
+      issue((S + STAGES - 1) % STAGES);
       ++issued;
     }
 #pragma unroll
-    for (int kk = 0; kk < BK / 16; ++kk) kstep(As + S * ASZ, Bs + S * BSZ, kk);
+    for (int kk = 0; kk < KB / 16; ++kk) kstep(As + S * ASZ, Bs + S * BSZ, kk);
   };
 
   if (nk > 0) {
     kp.init(p, kt0);
-    for (int s = 0; s < kStages - 1 && issued < nk; ++s) {
+    for (int s = 0; s < STAGES - 1 && issued < nk; ++s) {
       issue(s);
       ++issued;
     }
-    for (int64_t it = 0; it < nk; it += kStages) {
-      step(std::integral_constant<int, 0>(), it);
-      if (it + 1 < nk) step(std::integral_constant<int, 1>(), it + 1);
-      if (it + 2 < nk) step(std::integral_constant<int, 2>(), it + 2);
-      if (it + 3 < nk) step(std::integral_constant<int, 3>(), it + 3);
+    for (int64_t it = 0; it < nk; it += STAGES) {
+      StaticFor<0, STAGES>::run([&](auto s) {
+        constexpr int S = decltype(s)::value;
+        if (it + S < nk) step(s, it + S);
+      });
     }
   }
   // Pin the accumulators to AGPRs across the loop: otherwise an epilogue
@@ -350,8 +375,8 @@ void gemm_nt_kernel(Problem p, Epi epi) {
   StageLds lds;
   lds.a = As;
   lds.b = Bs;
-  lds.a_elems = ASZ;
-  lds.b_elems = BSZ;
+  lds.a_elems = STAGES * ASZ;
+  lds.b_elems = STAGES * BSZ;
   epi(f, lds);
 }
 

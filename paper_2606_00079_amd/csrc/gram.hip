@@ -84,24 +84,40 @@ struct PartialStore {
   }
 };
 
-// out[i][j] = scale * sum_s partial (fp64, splits in order), mirrored.
+// out = scale * sum over splits of the partial tiles (fp64, splits in
+// order), mirrored into the lower triangle.  One workgroup per 64 x 64 block
+// of an upper-triangle tile: reads are coalesced along the block's columns,
+// and blocks of off-diagonal tiles are also written transposed through LDS.
 template <typename OutT>
 __global__ __launch_bounds__(256) void sym_reduce_kernel(const float* __restrict__ part, int splits,
                                                          int64_t ntiles, int T, int64_t d,
                                                          double scale, OutT* __restrict__ out) {
-  const int64_t idx = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
-  if (idx >= d * d) return;
-  int64_t i = idx / d, j = idx % d;
-  int64_t ti = i / GT, tj = j / GT;
-  if (ti > tj) {
-    int64_t tmp = i; i = j; j = tmp;
-    tmp = ti; ti = tj; tj = tmp;
+  __shared__ double tile[64][65];
+  constexpr int NB = GT / 64;                       // 64-blocks per tile edge
+  const int64_t t = blockIdx.x / (NB * NB);         // upper-triangle tile
+  const int sb = blockIdx.x % (NB * NB);
+  int tm = 0, rem = static_cast<int>(t);
+  while (rem >= T - tm) {
+    rem -= T - tm;
+    ++tm;
   }
-  const int64_t t = (ti * (2 * T - ti + 1)) / 2 + (tj - ti);
-  const int64_t off = t * GT * GT + (i % GT) * GT + (j % GT);
-  double s = 0.0;
-  for (int k = 0; k < splits; ++k) s += static_cast<double>(part[k * ntiles * GT * GT + off]);
-  out[idx] = static_cast<OutT>(s * scale);
+  const int tn = tm + rem;
+  const int bi = sb / NB, bj = sb % NB;
+  const int c = threadIdx.x & 63, r0 = threadIdx.x >> 6;
+  const int64_t gi0 = static_cast<int64_t>(tm) * GT + 64 * bi;  // first output row
+  const int64_t gj0 = static_cast<int64_t>(tn) * GT + 64 * bj;  // first output column
+  const float* src = part + t * GT * GT + (64 * bi) * GT + 64 * bj;
+  for (int r = r0; r < 64; r += 4) {
+    double s = 0.0;
+    for (int k = 0; k < splits; ++k) s += static_cast<double>(src[k * ntiles * GT * GT + r * GT + c]);
+    s *= scale;
+    tile[r][c] = s;
+    if (gi0 + r < d && gj0 + c < d) out[(gi0 + r) * d + gj0 + c] = static_cast<OutT>(s);
+  }
+  if (tm == tn) return;  // a diagonal tile holds both triangles itself
+  __syncthreads();
+  for (int r = r0; r < 64; r += 4)
+    if (gj0 + r < d && gi0 + c < d) out[(gj0 + r) * d + gi0 + c] = static_cast<OutT>(tile[c][r]);
 }
 
 // Launches the symmetric split-K GEMM of p (tiles/splits already set) and
@@ -114,11 +130,12 @@ bitsmoe_status run_symmetric(gemm::Problem p, int64_t d, double scale, OutT* out
   const int64_t ntiles = static_cast<int64_t>(T) * (T + 1) / 2;
   p.tiles_m = p.tiles_n = T;
   p.symmetric = 1;
-  // K chunks of at most 4096 terms; at least ~2 workgroups per CU.
-  int64_t splits = (p.ktiles * BK + 4095) / 4096;
-  while (splits * ntiles < 512 && splits < p.ktiles) splits *= 2;
-  splits = std::min<int64_t>(splits, p.ktiles);
-  splits = std::max<int64_t>(splits, 1);
+  // K chunks of at most 4096 terms, at least ~3 workgroups per CU, and at
+  // least four K tiles per workgroup.
+  const int64_t kt = p.ktiles;  // in units of gemm::BK
+  int64_t splits = (kt * BK + 4095) / 4096;
+  splits = std::max<int64_t>(splits, (768 + ntiles - 1) / ntiles);
+  splits = std::min<int64_t>(splits, std::max<int64_t>(1, kt / 4));
   p.splits = static_cast<int>(splits);
   bitsmoe_status st;
   float* part = static_cast<float*>(
@@ -128,12 +145,12 @@ bitsmoe_status run_symmetric(gemm::Problem p, int64_t d, double scale, OutT* out
   dim3 grid(static_cast<unsigned>(ntiles), static_cast<unsigned>(splits), 1);
   {
     KernelTimer timer(name, stream);
-    hipLaunchKernelGGL((gemm::gemm_nt_kernel<GT, GT, PartialStore>), grid,
+    hipLaunchKernelGGL((gemm::gemm_nt_kernel<GT, GT, 32, 4, PartialStore>), grid,
                        dim3(gemm::kThreads), 0, s, p, epi);
   }
   BITSMOE_LAUNCH_CHECK("gram: gemm launch");
-  const int64_t total = d * d;
-  hipLaunchKernelGGL((sym_reduce_kernel<OutT>), dim3(static_cast<unsigned>((total + 255) / 256)),
+  constexpr int NB = GT / 64;
+  hipLaunchKernelGGL((sym_reduce_kernel<OutT>), dim3(static_cast<unsigned>(ntiles * NB * NB)),
                      dim3(256), 0, s, part, p.splits, ntiles, T, d, scale, out);
   BITSMOE_LAUNCH_CHECK("gram: reduce launch");
   return BITSMOE_OK;
@@ -151,7 +168,8 @@ extern "C" bitsmoe_status bitsmoe_gram(const void* X_dev, bitsmoe_dtype xt, int6
   if (xt != BITSMOE_F32 && xt != BITSMOE_BF16) return fail(BITSMOE_ERR_DTYPE, "gram: dtype");
   if (d % 64 != 0) return fail(BITSMOE_ERR_SHAPE, "gram: d must be a multiple of 64");
   hipStream_t s = static_cast<hipStream_t>(stream);
-  const int64_t npad = (n + BK - 1) / BK * BK;  // K padded with zero rows to the K step
+  // K padded with zero rows to a multiple of the engine's K alignment
+  const int64_t npad = (n + gemm::kKAlign - 1) / gemm::kKAlign * gemm::kKAlign;
   const bool f32 = xt == BITSMOE_F32;
   bitsmoe_status st;
   uint16_t* hi = static_cast<uint16_t*>(scratch(kScratchA, d * npad * 2, stream, &st));

@@ -64,6 +64,40 @@ __global__ __launch_bounds__(256) void batched_transpose_kernel(const void* __re
   }
 }
 
+// bf16 W [E][rows][cols] -> Wt [E][cols][rows], 64 x 64 tiles with 16-byte
+// loads and stores (rows and cols are multiples of 64).
+__global__ __launch_bounds__(256) void transpose_bf16_kernel(const uint16_t* __restrict__ W,
+                                                             int64_t rows, int64_t cols,
+                                                             uint16_t* __restrict__ Wt) {
+  __shared__ __align__(16) uint16_t tile[64][72];  // 144-byte rows: 16-byte aligned, spread over banks
+  const int64_t e = blockIdx.z;
+  const int64_t r0 = static_cast<int64_t>(blockIdx.y) * 64;
+  const int64_t c0 = static_cast<int64_t>(blockIdx.x) * 64;
+  const int64_t off = e * rows * cols;
+  const int t = threadIdx.x;
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int rr = (t >> 3) + 32 * h, cc = (t & 7) * 8;
+    *reinterpret_cast<uint4*>(&tile[rr][cc]) =
+        *reinterpret_cast<const uint4*>(W + off + (r0 + rr) * cols + c0 + cc);
+  }
+  __syncthreads();
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int oc = (t >> 3) + 32 * h;  // output row = input column c0 + oc
+    const int orr = (t & 7) * 8;       // first of 8 input rows
+    uint16_t v[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) v[i] = tile[orr + i][oc];
+    uint4 pk;
+    pk.x = v[0] | (static_cast<uint32_t>(v[1]) << 16);
+    pk.y = v[2] | (static_cast<uint32_t>(v[3]) << 16);
+    pk.z = v[4] | (static_cast<uint32_t>(v[5]) << 16);
+    pk.w = v[6] | (static_cast<uint32_t>(v[7]) << 16);
+    *reinterpret_cast<uint4*>(Wt + off + (c0 + oc) * rows + r0 + orr) = pk;
+  }
+}
+
 // C[z][row][col] = acc for row < r, col < d_in.
 struct FactorStore {
   float* C;
@@ -122,7 +156,8 @@ extern "C" bitsmoe_status bitsmoe_project(const float* Ut_dev, const void* W_dev
   if (f32)
     hipLaunchKernelGGL(batched_transpose_kernel<true>, tg, dim3(256), 0, s, W_dev, d_out, d_in, Wt, Wt_lo);
   else
-    hipLaunchKernelGGL(batched_transpose_kernel<false>, tg, dim3(256), 0, s, W_dev, d_out, d_in, Wt, Wt_lo);
+    hipLaunchKernelGGL(transpose_bf16_kernel, tg, dim3(256), 0, s,
+                       static_cast<const uint16_t*>(W_dev), d_out, d_in, Wt);
   BITSMOE_LAUNCH_CHECK("project: transpose launch");
 
   gemm::Problem p{};
@@ -156,7 +191,7 @@ extern "C" bitsmoe_status bitsmoe_project(const float* Ut_dev, const void* W_dev
   dim3 grid(static_cast<unsigned>(p.tiles_m * p.tiles_n), 1, static_cast<unsigned>(E));
   {
     KernelTimer timer("project", stream);
-    hipLaunchKernelGGL((gemm::gemm_nt_kernel<PM, PN, FactorStore>), grid,
+    hipLaunchKernelGGL((gemm::gemm_nt_kernel<PM, PN, 32, 4, FactorStore>), grid,
                        dim3(gemm::kThreads), 0, s, p, epi);
   }
   BITSMOE_LAUNCH_CHECK("project: gemm launch");

@@ -27,6 +27,8 @@ namespace {
 
 constexpr int SBM = 256;  // i (H row) tile
 constexpr int SBN = 256;  // D row tile
+constexpr int SKB = 32;   // K step of the loss-table GEMM
+constexpr int SSTAGES = 4;  // LDS stages (three in flight)
 using gemm::BK;
 
 __global__ __launch_bounds__(256) void hoff_kernel(const float* __restrict__ H, int64_t d,
@@ -157,7 +159,9 @@ struct RowDot {
   template <class F>
   __device__ void operator()(F& f, const gemm::StageLds& lds) const {
     static_assert(SBM == 256 && SBN == 256, "layout below assumes 256 x 256 tiles");
-    __shared__ float red[2][SBN];
+    static_assert(SSTAGES * SBM * SKB * 2 + SSTAGES * SBN * SKB * 2 >= 8 * 16384,
+                  "stage buffers must hold the 256 x 256 bf16 D block");
+    __shared__ float red[2][SBN];  // cross-wave reduction
     const int lane = opaque(f.lane);
     const int wave = lane >= 0 ? f.wave : 0;  // ties wave to the opaque lane
     const int64_t i_base = static_cast<int64_t>(f.tm) * SBM;
@@ -171,7 +175,7 @@ struct RowDot {
       const int64_t row0 = min(j_base + 2 * b, R - 1);
       const int64_t row = min(j_base + j, R - 1);
       const int64_t col = min(i_base + 8 * c, d - 8);
-      uint16_t* dst = lds.buf(b >> 4) + (b & 15) * 512;
+      uint16_t* dst = lds.piece(b >> 4) + (b & 15) * 512;
       gemm::dma16(D + row0 * d, static_cast<uint32_t>(((row - row0) * d + col) * 2), dst);
     }
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
@@ -183,7 +187,7 @@ struct RowDot {
       // next to all 256 accumulators
       __builtin_amdgcn_sched_barrier(0);
       const int jl = f.wn * F::WN + 32 * ni + (lane & 31);
-      const uint16_t* rowp = lds.buf(jl >> 5) + (jl & 31) * 256;
+      const uint16_t* rowp = lds.piece(jl >> 5) + (jl & 31) * 256;
       float acc = 0.0f;
 #pragma unroll
       for (int mi = 0; mi < F::FM; ++mi)
@@ -305,7 +309,7 @@ extern "C" bitsmoe_status bitsmoe_score(const float* C_dev, int64_t units, int64
   dim3 grid(static_cast<unsigned>(tiles_m * tiles_n), 1, 1);
   {
     KernelTimer timer("score_gemm", stream);
-    hipLaunchKernelGGL((gemm::gemm_nt_kernel<SBM, SBN, RowDot>), grid, dim3(gemm::kThreads),
+    hipLaunchKernelGGL((gemm::gemm_nt_kernel<SBM, SBN, SKB, SSTAGES, RowDot>), grid, dim3(gemm::kThreads),
                        0, s, p, epi);
   }
   BITSMOE_LAUNCH_CHECK("score: gemm launch");
