@@ -32,6 +32,9 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 METRIC = "ms per MoE layer quantized (Qwen3-30B-A3B shape); score-kernel TFLOP/s"
+SCORE_SOURCES = ("paper_2606_00079_amd/csrc/gemm.hpp", "paper_2606_00079_amd/csrc/score.hip",
+                 "paper_2606_00079_amd/csrc/common.hpp")
+TRAFFIC_FILE = "profiles/score_gemm_qwen_layer_traffic.txt"
 PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 matrix-core peak
 PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
 
@@ -40,13 +43,42 @@ def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
 
 
+def score_source_hash() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for f in SCORE_SOURCES:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic():
+    """HBM bytes per loss-table GEMM launch from the committed FETCH_SIZE / WRITE_SIZE
+    counter summary, or None when it is absent or the kernel sources changed since."""
+    path = os.path.join(ROOT, TRAFFIC_FILE)
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    with open(path) as fh:
+        for line in fh:
+            if ":" in line and not line.startswith(" "):
+                k, v = line.split(":", 1)
+                kv[k.strip()] = v.strip()
+    if kv.get("source_sha256_16") != score_source_hash():
+        return None
+    try:
+        return float(kv["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
 def workload_name(cfg) -> str:
     parts = ", ".join(f"{p.name} {p.d_out}x{p.d_in} r={p.r}" for p in cfg.projs)
     return (f"{cfg.name}: E={cfg.E} experts x {{{parts}}}, calibration {cfg.n_tokens} rows, "
             f"bits {list(cfg.bits)}, group {cfg.group}, budget {cfg.budget} bits/unit")
 
 
-def cpu_baseline(cfg, layer, budget_s: float = 20.0) -> dict:
+def cpu_baseline(cfg, layer) -> dict:
     """Times the fp64 oracle on a bounded sample of the layer; scales to the layer."""
     import numpy as np
     import oracle
@@ -58,10 +90,12 @@ def cpu_baseline(cfg, layer, budget_s: float = 20.0) -> dict:
         threads = os.cpu_count() or 1
     total_s = 0.0
     parts = []
+    t_sample = time.perf_counter()
     H_cache = {}
     for proj in layer:
         E = proj.E
-        e_s = min(E, 8)
+        e_s = min(E, 64)   # experts in the M sample
+        e_c = min(E, -(-16384 // proj.r))  # experts in the C sample (>= 16384 units)
         W64 = synth.as_f64(proj.W[:e_s], proj.dtype)
         key = id(proj.X)
         t = time.perf_counter()
@@ -76,15 +110,15 @@ def cpu_baseline(cfg, layer, budget_s: float = 20.0) -> dict:
         Ut, _ = oracle.shared_basis(M, proj.r)
         t_eig = time.perf_counter() - t
         t = time.perf_counter()
-        C = oracle.project(Ut, W64[:1])
-        t_c = (time.perf_counter() - t) * E
+        C = oracle.project(Ut, synth.as_f64(proj.W[:e_c], proj.dtype))
+        t_c = (time.perf_counter() - t) * E / e_c
         units = E * proj.r
-        rows = min(256, C.shape[0])
+        rows = min(16384, C.shape[0])
         t = time.perf_counter()
         L = oracle.score(C[:rows].astype(np.float32), H, proj.bits, proj.group)
         t_l = (time.perf_counter() - t) * units / rows
         # ILP: the exact DP on a sample of units scales with units * budget
-        us = 2048
+        us = min(32768, units)
         Ls = np.tile(L, (us // rows + 1, 1))[:us]
         t = time.perf_counter()
         oracle.allocate_dp(Ls, proj.bits, int(proj.cfg.budget * us))
@@ -97,8 +131,9 @@ def cpu_baseline(cfg, layer, budget_s: float = 20.0) -> dict:
         total_s += s
         parts.append(f"{proj.spec.name}: H {t_h:.2f}s M {t_m:.2f}s eig {t_eig:.2f}s C {t_c:.2f}s "
                      f"L {t_l:.1f}s ILP {t_ilp:.1f}s pack {t_p:.1f}s")
-    sample = ("fp64 numpy oracle per projection: full H and eigensolve; M on 8 experts, C on 1 "
-              "expert, L and pack on 256 units, exact ILP DP on 2048 units; scaled to the layer "
+    spent = time.perf_counter() - t_sample
+    sample = (f"{spent:.1f} s of host time; fp64 numpy oracle per projection: full H and eigensolve; M on 64 experts, C on the first "
+              "16384 units' experts, L and pack on 16384 units, exact ILP DP on 32768 units; scaled to the layer "
               "(linear in experts/units, quadratic for the DP). " + "; ".join(parts))
     return {"value": round(total_s * 1e3, 1), "unit": "ms per layer", "cores": int(threads),
             "kind": "oracle", "sample": sample}
@@ -111,6 +146,9 @@ def main(argv=None) -> int:
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", default="qwen_layer")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
+                    help="run one elementwise copy of MIB MiB before timing (calibrates HBM "
+                         "byte counters under rocprofv3 --pmc)")
     args = ap.parse_args(argv)
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported "
@@ -152,6 +190,14 @@ def main(argv=None) -> int:
         step()
         log(f"warmup {i + 1}/{args.warmup}")
     torch.cuda.synchronize()
+    if args.copy_probe > 0:
+        n = args.copy_probe * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        torch.neg(src, out=dst)
+        torch.cuda.synchronize()
+        log(f"copy probe: neg kernel reads {4 * n} B and writes {4 * n} B")
+        del src, dst
     bm.timing(True)
     for name in ("gram", "gram_experts", "project", "score_dgen", "score_gemm", "pack"):
         bm.kernel_time(name)  # discard anything recorded before
@@ -193,6 +239,7 @@ def main(argv=None) -> int:
         tflops=round(c_flops / (kt["project"][0] / steps * 1e-3) / 1e12, 1))
 
     value = float(np.median(gpu_ms))
+    traffic = measured_traffic()
     out = {
         "metric": METRIC,
         "value": round(value, 3),
@@ -216,8 +263,10 @@ def main(argv=None) -> int:
         "kernels": kernels,
         "roofline": {"bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-                     "traffic": None, "kernel": "score_gemm",
-                     "launches_per_step": n_gemm // max(steps, 1)},
+                     "traffic": traffic, "kernel": "score_gemm",
+                     "launches_per_step": n_gemm // max(steps, 1),
+                     "avg_launch_ms": round(ms_gemm / max(n_gemm, 1), 4),
+                     "flops_per_launch": score_flops / max(n_gemm // max(steps, 1), 1)},
     }
     if not args.no_cpu_baseline:
         log("timing the fp64 oracle on a sample")
