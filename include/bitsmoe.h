@@ -37,6 +37,9 @@
  *    is BITSMOE_ERR_DEVICE, and the outputs are unspecified.
  *    bitsmoe_last_error() gives a text for the last non-OK status of the
  *    calling thread.
+ *  - Device pointers must be 16-byte aligned (hipMalloc and the usual
+ *    framework allocators give 256 bytes); a misaligned one gives
+ *    BITSMOE_ERR_ARG.
  *  - Matrices are row-major and densely packed unless a stride is given.
  *  - Shape rules that are not met give BITSMOE_ERR_SHAPE; null pointers and
  *    non-positive sizes give BITSMOE_ERR_ARG.

@@ -298,6 +298,8 @@ bitsmoe_status bitsmoe_shared_basis(const double* M_dev, int64_t d_out, int64_t 
                                     double* eigvals_host, double* host_ms, void* stream) {
   auto t0 = std::chrono::steady_clock::now();
   if (!M_dev || !Ut_dev) return fail(BITSMOE_ERR_ARG, "shared_basis: null pointer");
+  if (!aligned16({M_dev, Ut_dev}))
+    return fail(BITSMOE_ERR_ARG, "shared_basis: device pointers must be 16-byte aligned");
   if (d_out <= 0 || r <= 0) return fail(BITSMOE_ERR_ARG, "shared_basis: non-positive size");
   if (r > d_out) return fail(BITSMOE_ERR_SHAPE, "shared_basis: r > d_out");
   hipStream_t s = static_cast<hipStream_t>(stream);

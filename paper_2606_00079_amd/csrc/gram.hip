@@ -85,39 +85,77 @@ struct PartialStore {
 };
 
 // out = scale * sum over splits of the partial tiles (fp64, splits in
-// order), mirrored into the lower triangle.  One workgroup per 64 x 64 block
-// of an upper-triangle tile: reads are coalesced along the block's columns,
-// and blocks of off-diagonal tiles are also written transposed through LDS.
+// order), mirrored into the lower triangle.  One workgroup per 16 x 64 block
+// of an upper-triangle tile; a thread owns four adjacent columns of one row
+// and keeps eight splits' loads in flight before adding them in order.
+// Blocks of off-diagonal tiles are also written transposed through LDS.
+constexpr int RB_ROWS = 16;
+constexpr int RB_COLS = 64;
+constexpr int RB_UNROLL = 8;
+
+__device__ __forceinline__ void store4(double* p, const double (&v)[4]) {
+  reinterpret_cast<double2*>(p)[0] = make_double2(v[0], v[1]);
+  reinterpret_cast<double2*>(p)[1] = make_double2(v[2], v[3]);
+}
+__device__ __forceinline__ void store4(float* p, const double (&v)[4]) {
+  *reinterpret_cast<float4*>(p) = make_float4(static_cast<float>(v[0]), static_cast<float>(v[1]),
+                                              static_cast<float>(v[2]), static_cast<float>(v[3]));
+}
+
 template <typename OutT>
 __global__ __launch_bounds__(256) void sym_reduce_kernel(const float* __restrict__ part, int splits,
                                                          int64_t ntiles, int T, int64_t d,
                                                          double scale, OutT* __restrict__ out) {
-  __shared__ double tile[64][65];
-  constexpr int NB = GT / 64;                       // 64-blocks per tile edge
-  const int64_t t = blockIdx.x / (NB * NB);         // upper-triangle tile
-  const int sb = blockIdx.x % (NB * NB);
+  __shared__ double tile[RB_ROWS][RB_COLS + 1];
+  constexpr int SR = GT / RB_ROWS, SC = GT / RB_COLS;  // blocks per tile edge
+  const int64_t t = blockIdx.x / (SR * SC);            // upper-triangle tile
+  const int sb = static_cast<int>(blockIdx.x % (SR * SC));
   int tm = 0, rem = static_cast<int>(t);
   while (rem >= T - tm) {
     rem -= T - tm;
     ++tm;
   }
   const int tn = tm + rem;
-  const int bi = sb / NB, bj = sb % NB;
-  const int c = threadIdx.x & 63, r0 = threadIdx.x >> 6;
-  const int64_t gi0 = static_cast<int64_t>(tm) * GT + 64 * bi;  // first output row
-  const int64_t gj0 = static_cast<int64_t>(tn) * GT + 64 * bj;  // first output column
-  const float* src = part + t * GT * GT + (64 * bi) * GT + 64 * bj;
-  for (int r = r0; r < 64; r += 4) {
-    double s = 0.0;
-    for (int k = 0; k < splits; ++k) s += static_cast<double>(src[k * ntiles * GT * GT + r * GT + c]);
-    s *= scale;
-    tile[r][c] = s;
-    if (gi0 + r < d && gj0 + c < d) out[(gi0 + r) * d + gj0 + c] = static_cast<OutT>(s);
+  const int bi = sb / SC, bj = sb % SC;
+  const int64_t gi0 = static_cast<int64_t>(tm) * GT + RB_ROWS * bi;  // first output row
+  const int64_t gj0 = static_cast<int64_t>(tn) * GT + RB_COLS * bj;  // first output column
+  // d is a multiple of 64, so a block is either wholly inside or wholly outside
+  if (gi0 >= d || gj0 >= d) return;
+  const int r = threadIdx.x >> 4, cq = threadIdx.x & 15;
+  const float* src = part + t * GT * GT + static_cast<int64_t>(RB_ROWS * bi + r) * GT + RB_COLS * bj + 4 * cq;
+  const int64_t kstride = ntiles * GT * GT;
+  double acc[4] = {0.0, 0.0, 0.0, 0.0};
+  int k = 0;
+  for (; k + RB_UNROLL <= splits; k += RB_UNROLL) {
+    float4 v[RB_UNROLL];
+#pragma unroll
+    for (int u = 0; u < RB_UNROLL; ++u) v[u] = *reinterpret_cast<const float4*>(src + (k + u) * kstride);
+#pragma unroll
+    for (int u = 0; u < RB_UNROLL; ++u) {
+      acc[0] += static_cast<double>(v[u].x);
+      acc[1] += static_cast<double>(v[u].y);
+      acc[2] += static_cast<double>(v[u].z);
+      acc[3] += static_cast<double>(v[u].w);
+    }
   }
+  for (; k < splits; ++k) {
+    const float4 v = *reinterpret_cast<const float4*>(src + k * kstride);
+    acc[0] += static_cast<double>(v.x);
+    acc[1] += static_cast<double>(v.y);
+    acc[2] += static_cast<double>(v.z);
+    acc[3] += static_cast<double>(v.w);
+  }
+#pragma unroll
+  for (int j = 0; j < 4; ++j) acc[j] *= scale;
+  store4(out + (gi0 + r) * d + gj0 + 4 * cq, acc);
   if (tm == tn) return;  // a diagonal tile holds both triangles itself
+#pragma unroll
+  for (int j = 0; j < 4; ++j) tile[r][4 * cq + j] = acc[j];
   __syncthreads();
-  for (int r = r0; r < 64; r += 4)
-    if (gj0 + r < d && gi0 + c < d) out[(gj0 + r) * d + gi0 + c] = static_cast<OutT>(tile[c][r]);
+  // transposed: output row gj0 + c, columns gi0 + 4q .. 4q + 3
+  const int c = threadIdx.x >> 2, q = threadIdx.x & 3;
+  const double tv[4] = {tile[4 * q][c], tile[4 * q + 1][c], tile[4 * q + 2][c], tile[4 * q + 3][c]};
+  store4(out + (gj0 + c) * d + gi0 + 4 * q, tv);
 }
 
 // Launches the symmetric split-K GEMM of p (tiles/splits already set) and
@@ -149,8 +187,8 @@ bitsmoe_status run_symmetric(gemm::Problem p, int64_t d, double scale, OutT* out
                        dim3(gemm::kThreads), 0, s, p, epi);
   }
   BITSMOE_LAUNCH_CHECK("gram: gemm launch");
-  constexpr int NB = GT / 64;
-  hipLaunchKernelGGL((sym_reduce_kernel<OutT>), dim3(static_cast<unsigned>(ntiles * NB * NB)),
+  constexpr int NB = (GT / RB_ROWS) * (GT / RB_COLS);
+  hipLaunchKernelGGL((sym_reduce_kernel<OutT>), dim3(static_cast<unsigned>(ntiles * NB)),
                      dim3(256), 0, s, part, p.splits, ntiles, T, d, scale, out);
   BITSMOE_LAUNCH_CHECK("gram: reduce launch");
   return BITSMOE_OK;
@@ -164,6 +202,7 @@ using namespace bitsmoe;
 extern "C" bitsmoe_status bitsmoe_gram(const void* X_dev, bitsmoe_dtype xt, int64_t n, int64_t d,
                                        float* H_dev, void* stream) {
   if (!X_dev || !H_dev) return fail(BITSMOE_ERR_ARG, "gram: null pointer");
+  if (!aligned16({X_dev, H_dev})) return fail(BITSMOE_ERR_ARG, "gram: device pointers must be 16-byte aligned");
   if (n <= 0 || d <= 0) return fail(BITSMOE_ERR_ARG, "gram: non-positive size");
   if (xt != BITSMOE_F32 && xt != BITSMOE_BF16) return fail(BITSMOE_ERR_DTYPE, "gram: dtype");
   if (d % 64 != 0) return fail(BITSMOE_ERR_SHAPE, "gram: d must be a multiple of 64");
@@ -209,6 +248,8 @@ extern "C" bitsmoe_status bitsmoe_gram_experts(const void* W_dev, bitsmoe_dtype 
                                                int64_t d_out, int64_t d_in, double* M_dev,
                                                void* stream) {
   if (!W_dev || !M_dev) return fail(BITSMOE_ERR_ARG, "gram_experts: null pointer");
+  if (!aligned16({W_dev, M_dev}))
+    return fail(BITSMOE_ERR_ARG, "gram_experts: device pointers must be 16-byte aligned");
   if (E <= 0 || d_out <= 0 || d_in <= 0) return fail(BITSMOE_ERR_ARG, "gram_experts: non-positive size");
   if (wt != BITSMOE_F32 && wt != BITSMOE_BF16) return fail(BITSMOE_ERR_DTYPE, "gram_experts: dtype");
   if (d_out % 64 != 0 || d_in % 64 != 0)

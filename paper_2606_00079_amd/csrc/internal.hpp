@@ -3,6 +3,7 @@
 
 #include <cstddef>
 #include <cstdint>
+#include <initializer_list>
 #include <string>
 
 #include "bitsmoe.h"
@@ -44,6 +45,14 @@ class KernelTimer {
   void* stream_;
   void* start_ = nullptr;
 };
+
+// True when every pointer is 16-byte aligned (the kernels use 16-byte
+// vector accesses on device buffers).
+inline bool aligned16(std::initializer_list<const void*> ptrs) {
+  for (const void* p : ptrs)
+    if (reinterpret_cast<uintptr_t>(p) % 16 != 0) return false;
+  return true;
+}
 
 inline bool is_pow2(int64_t v) { return v > 0 && (v & (v - 1)) == 0; }
 

@@ -125,6 +125,8 @@ extern "C" bitsmoe_status bitsmoe_pack(const float* C_dev, int64_t units, int64_
                                        uint16_t* params_dev, void* stream) {
   if (!C_dev || !bits_dev || !word_offsets_dev || !codes_dev || !params_dev)
     return fail(BITSMOE_ERR_ARG, "pack: null pointer");
+  if (!aligned16({C_dev, bits_dev, word_offsets_dev, codes_dev, params_dev}))
+    return fail(BITSMOE_ERR_ARG, "pack: device pointers must be 16-byte aligned");
   bitsmoe_status st = check_pack_args(units, d, group);
   if (st != BITSMOE_OK) return st;
   if (total_words < 0) return fail(BITSMOE_ERR_ARG, "pack: negative total_words");
@@ -162,6 +164,8 @@ extern "C" bitsmoe_status bitsmoe_unpack(const uint64_t* codes_dev, const uint16
                                          float* Chat_dev, void* stream) {
   if (!codes_dev || !params_dev || !bits_dev || !word_offsets_dev || !Chat_dev)
     return fail(BITSMOE_ERR_ARG, "unpack: null pointer");
+  if (!aligned16({codes_dev, params_dev, bits_dev, word_offsets_dev, Chat_dev}))
+    return fail(BITSMOE_ERR_ARG, "unpack: device pointers must be 16-byte aligned");
   bitsmoe_status st = check_pack_args(units, d, group);
   if (st != BITSMOE_OK) return st;
   hipStream_t s = static_cast<hipStream_t>(stream);

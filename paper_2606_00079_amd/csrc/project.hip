@@ -129,6 +129,8 @@ extern "C" bitsmoe_status bitsmoe_project(const float* Ut_dev, const void* W_dev
                                           int64_t E, int64_t d_out, int64_t d_in, int64_t r,
                                           float* C_dev, void* stream) {
   if (!Ut_dev || !W_dev || !C_dev) return fail(BITSMOE_ERR_ARG, "project: null pointer");
+  if (!aligned16({Ut_dev, W_dev, C_dev}))
+    return fail(BITSMOE_ERR_ARG, "project: device pointers must be 16-byte aligned");
   if (E <= 0 || d_out <= 0 || d_in <= 0 || r <= 0) return fail(BITSMOE_ERR_ARG, "project: non-positive size");
   if (wt != BITSMOE_F32 && wt != BITSMOE_BF16) return fail(BITSMOE_ERR_DTYPE, "project: dtype");
   if (d_out % 64 != 0 || d_in % 64 != 0)

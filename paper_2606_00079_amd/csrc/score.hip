@@ -238,6 +238,8 @@ extern "C" bitsmoe_status bitsmoe_score(const float* C_dev, int64_t units, int64
                                         const float* H_dev, const int* bits_host, int nbits,
                                         int group, float* L_dev, void* stream) {
   if (!C_dev || !H_dev || !bits_host || !L_dev) return fail(BITSMOE_ERR_ARG, "score: null pointer");
+  if (!aligned16({C_dev, H_dev, L_dev}))
+    return fail(BITSMOE_ERR_ARG, "score: device pointers must be 16-byte aligned");
   if (units <= 0 || d <= 0) return fail(BITSMOE_ERR_ARG, "score: non-positive size");
   if (nbits < 1 || nbits > BITSMOE_MAX_NBITS) return fail(BITSMOE_ERR_ARG, "score: nbits outside 1..8");
   QuantBits qb{};

@@ -159,3 +159,13 @@ def test_device_entry_points_validate_before_launch(lib):
     assert "r > d_out" in pkg.last_error()
     assert lib.bitsmoe_shared_basis(null, 64, 4, fake, null, null, s) == 1
     assert lib.bitsmoe_set_lapack(b"/nonexistent/liblapack.so") == 8
+    # misaligned device pointers are refused before any launch
+    odd = ctypes.c_void_p(0x1008)
+    assert lib.bitsmoe_gram(odd, 1, 64, 64, fake, s) == 1
+    assert "aligned" in pkg.last_error()
+    assert lib.bitsmoe_gram_experts(fake, 1, 2, 64, 64, odd, s) == 1
+    assert lib.bitsmoe_project(fake, odd, 1, 2, 64, 64, 8, fake, s) == 1
+    assert lib.bitsmoe_score(fake, 10, 256, fake, bits, 4, 64, odd, s) == 1
+    assert lib.bitsmoe_pack(fake, 10, 256, 64, fake, odd, 10, fake, fake, s) == 1
+    assert lib.bitsmoe_unpack(fake, fake, fake, fake, 10, 10, 256, 64, odd, s) == 1
+    assert lib.bitsmoe_shared_basis(odd, 64, 4, fake, null, null, s) == 1
