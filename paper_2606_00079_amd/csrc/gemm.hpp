@@ -111,42 +111,91 @@ __device__ __forceinline__ void tile_coords(const Problem& p, int t, int n, int*
   *tn = first_n + w / p.tiles_m;
 }
 
-__device__ __forceinline__ const uint16_t* pass_ptr(const Side& s, int pass) {
-  switch (pass) {
-    case 0: return s.pass[0];
-    case 1: return s.pass[1];
-    case 2: return s.pass[2];
-    default: return s.pass[3];
-  }
+// v made wave-uniform (held in scalar registers from here on).
+__device__ __forceinline__ int64_t uniform64(int64_t v) {
+  const uint64_t u = static_cast<uint64_t>(v);
+  const uint32_t lo = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<uint32_t>(u)));
+  const uint32_t hi = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<uint32_t>(u >> 32)));
+  return static_cast<int64_t>((static_cast<uint64_t>(hi) << 32) | lo);
 }
+__device__ __forceinline__ int uniform32(int v) { return __builtin_amdgcn_readfirstlane(v); }
 
-// Position of a K tile in the flattened (pass, segment, k) index.  Advanced
-// incrementally inside the K loop so that no division runs there.
+// The pass bases of one side for batch z and first tile row row0, as a
+// shift register: q0 is the current pass, and moving to the next pass shifts
+// the others down by selects (indexing the bases by pass number would turn
+// them into a memory table).
+struct PassBases {
+  const uint16_t* q0;
+  const uint16_t* q1;
+  const uint16_t* q2;
+  const uint16_t* q3;
+  __device__ __forceinline__ void init(const Side& s, int64_t z, int64_t row0) {
+    const int64_t off = z * s.bstride + row0 * s.ld;
+    q0 = s.pass[0] + off;
+    q1 = s.pass[1] + off;
+    q2 = s.pass[2] + off;
+    q3 = s.pass[3] + off;
+  }
+  __device__ __forceinline__ void advance(bool w) {
+    q0 = w ? q1 : q0;
+    q1 = w ? q2 : q1;
+    q2 = w ? q3 : q2;
+  }
+  __device__ __forceinline__ void make_uniform() {
+    auto u = [](const uint16_t* ptr) {
+      return reinterpret_cast<const uint16_t*>(uniform64(reinterpret_cast<int64_t>(ptr)));
+    };
+    q0 = u(q0);
+    q1 = u(q1);
+    q2 = u(q2);
+    q3 = u(q3);
+  }
+};
+
+// Position of a K tile in the flattened (pass, segment, k) index: the base
+// of its pass and its element offset from that base on each side.  Advanced
+// by scalar selects inside the K loop (no division, branch or memory load).
 template <int KB>
 struct KPos {
-  int pass;
   int64_t seg, k0;
-  __device__ __forceinline__ void init(const Problem& p, int64_t kt) {
+  int64_t offa, offb;
+  PassBases ba, bb;
+  __device__ __forceinline__ void init(const Problem& p, int64_t kt, int64_t z, int64_t arow0,
+                                       int64_t brow0) {
     const int64_t tiles_seg = p.kseg / KB;
     const int64_t per_pass = static_cast<int64_t>(p.segs) * tiles_seg;
-    pass = static_cast<int>(kt / per_pass);
+    const int pass = static_cast<int>(kt / per_pass);
     const int64_t rem = kt - static_cast<int64_t>(pass) * per_pass;
     seg = rem / tiles_seg;
     k0 = (rem - seg * tiles_seg) * KB;
+    ba.init(p.a, z, arow0);
+    bb.init(p.b, z, brow0);
+    for (int q = 0; q < pass; ++q) {
+      ba.advance(true);
+      bb.advance(true);
+    }
+    ba.make_uniform();
+    bb.make_uniform();
+    seg = uniform64(seg);
+    k0 = uniform64(k0);
+    offa = uniform64(seg * p.a.estride + k0);
+    offb = uniform64(seg * p.b.estride + k0);
   }
   __device__ __forceinline__ void next(const Problem& p) {
     k0 += KB;
-    if (k0 == p.kseg) {
-      k0 = 0;
-      if (++seg == p.segs) {
-        seg = 0;
-        ++pass;
-      }
-    }
-  }
-  // first element of this K tile in row 0 of batch z for side s
-  __device__ __forceinline__ const uint16_t* base(const Side& s, int64_t z) const {
-    return pass_ptr(s, pass) + z * s.bstride + seg * s.estride + k0;
+    offa += KB;
+    offb += KB;
+    const bool wrap = k0 == p.kseg;
+    k0 = wrap ? 0 : k0;
+    offa = wrap ? offa - p.kseg + p.a.estride : offa;
+    offb = wrap ? offb - p.kseg + p.b.estride : offb;
+    seg += wrap ? 1 : 0;
+    const bool wrap2 = seg == p.segs;
+    seg = wrap2 ? 0 : seg;
+    offa = wrap2 ? 0 : offa;
+    offb = wrap2 ? 0 : offb;
+    ba.advance(wrap2);
+    bb.advance(wrap2);
   }
 };
 
@@ -292,76 +341,139 @@ void gemm_nt_kernel(Problem p, Epi epi) {
     ob[i] = static_cast<uint32_t>(((gr - b_row0) * p.b.ld + 8 * j) * 2);
   }
   KPos<KB> kp;
-  auto issue = [&](int s) {
-    const uint16_t* pa = kp.base(p.a, f.z) + a_row0 * p.a.ld;
-    const uint16_t* pb = kp.base(p.b, f.z) + b_row0 * p.b.ld;
-#pragma unroll
-    for (int i = 0; i < AW; ++i) dma16(pa, oa[i], As + s * ASZ + (f.wave + 4 * i) * (RPB * KB));
-#pragma unroll
-    for (int i = 0; i < BW; ++i) dma16(pb, ob[i], Bs + s * BSZ + (f.wave + 4 * i) * (RPB * KB));
+  // Loads of the next K tile into stage buffer s, one wave instruction at a
+  // time (q < LPS) so that they can be spread between matrix-core ops.
+  struct Issue {
+    const uint16_t* pa;
+    const uint16_t* pb;
+    int s;
+  };
+  auto issue_begin = [&](int s) {
+    Issue is{kp.ba.q0 + kp.offa, kp.bb.q0 + kp.offb, s};
     kp.next(p);
+    return is;
+  };
+  auto issue_part = [&](const Issue& is, int q) {
+    if (q < AW)
+      dma16(is.pa, oa[q], As + is.s * ASZ + (f.wave + 4 * q) * (RPB * KB));
+    else
+      dma16(is.pb, ob[q - AW], Bs + is.s * BSZ + (f.wave + 4 * (q - AW)) * (RPB * KB));
+  };
+  auto issue = [&](int s) {
+    const Issue is = issue_begin(s);
+#pragma unroll
+    for (int q = 0; q < LPS; ++q) issue_part(is, q);
   };
 
   const int arow = f.wm * F::WM + (f.lane & 31);
   const int brow = f.wn * F::WN + (f.lane & 31);
   const int jq = f.lane >> 5;
-  // one K=16 step: operand fragments from LDS, then FM x FN matrix-core ops
-  auto kstep = [&](const uint16_t* la, const uint16_t* lb, int kk) {
+  // Two register sets of operand fragments: while the matrix cores work on
+  // one K=16 step, the fragments of the next step are read into the other.
+  bf16x8 fa[2][F::FM], fb[2][F::FN];
+  auto read_frags = [&](auto set, int s, int kk) {
+    constexpr int T = decltype(set)::value;
+    const uint16_t* la = As + s * ASZ;
+    const uint16_t* lb = Bs + s * BSZ;
     const int j = 2 * kk + jq;
-    bf16x8 fa[F::FM], fb[F::FN];
 #pragma unroll
     for (int mi = 0; mi < F::FM; ++mi)
-      fa[mi] = *reinterpret_cast<const bf16x8*>(&la[lds_off<KB>(arow + 32 * mi, j)]);
+      fa[T][mi] = *reinterpret_cast<const bf16x8*>(&la[lds_off<KB>(arow + 32 * mi, j)]);
 #pragma unroll
     for (int ni = 0; ni < F::FN; ++ni)
-      fb[ni] = *reinterpret_cast<const bf16x8*>(&lb[lds_off<KB>(brow + 32 * ni, j)]);
+      fb[T][ni] = *reinterpret_cast<const bf16x8*>(&lb[lds_off<KB>(brow + 32 * ni, j)]);
+  };
+  // The matrix-core ops of one K=16 step from fragment set `set`; with a
+  // refill, its LPS loads are issued one after each of the first LPS ops.
+  // Scheduling barriers keep this order (the compiler would otherwise sink
+  // the fragment reads of the next step below the ops of this one).
+  static_assert(LPS <= F::FM * F::FN, "one load per matrix-core op at most");
+  auto mfmas = [&](auto set, const Issue* is) {
+    constexpr int T = decltype(set)::value;
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int mi = 0; mi < F::FM; ++mi)
 #pragma unroll
-      for (int ni = 0; ni < F::FN; ++ni)
-        f.acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[mi], fb[ni], f.acc[mi][ni], 0, 0, 0);
+      for (int ni = 0; ni < F::FN; ++ni) {
+        f.acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[T][mi], fb[T][ni], f.acc[mi][ni], 0, 0, 0);
+        const int q = mi * F::FN + ni;
+        if (is != nullptr && q < LPS) {
+          __builtin_amdgcn_sched_barrier(0);
+          issue_part(*is, q);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      }
+    __builtin_amdgcn_sched_barrier(0);
   };
 
   const int64_t nk = kt1 - kt0;
-  int64_t issued = 0;
-  // One K stage: wait until stage i has landed in every wave (the stages
-  // issued after it may stay in flight), refill the buffer freed by stage
-  // i - 1, and multiply stage i.
-  auto step = [&](auto s, int64_t i) {
-    constexpr int S = decltype(s)::value;
-    const int64_t after = issued - 1 - i;  // stages in flight behind stage i
-    static_assert((STAGES - 1) * LPS < 64, "vmcnt holds at most 63 outstanding loads");
-    StaticFor<0, STAGES>::run([&](auto q) {
-      // wait_vmcnt<N> for the largest N = n * LPS with n <= after
-      constexpr int n = STAGES - 1 - decltype(q)::value;
-      if (after == n || (n == STAGES - 1 && after > n)) wait_vmcnt<n * LPS>();
-    });
-    // Bare barrier: __syncthreads() would also wait for every load in flight.
-    // This wave's part of stage i has landed (the wait above), and the LDS
-    // reads of stage i - 1 were consumed by its matrix-core instructions.
+  int64_t issued = 0;  // K tiles whose loads have been issued
+  // Makes K tile `next` visible to every wave: wait for this wave's loads of
+  // it (the tile issued after it may stay in flight), then a bare barrier
+  // (__syncthreads() would also wait for the loads still in flight).  After
+  // the barrier every wave has also consumed the fragments of the buffer of
+  // tile next - 2, which is refilled with tile next + STAGES - 2.
+  static_assert(STAGES == 4, "the pipeline below keeps two tiles in flight in four buffers");
+  auto sync_tile = [&](int64_t next, auto tail) {
+    if constexpr (decltype(tail)::value) {
+      if (issued - 1 - next > 0) wait_vmcnt<LPS>(); else wait_vmcnt<0>();
+    } else {
+      wait_vmcnt<LPS>();
+    }
     asm volatile("" ::: "memory");
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
-    if (issued < nk) {
-      issue((S + STAGES - 1) % STAGES);
-      ++issued;
-    }
-#pragma unroll
-    for (int kk = 0; kk < KB / 16; ++kk) kstep(As + S * ASZ, Bs + S * BSZ, kk);
+  };
+  using True = std::integral_constant<bool, true>;
+  using False = std::integral_constant<bool, false>;
+  using Set0 = std::integral_constant<int, 0>;
+  using Set1 = std::integral_constant<int, 1>;
+  constexpr int KS = KB / 16;  // K=16 steps per tile (even)
+  // K tile i (fragments of its first step already requested into set 0).
+  // has_next: tile i + 1 exists; refill: tile i + STAGES - 1 exists.
+  auto tile = [&](int64_t i, auto has_next, auto refill, auto tail) {
+    const int s = static_cast<int>(i % STAGES);
+    StaticFor<0, KS>::run([&](auto kq) {
+      constexpr int kk = decltype(kq)::value;
+      using Cur = std::integral_constant<int, kk & 1>;
+      using Nxt = std::integral_constant<int, (kk + 1) & 1>;
+      if constexpr (kk + 1 < KS) {
+        read_frags(Nxt(), s, kk + 1);
+        mfmas(Cur(), nullptr);
+      } else if constexpr (decltype(has_next)::value) {
+        sync_tile(i + 1, tail);
+        read_frags(Nxt(), static_cast<int>((i + 1) % STAGES), 0);
+        if constexpr (decltype(refill)::value) {
+          const Issue is = issue_begin(static_cast<int>(issued % STAGES));
+          ++issued;
+          mfmas(Cur(), &is);
+        } else {
+          mfmas(Cur(), nullptr);
+        }
+      } else {
+        mfmas(Cur(), nullptr);
+      }
+    });
   };
 
   if (nk > 0) {
-    kp.init(p, kt0);
-    for (int s = 0; s < STAGES - 1 && issued < nk; ++s) {
-      issue(s);
+    kp.init(p, kt0, f.z, a_row0, b_row0);
+    issue(0);
+    ++issued;
+    if (nk > 1) {
+      issue(1);
       ++issued;
     }
-    for (int64_t it = 0; it < nk; it += STAGES) {
-      StaticFor<0, STAGES>::run([&](auto s) {
-        constexpr int S = decltype(s)::value;
-        if (it + S < nk) step(s, it + S);
-      });
+    sync_tile(0, True());
+    if (nk > 2) {
+      issue(2);
+      ++issued;
     }
+    read_frags(Set0(), 0, 0);
+    int64_t i = 0;
+    for (; i + 3 < nk; ++i) tile(i, True(), True(), False());
+    for (; i + 1 < nk; ++i) tile(i, True(), False(), True());
+    tile(i, False(), False(), True());
   }
   // Pin the accumulators to AGPRs across the loop: otherwise an epilogue
   // that feeds them to VALU instructions can pull part of them into VGPRs,
