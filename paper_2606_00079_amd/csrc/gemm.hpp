@@ -63,13 +63,29 @@ struct StaticFor<N, N> {
 };
 constexpr int kXcds = 8;
 
+// Operand layouts.  Row-major (kstep == 0): row r, column k at r * ld + k;
+// rows past `rows` are clamped to the last row.  K-tiled (kstep != 0, for a
+// kernel with BK-wide K steps and tiles of T rows on this side): the T x BK
+// block of row tile t and K tile q is contiguous, at t * rtile + q * kstep
+// (kstep = T * BK), rows BK elements apart inside it; every row tile is
+// allocated in full, so nothing is clamped.  A K step then reads whole cache
+// lines instead of 64-byte halves of them.
+constexpr int kTileK = 32;  // K width of a K-tiled block (must equal the kernel's K step)
 struct Side {
   const uint16_t* pass[4];  // base pointer of each pass
-  int64_t ld;               // elements between consecutive rows
+  int64_t ld;               // row-major: elements between consecutive rows
   int64_t estride;          // elements between consecutive K segments
   int64_t bstride;          // elements between batches (blockIdx.z)
-  int64_t rows;             // valid rows (rows beyond are read as zero)
+  int64_t rows;             // row-major: valid rows
+  int64_t kstep;            // K-tiled: elements between consecutive K tiles (0 = row-major)
+  int64_t rtile;            // K-tiled: elements between consecutive row tiles
 };
+
+// Element offset of (r, k) in a K-tiled matrix of K columns with T-row tiles.
+__host__ __device__ __forceinline__ int64_t tiled_offset(int64_t r, int64_t k, int64_t K, int T) {
+  return ((r / T) * (K / kTileK) + k / kTileK) * (static_cast<int64_t>(T) * kTileK) +
+         (r % T) * kTileK + (k % kTileK);
+}
 
 struct Problem {
   Side a, b;
@@ -129,8 +145,8 @@ struct PassBases {
   const uint16_t* q1;
   const uint16_t* q2;
   const uint16_t* q3;
-  __device__ __forceinline__ void init(const Side& s, int64_t z, int64_t row0) {
-    const int64_t off = z * s.bstride + row0 * s.ld;
+  __device__ __forceinline__ void init(const Side& s, int64_t z, int64_t tile, int rows_per_tile) {
+    const int64_t off = z * s.bstride + (s.kstep != 0 ? tile * s.rtile : tile * rows_per_tile * s.ld);
     q0 = s.pass[0] + off;
     q1 = s.pass[1] + off;
     q2 = s.pass[2] + off;
@@ -158,37 +174,44 @@ struct PassBases {
 template <int KB>
 struct KPos {
   int64_t seg, k0;
-  int64_t offa, offb;
+  int64_t offa, offb;    // element offsets of the tile from the pass bases
+  int64_t stepa, stepb;  // per K tile
+  int64_t jumpa, jumpb;  // extra at a segment boundary
   PassBases ba, bb;
-  __device__ __forceinline__ void init(const Problem& p, int64_t kt, int64_t z, int64_t arow0,
-                                       int64_t brow0) {
+  __device__ __forceinline__ void init(const Problem& p, int64_t kt, int64_t z, int tm, int tn,
+                                       int BM, int BN) {
     const int64_t tiles_seg = p.kseg / KB;
     const int64_t per_pass = static_cast<int64_t>(p.segs) * tiles_seg;
     const int pass = static_cast<int>(kt / per_pass);
     const int64_t rem = kt - static_cast<int64_t>(pass) * per_pass;
     seg = rem / tiles_seg;
-    k0 = (rem - seg * tiles_seg) * KB;
-    ba.init(p.a, z, arow0);
-    bb.init(p.b, z, brow0);
+    const int64_t ki = rem - seg * tiles_seg;  // K tile within the segment
+    k0 = ki * KB;
+    ba.init(p.a, z, tm, BM);
+    bb.init(p.b, z, tn, BN);
     for (int q = 0; q < pass; ++q) {
       ba.advance(true);
       bb.advance(true);
     }
     ba.make_uniform();
     bb.make_uniform();
+    stepa = uniform64(p.a.kstep != 0 ? p.a.kstep : KB);
+    stepb = uniform64(p.b.kstep != 0 ? p.b.kstep : KB);
+    jumpa = uniform64(p.a.estride - tiles_seg * stepa);
+    jumpb = uniform64(p.b.estride - tiles_seg * stepb);
     seg = uniform64(seg);
     k0 = uniform64(k0);
-    offa = uniform64(seg * p.a.estride + k0);
-    offb = uniform64(seg * p.b.estride + k0);
+    offa = uniform64(seg * p.a.estride + ki * stepa);
+    offb = uniform64(seg * p.b.estride + ki * stepb);
   }
   __device__ __forceinline__ void next(const Problem& p) {
     k0 += KB;
-    offa += KB;
-    offb += KB;
+    offa += stepa;
+    offb += stepb;
     const bool wrap = k0 == p.kseg;
     k0 = wrap ? 0 : k0;
-    offa = wrap ? offa - p.kseg + p.a.estride : offa;
-    offb = wrap ? offb - p.kseg + p.b.estride : offb;
+    offa = wrap ? offa + jumpa : offa;
+    offb = wrap ? offb + jumpb : offb;
     seg += wrap ? 1 : 0;
     const bool wrap2 = seg == p.segs;
     seg = wrap2 ? 0 : seg;
@@ -325,20 +348,23 @@ void gemm_nt_kernel(Problem p, Epi epi) {
   // are clamped to the last row: their accumulators are never stored.
   const int64_t a_row0 = static_cast<int64_t>(f.tm) * BM;
   const int64_t b_row0 = static_cast<int64_t>(f.tn) * BN;
-  uint32_t oa[AW], ob[BW];  // byte offsets from the tile's first row
+  uint32_t oa[AW], ob[BW];  // byte offsets from the tile's first element
+  const bool a_tiled = p.a.kstep != 0, b_tiled = p.b.kstep != 0;
 #pragma unroll
   for (int i = 0; i < AW; ++i) {
     const int r = (f.wave + 4 * i) * RPB + f.lane / KC;
     const int j = swz<KB>(r, f.lane % KC);
     const int64_t gr = (a_row0 + r < p.a.rows) ? a_row0 + r : p.a.rows - 1;
-    oa[i] = static_cast<uint32_t>(((gr - a_row0) * p.a.ld + 8 * j) * 2);
+    oa[i] = a_tiled ? static_cast<uint32_t>((r * KB + 8 * j) * 2)
+                    : static_cast<uint32_t>(((gr - a_row0) * p.a.ld + 8 * j) * 2);
   }
 #pragma unroll
   for (int i = 0; i < BW; ++i) {
     const int r = (f.wave + 4 * i) * RPB + f.lane / KC;
     const int j = swz<KB>(r, f.lane % KC);
     const int64_t gr = (b_row0 + r < p.b.rows) ? b_row0 + r : p.b.rows - 1;
-    ob[i] = static_cast<uint32_t>(((gr - b_row0) * p.b.ld + 8 * j) * 2);
+    ob[i] = b_tiled ? static_cast<uint32_t>((r * KB + 8 * j) * 2)
+                    : static_cast<uint32_t>(((gr - b_row0) * p.b.ld + 8 * j) * 2);
   }
   KPos<KB> kp;
   // Loads of the next K tile into stage buffer s, one wave instruction at a
@@ -457,7 +483,7 @@ void gemm_nt_kernel(Problem p, Epi epi) {
   };
 
   if (nk > 0) {
-    kp.init(p, kt0, f.z, a_row0, b_row0);
+    kp.init(p, kt0, f.z, f.tm, f.tn, BM, BN);
     issue(0);
     ++issued;
     if (nk > 1) {

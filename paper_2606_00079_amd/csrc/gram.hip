@@ -15,8 +15,9 @@ namespace {
 constexpr int GT = 256;  // tile edge of the symmetric GEMMs
 using gemm::BK;
 
-// X [n][d] -> Xt [d][npad] (bf16), rows beyond n zero.  For fp32 input the
-// value is split x = hi + lo with hi = bf16(x), lo = bf16(x - hi).
+// X [n][d] -> Xt [d_pad][npad] (bf16) in the K-tiled layout of GT-row tiles
+// (K = tokens), tokens beyond n zero.  For fp32 input the value is split
+// x = hi + lo with hi = bf16(x), lo = bf16(x - hi).
 template <bool F32>
 __global__ __launch_bounds__(256) void transpose_split_kernel(const void* __restrict__ X, int64_t n,
                                                               int64_t d, int64_t npad,
@@ -43,8 +44,9 @@ __global__ __launch_bounds__(256) void transpose_split_kernel(const void* __rest
     if (c < d && t < npad) {
       const float v = tile[tx][i];
       const uint16_t h = f32_to_bf16(v);
-      hi[c * npad + t] = h;
-      if (F32) lo[c * npad + t] = f32_to_bf16(v - bf16_to_f32(h));
+      const int64_t o = gemm::tiled_offset(c, t, npad, GT);
+      hi[o] = h;
+      if (F32) lo[o] = f32_to_bf16(v - bf16_to_f32(h));
     }
   }
 }
@@ -211,11 +213,12 @@ extern "C" bitsmoe_status bitsmoe_gram(const void* X_dev, bitsmoe_dtype xt, int6
   const int64_t npad = (n + gemm::kKAlign - 1) / gemm::kKAlign * gemm::kKAlign;
   const bool f32 = xt == BITSMOE_F32;
   bitsmoe_status st;
-  uint16_t* hi = static_cast<uint16_t*>(scratch(kScratchA, d * npad * 2, stream, &st));
+  const int64_t d_pad = (d + GT - 1) / GT * GT;  // whole K-tiled row tiles
+  uint16_t* hi = static_cast<uint16_t*>(scratch(kScratchA, d_pad * npad * 2, stream, &st));
   if (!hi) return st;
   uint16_t* lo = nullptr;
   if (f32) {
-    lo = static_cast<uint16_t*>(scratch(kScratchB, d * npad * 2, stream, &st));
+    lo = static_cast<uint16_t*>(scratch(kScratchB, d_pad * npad * 2, stream, &st));
     if (!lo) return st;
   }
   dim3 tg(static_cast<unsigned>((npad + 63) / 64), static_cast<unsigned>((d + 63) / 64));
@@ -225,8 +228,10 @@ extern "C" bitsmoe_status bitsmoe_gram(const void* X_dev, bitsmoe_dtype xt, int6
     hipLaunchKernelGGL(transpose_split_kernel<false>, tg, dim3(256), 0, s, X_dev, n, d, npad, hi, lo);
   BITSMOE_LAUNCH_CHECK("gram: transpose launch");
   gemm::Problem p{};
-  p.a.ld = p.b.ld = npad;
-  p.a.rows = p.b.rows = d;
+  static_assert(BK == gemm::kTileK, "the K-tiled operands need the kernel's K step");
+  p.a.rows = p.b.rows = d_pad;
+  p.a.kstep = p.b.kstep = static_cast<int64_t>(GT) * gemm::kTileK;
+  p.a.rtile = p.b.rtile = static_cast<int64_t>(GT) * npad;
   p.segs = 1;
   p.kseg = npad;
   if (f32) {

@@ -16,23 +16,33 @@ constexpr int PM = 128;  // basis-vector tile
 constexpr int PN = 256;  // input-channel tile
 using gemm::BK;
 
-// fp32 -> (hi, lo) bf16, same layout.
-__global__ __launch_bounds__(256) void split_f32_kernel(const float* __restrict__ x, int64_t count,
+// fp32 U^T [r][K] -> (hi, lo) bf16 in the K-tiled layout of PM-row tiles,
+// rows padded to r_pad with zeros.
+__global__ __launch_bounds__(256) void split_f32_kernel(const float* __restrict__ x, int64_t r,
+                                                        int64_t r_pad, int64_t K,
                                                         uint16_t* __restrict__ hi,
                                                         uint16_t* __restrict__ lo) {
+  const int64_t count = r_pad * K;
+  const int64_t nkt = K / gemm::kTileK;
+  constexpr int64_t TB = static_cast<int64_t>(PM) * gemm::kTileK;
   for (int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; i < count;
        i += static_cast<int64_t>(gridDim.x) * 256) {
-    const float v = x[i];
+    const int64_t t = i / TB, w = i - t * TB;
+    const int64_t row = (t / nkt) * PM + w / gemm::kTileK;
+    const int64_t k = (t % nkt) * gemm::kTileK + w % gemm::kTileK;
+    const float v = row < r ? x[row * K + k] : 0.0f;
     const uint16_t h = f32_to_bf16(v);
     hi[i] = h;
     lo[i] = f32_to_bf16(v - bf16_to_f32(h));
   }
 }
 
-// W [E][rows][cols] -> Wt [E][cols][rows] as bf16 (hi, and lo for fp32 input).
+// W [E][rows][cols] -> Wt [E][cols_pad][rows] as bf16 (hi, and lo for fp32
+// input), K-tiled with PN-row tiles (rows of Wt = columns of W; K = rows).
 template <bool F32>
 __global__ __launch_bounds__(256) void batched_transpose_kernel(const void* __restrict__ W,
                                                                 int64_t rows, int64_t cols,
+                                                                int64_t cols_pad,
                                                                 uint16_t* __restrict__ hi,
                                                                 uint16_t* __restrict__ lo) {
   __shared__ float tile[64][65];
@@ -58,16 +68,19 @@ __global__ __launch_bounds__(256) void batched_transpose_kernel(const void* __re
     if (c < cols && r < rows) {
       const float v = tile[tx][i];
       const uint16_t h = f32_to_bf16(v);
-      hi[in_off + c * rows + r] = h;
-      if (F32) lo[in_off + c * rows + r] = f32_to_bf16(v - bf16_to_f32(h));
+      const int64_t o = e * cols_pad * rows + gemm::tiled_offset(c, r, rows, PN);
+      hi[o] = h;
+      if (F32) lo[o] = f32_to_bf16(v - bf16_to_f32(h));
     }
   }
 }
 
-// bf16 W [E][rows][cols] -> Wt [E][cols][rows], 64 x 64 tiles with 16-byte
-// loads and stores (rows and cols are multiples of 64).
+// bf16 W [E][rows][cols] -> Wt [E][cols_pad][rows], K-tiled with PN-row
+// tiles; 64 x 64 blocks with 16-byte loads and stores (rows and cols are
+// multiples of 64).
 __global__ __launch_bounds__(256) void transpose_bf16_kernel(const uint16_t* __restrict__ W,
                                                              int64_t rows, int64_t cols,
+                                                             int64_t cols_pad,
                                                              uint16_t* __restrict__ Wt) {
   __shared__ __align__(16) uint16_t tile[64][72];  // 144-byte rows: 16-byte aligned, spread over banks
   const int64_t e = blockIdx.z;
@@ -94,7 +107,7 @@ __global__ __launch_bounds__(256) void transpose_bf16_kernel(const uint16_t* __r
     pk.y = v[2] | (static_cast<uint32_t>(v[3]) << 16);
     pk.z = v[4] | (static_cast<uint32_t>(v[5]) << 16);
     pk.w = v[6] | (static_cast<uint32_t>(v[7]) << 16);
-    *reinterpret_cast<uint4*>(Wt + off + (c0 + oc) * rows + r0 + orr) = pk;
+    *reinterpret_cast<uint4*>(Wt + e * cols_pad * rows + gemm::tiled_offset(c0 + oc, r0 + orr, rows, PN)) = pk;
   }
 }
 
@@ -140,37 +153,45 @@ extern "C" bitsmoe_status bitsmoe_project(const float* Ut_dev, const void* W_dev
   hipStream_t s = static_cast<hipStream_t>(stream);
   const bool f32 = wt == BITSMOE_F32;
   bitsmoe_status st;
-  // scratch A: U hi/lo [2][r][d_out];  scratch B: Wt hi (and lo) [E][d_in][d_out]
-  uint16_t* U2 = static_cast<uint16_t*>(scratch(kScratchMisc, 2 * r * d_out * 2, stream, &st));
+  // K-tiled operands: U hi/lo [2][r_pad][d_out] (PM-row tiles) and
+  // Wt hi (and lo) [E][d_in_pad][d_out] (PN-row tiles)
+  const int64_t r_pad = (r + PM - 1) / PM * PM;
+  const int64_t d_in_pad = (d_in + PN - 1) / PN * PN;
+  uint16_t* U2 = static_cast<uint16_t*>(scratch(kScratchMisc, 2 * r_pad * d_out * 2, stream, &st));
   if (!U2) return st;
-  const int64_t wcount = E * d_out * d_in;
+  const int64_t wcount = E * d_out * d_in_pad;
   uint16_t* Wt = static_cast<uint16_t*>(scratch(kScratchB, (f32 ? 2 : 1) * wcount * 2, stream, &st));
   if (!Wt) return st;
   uint16_t* Wt_lo = f32 ? Wt + wcount : nullptr;
   {
-    const int64_t count = r * d_out;
+    const int64_t count = r_pad * d_out;
     const unsigned blocks = static_cast<unsigned>(std::min<int64_t>((count + 255) / 256, 65536));
-    hipLaunchKernelGGL(split_f32_kernel, dim3(blocks), dim3(256), 0, s, Ut_dev, count, U2, U2 + count);
+    hipLaunchKernelGGL(split_f32_kernel, dim3(blocks), dim3(256), 0, s, Ut_dev, r, r_pad, d_out, U2,
+                       U2 + count);
     BITSMOE_LAUNCH_CHECK("project: split launch");
   }
   dim3 tg(static_cast<unsigned>((d_in + 63) / 64), static_cast<unsigned>((d_out + 63) / 64),
           static_cast<unsigned>(E));
   if (f32)
-    hipLaunchKernelGGL(batched_transpose_kernel<true>, tg, dim3(256), 0, s, W_dev, d_out, d_in, Wt, Wt_lo);
+    hipLaunchKernelGGL(batched_transpose_kernel<true>, tg, dim3(256), 0, s, W_dev, d_out, d_in,
+                       d_in_pad, Wt, Wt_lo);
   else
     hipLaunchKernelGGL(transpose_bf16_kernel, tg, dim3(256), 0, s,
-                       static_cast<const uint16_t*>(W_dev), d_out, d_in, Wt);
+                       static_cast<const uint16_t*>(W_dev), d_out, d_in, d_in_pad, Wt);
   BITSMOE_LAUNCH_CHECK("project: transpose launch");
 
   gemm::Problem p{};
   const uint16_t* Uhi = U2;
-  const uint16_t* Ulo = U2 + r * d_out;
-  p.a.ld = d_out;
-  p.a.rows = r;
+  const uint16_t* Ulo = U2 + r_pad * d_out;
+  static_assert(BK == gemm::kTileK, "the K-tiled operands need the kernel's K step");
+  p.a.rows = r_pad;
+  p.a.kstep = static_cast<int64_t>(PM) * gemm::kTileK;
+  p.a.rtile = static_cast<int64_t>(PM) * d_out;
   p.a.bstride = 0;
-  p.b.ld = d_out;
-  p.b.rows = d_in;
-  p.b.bstride = d_in * d_out;
+  p.b.rows = d_in_pad;
+  p.b.kstep = static_cast<int64_t>(PN) * gemm::kTileK;
+  p.b.rtile = static_cast<int64_t>(PN) * d_out;
+  p.b.bstride = d_in_pad * d_out;
   p.segs = 1;
   p.kseg = d_out;
   if (f32) {

@@ -31,16 +31,29 @@ constexpr int SKB = 32;   // K step of the loss-table GEMM
 constexpr int SSTAGES = 4;  // LDS stages (three in flight)
 using gemm::BK;
 
+// H -> bf16 H_off (zero diagonal) in the K-tiled layout of 256-row tiles
+// (rows padded to a multiple of 256 with zeros), and fp32 diag(H).
 __global__ __launch_bounds__(256) void hoff_kernel(const float* __restrict__ H, int64_t d,
-                                                   uint16_t* __restrict__ Hoff,
+                                                   int64_t d_pad, uint16_t* __restrict__ Hoff,
                                                    float* __restrict__ hdiag) {
-  const int64_t total = d * d;
+  const int64_t total = d_pad * d;
+  const int64_t nkt = d / gemm::kTileK;
+  constexpr int64_t TB = static_cast<int64_t>(SBM) * gemm::kTileK;  // elements per tiled block
   for (int64_t idx = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; idx < total;
        idx += static_cast<int64_t>(gridDim.x) * 256) {
-    const int64_t i = idx / d, k = idx - i * d;
-    const float v = H[idx];
-    Hoff[idx] = (i == k) ? uint16_t(0) : f32_to_bf16(v);
-    if (i == k) hdiag[i] = v;
+    const int64_t t = idx / TB, w = idx - t * TB;
+    const int64_t rt = t / nkt, kt = t - rt * nkt;
+    const int64_t i = rt * SBM + w / gemm::kTileK;
+    const int64_t k = kt * gemm::kTileK + w % gemm::kTileK;
+    uint16_t v = 0;
+    if (i < d) {
+      const float h = H[i * d + k];
+      if (i == k)
+        hdiag[i] = h;
+      else
+        v = f32_to_bf16(h);
+    }
+    Hoff[idx] = v;
   }
 }
 
@@ -132,7 +145,7 @@ __global__ __launch_bounds__(256) void dgen_kernel(const float* __restrict__ C, 
       pk.y = static_cast<uint32_t>(out[2]) | (static_cast<uint32_t>(out[3]) << 16);
       pk.z = static_cast<uint32_t>(out[4]) | (static_cast<uint32_t>(out[5]) << 16);
       pk.w = static_cast<uint32_t>(out[6]) | (static_cast<uint32_t>(out[7]) << 16);
-      *reinterpret_cast<uint4*>(D + (u * nb + j) * d + k) = pk;
+      *reinterpret_cast<uint4*>(D + gemm::tiled_offset(u * nb + j, k, d, SBN)) = pk;
     }
   }
 #pragma unroll
@@ -149,8 +162,9 @@ __global__ __launch_bounds__(256) void dgen_kernel(const float* __restrict__ C, 
 // per row, 32 rows per 16 KiB buffer, the 16-byte chunk c of row j stored in
 // slot c ^ (j mod 32) so that 32 lanes reading 32 rows at one chunk spread
 // over the banks.  Each lane then reads its D values (one row per column
-// fragment, four 8-byte runs per row fragment) from LDS.  Rows and columns
-// past the end are clamped on load and weighted by zero.
+// fragment, four 8-byte runs per row fragment) from LDS.  Columns past the
+// end are clamped on load and left out of the sum; rows past the end (the
+// padding of the last row tile) are computed and never stored.
 struct RowDot {
   const uint16_t* D;
   float* part;
@@ -167,16 +181,22 @@ struct RowDot {
     const int64_t i_base = static_cast<int64_t>(f.tm) * SBM;
     const int64_t j_base = static_cast<int64_t>(f.tn) * SBN;
     // 1 KiB block b holds rows 2b, 2b+1; wave w loads blocks w, w+4, ...
+    // D is K-tiled (256-row tiles, 32-wide K tiles): the block's eight K
+    // tiles are contiguous 16 KiB pieces, and rows 2b, 2b+1 of one K tile
+    // are one 128-byte line.  K tiles past the end are clamped (and weighted
+    // out below).
+    const int64_t nkt = d / gemm::kTileK;
+    const int64_t kt0 = i_base / gemm::kTileK;
+    const int kt_last = static_cast<int>(nkt - 1 - kt0);
+    const uint16_t* blk = D + (static_cast<int64_t>(f.tn) * nkt + kt0) * (SBN * gemm::kTileK);
 #pragma unroll 4
     for (int b = wave; b < 128; b += 4) {
       const int j = 2 * b + (lane >> 5);
       const int c = (lane & 31) ^ (j & 31);
-      // uniform base row of this block; the lane's row is it or the next one
-      const int64_t row0 = min(j_base + 2 * b, R - 1);
-      const int64_t row = min(j_base + j, R - 1);
-      const int64_t col = min(i_base + 8 * c, d - 8);
+      const int ktr = min(c >> 2, kt_last);
+      const uint32_t off = static_cast<uint32_t>((ktr * (SBN * gemm::kTileK) + j * gemm::kTileK + 8 * (c & 3)) * 2);
       uint16_t* dst = lds.piece(b >> 4) + (b & 15) * 512;
-      gemm::dma16(D + row0 * d, static_cast<uint32_t>(((row - row0) * d + col) * 2), dst);
+      gemm::dma16(blk, off, dst);
     }
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
@@ -197,11 +217,11 @@ struct RowDot {
           const int c = il >> 3;
           const uint2 v = *reinterpret_cast<const uint2*>(rowp + ((c ^ (jl & 31)) << 3) +
                                                           4 * (lane >> 5));
-          const float w = (i_base + il + 4 * (lane >> 5) < d) ? 1.0f : 0.0f;
-          acc += w * (bf16_to_f32(static_cast<uint16_t>(v.x & 0xffff)) * f.acc[mi][ni][4 * g + 0] +
-                      bf16_to_f32(static_cast<uint16_t>(v.x >> 16)) * f.acc[mi][ni][4 * g + 1] +
-                      bf16_to_f32(static_cast<uint16_t>(v.y & 0xffff)) * f.acc[mi][ni][4 * g + 2] +
-                      bf16_to_f32(static_cast<uint16_t>(v.y >> 16)) * f.acc[mi][ni][4 * g + 3]);
+          const float t = bf16_to_f32(static_cast<uint16_t>(v.x & 0xffff)) * f.acc[mi][ni][4 * g + 0] +
+                          bf16_to_f32(static_cast<uint16_t>(v.x >> 16)) * f.acc[mi][ni][4 * g + 1] +
+                          bf16_to_f32(static_cast<uint16_t>(v.y & 0xffff)) * f.acc[mi][ni][4 * g + 2] +
+                          bf16_to_f32(static_cast<uint16_t>(v.y >> 16)) * f.acc[mi][ni][4 * g + 3];
+          acc += (i_base + il + 4 * (lane >> 5) < d) ? t : 0.0f;
         }
       s[ni] = acc + __shfl_xor(acc, 32, 64);
     }
@@ -261,19 +281,22 @@ extern "C" bitsmoe_status bitsmoe_score(const float* C_dev, int64_t units, int64
   const int64_t tiles_n = (R + SBN - 1) / SBN;
   if (tiles_n * tiles_m > INT32_MAX) return fail(BITSMOE_ERR_SHAPE, "score: too many units");
   bitsmoe_status st;
-  uint16_t* Hoff = static_cast<uint16_t*>(scratch(kScratchA, d * d * 2, stream, &st));
+  // H_off and D are K-tiled with 256-row tiles, rows padded to whole tiles
+  const int64_t d_pad = tiles_m * static_cast<int64_t>(SBM);
+  const int64_t R_pad = tiles_n * static_cast<int64_t>(SBN);
+  uint16_t* Hoff = static_cast<uint16_t*>(scratch(kScratchA, d_pad * d * 2, stream, &st));
   if (!Hoff) return st;
   float* small = static_cast<float*>(scratch(kScratchMisc, (d + R) * sizeof(float), stream, &st));
   if (!small) return st;
   float* hdiag = small;
   float* diag = small + d;
-  uint16_t* D = static_cast<uint16_t*>(scratch(kScratchD, R * d * 2, stream, &st));
+  uint16_t* D = static_cast<uint16_t*>(scratch(kScratchD, R_pad * d * 2, stream, &st));
   if (!D) return st;
   float* part = static_cast<float*>(scratch(kScratchPart, R * tiles_m * sizeof(float), stream, &st));
   if (!part) return st;
 
-  const unsigned hb = static_cast<unsigned>(std::min<int64_t>((d * d + 255) / 256, 16384));
-  hipLaunchKernelGGL(hoff_kernel, dim3(hb), dim3(256), 0, s, H_dev, d, Hoff, hdiag);
+  const unsigned hb = static_cast<unsigned>(std::min<int64_t>((d_pad * d + 255) / 256, 16384));
+  hipLaunchKernelGGL(hoff_kernel, dim3(hb), dim3(256), 0, s, H_dev, d, d_pad, Hoff, hdiag);
   BITSMOE_LAUNCH_CHECK("score: hoff launch");
   const unsigned db = static_cast<unsigned>((units + 3) / 4);
   {
@@ -292,12 +315,15 @@ extern "C" bitsmoe_status bitsmoe_score(const float* C_dev, int64_t units, int64
   BITSMOE_LAUNCH_CHECK("score: dgen launch");
 
   gemm::Problem p{};
+  static_assert(SKB == gemm::kTileK, "the K-tiled operands need the kernel's K step");
   p.a.pass[0] = Hoff;
-  p.a.ld = d;
-  p.a.rows = d;
+  p.a.rows = d_pad;
+  p.a.kstep = static_cast<int64_t>(SBM) * gemm::kTileK;
+  p.a.rtile = static_cast<int64_t>(SBM) * d;
   p.b.pass[0] = D;
-  p.b.ld = d;
-  p.b.rows = R;
+  p.b.rows = R_pad;
+  p.b.kstep = static_cast<int64_t>(SBN) * gemm::kTileK;
+  p.b.rtile = static_cast<int64_t>(SBN) * d;
   p.passes = 1;
   p.segs = 1;
   p.kseg = d;
