@@ -435,16 +435,21 @@ void gemm_nt_kernel(Problem p, Epi epi) {
   const int64_t nk = kt1 - kt0;
   int64_t issued = 0;  // K tiles whose loads have been issued
   // Makes K tile `next` visible to every wave: wait for this wave's loads of
-  // it (the tile issued after it may stay in flight), then a bare barrier
-  // (__syncthreads() would also wait for the loads still in flight).  After
-  // the barrier every wave has also consumed the fragments of the buffer of
-  // tile next - 2, which is refilled with tile next + STAGES - 2.
-  static_assert(STAGES == 4, "the pipeline below keeps two tiles in flight in four buffers");
+  // it (the STAGES - 3 tiles issued after it may stay in flight), then a bare
+  // barrier (__syncthreads() would also wait for the loads still in flight).
+  // After the barrier every wave has also consumed the fragments of the
+  // buffer of tile next - 2, which is refilled with tile next + STAGES - 2.
+  static_assert(STAGES >= 3, "one buffer being read, one about to be read, one or more in flight");
+  static_assert((STAGES - 3) * LPS < 64, "vmcnt holds at most 63 outstanding loads");
   auto sync_tile = [&](int64_t next, auto tail) {
     if constexpr (decltype(tail)::value) {
-      if (issued - 1 - next > 0) wait_vmcnt<LPS>(); else wait_vmcnt<0>();
+      const int64_t after = issued - 1 - next;  // 0 .. STAGES - 3
+      StaticFor<0, STAGES - 2>::run([&](auto q) {
+        constexpr int n = decltype(q)::value;
+        if (after == n) wait_vmcnt<n * LPS>();
+      });
     } else {
-      wait_vmcnt<LPS>();
+      wait_vmcnt<(STAGES - 3) * LPS>();
     }
     asm volatile("" ::: "memory");
     __builtin_amdgcn_s_barrier();
@@ -453,7 +458,6 @@ void gemm_nt_kernel(Problem p, Epi epi) {
   using True = std::integral_constant<bool, true>;
   using False = std::integral_constant<bool, false>;
   using Set0 = std::integral_constant<int, 0>;
-  using Set1 = std::integral_constant<int, 1>;
   constexpr int KS = KB / 16;  // K=16 steps per tile (even)
   // K tile i (fragments of its first step already requested into set 0).
   // has_next: tile i + 1 exists; refill: tile i + STAGES - 1 exists.
@@ -484,20 +488,19 @@ void gemm_nt_kernel(Problem p, Epi epi) {
 
   if (nk > 0) {
     kp.init(p, kt0, f.z, f.tm, f.tn, BM, BN);
-    issue(0);
-    ++issued;
-    if (nk > 1) {
-      issue(1);
+    // tiles 0 .. STAGES - 3 up front, tile STAGES - 2 once tile 0 is visible
+    for (int q = 0; q < STAGES - 2 && issued < nk; ++q) {
+      issue(q);
       ++issued;
     }
     sync_tile(0, True());
-    if (nk > 2) {
-      issue(2);
+    if (issued < nk) {
+      issue(STAGES - 2);
       ++issued;
     }
     read_frags(Set0(), 0, 0);
     int64_t i = 0;
-    for (; i + 3 < nk; ++i) tile(i, True(), True(), False());
+    for (; i + STAGES - 1 < nk; ++i) tile(i, True(), True(), False());
     for (; i + 1 < nk; ++i) tile(i, True(), False(), True());
     tile(i, False(), False(), True());
   }

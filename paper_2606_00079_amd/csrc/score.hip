@@ -28,7 +28,7 @@ namespace {
 constexpr int SBM = 256;  // i (H row) tile
 constexpr int SBN = 256;  // D row tile
 constexpr int SKB = 32;   // K step of the loss-table GEMM
-constexpr int SSTAGES = 4;  // LDS stages (three in flight)
+constexpr int SSTAGES = 4;  // LDS stages (two K tiles in flight)
 using gemm::BK;
 
 // H -> bf16 H_off (zero diagonal) in the K-tiled layout of 256-row tiles
@@ -175,7 +175,7 @@ struct RowDot {
     static_assert(SBM == 256 && SBN == 256, "layout below assumes 256 x 256 tiles");
     static_assert(SSTAGES * SBM * SKB * 2 + SSTAGES * SBN * SKB * 2 >= 8 * 16384,
                   "stage buffers must hold the 256 x 256 bf16 D block");
-    __shared__ float red[2][SBN];  // cross-wave reduction
+    __shared__ float red[2 * SBN];  // cross-wave reduction
     const int lane = opaque(f.lane);
     const int wave = lane >= 0 ? f.wave : 0;  // ties wave to the opaque lane
     const int64_t i_base = static_cast<int64_t>(f.tm) * SBM;
@@ -228,12 +228,12 @@ struct RowDot {
     // combine the waves that share these rows (wm = 0, 1)
     if ((lane >> 5) == 0) {
 #pragma unroll
-      for (int ni = 0; ni < F::FN; ++ni) red[f.wm][f.wn * F::WN + 32 * ni + lane] = s[ni];
+      for (int ni = 0; ni < F::FN; ++ni) red[f.wm * SBN + f.wn * F::WN + 32 * ni + lane] = s[ni];
     }
     __syncthreads();
     for (int t = threadIdx.x; t < SBN; t += gemm::kThreads) {
       const int64_t row = j_base + t;
-      if (row < R) part[row * tiles_m + f.tm] = red[0][t] + red[1][t];
+      if (row < R) part[row * tiles_m + f.tm] = red[t] + red[SBN + t];
     }
   }
 };
