@@ -11,6 +11,7 @@
 //
 // Kernel shape: a BM x BN workgroup tile, 4 waves of 64 lanes in a 2 x 2
 // grid, each wave owning a (BM/2) x (BN/2) block of v_mfma_f32_32x32x16_bf16
+// (or _f16 when the operands are fp16)
 // accumulators.  K advances 32 at a time through four LDS stages filled by
 // direct global->LDS loads (global_load_lds_dwordx4), so three stages are in
 // flight while one is multiplied; the stages are distinct LDS arrays and the
@@ -300,7 +301,23 @@ struct Frag {
   __device__ __forceinline__ int col(int ni) const { return col0 + 32 * ni + (lane & 31); }
 };
 
-template <int BM, int BN, int KB, int STAGES, class Epi>
+// 16-bit operand element: bf16 (default) or fp16.
+template <bool F16>
+struct Operand {
+  typedef bf16x8 vec;
+  static __device__ __forceinline__ f32x16 mfma(vec a, vec b, f32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+  }
+};
+template <>
+struct Operand<true> {
+  typedef f16x8 vec;
+  static __device__ __forceinline__ f32x16 mfma(vec a, vec b, f32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
+  }
+};
+
+template <int BM, int BN, int KB, int STAGES, class Epi, bool F16 = false>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void gemm_nt_kernel(Problem p, Epi epi) {
   static_assert(BM % 64 == 0 && BN % 64 == 0, "tile");
@@ -396,7 +413,8 @@ void gemm_nt_kernel(Problem p, Epi epi) {
   const int jq = f.lane >> 5;
   // Two register sets of operand fragments: while the matrix cores work on
   // one K=16 step, the fragments of the next step are read into the other.
-  bf16x8 fa[2][F::FM], fb[2][F::FN];
+  using Op = Operand<F16>;
+  typename Op::vec fa[2][F::FM], fb[2][F::FN];
   auto read_frags = [&](auto set, int s, int kk) {
     constexpr int T = decltype(set)::value;
     const uint16_t* la = As + s * ASZ;
@@ -404,10 +422,10 @@ void gemm_nt_kernel(Problem p, Epi epi) {
     const int j = 2 * kk + jq;
 #pragma unroll
     for (int mi = 0; mi < F::FM; ++mi)
-      fa[T][mi] = *reinterpret_cast<const bf16x8*>(&la[lds_off<KB>(arow + 32 * mi, j)]);
+      fa[T][mi] = *reinterpret_cast<const typename Op::vec*>(&la[lds_off<KB>(arow + 32 * mi, j)]);
 #pragma unroll
     for (int ni = 0; ni < F::FN; ++ni)
-      fb[T][ni] = *reinterpret_cast<const bf16x8*>(&lb[lds_off<KB>(brow + 32 * ni, j)]);
+      fb[T][ni] = *reinterpret_cast<const typename Op::vec*>(&lb[lds_off<KB>(brow + 32 * ni, j)]);
   };
   // The matrix-core ops of one K=16 step from fragment set `set`; with a
   // refill, its LPS loads are issued one after each of the first LPS ops.
@@ -421,7 +439,7 @@ void gemm_nt_kernel(Problem p, Epi epi) {
     for (int mi = 0; mi < F::FM; ++mi)
 #pragma unroll
       for (int ni = 0; ni < F::FN; ++ni) {
-        f.acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[T][mi], fb[T][ni], f.acc[mi][ni], 0, 0, 0);
+        f.acc[mi][ni] = Op::mfma(fa[T][mi], fb[T][ni], f.acc[mi][ni]);
         const int q = mi * F::FN + ni;
         if (is != nullptr && q < LPS) {
           __builtin_amdgcn_sched_barrier(0);

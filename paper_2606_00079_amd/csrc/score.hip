@@ -7,14 +7,22 @@
 //     delta H delta^T = sum_k H_kk delta_k^2  +  delta H_off delta^T,
 // the diagonal part is summed in fp32 from the fp32 error, and the
 // off-diagonal part, a GEMM of the error rows with H_off, runs on the matrix
-// cores in bf16 with fp32 accumulation:
-//   1. hoff_kernel   H -> bf16 H_off (zero diagonal) and fp32 diag(H)
-//   2. dgen_kernel   one wave per unit: group min/max, fake-quant at every
-//                    width, bf16 error rows D[u*nb + j][:] and the diagonal
-//                    term of each (u, j)
+// cores in fp16 with fp32 accumulation.  Both fp16 operands are scaled by
+// exact powers of two into the upper half of the fp16 range: H_off by 2^F
+// (from max |H|), the error rows of unit u by 2^E_u (from max |c_u|), so
+// that rows of any magnitude keep fp16's 11-bit precision; the partial sums
+// are scaled back by 2^-(2 E_u + F).  (bf16 operands, 8-bit precision, leave
+// per-entry errors close to 1e-3 on strongly correlated H; fp16 keeps them
+// near 1e-4 at the same matrix-core rate.)
+//   1. habsmax_kernel, hoff_kernel
+//                    H -> scaled fp16 H_off (zero diagonal), fp32 diag(H)
+//   2. dgen_kernel   one wave per unit: max |c_u|, group min/max, fake-quant
+//                    at every width, scaled fp16 error rows D[u*nb + j][:] and
+//                    the diagonal term of each (u, j)
 //   3. gemm          acc[i][row] = sum_k H_off[i][k] D[row][k], epilogue
-//                    sum_i D[row][i] acc[i][row] per 128-wide i tile
-//   4. finalize      L = diagonal term + the tile partials, in a fixed order.
+//                    sum_i D[row][i] acc[i][row] per 256-wide i tile
+//   4. finalize      L = diagonal term + the unscaled tile partials, in a fixed
+//                    order.
 #include <algorithm>
 
 #include "bitsmoe.h"
@@ -31,11 +39,57 @@ constexpr int SKB = 32;   // K step of the loss-table GEMM
 constexpr int SSTAGES = 4;  // LDS stages (two K tiles in flight)
 using gemm::BK;
 
-// H -> bf16 H_off (zero diagonal) in the K-tiled layout of 256-row tiles
-// (rows padded to a multiple of 256 with zeros), and fp32 diag(H).
+constexpr int kAbsMaxBlocks = 256;  // partial maxima of |H_off|
+constexpr int kF16Top = 14;         // scaled fp16 operands stay below 2^14
+
+// Exponent e with 0 <= v < 2^e (v finite, >= 0); 0 for v == 0.
+__device__ __forceinline__ int exponent_above(float v) {
+  int e = 0;
+  (void)frexpf(v, &e);  // v = m 2^e, 0.5 <= m < 1
+  return v > 0.0f ? e : 0;
+}
+
+// Partial maxima of |H_ik| over the whole matrix (a bound for the
+// off-diagonal maximum), one per block; d * d is a multiple of 4.
+__global__ __launch_bounds__(256) void habsmax_kernel(const float* __restrict__ H, int64_t d,
+                                                      float* __restrict__ partial) {
+  __shared__ float red[256];
+  float m = 0.0f;
+  const int64_t n4 = d * d / 4;
+  for (int64_t idx = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; idx < n4;
+       idx += static_cast<int64_t>(gridDim.x) * 256) {
+    const float4 v = reinterpret_cast<const float4*>(H)[idx];
+    m = fmaxf(m, fmaxf(fmaxf(fabsf(v.x), fabsf(v.y)), fmaxf(fabsf(v.z), fabsf(v.w))));
+  }
+  red[threadIdx.x] = m;
+  __syncthreads();
+  for (int o = 128; o > 0; o >>= 1) {
+    if (threadIdx.x < o) red[threadIdx.x] = fmaxf(red[threadIdx.x], red[threadIdx.x + o]);
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) partial[blockIdx.x] = red[0];
+}
+
+// H -> fp16 H_off * 2^F (zero diagonal) in the K-tiled layout of 256-row
+// tiles (rows padded to a multiple of 256 with zeros), and fp32 diag(H).
+// F = kF16Top - e(max |H|); block 0 also stores F for the finalize step.
 __global__ __launch_bounds__(256) void hoff_kernel(const float* __restrict__ H, int64_t d,
-                                                   int64_t d_pad, uint16_t* __restrict__ Hoff,
-                                                   float* __restrict__ hdiag) {
+                                                   int64_t d_pad, const float* __restrict__ partial,
+                                                   uint16_t* __restrict__ Hoff,
+                                                   float* __restrict__ hdiag, int* __restrict__ hexp) {
+  __shared__ int sF;
+  if (threadIdx.x < 64) {  // wave 0 reduces the partial maxima
+    float m = 0.0f;
+    for (int b = threadIdx.x; b < kAbsMaxBlocks; b += 64) m = fmaxf(m, partial[b]);
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
+    if (threadIdx.x == 0) {
+      sF = kF16Top - exponent_above(m);
+      if (blockIdx.x == 0) *hexp = sF;
+    }
+  }
+  __syncthreads();
+  const int F = sF;
   const int64_t total = d_pad * d;
   const int64_t nkt = d / gemm::kTileK;
   constexpr int64_t TB = static_cast<int64_t>(SBM) * gemm::kTileK;  // elements per tiled block
@@ -51,7 +105,7 @@ __global__ __launch_bounds__(256) void hoff_kernel(const float* __restrict__ H, 
       if (i == k)
         hdiag[i] = h;
       else
-        v = f32_to_bf16(h);
+        v = f32_to_f16_bits(ldexpf(h, F));
     }
     Hoff[idx] = v;
   }
@@ -67,12 +121,17 @@ struct QuantBits {
 // consecutive lanes.  Codes follow the fp64 rule exactly: the fp32 quotient
 // is used unless it lies within 1e-4 of a rounding boundary (its error is
 // below 5e-5 for codes up to 255), in which case fp64 decides.
-template <int NB>
+// Rows of at most kRegChunks * 512 entries are held in registers between
+// the max |c| pass and the quantization pass (C is read once) when there are
+// at most four widths; otherwise rows are read twice.
+constexpr int kRegChunks = 8;
+
+template <int NB, bool CACHED>
 __global__ __launch_bounds__(256) void dgen_kernel(const float* __restrict__ C, int64_t units,
                                                    int64_t d, int G, QuantBits qb,
                                                    const float* __restrict__ hdiag,
                                                    uint16_t* __restrict__ D,
-                                                   float* __restrict__ diag) {
+                                                   float* __restrict__ diag, int* __restrict__ uexp) {
   const int lane = threadIdx.x & 63;
   const int64_t u = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
   if (u >= units) return;  // whole wave exits together
@@ -82,24 +141,52 @@ __global__ __launch_bounds__(256) void dgen_kernel(const float* __restrict__ C, 
 #pragma unroll
   for (int j = 0; j < NB; ++j) dacc[j] = 0.0f;
   const float* crow = C + u * d;
-  for (int64_t k0 = 0; k0 < d; k0 += 512) {
+
+  // lane's 8 entries of the 512-entry chunk at k0 (zeros past the end)
+  auto load8 = [&](int64_t k0, float (&c)[8]) {
     const int64_t k = k0 + 8 * lane;
-    const bool active = k < d;
-    float c[8];
-    float hd[8];
-    if (active) {
+    if (k < d) {
       const float4 v0 = *reinterpret_cast<const float4*>(crow + k);
       const float4 v1 = *reinterpret_cast<const float4*>(crow + k + 4);
       c[0] = v0.x; c[1] = v0.y; c[2] = v0.z; c[3] = v0.w;
       c[4] = v1.x; c[5] = v1.y; c[6] = v1.z; c[7] = v1.w;
-      const float4 h0 = *reinterpret_cast<const float4*>(hdiag + k);
-      const float4 h1 = *reinterpret_cast<const float4*>(hdiag + k + 4);
-      hd[0] = h0.x; hd[1] = h0.y; hd[2] = h0.z; hd[3] = h0.w;
-      hd[4] = h1.x; hd[5] = h1.y; hd[6] = h1.z; hd[7] = h1.w;
     } else {
 #pragma unroll
-      for (int i = 0; i < 8; ++i) c[i] = hd[i] = 0.0f;
+      for (int i = 0; i < 8; ++i) c[i] = 0.0f;
     }
+  };
+  auto absmax8 = [](const float (&c)[8]) {
+    float m = 0.0f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) m = fmaxf(m, fabsf(c[i]));
+    return m;
+  };
+
+  // |delta| <= max - min <= 2 max |c| < 2^(e + 1): the error rows are stored
+  // as fp16(delta * 2^E) with E = kF16Top - 1 - e
+  float cc[CACHED ? kRegChunks : 1][8];
+  float amax = 0.0f;
+  if constexpr (CACHED) {
+#pragma unroll
+    for (int ch = 0; ch < kRegChunks; ++ch) {
+      load8(512 * ch, cc[ch]);
+      amax = fmaxf(amax, absmax8(cc[ch]));
+    }
+  } else {
+    for (int64_t k0 = 0; k0 < d; k0 += 512) {
+      load8(k0, cc[0]);
+      amax = fmaxf(amax, absmax8(cc[0]));
+    }
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) amax = fmaxf(amax, __shfl_xor(amax, o, 64));
+  const int E = kF16Top - 1 - exponent_above(amax);
+  if (lane == 0) uexp[u] = E;
+
+  // quantize one 512-entry chunk at every width
+  auto chunk = [&](int64_t k0, const float (&c)[8]) {
+    const int64_t k = k0 + 8 * lane;
+    const bool active = k < d;
     float mn = c[0], mx = c[0];
 #pragma unroll
     for (int i = 1; i < 8; ++i) {
@@ -110,7 +197,12 @@ __global__ __launch_bounds__(256) void dgen_kernel(const float* __restrict__ C, 
       mn = fminf(mn, __shfl_xor(mn, o, 64));
       mx = fmaxf(mx, __shfl_xor(mx, o, 64));
     }
-    if (!active) continue;
+    if (!active) return;
+    float hd[8];
+    const float4 h0 = *reinterpret_cast<const float4*>(hdiag + k);
+    const float4 h1 = *reinterpret_cast<const float4*>(hdiag + k + 4);
+    hd[0] = h0.x; hd[1] = h0.y; hd[2] = h0.z; hd[3] = h0.w;
+    hd[4] = h1.x; hd[5] = h1.y; hd[6] = h1.z; hd[7] = h1.w;
     const float mf = f16_bits_to_f32(f32_to_f16_bits(mn));
     const float range = mx - mn;
 #pragma unroll
@@ -137,7 +229,7 @@ __global__ __launch_bounds__(256) void dgen_kernel(const float* __restrict__ C, 
         }
         const float xh = fmaf(q, sf, mf);
         const float dl = c[i] - xh;
-        out[i] = f32_to_bf16(dl);
+        out[i] = f32_to_f16_bits(ldexpf(dl, E));
         dacc[j] = fmaf(hd[i] * dl, dl, dacc[j]);
       }
       uint4 pk;
@@ -146,6 +238,16 @@ __global__ __launch_bounds__(256) void dgen_kernel(const float* __restrict__ C, 
       pk.z = static_cast<uint32_t>(out[4]) | (static_cast<uint32_t>(out[5]) << 16);
       pk.w = static_cast<uint32_t>(out[6]) | (static_cast<uint32_t>(out[7]) << 16);
       *reinterpret_cast<uint4*>(D + gemm::tiled_offset(u * nb + j, k, d, SBN)) = pk;
+    }
+  };
+  if constexpr (CACHED) {
+#pragma unroll
+    for (int ch = 0; ch < kRegChunks; ++ch)
+      if (512 * ch < d) chunk(512 * ch, cc[ch]);
+  } else {
+    for (int64_t k0 = 0; k0 < d; k0 += 512) {
+      load8(k0, cc[0]);
+      chunk(k0, cc[0]);
     }
   }
 #pragma unroll
@@ -217,10 +319,10 @@ struct RowDot {
           const int c = il >> 3;
           const uint2 v = *reinterpret_cast<const uint2*>(rowp + ((c ^ (jl & 31)) << 3) +
                                                           4 * (lane >> 5));
-          const float t = bf16_to_f32(static_cast<uint16_t>(v.x & 0xffff)) * f.acc[mi][ni][4 * g + 0] +
-                          bf16_to_f32(static_cast<uint16_t>(v.x >> 16)) * f.acc[mi][ni][4 * g + 1] +
-                          bf16_to_f32(static_cast<uint16_t>(v.y & 0xffff)) * f.acc[mi][ni][4 * g + 2] +
-                          bf16_to_f32(static_cast<uint16_t>(v.y >> 16)) * f.acc[mi][ni][4 * g + 3];
+          const float t = f16_bits_to_f32(static_cast<uint16_t>(v.x & 0xffff)) * f.acc[mi][ni][4 * g + 0] +
+                          f16_bits_to_f32(static_cast<uint16_t>(v.x >> 16)) * f.acc[mi][ni][4 * g + 1] +
+                          f16_bits_to_f32(static_cast<uint16_t>(v.y & 0xffff)) * f.acc[mi][ni][4 * g + 2] +
+                          f16_bits_to_f32(static_cast<uint16_t>(v.y >> 16)) * f.acc[mi][ni][4 * g + 3];
           acc += (i_base + il + 4 * (lane >> 5) < d) ? t : 0.0f;
         }
       s[ni] = acc + __shfl_xor(acc, 32, 64);
@@ -238,15 +340,19 @@ struct RowDot {
   }
 };
 
+// L = diagonal term + (sum of the tile partials, in tile order) * 2^-(2 E_u + F).
 __global__ __launch_bounds__(256) void finalize_kernel(const float* __restrict__ diag,
                                                        const float* __restrict__ part, int64_t R,
-                                                       int tiles_m, float* __restrict__ L) {
+                                                       int tiles_m, int nb,
+                                                       const int* __restrict__ uexp,
+                                                       const int* __restrict__ hexp,
+                                                       float* __restrict__ L) {
   const int64_t row = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
   if (row >= R) return;
-  float s = diag[row];
   const float* p = part + row * tiles_m;
+  float s = 0.0f;
   for (int t = 0; t < tiles_m; ++t) s += p[t];
-  L[row] = s;
+  L[row] = diag[row] + ldexpf(s, -(2 * uexp[row / nb] + *hexp));
 }
 
 }  // namespace
@@ -286,26 +392,38 @@ extern "C" bitsmoe_status bitsmoe_score(const float* C_dev, int64_t units, int64
   const int64_t R_pad = tiles_n * static_cast<int64_t>(SBN);
   uint16_t* Hoff = static_cast<uint16_t*>(scratch(kScratchA, d_pad * d * 2, stream, &st));
   if (!Hoff) return st;
-  float* small = static_cast<float*>(scratch(kScratchMisc, (d + R) * sizeof(float), stream, &st));
+  // small tables: diag(H) [d], diagonal terms [R], unit exponents [units],
+  // partial maxima of |H_off| [kAbsMaxBlocks], the H_off exponent [1]
+  const int64_t small_words = d + R + units + kAbsMaxBlocks + 1;
+  float* small = static_cast<float*>(scratch(kScratchMisc, small_words * sizeof(float), stream, &st));
   if (!small) return st;
   float* hdiag = small;
-  float* diag = small + d;
+  float* diag = hdiag + d;
+  int* uexp = reinterpret_cast<int*>(diag + R);
+  float* hpart = reinterpret_cast<float*>(uexp + units);
+  int* hexp = reinterpret_cast<int*>(hpart + kAbsMaxBlocks);
   uint16_t* D = static_cast<uint16_t*>(scratch(kScratchD, R_pad * d * 2, stream, &st));
   if (!D) return st;
   float* part = static_cast<float*>(scratch(kScratchPart, R * tiles_m * sizeof(float), stream, &st));
   if (!part) return st;
 
+  hipLaunchKernelGGL(habsmax_kernel, dim3(kAbsMaxBlocks), dim3(256), 0, s, H_dev, d, hpart);
+  BITSMOE_LAUNCH_CHECK("score: habsmax launch");
   const unsigned hb = static_cast<unsigned>(std::min<int64_t>((d_pad * d + 255) / 256, 16384));
-  hipLaunchKernelGGL(hoff_kernel, dim3(hb), dim3(256), 0, s, H_dev, d, d_pad, Hoff, hdiag);
+  hipLaunchKernelGGL(hoff_kernel, dim3(hb), dim3(256), 0, s, H_dev, d, d_pad, hpart, Hoff, hdiag, hexp);
   BITSMOE_LAUNCH_CHECK("score: hoff launch");
   const unsigned db = static_cast<unsigned>((units + 3) / 4);
   {
   KernelTimer dgen_timer("score_dgen", stream);
   switch (nbits) {
-#define BITSMOE_DGEN(NB)                                                                       \
-  case NB:                                                                                     \
-    hipLaunchKernelGGL(dgen_kernel<NB>, dim3(db), dim3(256), 0, s, C_dev, units, d, group, qb, \
-                       hdiag, D, diag);                                                        \
+#define BITSMOE_DGEN(NB)                                                                         \
+  case NB:                                                                                       \
+    if (NB <= 4 && d <= 512 * kRegChunks)                                                        \
+      hipLaunchKernelGGL((dgen_kernel<NB, (NB <= 4)>), dim3(db), dim3(256), 0, s, C_dev, units, d, \
+                         group, qb, hdiag, D, diag, uexp);                                       \
+    else                                                                                         \
+      hipLaunchKernelGGL((dgen_kernel<NB, false>), dim3(db), dim3(256), 0, s, C_dev, units, d,   \
+                         group, qb, hdiag, D, diag, uexp);                                       \
     break;
     BITSMOE_DGEN(1) BITSMOE_DGEN(2) BITSMOE_DGEN(3) BITSMOE_DGEN(4)
     BITSMOE_DGEN(5) BITSMOE_DGEN(6) BITSMOE_DGEN(7) BITSMOE_DGEN(8)
@@ -337,12 +455,12 @@ extern "C" bitsmoe_status bitsmoe_score(const float* C_dev, int64_t units, int64
   dim3 grid(static_cast<unsigned>(tiles_m * tiles_n), 1, 1);
   {
     KernelTimer timer("score_gemm", stream);
-    hipLaunchKernelGGL((gemm::gemm_nt_kernel<SBM, SBN, SKB, SSTAGES, RowDot>), grid, dim3(gemm::kThreads),
-                       0, s, p, epi);
+    hipLaunchKernelGGL((gemm::gemm_nt_kernel<SBM, SBN, SKB, SSTAGES, RowDot, true>), grid,
+                       dim3(gemm::kThreads), 0, s, p, epi);
   }
   BITSMOE_LAUNCH_CHECK("score: gemm launch");
   hipLaunchKernelGGL(finalize_kernel, dim3(static_cast<unsigned>((R + 255) / 256)), dim3(256), 0, s,
-                     diag, part, R, tiles_m, L_dev);
+                     diag, part, R, tiles_m, nbits, uexp, hexp, L_dev);
   BITSMOE_LAUNCH_CHECK("score: finalize launch");
   return ok();
 }
