@@ -146,13 +146,17 @@ bitsmoe_status bitsmoe_project(const float* Ut_dev, const void* W_dev, bitsmoe_d
  * the per-component term of the exact output-space loss
  * sum_k alpha_k^2 eps_k^T H eps_k (App. B.2, Eq. app_down_exact_metric).
  *   C_dev      [units][d] fp32
- *   H_dev      [d][d] fp32 symmetric positive semidefinite
+ *   H_dev      [d][d] fp32 symmetric positive semidefinite (as bitsmoe_gram
+ *              writes it); the call relies on the symmetry and reads the
+ *              upper triangle of 256 x 256 blocks and the diagonal
  *   bits_host  [nbits] widths, strictly ascending, each in 1..8
  *   L_dev      [units][nbits] fp32 output
  * Shape rules: d % 64 == 0, group in {32, 64, 128, 256}, d % group == 0,
  * 1 <= nbits <= 8.
- * Accuracy: the off-diagonal part of H enters through bf16 matrix-core
- * products with fp32 accumulation; the diagonal part is added in fp32.
+ * Accuracy: the off-diagonal part of H enters through fp16 matrix-core
+ * products of operands scaled by exact powers of two (per row for the
+ * errors, per call for H), with fp32 accumulation; the diagonal part is
+ * added in fp32.  Per-entry relative error is typically ~1e-4.
  */
 bitsmoe_status bitsmoe_score(const float* C_dev, int64_t units, int64_t d, const float* H_dev,
                              const int* bits_host, int nbits, int group, float* L_dev,

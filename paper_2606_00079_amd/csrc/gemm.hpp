@@ -98,6 +98,8 @@ struct Problem {
   int tiles_m, tiles_n;
   int symmetric;     // 1: only tiles with tm <= tn are launched (gridDim.x = T(T+1)/2)
   int group_n;       // column tiles per ordering group (non-symmetric)
+  int ktri;          // 1 (no split-K): row tile tm only visits K tiles from tm * BM / KB on
+                     // (the A operand's upper block triangle)
 };
 
 // XCD-contiguous logical id of the linear workgroup id t (of n in total).
@@ -355,8 +357,9 @@ void gemm_nt_kernel(Problem p, Epi epi) {
       for (int r = 0; r < 16; ++r) f.acc[mi][ni][r] = 0.0f;
 
   const int64_t ktiles = p.ktiles * BK / KB;  // K tiles of this kernel's step
-  const int64_t kt0 = ktiles * f.ks / p.splits;
+  int64_t kt0 = ktiles * f.ks / p.splits;
   const int64_t kt1 = ktiles * (f.ks + 1) / p.splits;
+  if (p.ktri) kt0 = static_cast<int64_t>(f.tm) * (BM / KB);
 
   // Direct global->LDS loads.  Wave instruction i of this wave fills the
   // 1 KiB LDS block b = wave + 4 i (rows b*RPB .. b*RPB+RPB-1); lane l lands

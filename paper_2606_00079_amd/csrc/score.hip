@@ -19,7 +19,9 @@
 //   2. dgen_kernel   one wave per unit: max |c_u|, group min/max, fake-quant
 //                    at every width, scaled fp16 error rows D[u*nb + j][:] and
 //                    the diagonal term of each (u, j)
-//   3. gemm          acc[i][row] = sum_k H_off[i][k] D[row][k], epilogue
+//   3. gemm          acc[i][row] = sum_k H'[i][k] D[row][k] over the k blocks at
+//                    and right of i's block (H' = H_off there, doubled right of
+//                    the diagonal block: H is symmetric), epilogue
 //                    sum_i D[row][i] acc[i][row] per 256-wide i tile
 //   4. finalize      L = diagonal term + the unscaled tile partials, in a fixed
 //                    order.
@@ -72,7 +74,11 @@ __global__ __launch_bounds__(256) void habsmax_kernel(const float* __restrict__ 
 
 // H -> fp16 H_off * 2^F (zero diagonal) in the K-tiled layout of 256-row
 // tiles (rows padded to a multiple of 256 with zeros), and fp32 diag(H).
-// F = kF16Top - e(max |H|); block 0 also stores F for the finalize step.
+// H is symmetric and the GEMM reads only the upper block triangle: row tile
+// t uses column blocks t (weight 1) and t + 1, ... (weight 2, which stands
+// for the mirrored lower blocks); blocks left of the diagonal are never read.
+// F = kF16Top - 1 - e(max |H|), so that doubled entries stay below 2^14;
+// block 0 also stores F for the finalize step.
 __global__ __launch_bounds__(256) void hoff_kernel(const float* __restrict__ H, int64_t d,
                                                    int64_t d_pad, const float* __restrict__ partial,
                                                    uint16_t* __restrict__ Hoff,
@@ -84,7 +90,7 @@ __global__ __launch_bounds__(256) void hoff_kernel(const float* __restrict__ H, 
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
     if (threadIdx.x == 0) {
-      sF = kF16Top - exponent_above(m);
+      sF = kF16Top - 1 - exponent_above(m);
       if (blockIdx.x == 0) *hexp = sF;
     }
   }
@@ -104,8 +110,8 @@ __global__ __launch_bounds__(256) void hoff_kernel(const float* __restrict__ H, 
       const float h = H[i * d + k];
       if (i == k)
         hdiag[i] = h;
-      else
-        v = f32_to_f16_bits(ldexpf(h, F));
+      else if (k / SBM >= i / SBM)  // at or right of the diagonal block
+        v = f32_to_f16_bits(ldexpf(h, k / SBM > i / SBM ? F + 1 : F));
     }
     Hoff[idx] = v;
   }
@@ -451,6 +457,7 @@ extern "C" bitsmoe_status bitsmoe_score(const float* C_dev, int64_t units, int64
   p.tiles_n = static_cast<int>(tiles_n);
   p.symmetric = 0;
   p.group_n = std::max(1, 32 / tiles_m);  // ~one XCD's worth of workgroups per group
+  p.ktri = 1;  // H symmetric: upper block triangle of H_off only
   RowDot epi{D, part, R, d, tiles_m};
   dim3 grid(static_cast<unsigned>(tiles_m * tiles_n), 1, 1);
   {
