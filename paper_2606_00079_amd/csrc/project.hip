@@ -12,19 +12,20 @@
 namespace bitsmoe {
 namespace {
 
-constexpr int PM = 128;  // basis-vector tile
+// Basis-vector tile: 256, 192 or 128 rows, the largest that pads r least
+// (taller tiles read fewer LDS fragments per matrix-core op).
 constexpr int PN = 256;  // input-channel tile
 using gemm::BK;
 
 // fp32 U^T [r][K] -> (hi, lo) bf16 in the K-tiled layout of PM-row tiles,
 // rows padded to r_pad with zeros.
 __global__ __launch_bounds__(256) void split_f32_kernel(const float* __restrict__ x, int64_t r,
-                                                        int64_t r_pad, int64_t K,
+                                                        int64_t r_pad, int64_t K, int PM,
                                                         uint16_t* __restrict__ hi,
                                                         uint16_t* __restrict__ lo) {
   const int64_t count = r_pad * K;
   const int64_t nkt = K / gemm::kTileK;
-  constexpr int64_t TB = static_cast<int64_t>(PM) * gemm::kTileK;
+  const int64_t TB = static_cast<int64_t>(PM) * gemm::kTileK;
   for (int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; i < count;
        i += static_cast<int64_t>(gridDim.x) * 256) {
     const int64_t t = i / TB, w = i - t * TB;
@@ -155,6 +156,9 @@ extern "C" bitsmoe_status bitsmoe_project(const float* Ut_dev, const void* W_dev
   bitsmoe_status st;
   // K-tiled operands: U hi/lo [2][r_pad][d_out] (PM-row tiles) and
   // Wt hi (and lo) [E][d_in_pad][d_out] (PN-row tiles)
+  int PM = 256;
+  for (int t : {192, 128})
+    if ((r + t - 1) / t * t < (r + PM - 1) / PM * PM) PM = t;
   const int64_t r_pad = (r + PM - 1) / PM * PM;
   const int64_t d_in_pad = (d_in + PN - 1) / PN * PN;
   uint16_t* U2 = static_cast<uint16_t*>(scratch(kScratchMisc, 2 * r_pad * d_out * 2, stream, &st));
@@ -166,8 +170,8 @@ extern "C" bitsmoe_status bitsmoe_project(const float* Ut_dev, const void* W_dev
   {
     const int64_t count = r_pad * d_out;
     const unsigned blocks = static_cast<unsigned>(std::min<int64_t>((count + 255) / 256, 65536));
-    hipLaunchKernelGGL(split_f32_kernel, dim3(blocks), dim3(256), 0, s, Ut_dev, r, r_pad, d_out, U2,
-                       U2 + count);
+    hipLaunchKernelGGL(split_f32_kernel, dim3(blocks), dim3(256), 0, s, Ut_dev, r, r_pad, d_out, PM,
+                       U2, U2 + count);
     BITSMOE_LAUNCH_CHECK("project: split launch");
   }
   dim3 tg(static_cast<unsigned>((d_in + 63) / 64), static_cast<unsigned>((d_out + 63) / 64),
@@ -214,8 +218,15 @@ extern "C" bitsmoe_status bitsmoe_project(const float* Ut_dev, const void* W_dev
   dim3 grid(static_cast<unsigned>(p.tiles_m * p.tiles_n), 1, static_cast<unsigned>(E));
   {
     KernelTimer timer("project", stream);
-    hipLaunchKernelGGL((gemm::gemm_nt_kernel<PM, PN, 32, 4, FactorStore>), grid,
-                       dim3(gemm::kThreads), 0, s, p, epi);
+    if (PM == 256)
+      hipLaunchKernelGGL((gemm::gemm_nt_kernel<256, PN, 32, 4, FactorStore>), grid,
+                         dim3(gemm::kThreads), 0, s, p, epi);
+    else if (PM == 192)
+      hipLaunchKernelGGL((gemm::gemm_nt_kernel<192, PN, 32, 4, FactorStore>), grid,
+                         dim3(gemm::kThreads), 0, s, p, epi);
+    else
+      hipLaunchKernelGGL((gemm::gemm_nt_kernel<128, PN, 32, 4, FactorStore>), grid,
+                         dim3(gemm::kThreads), 0, s, p, epi);
   }
   BITSMOE_LAUNCH_CHECK("project: gemm launch");
   return ok();
