@@ -13,8 +13,10 @@ device memory before timing starts.  One JSON line is printed:
                the host eigensolve and ILP are reported beside it
   ms_per_step  wall time per step, host steps and transfers included
   roofline     the loss-table GEMM (the dominant kernel): algorithmic flops
-               2 * units * nbits * d^2 over its event-timed duration,
-               against the bf16 dense matrix-core peak
+               2 * units * nbits * d^2 (the dense form) over its event-timed
+               duration, against the dense 16-bit matrix-core peak; since the
+               kernel uses the symmetry of H it executes about half of those,
+               reported beside it as executed_tflops / executed_frac
   cpu_baseline the fp64 oracle timed on a bounded sample of the same layer
                on this host, scaled to the layer
 """
@@ -35,7 +37,7 @@ METRIC = "ms per MoE layer quantized (Qwen3-30B-A3B shape); score-kernel TFLOP/s
 SCORE_SOURCES = ("paper_2606_00079_amd/csrc/gemm.hpp", "paper_2606_00079_amd/csrc/score.hip",
                  "paper_2606_00079_amd/csrc/common.hpp")
 TRAFFIC_FILE = "profiles/score_gemm_qwen_layer_traffic.txt"
-PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 matrix-core peak
+PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 / fp16 matrix-core peak
 PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
 
 
@@ -218,6 +220,14 @@ def main(argv=None) -> int:
 
     # algorithmic work per step
     score_flops = sum(2.0 * p.E * p.r * len(p.bits) * p.spec.d_in ** 2 for p in layer)
+
+    def score_executed(p):
+        # the kernel reads only the upper block triangle of the symmetric H
+        # (256 x 256 blocks): row tile t of H multiplies K = d - 256 t columns
+        d = p.spec.d_in
+        rows = math.ceil(p.E * p.r * len(p.bits) / 256) * 256
+        return sum(2.0 * rows * 256 * (d - 256 * t) for t in range(math.ceil(d / 256)))
+    score_exec_flops = sum(score_executed(p) for p in layer)
     dgen_bytes = sum(p.E * p.r * p.spec.d_in * (4 + 2 * len(p.bits)) for p in layer)
     pack_bytes = sum(p.E * p.r * p.spec.d_in * 4 + p.budget_bits * p.spec.d_in / 8
                      + p.E * p.r * p.spec.d_in / p.group * 4 + p.E * p.r for p in layer)
@@ -266,7 +276,11 @@ def main(argv=None) -> int:
                      "traffic": traffic, "kernel": "score_gemm",
                      "launches_per_step": n_gemm // max(steps, 1),
                      "avg_launch_ms": round(ms_gemm / max(n_gemm, 1), 4),
-                     "flops_per_launch": score_flops / max(n_gemm // max(steps, 1), 1)},
+                     "flops_per_launch": score_flops / max(n_gemm // max(steps, 1), 1),
+                     "executed_flops_per_launch": score_exec_flops / max(n_gemm // max(steps, 1), 1),
+                     "executed_tflops": round(score_exec_flops / (score_ms_step * 1e-3) / 1e12, 1),
+                     "executed_frac": round(score_exec_flops / (score_ms_step * 1e-3) / 1e12
+                                            / PEAK_BF16_TFLOPS, 4)},
     }
     if not args.no_cpu_baseline:
         log("timing the fp64 oracle on a sample")

@@ -3,9 +3,10 @@
 //
 // One wave per unit.  Word w of the row holds entries 64 w .. 64 w + 63, one
 // per lane, so the plane-t word of w is the wave ballot of bit t of the lane
-// codes.  Words are gathered in LDS and written out contiguously.  Codes use
-// the fp64 quotient rule of the quantizer, so they match an fp64 reference
-// bit for bit given the same fp32 row.
+// codes.  Words are gathered in LDS and written out contiguously.  Codes
+// follow the fp64 quotient rule of the quantizer (decided in fp32 where that
+// provably gives the same integer), so they match an fp64 reference bit for
+// bit given the same fp32 row.
 #include <algorithm>
 
 #include "bitsmoe.h"
@@ -54,17 +55,32 @@ __global__ __launch_bounds__(64) void pack_kernel(const float* __restrict__ C, i
     }
     const uint16_t m16 = f32_to_f16_bits(mn);
     const uint16_t s16 = f32_to_f16_bits((mx - mn) / qmaxf);
-    const double md = f16_bits_to_f64(m16);
-    const double sd = f16_bits_to_f64(s16);
+    const float mf = f16_bits_to_f32(m16);
+    const float sf = f16_bits_to_f32(s16);
+    const float inv = sf > 0.0f ? 1.0f / sf : 0.0f;
+    // codes from the fp32 quotient, which is within 5e-5 of the fp64 one for
+    // codes up to 255: it rounds the same way unless it lies within 1e-4 of
+    // a rounding boundary, and those (rare) lanes decide in fp64
+    int q[WPB];
+    bool near = false;
 #pragma unroll
     for (int i = 0; i < WPB; ++i) {
-      int q = 0;
-      if (sd > 0.0) {
+      const float t = (c[i] - mf) * inv;
+      near |= fabsf(t - floorf(t) - 0.5f) < 1e-4f;
+      q[i] = static_cast<int>(fminf(fmaxf(rintf(t), 0.0f), qmaxf));
+    }
+    if (near && sf > 0.0f) {
+      const double md = static_cast<double>(mf), sd = static_cast<double>(sf);
+#pragma unroll
+      for (int i = 0; i < WPB; ++i) {
         const double t = (static_cast<double>(c[i]) - md) / sd;
-        q = static_cast<int>(fmin(fmax(rint(t), 0.0), qmax));
+        q[i] = static_cast<int>(fmin(fmax(rint(t), 0.0), qmax));
       }
+    }
+#pragma unroll
+    for (int i = 0; i < WPB; ++i) {
       for (int t = 0; t < b; ++t) {
-        const uint64_t word = __ballot((q >> t) & 1);
+        const uint64_t word = __ballot((q[i] >> t) & 1);
         if (lane == 0) wbuf[t * nw + w0 + i] = word;
       }
     }

@@ -127,12 +127,10 @@ struct QuantBits {
 // consecutive lanes.  Codes follow the fp64 rule exactly: the fp32 quotient
 // is used unless it lies within 1e-4 of a rounding boundary (its error is
 // below 5e-5 for codes up to 255), in which case fp64 decides.
-// Rows of at most kRegChunks * 512 entries are held in registers between
-// the max |c| pass and the quantization pass (C is read once) when there are
-// at most four widths; otherwise rows are read twice.
-constexpr int kRegChunks = 8;
-
-template <int NB, bool CACHED>
+// The row is read twice: once for max |c|, once to quantize (the second read
+// mostly hits in the caches; holding the row in registers instead costs more
+// in occupancy than it saves).
+template <int NB>
 __global__ __launch_bounds__(256) void dgen_kernel(const float* __restrict__ C, int64_t units,
                                                    int64_t d, int G, QuantBits qb,
                                                    const float* __restrict__ hdiag,
@@ -170,19 +168,11 @@ __global__ __launch_bounds__(256) void dgen_kernel(const float* __restrict__ C, 
 
   // |delta| <= max - min <= 2 max |c| < 2^(e + 1): the error rows are stored
   // as fp16(delta * 2^E) with E = kF16Top - 1 - e
-  float cc[CACHED ? kRegChunks : 1][8];
+  float cc[8];
   float amax = 0.0f;
-  if constexpr (CACHED) {
-#pragma unroll
-    for (int ch = 0; ch < kRegChunks; ++ch) {
-      load8(512 * ch, cc[ch]);
-      amax = fmaxf(amax, absmax8(cc[ch]));
-    }
-  } else {
-    for (int64_t k0 = 0; k0 < d; k0 += 512) {
-      load8(k0, cc[0]);
-      amax = fmaxf(amax, absmax8(cc[0]));
-    }
+  for (int64_t k0 = 0; k0 < d; k0 += 512) {
+    load8(k0, cc);
+    amax = fmaxf(amax, absmax8(cc));
   }
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) amax = fmaxf(amax, __shfl_xor(amax, o, 64));
@@ -211,6 +201,13 @@ __global__ __launch_bounds__(256) void dgen_kernel(const float* __restrict__ C, 
     hd[4] = h1.x; hd[5] = h1.y; hd[6] = h1.z; hd[7] = h1.w;
     const float mf = f16_bits_to_f32(f32_to_f16_bits(mn));
     const float range = mx - mn;
+    // c - m16 once per entry, and its image scaled by 2^E (exact)
+    float cm[8], cms[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      cm[i] = c[i] - mf;
+      cms[i] = ldexpf(cm[i], E);
+    }
 #pragma unroll
     for (int j = 0; j < NB; ++j) {
       const int b = qb.b[j];
@@ -218,25 +215,35 @@ __global__ __launch_bounds__(256) void dgen_kernel(const float* __restrict__ C, 
       const float s32 = range / qmax;
       const float sf = f16_bits_to_f32(f32_to_f16_bits(s32));
       const float inv = sf > 0.0f ? 1.0f / sf : 0.0f;
+      const float sfs = ldexpf(sf, E);
+      // codes from the fp32 quotient (inv = 0 gives q = 0 for a constant
+      // group); a quotient within 1e-4 of a rounding boundary is decided in
+      // fp64 instead, for the whole lane, in one rarely taken branch
+      float q[8];
+      bool near = false;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const float t = cm[i] * inv;
+        const float r = rintf(t);
+        near |= fabsf(t - r) > 0.4999f;
+        q[i] = __builtin_amdgcn_fmed3f(r, 0.0f, qmax);
+      }
+      if (near && sf > 0.0f) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          const double td = (static_cast<double>(c[i]) - static_cast<double>(mf)) /
+                            static_cast<double>(sf);
+          q[i] = static_cast<float>(fmin(fmax(rint(td), 0.0), static_cast<double>(qmax)));
+        }
+      }
+      // delta * 2^E = (c - m16) 2^E - q s16 2^E; the diagonal term is summed
+      // from the scaled error and scaled back once at the end
       uint16_t out[8];
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
-        float q = 0.0f;
-        if (sf > 0.0f) {
-          const float t = (c[i] - mf) * inv;
-          const float fl = floorf(t);
-          if (fabsf(t - fl - 0.5f) < 1e-4f) {
-            const double td = (static_cast<double>(c[i]) - static_cast<double>(mf)) /
-                              static_cast<double>(sf);
-            q = static_cast<float>(fmin(fmax(rint(td), 0.0), static_cast<double>(qmax)));
-          } else {
-            q = fminf(fmaxf(rintf(t), 0.0f), qmax);
-          }
-        }
-        const float xh = fmaf(q, sf, mf);
-        const float dl = c[i] - xh;
-        out[i] = f32_to_f16_bits(ldexpf(dl, E));
-        dacc[j] = fmaf(hd[i] * dl, dl, dacc[j]);
+        const float dls = fmaf(-q[i], sfs, cms[i]);
+        out[i] = f32_to_f16_bits(dls);
+        dacc[j] = fmaf(hd[i] * dls, dls, dacc[j]);
       }
       uint4 pk;
       pk.x = static_cast<uint32_t>(out[0]) | (static_cast<uint32_t>(out[1]) << 16);
@@ -246,19 +253,13 @@ __global__ __launch_bounds__(256) void dgen_kernel(const float* __restrict__ C, 
       *reinterpret_cast<uint4*>(D + gemm::tiled_offset(u * nb + j, k, d, SBN)) = pk;
     }
   };
-  if constexpr (CACHED) {
-#pragma unroll
-    for (int ch = 0; ch < kRegChunks; ++ch)
-      if (512 * ch < d) chunk(512 * ch, cc[ch]);
-  } else {
-    for (int64_t k0 = 0; k0 < d; k0 += 512) {
-      load8(k0, cc[0]);
-      chunk(k0, cc[0]);
-    }
+  for (int64_t k0 = 0; k0 < d; k0 += 512) {
+    load8(k0, cc);
+    chunk(k0, cc);
   }
 #pragma unroll
   for (int j = 0; j < NB; ++j) {
-    const float v = wave_sum(dacc[j]);
+    const float v = ldexpf(wave_sum(dacc[j]), -2 * E);
     if (lane == 0) diag[u * nb + j] = v;
   }
 }
@@ -422,14 +423,10 @@ extern "C" bitsmoe_status bitsmoe_score(const float* C_dev, int64_t units, int64
   {
   KernelTimer dgen_timer("score_dgen", stream);
   switch (nbits) {
-#define BITSMOE_DGEN(NB)                                                                         \
-  case NB:                                                                                       \
-    if (NB <= 4 && d <= 512 * kRegChunks)                                                        \
-      hipLaunchKernelGGL((dgen_kernel<NB, (NB <= 4)>), dim3(db), dim3(256), 0, s, C_dev, units, d, \
-                         group, qb, hdiag, D, diag, uexp);                                       \
-    else                                                                                         \
-      hipLaunchKernelGGL((dgen_kernel<NB, false>), dim3(db), dim3(256), 0, s, C_dev, units, d,   \
-                         group, qb, hdiag, D, diag, uexp);                                       \
+#define BITSMOE_DGEN(NB)                                                                       \
+  case NB:                                                                                     \
+    hipLaunchKernelGGL(dgen_kernel<NB>, dim3(db), dim3(256), 0, s, C_dev, units, d, group, qb, \
+                       hdiag, D, diag, uexp);                                                  \
     break;
     BITSMOE_DGEN(1) BITSMOE_DGEN(2) BITSMOE_DGEN(3) BITSMOE_DGEN(4)
     BITSMOE_DGEN(5) BITSMOE_DGEN(6) BITSMOE_DGEN(7) BITSMOE_DGEN(8)
