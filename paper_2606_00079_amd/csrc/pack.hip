@@ -38,55 +38,65 @@ __global__ __launch_bounds__(64) void pack_kernel(const float* __restrict__ C, i
   const double qmax = static_cast<double>((1 << b) - 1);
   const float qmaxf = static_cast<float>((1 << b) - 1);
   const float* crow = C + u * d;
-  for (int64_t w0 = 0; w0 < nw; w0 += WPB) {
-    float c[WPB];
+  // words are processed in segments of kSegWords: every load of a segment is
+  // issued before any of its values is used
+  constexpr int kSegWords = 32;
+  static_assert(kSegWords % WPB == 0, "segments hold whole groups");
+  for (int64_t s0 = 0; s0 < nw; s0 += kSegWords) {
+    float cv[kSegWords];
 #pragma unroll
-    for (int i = 0; i < WPB; ++i) c[i] = crow[64 * (w0 + i) + lane];
-    float mn = c[0], mx = c[0];
+    for (int i = 0; i < kSegWords; ++i) cv[i] = (s0 + i < nw) ? crow[64 * (s0 + i) + lane] : 0.0f;
 #pragma unroll
-    for (int i = 1; i < WPB; ++i) {
-      mn = fminf(mn, c[i]);
-      mx = fmaxf(mx, c[i]);
-    }
+    for (int g0 = 0; g0 < kSegWords; g0 += WPB) {
+      const int64_t w0 = s0 + g0;
+      if (w0 >= nw) break;
+      float mn = cv[g0], mx = cv[g0];
 #pragma unroll
-    for (int o = RED / 2; o > 0; o >>= 1) {
-      mn = fminf(mn, __shfl_xor(mn, o, 64));
-      mx = fmaxf(mx, __shfl_xor(mx, o, 64));
-    }
-    const uint16_t m16 = f32_to_f16_bits(mn);
-    const uint16_t s16 = f32_to_f16_bits((mx - mn) / qmaxf);
-    const float mf = f16_bits_to_f32(m16);
-    const float sf = f16_bits_to_f32(s16);
-    const float inv = sf > 0.0f ? 1.0f / sf : 0.0f;
-    // codes from the fp32 quotient, which is within 5e-5 of the fp64 one for
-    // codes up to 255: it rounds the same way unless it lies within 1e-4 of
-    // a rounding boundary, and those (rare) lanes decide in fp64
-    int q[WPB];
-    bool near = false;
+      for (int i = 1; i < WPB; ++i) {
+        mn = fminf(mn, cv[g0 + i]);
+        mx = fmaxf(mx, cv[g0 + i]);
+      }
 #pragma unroll
-    for (int i = 0; i < WPB; ++i) {
-      const float t = (c[i] - mf) * inv;
-      near |= fabsf(t - floorf(t) - 0.5f) < 1e-4f;
-      q[i] = static_cast<int>(fminf(fmaxf(rintf(t), 0.0f), qmaxf));
-    }
-    if (near && sf > 0.0f) {
-      const double md = static_cast<double>(mf), sd = static_cast<double>(sf);
+      for (int o = RED / 2; o > 0; o >>= 1) {
+        mn = fminf(mn, __shfl_xor(mn, o, 64));
+        mx = fmaxf(mx, __shfl_xor(mx, o, 64));
+      }
+      const uint16_t m16 = f32_to_f16_bits(mn);
+      const uint16_t s16 = f32_to_f16_bits((mx - mn) / qmaxf);
+      const float mf = f16_bits_to_f32(m16);
+      const float sf = f16_bits_to_f32(s16);
+      const float inv = sf > 0.0f ? 1.0f / sf : 0.0f;
+      // codes from the fp32 quotient, which is within 5e-5 of the fp64 one
+      // for codes up to 255: it rounds the same way unless it lies within
+      // 1e-4 of a rounding boundary, and those (rare) lanes decide in fp64
+      int q[WPB];
+      bool near = false;
 #pragma unroll
       for (int i = 0; i < WPB; ++i) {
-        const double t = (static_cast<double>(c[i]) - md) / sd;
-        q[i] = static_cast<int>(fmin(fmax(rint(t), 0.0), qmax));
+        const float t = (cv[g0 + i] - mf) * inv;
+        const float r = rintf(t);
+        near |= fabsf(t - r) > 0.4999f;
+        q[i] = static_cast<int>(__builtin_amdgcn_fmed3f(r, 0.0f, qmaxf));
       }
-    }
+      if (near && sf > 0.0f) {
+        const double md = static_cast<double>(mf), sd = static_cast<double>(sf);
 #pragma unroll
-    for (int i = 0; i < WPB; ++i) {
-      for (int t = 0; t < b; ++t) {
-        const uint64_t word = __ballot((q[i] >> t) & 1);
-        if (lane == 0) wbuf[t * nw + w0 + i] = word;
+        for (int i = 0; i < WPB; ++i) {
+          const double t = (static_cast<double>(cv[g0 + i]) - md) / sd;
+          q[i] = static_cast<int>(fmin(fmax(rint(t), 0.0), qmax));
+        }
       }
-    }
-    if ((lane % RED) == 0) {
-      const int64_t g = (64 * w0 + lane) / G;
-      pbuf[g] = static_cast<uint32_t>(s16) | (static_cast<uint32_t>(m16) << 16);
+#pragma unroll
+      for (int i = 0; i < WPB; ++i) {
+        for (int t = 0; t < b; ++t) {
+          const uint64_t word = __ballot((q[i] >> t) & 1);
+          if (lane == 0) wbuf[t * nw + w0 + i] = word;
+        }
+      }
+      if ((lane % RED) == 0) {
+        const int64_t g = (64 * w0 + lane) / G;
+        pbuf[g] = static_cast<uint32_t>(s16) | (static_cast<uint32_t>(m16) << 16);
+      }
     }
   }
   __syncthreads();
