@@ -261,7 +261,7 @@ def main(argv=None) -> int:
         "higher_is_better": False,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16",
+        "dtype": "bf16+fp16",
         "data": "synthetic",
         "config": {"workload": workload_name(cfg), "experts": cfg.E,
                    "projections": [f"{p.name} {p.d_out}x{p.d_in} r={p.r}" for p in cfg.projs],

