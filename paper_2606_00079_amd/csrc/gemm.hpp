@@ -100,6 +100,9 @@ struct Problem {
   int group_n;       // column tiles per ordering group (non-symmetric)
   int ktri;          // 1 (no split-K): row tile tm only visits K tiles from tm * BM / KB on
                      // (the A operand's upper block triangle)
+  int krev;          // 1 (one pass, one segment): K tiles in descending order, so that
+                     // tiles whose K ranges start at different places but end at the
+                     // same one read the shared B operand in step
 };
 
 // XCD-contiguous logical id of the linear workgroup id t (of n in total).
@@ -180,9 +183,10 @@ struct KPos {
   int64_t offa, offb;    // element offsets of the tile from the pass bases
   int64_t stepa, stepb;  // per K tile
   int64_t jumpa, jumpb;  // extra at a segment boundary
+  int64_t kdir;          // +KB, or -KB in descending order
   PassBases ba, bb;
   __device__ __forceinline__ void init(const Problem& p, int64_t kt, int64_t z, int tm, int tn,
-                                       int BM, int BN) {
+                                       int BM, int BN, bool reverse) {
     const int64_t tiles_seg = p.kseg / KB;
     const int64_t per_pass = static_cast<int64_t>(p.segs) * tiles_seg;
     const int pass = static_cast<int>(kt / per_pass);
@@ -200,15 +204,20 @@ struct KPos {
     bb.make_uniform();
     stepa = uniform64(p.a.kstep != 0 ? p.a.kstep : KB);
     stepb = uniform64(p.b.kstep != 0 ? p.b.kstep : KB);
+    kdir = reverse ? -KB : KB;
     jumpa = uniform64(p.a.estride - tiles_seg * stepa);
     jumpb = uniform64(p.b.estride - tiles_seg * stepb);
     seg = uniform64(seg);
     k0 = uniform64(k0);
     offa = uniform64(seg * p.a.estride + ki * stepa);
     offb = uniform64(seg * p.b.estride + ki * stepb);
+    if (reverse) {  // one pass, one segment: walk down, never wrap
+      stepa = -stepa;
+      stepb = -stepb;
+    }
   }
   __device__ __forceinline__ void next(const Problem& p) {
-    k0 += KB;
+    k0 += kdir;
     offa += stepa;
     offb += stepb;
     const bool wrap = k0 == p.kseg;
@@ -508,7 +517,8 @@ void gemm_nt_kernel(Problem p, Epi epi) {
   };
 
   if (nk > 0) {
-    kp.init(p, kt0, f.z, f.tm, f.tn, BM, BN);
+    const bool rev = p.krev != 0 && p.passes == 1 && p.segs == 1;
+    kp.init(p, rev ? kt1 - 1 : kt0, f.z, f.tm, f.tn, BM, BN, rev);
     // tiles 0 .. STAGES - 3 up front, tile STAGES - 2 once tile 0 is visible
     for (int q = 0; q < STAGES - 2 && issued < nk; ++q) {
       issue(q);

@@ -455,6 +455,7 @@ extern "C" bitsmoe_status bitsmoe_score(const float* C_dev, int64_t units, int64
   p.symmetric = 0;
   p.group_n = std::max(1, 32 / tiles_m);  // ~one XCD's worth of workgroups per group
   p.ktri = 1;  // H symmetric: upper block triangle of H_off only
+  p.krev = 1;  // all row tiles walk K down from the end, in step
   RowDot epi{D, part, R, d, tiles_m};
   dim3 grid(static_cast<unsigned>(tiles_m * tiles_n), 1, 1);
   {
