@@ -272,8 +272,8 @@ __global__ __launch_bounds__(256) void dgen_kernel(const float* __restrict__ C, 
 // slot c ^ (j mod 32) so that 32 lanes reading 32 rows at one chunk spread
 // over the banks.  Each lane then reads its D values (one row per column
 // fragment, four 8-byte runs per row fragment) from LDS.  Columns past the
-// end are clamped on load and left out of the sum; rows past the end (the
-// padding of the last row tile) are computed and never stored.
+// end are clamped on load (their accumulators are exactly zero); rows past
+// the end (the padding of the last row tile) are computed and never stored.
 struct RowDot {
   const uint16_t* D;
   float* part;
@@ -317,6 +317,8 @@ struct RowDot {
       __builtin_amdgcn_sched_barrier(0);
       const int jl = f.wn * F::WN + 32 * ni + (lane & 31);
       const uint16_t* rowp = lds.piece(jl >> 5) + (jl & 31) * 256;
+      // i past d: H_off's pad rows are zero, so acc is exactly 0 there and the
+      // (finite) clamped D values add nothing
       float acc = 0.0f;
 #pragma unroll
       for (int mi = 0; mi < F::FM; ++mi)
@@ -326,11 +328,11 @@ struct RowDot {
           const int c = il >> 3;
           const uint2 v = *reinterpret_cast<const uint2*>(rowp + ((c ^ (jl & 31)) << 3) +
                                                           4 * (lane >> 5));
-          const float t = f16_bits_to_f32(static_cast<uint16_t>(v.x & 0xffff)) * f.acc[mi][ni][4 * g + 0] +
-                          f16_bits_to_f32(static_cast<uint16_t>(v.x >> 16)) * f.acc[mi][ni][4 * g + 1] +
-                          f16_bits_to_f32(static_cast<uint16_t>(v.y & 0xffff)) * f.acc[mi][ni][4 * g + 2] +
-                          f16_bits_to_f32(static_cast<uint16_t>(v.y >> 16)) * f.acc[mi][ni][4 * g + 3];
-          acc += (i_base + il + 4 * (lane >> 5) < d) ? t : 0.0f;
+          const _Float16* h = reinterpret_cast<const _Float16*>(&v);
+          acc = fmaf(static_cast<float>(h[0]), f.acc[mi][ni][4 * g + 0], acc);
+          acc = fmaf(static_cast<float>(h[1]), f.acc[mi][ni][4 * g + 1], acc);
+          acc = fmaf(static_cast<float>(h[2]), f.acc[mi][ni][4 * g + 2], acc);
+          acc = fmaf(static_cast<float>(h[3]), f.acc[mi][ni][4 * g + 3], acc);
         }
       s[ni] = acc + __shfl_xor(acc, 32, 64);
     }
