@@ -285,6 +285,11 @@ struct StageLds {
   uint16_t* a;        // A stage buffers, a_elems bf16 in all, contiguous
   uint16_t* b;        // B stage buffers, b_elems bf16 in all, contiguous
   int a_elems, b_elems;
+  // K tiles this workgroup visited; the n-th visited tile (n = 0, 1, ...)
+  // was staged in buffer n % stages, so the last `stages` of them are still
+  // there (in the swizzled stage layout)
+  int64_t nk;
+  int stages;
   // 16 KiB piece k of the A buffers followed by the B buffers
   __device__ __forceinline__ uint16_t* piece(int k) const {
     const int per_a = a_elems / 8192;
@@ -549,6 +554,8 @@ void gemm_nt_kernel(Problem p, Epi epi) {
   lds.b = Bs;
   lds.a_elems = STAGES * ASZ;
   lds.b_elems = STAGES * BSZ;
+  lds.nk = kt1 - kt0;
+  lds.stages = STAGES;
   epi(f, lds);
 }
 

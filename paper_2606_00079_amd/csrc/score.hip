@@ -266,14 +266,17 @@ __global__ __launch_bounds__(256) void dgen_kernel(const float* __restrict__ C, 
 
 // part[row][tm] = sum over this tile's i of D[row][i] * acc[i][row].
 //
-// The tile's 256 x 256 block of D (rows tn*256.., columns tm*256..) is first
-// brought into the free stage buffers by direct global->LDS loads: 512 bytes
-// per row, 32 rows per 16 KiB buffer, the 16-byte chunk c of row j stored in
-// slot c ^ (j mod 32) so that 32 lanes reading 32 rows at one chunk spread
-// over the banks.  Each lane then reads its D values (one row per column
-// fragment, four 8-byte runs per row fragment) from LDS.  Columns past the
-// end are clamped on load (their accumulators are exactly zero); rows past
-// the end (the padding of the last row tile) are computed and never stored.
+// The i range of the tile is K tiles 8 tm .. 8 tm + 7 of D (the diagonal
+// block), which the K loop visits last, in descending order: the first four
+// (the i range of the waves with wm = 0) are the last four tiles staged and
+// are still in the B halves of the stage buffers; the other four (wm = 1)
+// are loaded again into the A halves, which are free once the loop is done.
+// Both use the stage layout (256 rows x 32 entries, swizzled 16-byte
+// chunks).  Each lane then reads its D values (one row per column fragment,
+// four 8-byte runs per row fragment).  K tiles past the end of the row are
+// clamped (their accumulators are exactly zero: H_off's pad rows are zero);
+// rows past the end (the padding of the last row tile) are computed and
+// never stored.
 struct RowDot {
   const uint16_t* D;
   float* part;
@@ -281,31 +284,27 @@ struct RowDot {
   int tiles_m;
   template <class F>
   __device__ void operator()(F& f, const gemm::StageLds& lds) const {
-    static_assert(SBM == 256 && SBN == 256, "layout below assumes 256 x 256 tiles");
-    static_assert(SSTAGES * SBM * SKB * 2 + SSTAGES * SBN * SKB * 2 >= 8 * 16384,
-                  "stage buffers must hold the 256 x 256 bf16 D block");
+    static_assert(SBM == 256 && SBN == 256 && SKB == 32 && SSTAGES >= 4,
+                  "layout below assumes 256 x 256 tiles, 32-wide K tiles, four or more stages");
+    constexpr int TE = SBN * SKB;  // elements of one staged K tile of D (and of H_off)
     __shared__ float red[2 * SBN];  // cross-wave reduction
     const int lane = opaque(f.lane);
     const int wave = lane >= 0 ? f.wave : 0;  // ties wave to the opaque lane
-    const int64_t i_base = static_cast<int64_t>(f.tm) * SBM;
-    const int64_t j_base = static_cast<int64_t>(f.tn) * SBN;
-    // 1 KiB block b holds rows 2b, 2b+1; wave w loads blocks w, w+4, ...
-    // D is K-tiled (256-row tiles, 32-wide K tiles): the block's eight K
-    // tiles are contiguous 16 KiB pieces, and rows 2b, 2b+1 of one K tile
-    // are one 128-byte line.  K tiles past the end are clamped (and weighted
-    // out below).
     const int64_t nkt = d / gemm::kTileK;
-    const int64_t kt0 = i_base / gemm::kTileK;
-    const int kt_last = static_cast<int>(nkt - 1 - kt0);
-    const uint16_t* blk = D + (static_cast<int64_t>(f.tn) * nkt + kt0) * (SBN * gemm::kTileK);
-#pragma unroll 4
-    for (int b = wave; b < 128; b += 4) {
-      const int j = 2 * b + (lane >> 5);
-      const int c = (lane & 31) ^ (j & 31);
-      const int ktr = min(c >> 2, kt_last);
-      const uint32_t off = static_cast<uint32_t>((ktr * (SBN * gemm::kTileK) + j * gemm::kTileK + 8 * (c & 3)) * 2);
-      uint16_t* dst = lds.piece(b >> 4) + (b & 15) * 512;
-      gemm::dma16(blk, off, dst);
+    const int64_t kt0 = static_cast<int64_t>(f.tm) * (SBM / SKB);  // first K tile of the block
+    const uint16_t* dtile = D + static_cast<int64_t>(f.tn) * SBN * d;  // row tile tn of D
+    // reload block K tiles 4..7 (clamped) into A buffers 0..3
+#pragma unroll
+    for (int x = 0; x < 4; ++x) {
+      const int64_t q = min(kt0 + 4 + x, nkt - 1);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int blk = wave + 4 * i;                 // 1 KiB block: rows 16 blk .. 16 blk + 15
+        const int r = 16 * blk + (lane >> 2);
+        const int j = gemm::swz<SKB>(r, lane & 3);
+        gemm::dma16(dtile + q * TE, static_cast<uint32_t>((r * SKB + 8 * j) * 2),
+                    lds.a + x * TE + blk * 512);
+      }
     }
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
@@ -316,24 +315,25 @@ struct RowDot {
       // next to all 256 accumulators
       __builtin_amdgcn_sched_barrier(0);
       const int jl = f.wn * F::WN + 32 * ni + (lane & 31);
-      const uint16_t* rowp = lds.piece(jl >> 5) + (jl & 31) * 256;
-      // i past d: H_off's pad rows are zero, so acc is exactly 0 there and the
-      // (finite) clamped D values add nothing
       float acc = 0.0f;
 #pragma unroll
-      for (int mi = 0; mi < F::FM; ++mi)
+      for (int mi = 0; mi < F::FM; ++mi) {
+        const int rq = 4 * f.wm + mi;  // block K tile (uniform per wave)
+        // rq < 4: staged as visit n = nk - 1 - rq, still in B buffer n % stages
+        const int64_t n = lds.nk - 1 - rq;
+        const uint16_t* tb = rq < 4 ? lds.b + static_cast<int>((n < 0 ? 0 : n) % lds.stages) * TE
+                                    : lds.a + (rq - 4) * TE;
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
-          const int il = f.wm * F::WM + 32 * mi + 8 * g;      // first i of the chunk
-          const int c = il >> 3;
-          const uint2 v = *reinterpret_cast<const uint2*>(rowp + ((c ^ (jl & 31)) << 3) +
-                                                          4 * (lane >> 5));
+          const int k = 8 * g + 4 * (lane >> 5);  // entry within the K tile
+          const uint2 v = *reinterpret_cast<const uint2*>(tb + gemm::lds_off<SKB>(jl, k >> 3) + (k & 7));
           const _Float16* h = reinterpret_cast<const _Float16*>(&v);
           acc = fmaf(static_cast<float>(h[0]), f.acc[mi][ni][4 * g + 0], acc);
           acc = fmaf(static_cast<float>(h[1]), f.acc[mi][ni][4 * g + 1], acc);
           acc = fmaf(static_cast<float>(h[2]), f.acc[mi][ni][4 * g + 2], acc);
           acc = fmaf(static_cast<float>(h[3]), f.acc[mi][ni][4 * g + 3], acc);
         }
+      }
       s[ni] = acc + __shfl_xor(acc, 32, 64);
     }
     // combine the waves that share these rows (wm = 0, 1)
@@ -342,6 +342,7 @@ struct RowDot {
       for (int ni = 0; ni < F::FN; ++ni) red[f.wm * SBN + f.wn * F::WN + 32 * ni + lane] = s[ni];
     }
     __syncthreads();
+    const int64_t j_base = static_cast<int64_t>(f.tn) * SBN;
     for (int t = threadIdx.x; t < SBN; t += gemm::kThreads) {
       const int64_t row = j_base + t;
       if (row < R) part[row * tiles_m + f.tm] = red[t] + red[SBN + t];
