@@ -36,7 +36,7 @@ if ROOT not in sys.path:
 METRIC = "ms per MoE layer quantized (Qwen3-30B-A3B shape); score-kernel TFLOP/s"
 SCORE_SOURCES = ("paper_2606_00079_amd/csrc/gemm.hpp", "paper_2606_00079_amd/csrc/score.hip",
                  "paper_2606_00079_amd/csrc/common.hpp")
-TRAFFIC_FILE = "profiles/score_gemm_qwen_layer_traffic.txt"
+TRAFFIC_FILE = "profiles/score_gemm_{config}_traffic.txt"
 PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 / fp16 matrix-core peak
 PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
 
@@ -54,10 +54,11 @@ def score_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def measured_traffic():
+def measured_traffic(config: str):
     """HBM bytes per loss-table GEMM launch from the committed FETCH_SIZE / WRITE_SIZE
-    counter summary, or None when it is absent or the kernel sources changed since."""
-    path = os.path.join(ROOT, TRAFFIC_FILE)
+    counter summary of this workload, or None when it is absent or the kernel
+    sources changed since."""
+    path = os.path.join(ROOT, TRAFFIC_FILE.format(config=config))
     if not os.path.exists(path):
         return None
     kv = {}
@@ -78,6 +79,15 @@ def workload_name(cfg) -> str:
     parts = ", ".join(f"{p.name} {p.d_out}x{p.d_in} r={p.r}" for p in cfg.projs)
     return (f"{cfg.name}: E={cfg.E} experts x {{{parts}}}, calibration {cfg.n_tokens} rows, "
             f"bits {list(cfg.bits)}, group {cfg.group}, budget {cfg.budget} bits/unit")
+
+
+class _LayerProj:
+    """Shape-only stand-in for synth.Projection when the inputs live on the device."""
+
+    def __init__(self, cfg, spec):
+        self.cfg, self.spec = cfg, spec
+        self.E, self.r, self.bits, self.group = cfg.E, spec.r, cfg.bits, cfg.group
+        self.budget_bits = cfg.budget_bits(spec)
 
 
 def cpu_baseline(cfg, layer) -> dict:
@@ -148,6 +158,9 @@ def main(argv=None) -> int:
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", default="qwen_layer")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--device-inputs", action="store_true",
+                    help="draw the layer's inputs directly in device memory (same recipes, "
+                         "torch's RNG; for the configurations too large to draw on the host)")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="run one elementwise copy of MIB MiB before timing (calibrates HBM "
                          "byte counters under rocprofv3 --pmc)")
@@ -166,27 +179,49 @@ def main(argv=None) -> int:
 
     bm.lib()
     cfg = synth.CONFIGS[args.config]
-    log("generating", workload_name(cfg))
+    log("generating", workload_name(cfg), "(in device memory)" if args.device_inputs else "")
     t0 = time.perf_counter()
-    layer = synth.make_layer(args.config)
+    dev_inputs = []
+    if args.device_inputs:
+        from synth import device as sdev
+        layer = [_LayerProj(cfg, p) for p in cfg.projs]
+        xcache = {}
+        for p in cfg.projs:
+            key = p.input
+            if key not in xcache:
+                xcache[key] = sdev.calibration_input(cfg, p.name)
+            dev_inputs.append(dict(W=sdev.expert_weights(cfg, p.name), X=xcache[key], r=p.r,
+                                   bits=cfg.bits, group=cfg.group, budget=cfg.budget_bits(p)))
+    else:
+        layer = synth.make_layer(args.config)
+
+        def to_dev(a, dtype):
+            if dtype == "bf16":
+                return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).cuda()
+            return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).cuda()
+
+        xcache = {}
+        for p in layer:
+            if id(p.X) not in xcache:
+                xcache[id(p.X)] = to_dev(p.X, p.dtype)
+            dev_inputs.append(dict(W=to_dev(p.W, p.dtype), X=xcache[id(p.X)], r=p.r, bits=p.bits,
+                                   group=p.group, budget=p.budget_bits))
+    torch.cuda.synchronize()
     log(f"inputs ready in {time.perf_counter() - t0:.1f}s")
 
-    def to_dev(a, dtype):
-        if dtype == "bf16":
-            return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).cuda()
-        return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).cuda()
-
-    dev_inputs = []
-    xcache = {}
-    for p in layer:
-        if id(p.X) not in xcache:
-            xcache[id(p.X)] = to_dev(p.X, p.dtype)
-        dev_inputs.append(dict(W=to_dev(p.W, p.dtype), X=xcache[id(p.X)], r=p.r, bits=p.bits,
-                               group=p.group, budget=p.budget_bits))
-    torch.cuda.synchronize()
-
     def step():
-        return pipeline.quantize_layer(dev_inputs)
+        if not args.device_inputs:
+            return pipeline.quantize_layer(dev_inputs)
+        # large layers: the same as quantize_layer, with a progress line per projection
+        res, hcache = [], {}
+        for i, p in enumerate(dev_inputs):
+            r = pipeline.quantize_projection(p["W"], p["X"], p["r"], p["bits"], p["group"],
+                                             p["budget"], H=hcache.get(id(p["X"])))
+            hcache[id(p["X"])] = r.H
+            res.append(r)
+            log(f"projection {i + 1}/{len(dev_inputs)}: gpu {r.times['gpu_ms']:.2f} ms, "
+                f"eig {r.times['host_eig_ms']:.0f} ms, ilp {r.times['host_ilp_ms']:.0f} ms")
+        return res
 
     for i in range(args.warmup):
         step()
@@ -249,7 +284,7 @@ def main(argv=None) -> int:
         tflops=round(c_flops / (kt["project"][0] / steps * 1e-3) / 1e12, 1))
 
     value = float(np.median(gpu_ms))
-    traffic = measured_traffic()
+    traffic = measured_traffic(args.config)
     out = {
         "metric": METRIC,
         "value": round(value, 3),
@@ -282,7 +317,7 @@ def main(argv=None) -> int:
                      "executed_frac": round(score_exec_flops / (score_ms_step * 1e-3) / 1e12
                                             / PEAK_BF16_TFLOPS, 4)},
     }
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and not args.device_inputs:
         log("timing the fp64 oracle on a sample")
         out["cpu_baseline"] = cpu_baseline(cfg, layer)
     print(json.dumps(out), flush=True)
