@@ -70,7 +70,10 @@ constexpr int kXcds = 8;
 // block of row tile t and K tile q is contiguous, at t * rtile + q * kstep
 // (kstep = T * BK), rows BK elements apart inside it; every row tile is
 // allocated in full, so nothing is clamped.  A K step then reads whole cache
-// lines instead of 64-byte halves of them.
+// lines instead of 64-byte halves of them.  K-major ("KN", B side only, with
+// the kernel's BKN flag): element (k, n) at k * ld + n, i.e. K runs over
+// rows; kstep = BK * ld, rtile = BN, columns past `rows` are clamped.  The
+// B fragments are then read from LDS with the 16-bit transposing read.
 constexpr int kTileK = 32;  // K width of a K-tiled block (must equal the kernel's K step)
 struct Side {
   const uint16_t* pass[4];  // base pointer of each pass
@@ -333,10 +336,27 @@ struct Operand<true> {
   }
 };
 
-template <int BM, int BN, int KB, int STAGES, class Epi, bool F16 = false>
+// Transposing 16-bit LDS read: within each group of 16 lanes, lane j gets
+// element (j mod 4) of the 8-byte run addressed by lane 4 q + j / 4 as its
+// element q.  So if lane s of a group points at row k + s / 4, columns
+// c + 4 (s mod 4) .. + 3 of a row-major [K][N] tile, lane j receives rows
+// k .. k + 3 of column c + j.
+typedef short __attribute__((ext_vector_type(4))) s16x4;
+__device__ __forceinline__ s16x4 ds_read_tr16(const uint16_t* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) s16x4*)(reinterpret_cast<uintptr_t>(p)));
+}
+
+// KN stage layout: BK rows of BN entries (512-byte rows for BN = 256), the
+// 16-byte chunk c of row r stored at chunk c ^ (4 (r mod 4)): one half-wave
+// of transposing reads (4 rows x 4 chunks x 2 halves) covers all 64 banks.
+__device__ __forceinline__ int kn_swz(int r, int c) { return c ^ (4 * (r & 3)); }
+
+template <int BM, int BN, int KB, int STAGES, class Epi, bool F16 = false, bool BKN = false>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void gemm_nt_kernel(Problem p, Epi epi) {
   static_assert(BM % 64 == 0 && BN % 64 == 0, "tile");
+  static_assert(!BKN || (BN == 256 && KB == 32), "KN B operand: 256-wide N tiles, 32-wide K steps");
   static_assert(KB == 32 || KB == 64, "K step");
   static_assert(STAGES >= 2 && STAGES <= 6, "stages");
   constexpr int KC = KB / 8;        // 16-byte chunks per LDS row
@@ -394,11 +414,21 @@ void gemm_nt_kernel(Problem p, Epi epi) {
   }
 #pragma unroll
   for (int i = 0; i < BW; ++i) {
-    const int r = (f.wave + 4 * i) * RPB + f.lane / KC;
-    const int j = swz<KB>(r, f.lane % KC);
-    const int64_t gr = (b_row0 + r < p.b.rows) ? b_row0 + r : p.b.rows - 1;
-    ob[i] = b_tiled ? static_cast<uint32_t>((r * KB + 8 * j) * 2)
-                    : static_cast<uint32_t>(((gr - b_row0) * p.b.ld + 8 * j) * 2);
+    if constexpr (BKN) {
+      // 1 KiB block b = rows 2b, 2b+1 (K) of the tile, 512 bytes (N) each;
+      // chunks past column `rows` are clamped to the last full chunk
+      const int r = 2 * (f.wave + 4 * i) + f.lane / 32;
+      const int c = kn_swz(r, f.lane % 32);
+      int64_t col = b_row0 + 8 * c;
+      col = col + 8 <= p.b.rows ? col : p.b.rows - 8;
+      ob[i] = static_cast<uint32_t>((r * p.b.ld + (col - b_row0)) * 2);
+    } else {
+      const int r = (f.wave + 4 * i) * RPB + f.lane / KC;
+      const int j = swz<KB>(r, f.lane % KC);
+      const int64_t gr = (b_row0 + r < p.b.rows) ? b_row0 + r : p.b.rows - 1;
+      ob[i] = b_tiled ? static_cast<uint32_t>((r * KB + 8 * j) * 2)
+                      : static_cast<uint32_t>(((gr - b_row0) * p.b.ld + 8 * j) * 2);
+    }
   }
   KPos<KB> kp;
   // Loads of the next K tile into stage buffer s, one wave instruction at a
@@ -441,8 +471,23 @@ void gemm_nt_kernel(Problem p, Epi epi) {
     for (int mi = 0; mi < F::FM; ++mi)
       fa[T][mi] = *reinterpret_cast<const typename Op::vec*>(&la[lds_off<KB>(arow + 32 * mi, j)]);
 #pragma unroll
-    for (int ni = 0; ni < F::FN; ++ni)
-      fb[T][ni] = *reinterpret_cast<const typename Op::vec*>(&lb[lds_off<KB>(brow + 32 * ni, j)]);
+    for (int ni = 0; ni < F::FN; ++ni) {
+      if constexpr (BKN) {
+        // rows 16 kk + 8 (lane / 32) + 4 t + (lane % 16) / 4, column
+        // n + 16 ((lane / 16) % 2) + 4 (lane % 4) of the [32][256] stage tile
+        const int col = f.wn * F::WN + 32 * ni + 16 * ((f.lane >> 4) & 1) + 4 * (f.lane & 3);
+        s16x4 h[2];
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+          const int r = 16 * kk + 8 * jq + 4 * t + ((f.lane & 15) >> 2);
+          h[t] = ds_read_tr16(lb + r * BN + (kn_swz(r, col >> 3) << 3) + (col & 7));
+        }
+        fb[T][ni] = __builtin_bit_cast(typename Op::vec,
+                                       __builtin_shufflevector(h[0], h[1], 0, 1, 2, 3, 4, 5, 6, 7));
+      } else {
+        fb[T][ni] = *reinterpret_cast<const typename Op::vec*>(&lb[lds_off<KB>(brow + 32 * ni, j)]);
+      }
+    }
   };
   // The matrix-core ops of one K=16 step from fragment set `set`; with a
   // refill, its LPS loads are issued one after each of the first LPS ops.

@@ -1,7 +1,9 @@
 // Step 3: expert spectral factors C_e = U^T W_e for all experts in one batched
 // matrix-core launch.  U is fp32; it is split U = U_hi + U_lo into two bf16
 // terms so that the product keeps fp32 accuracy (bf16 W is exact; fp32 W is
-// split as well).
+// split as well).  bf16 W is read where it lies: the contraction runs over
+// its rows, which the GEMM stages as [32 K][256 N] tiles and reads with the
+// transposing LDS read, so no transposed copy is made.
 #include <algorithm>
 
 #include "bitsmoe.h"
@@ -76,42 +78,6 @@ __global__ __launch_bounds__(256) void batched_transpose_kernel(const void* __re
   }
 }
 
-// bf16 W [E][rows][cols] -> Wt [E][cols_pad][rows], K-tiled with PN-row
-// tiles; 64 x 64 blocks with 16-byte loads and stores (rows and cols are
-// multiples of 64).
-__global__ __launch_bounds__(256) void transpose_bf16_kernel(const uint16_t* __restrict__ W,
-                                                             int64_t rows, int64_t cols,
-                                                             int64_t cols_pad,
-                                                             uint16_t* __restrict__ Wt) {
-  __shared__ __align__(16) uint16_t tile[64][72];  // 144-byte rows: 16-byte aligned, spread over banks
-  const int64_t e = blockIdx.z;
-  const int64_t r0 = static_cast<int64_t>(blockIdx.y) * 64;
-  const int64_t c0 = static_cast<int64_t>(blockIdx.x) * 64;
-  const int64_t off = e * rows * cols;
-  const int t = threadIdx.x;
-#pragma unroll
-  for (int h = 0; h < 2; ++h) {
-    const int rr = (t >> 3) + 32 * h, cc = (t & 7) * 8;
-    *reinterpret_cast<uint4*>(&tile[rr][cc]) =
-        *reinterpret_cast<const uint4*>(W + off + (r0 + rr) * cols + c0 + cc);
-  }
-  __syncthreads();
-#pragma unroll
-  for (int h = 0; h < 2; ++h) {
-    const int oc = (t >> 3) + 32 * h;  // output row = input column c0 + oc
-    const int orr = (t & 7) * 8;       // first of 8 input rows
-    uint16_t v[8];
-#pragma unroll
-    for (int i = 0; i < 8; ++i) v[i] = tile[orr + i][oc];
-    uint4 pk;
-    pk.x = v[0] | (static_cast<uint32_t>(v[1]) << 16);
-    pk.y = v[2] | (static_cast<uint32_t>(v[3]) << 16);
-    pk.z = v[4] | (static_cast<uint32_t>(v[5]) << 16);
-    pk.w = v[6] | (static_cast<uint32_t>(v[7]) << 16);
-    *reinterpret_cast<uint4*>(Wt + e * cols_pad * rows + gemm::tiled_offset(c0 + oc, r0 + orr, rows, PN)) = pk;
-  }
-}
-
 // C[z][row][col] = acc for row < r, col < d_in.
 struct FactorStore {
   float* C;
@@ -154,8 +120,9 @@ extern "C" bitsmoe_status bitsmoe_project(const float* Ut_dev, const void* W_dev
   hipStream_t s = static_cast<hipStream_t>(stream);
   const bool f32 = wt == BITSMOE_F32;
   bitsmoe_status st;
-  // K-tiled operands: U hi/lo [2][r_pad][d_out] (PM-row tiles) and
-  // Wt hi (and lo) [E][d_in_pad][d_out] (PN-row tiles)
+  // A: U hi/lo, K-tiled [2][r_pad][d_out] (PM-row tiles).  B: bf16 W is read
+  // in place as a K-major operand (K = d_out runs over its rows); fp32 W is
+  // split into K-tiled transposed hi/lo copies [E][d_in_pad][d_out].
   int PM = 256;
   for (int t : {192, 128})
     if ((r + t - 1) / t * t < (r + PM - 1) / PM * PM) PM = t;
@@ -163,10 +130,6 @@ extern "C" bitsmoe_status bitsmoe_project(const float* Ut_dev, const void* W_dev
   const int64_t d_in_pad = (d_in + PN - 1) / PN * PN;
   uint16_t* U2 = static_cast<uint16_t*>(scratch(kScratchMisc, 2 * r_pad * d_out * 2, stream, &st));
   if (!U2) return st;
-  const int64_t wcount = E * d_out * d_in_pad;
-  uint16_t* Wt = static_cast<uint16_t*>(scratch(kScratchB, (f32 ? 2 : 1) * wcount * 2, stream, &st));
-  if (!Wt) return st;
-  uint16_t* Wt_lo = f32 ? Wt + wcount : nullptr;
   {
     const int64_t count = r_pad * d_out;
     const unsigned blocks = static_cast<unsigned>(std::min<int64_t>((count + 255) / 256, 65536));
@@ -174,16 +137,6 @@ extern "C" bitsmoe_status bitsmoe_project(const float* Ut_dev, const void* W_dev
                        U2, U2 + count);
     BITSMOE_LAUNCH_CHECK("project: split launch");
   }
-  dim3 tg(static_cast<unsigned>((d_in + 63) / 64), static_cast<unsigned>((d_out + 63) / 64),
-          static_cast<unsigned>(E));
-  if (f32)
-    hipLaunchKernelGGL(batched_transpose_kernel<true>, tg, dim3(256), 0, s, W_dev, d_out, d_in,
-                       d_in_pad, Wt, Wt_lo);
-  else
-    hipLaunchKernelGGL(transpose_bf16_kernel, tg, dim3(256), 0, s,
-                       static_cast<const uint16_t*>(W_dev), d_out, d_in, d_in_pad, Wt);
-  BITSMOE_LAUNCH_CHECK("project: transpose launch");
-
   gemm::Problem p{};
   const uint16_t* Uhi = U2;
   const uint16_t* Ulo = U2 + r_pad * d_out;
@@ -192,21 +145,36 @@ extern "C" bitsmoe_status bitsmoe_project(const float* Ut_dev, const void* W_dev
   p.a.kstep = static_cast<int64_t>(PM) * gemm::kTileK;
   p.a.rtile = static_cast<int64_t>(PM) * d_out;
   p.a.bstride = 0;
-  p.b.rows = d_in_pad;
-  p.b.kstep = static_cast<int64_t>(PN) * gemm::kTileK;
-  p.b.rtile = static_cast<int64_t>(PN) * d_out;
-  p.b.bstride = d_in_pad * d_out;
   p.segs = 1;
   p.kseg = d_out;
   if (f32) {
+    const int64_t wcount = E * d_out * d_in_pad;
+    uint16_t* Wt = static_cast<uint16_t*>(scratch(kScratchB, 2 * wcount * 2, stream, &st));
+    if (!Wt) return st;
+    uint16_t* Wt_lo = Wt + wcount;
+    dim3 tg(static_cast<unsigned>((d_in + 63) / 64), static_cast<unsigned>((d_out + 63) / 64),
+            static_cast<unsigned>(E));
+    hipLaunchKernelGGL(batched_transpose_kernel<true>, tg, dim3(256), 0, s, W_dev, d_out, d_in,
+                       d_in_pad, Wt, Wt_lo);
+    BITSMOE_LAUNCH_CHECK("project: transpose launch");
+    p.b.rows = d_in_pad;
+    p.b.kstep = static_cast<int64_t>(PN) * gemm::kTileK;
+    p.b.rtile = static_cast<int64_t>(PN) * d_out;
+    p.b.bstride = d_in_pad * d_out;
     p.passes = 3;  // Uhi*Whi + Uhi*Wlo + Ulo*Whi
     p.a.pass[0] = Uhi; p.b.pass[0] = Wt;
     p.a.pass[1] = Uhi; p.b.pass[1] = Wt_lo;
     p.a.pass[2] = Ulo; p.b.pass[2] = Wt;
   } else {
+    const uint16_t* Wb = static_cast<const uint16_t*>(W_dev);
+    p.b.ld = d_in;
+    p.b.rows = d_in;  // N extent (columns past it are clamped)
+    p.b.kstep = static_cast<int64_t>(gemm::kTileK) * d_in;
+    p.b.rtile = PN;
+    p.b.bstride = d_out * d_in;
     p.passes = 2;  // Uhi*W + Ulo*W
-    p.a.pass[0] = Uhi; p.b.pass[0] = Wt;
-    p.a.pass[1] = Ulo; p.b.pass[1] = Wt;
+    p.a.pass[0] = Uhi; p.b.pass[0] = Wb;
+    p.a.pass[1] = Ulo; p.b.pass[1] = Wb;
   }
   p.ktiles = static_cast<int64_t>(p.passes) * d_out / BK;
   p.splits = 1;
@@ -218,15 +186,17 @@ extern "C" bitsmoe_status bitsmoe_project(const float* Ut_dev, const void* W_dev
   dim3 grid(static_cast<unsigned>(p.tiles_m * p.tiles_n), 1, static_cast<unsigned>(E));
   {
     KernelTimer timer("project", stream);
-    if (PM == 256)
-      hipLaunchKernelGGL((gemm::gemm_nt_kernel<256, PN, 32, 4, FactorStore>), grid,
-                         dim3(gemm::kThreads), 0, s, p, epi);
-    else if (PM == 192)
-      hipLaunchKernelGGL((gemm::gemm_nt_kernel<192, PN, 32, 4, FactorStore>), grid,
-                         dim3(gemm::kThreads), 0, s, p, epi);
-    else
-      hipLaunchKernelGGL((gemm::gemm_nt_kernel<128, PN, 32, 4, FactorStore>), grid,
-                         dim3(gemm::kThreads), 0, s, p, epi);
+#define BITSMOE_PROJECT(TM, KN)                                                              \
+  hipLaunchKernelGGL((gemm::gemm_nt_kernel<TM, PN, 32, 4, FactorStore, false, KN>), grid,   \
+                     dim3(gemm::kThreads), 0, s, p, epi)
+    if (PM == 256) {
+      if (f32) BITSMOE_PROJECT(256, false); else BITSMOE_PROJECT(256, true);
+    } else if (PM == 192) {
+      if (f32) BITSMOE_PROJECT(192, false); else BITSMOE_PROJECT(192, true);
+    } else {
+      if (f32) BITSMOE_PROJECT(128, false); else BITSMOE_PROJECT(128, true);
+    }
+#undef BITSMOE_PROJECT
   }
   BITSMOE_LAUNCH_CHECK("project: gemm launch");
   return ok();
