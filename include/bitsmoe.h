@@ -151,8 +151,8 @@ bitsmoe_status bitsmoe_project(const float* Ut_dev, const void* W_dev, bitsmoe_d
  *              upper triangle of 256 x 256 blocks and the diagonal
  *   bits_host  [nbits] widths, strictly ascending, each in 1..8
  *   L_dev      [units][nbits] fp32 output
- * Shape rules: d % 64 == 0, group in {32, 64, 128, 256}, d % group == 0,
- * 1 <= nbits <= 8.
+ * Shape rules: d % 64 == 0, d < 2^22, group in {32, 64, 128, 256},
+ * d % group == 0, 1 <= nbits <= 8.
  * Accuracy: the off-diagonal part of H enters through fp16 matrix-core
  * products of operands scaled by exact powers of two (per row for the
  * errors, per call for H), with fp32 accumulation; the diagonal part is

@@ -100,12 +100,8 @@ struct Problem {
   int splits;        // gridDim.y
   int tiles_m, tiles_n;
   int symmetric;     // 1: only tiles with tm <= tn are launched (gridDim.x = T(T+1)/2)
-  int group_n;       // column tiles per ordering group (non-symmetric)
-  int ktri;          // 1 (no split-K): row tile tm only visits K tiles from tm * BM / KB on
-                     // (the A operand's upper block triangle)
-  int krev;          // 1 (one pass, one segment): K tiles in descending order, so that
-                     // tiles whose K ranges start at different places but end at the
-                     // same one read the shared B operand in step
+  int group_n;       // column tiles per ordering group (non-symmetric; paired: per
+                     // group_n column tiles, all pairs of each)
 };
 
 // XCD-contiguous logical id of the linear workgroup id t (of n in total).
@@ -134,6 +130,51 @@ __device__ __forceinline__ void tile_coords(const Problem& p, int t, int n, int*
   // narrower) group still has w / tiles_m < its width
   *tm = w % p.tiles_m;
   *tn = first_n + w / p.tiles_m;
+}
+
+// Paired upper-triangle schedule (for a symmetric form: A is the square
+// d x d operand, one pass, one segment, no split-K, BM-wide K blocks).  Row
+// tile tm needs only the K blocks at and right of its diagonal block
+// (tiles_m - tm of them), so every workgroup runs two jobs of tiles_m + 1
+// blocks in all: row tiles tm and tiles_m - 1 - tm of one column tile, or,
+// for an odd tiles_m, the middle row tile of two neighbouring column tiles.
+// Jobs are counted in units of one column tile (even tiles_m, tiles_m / 2
+// workgroups each) or two (odd, tiles_m workgroups each); group_n units
+// form an ordering group, workgroups of a unit consecutive.
+__host__ __device__ __forceinline__ int64_t paired_workgroups(int tiles_m, int64_t tiles_n) {
+  return (tiles_m % 2 == 0) ? tiles_n * (tiles_m / 2) : (tiles_n + 1) / 2 * tiles_m;
+}
+__host__ __device__ __forceinline__ int paired_unit_workgroups(int tiles_m) {
+  return (tiles_m % 2 == 0) ? tiles_m / 2 : tiles_m;
+}
+// Jobs (tm0, tn0) then (tm1, tn1) of workgroup t (of n); returns how many
+// exist (0, 1 or 2: the second column tile of the last unit may be missing).
+__device__ __forceinline__ int paired_jobs(const Problem& p, int t, int n, int* tm0, int* tn0,
+                                           int* tm1, int* tn1) {
+  const int T = p.tiles_m;
+  const int per_unit = paired_unit_workgroups(T);
+  t = xcd_remap(t, n);
+  const int per_group = p.group_n * per_unit;
+  const int g = t / per_group, w = t - g * per_group;
+  const int unit = g * p.group_n + w / per_unit, s = w % per_unit;
+  if (T % 2 == 0) {
+    *tm0 = s;
+    *tm1 = T - 1 - s;
+    *tn0 = *tn1 = unit;
+    return 2;
+  }
+  const int h = (T - 1) / 2;  // pairs per column tile; the middle row tile is h
+  if (s < T - 1) {
+    const int tn = 2 * unit + s / h;
+    *tm0 = s % h;
+    *tm1 = T - 1 - s % h;
+    *tn0 = *tn1 = tn;
+    return tn < p.tiles_n ? 2 : 0;
+  }
+  *tm0 = *tm1 = h;
+  *tn0 = 2 * unit;
+  *tn1 = 2 * unit + 1;
+  return *tn1 < p.tiles_n ? 2 : 1;
 }
 
 // v made wave-uniform (held in scalar registers from here on).
@@ -186,10 +227,9 @@ struct KPos {
   int64_t offa, offb;    // element offsets of the tile from the pass bases
   int64_t stepa, stepb;  // per K tile
   int64_t jumpa, jumpb;  // extra at a segment boundary
-  int64_t kdir;          // +KB, or -KB in descending order
   PassBases ba, bb;
   __device__ __forceinline__ void init(const Problem& p, int64_t kt, int64_t z, int tm, int tn,
-                                       int BM, int BN, bool reverse) {
+                                       int BM, int BN) {
     const int64_t tiles_seg = p.kseg / KB;
     const int64_t per_pass = static_cast<int64_t>(p.segs) * tiles_seg;
     const int pass = static_cast<int>(kt / per_pass);
@@ -207,20 +247,15 @@ struct KPos {
     bb.make_uniform();
     stepa = uniform64(p.a.kstep != 0 ? p.a.kstep : KB);
     stepb = uniform64(p.b.kstep != 0 ? p.b.kstep : KB);
-    kdir = reverse ? -KB : KB;
     jumpa = uniform64(p.a.estride - tiles_seg * stepa);
     jumpb = uniform64(p.b.estride - tiles_seg * stepb);
     seg = uniform64(seg);
     k0 = uniform64(k0);
     offa = uniform64(seg * p.a.estride + ki * stepa);
     offb = uniform64(seg * p.b.estride + ki * stepb);
-    if (reverse) {  // one pass, one segment: walk down, never wrap
-      stepa = -stepa;
-      stepb = -stepb;
-    }
   }
   __device__ __forceinline__ void next(const Problem& p) {
-    k0 += kdir;
+    k0 += KB;
     offa += stepa;
     offb += stepb;
     const bool wrap = k0 == p.kseg;
@@ -234,6 +269,48 @@ struct KPos {
     offb = wrap2 ? 0 : offb;
     ba.advance(wrap2);
     bb.advance(wrap2);
+  }
+};
+
+// K walk of one job of the paired-triangle schedule (one pass, one segment,
+// no split-K): K tiles q0, q0 + 1, ... (or q0, q0 - 1, ...) for `turn`
+// visits, then from tile qt downwards.  Scalar selects only; offsets within a
+// row tile are 32-bit (the caller keeps ktiles * kstep below 2^31).
+template <int KB>
+struct TriWalk {
+  const uint16_t* ba;
+  const uint16_t* bb;
+  int offa, offb;    // element offsets of the current tile from the tile bases
+  int stepa, stepb;  // signed, per K tile
+  int n, turn;       // visits so far; the visit at which the walk turns (-1: never)
+  int toffa, toffb;  // offsets of tile qt
+  __device__ __forceinline__ void init(const Problem& p, int64_t z, int tm, int tn, int BM, int BN,
+                                       int64_t q0, bool up, int64_t turn_at, int64_t qt) {
+    PassBases a, b;
+    a.init(p.a, z, tm, BM);
+    b.init(p.b, z, tn, BN);
+    ba = reinterpret_cast<const uint16_t*>(uniform64(reinterpret_cast<int64_t>(a.q0)));
+    bb = reinterpret_cast<const uint16_t*>(uniform64(reinterpret_cast<int64_t>(b.q0)));
+    const int sa = static_cast<int>(p.a.kstep != 0 ? p.a.kstep : KB);
+    const int sb = static_cast<int>(p.b.kstep != 0 ? p.b.kstep : KB);
+    offa = uniform32(static_cast<int>(q0) * sa);
+    offb = uniform32(static_cast<int>(q0) * sb);
+    stepa = uniform32(up ? sa : -sa);
+    stepb = uniform32(up ? sb : -sb);
+    n = 0;
+    turn = uniform32(static_cast<int>(turn_at));
+    toffa = uniform32(static_cast<int>(qt) * sa);
+    toffb = uniform32(static_cast<int>(qt) * sb);
+  }
+  __device__ __forceinline__ void next() {
+    ++n;
+    offa += stepa;
+    offb += stepb;
+    const bool t = n == turn;
+    offa = t ? toffa : offa;
+    offb = t ? toffb : offb;
+    stepa = t ? -stepa : stepa;
+    stepb = t ? -stepb : stepb;
   }
 };
 
@@ -352,7 +429,8 @@ __device__ __forceinline__ s16x4 ds_read_tr16(const uint16_t* p) {
 // of transposing reads (4 rows x 4 chunks x 2 halves) covers all 64 banks.
 __device__ __forceinline__ int kn_swz(int r, int c) { return c ^ (4 * (r & 3)); }
 
-template <int BM, int BN, int KB, int STAGES, class Epi, bool F16 = false, bool BKN = false>
+template <int BM, int BN, int KB, int STAGES, class Epi, bool F16 = false, bool BKN = false,
+          bool PAIRED = false>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void gemm_nt_kernel(Problem p, Epi epi) {
   static_assert(BM % 64 == 0 && BN % 64 == 0, "tile");
@@ -378,32 +456,34 @@ void gemm_nt_kernel(Problem p, Epi epi) {
   f.wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   f.wm = f.wave >> 1;
   f.wn = f.wave & 1;
-  tile_coords(p, blockIdx.x, gridDim.x, &f.tm, &f.tn);
+  // PAIRED: gridDim.x = paired_workgroups(tiles_m, tiles_n), two jobs each
+  // (see paired_jobs); otherwise one tile per workgroup.
+  int njobs = 1, tm0 = 0, tn0 = 0, tm1 = 0, tn1 = 0;
+  if constexpr (PAIRED) {
+    njobs = paired_jobs(p, blockIdx.x, gridDim.x, &tm0, &tn0, &tm1, &tn1);
+    if (njobs == 0) return;  // whole workgroup: past the last column tile
+  } else {
+    tile_coords(p, blockIdx.x, gridDim.x, &tm0, &tn0);
+  }
+  f.tm = tm0;
+  f.tn = tn0;
   f.ks = blockIdx.y;
   f.z = blockIdx.z;
-  f.row0 = f.tm * BM + f.wm * F::WM;
-  f.col0 = f.tn * BN + f.wn * F::WN;
-#pragma unroll
-  for (int mi = 0; mi < F::FM; ++mi)
-#pragma unroll
-    for (int ni = 0; ni < F::FN; ++ni)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) f.acc[mi][ni][r] = 0.0f;
 
   const int64_t ktiles = p.ktiles * BK / KB;  // K tiles of this kernel's step
-  int64_t kt0 = ktiles * f.ks / p.splits;
+  const int64_t kt0 = ktiles * f.ks / p.splits;
   const int64_t kt1 = ktiles * (f.ks + 1) / p.splits;
-  if (p.ktri) kt0 = static_cast<int64_t>(f.tm) * (BM / KB);
 
   // Direct global->LDS loads.  Wave instruction i of this wave fills the
   // 1 KiB LDS block b = wave + 4 i (rows b*RPB .. b*RPB+RPB-1); lane l lands
   // at byte 16 l of the block, i.e. row b*RPB + l/KC, slot l%KC, so it fetches
   // the global chunk that the swizzle stores in that slot.  Rows past the end
   // are clamped to the last row: their accumulators are never stored.
-  const int64_t a_row0 = static_cast<int64_t>(f.tm) * BM;
-  const int64_t b_row0 = static_cast<int64_t>(f.tn) * BN;
   uint32_t oa[AW], ob[BW];  // byte offsets from the tile's first element
   const bool a_tiled = p.a.kstep != 0, b_tiled = p.b.kstep != 0;
+  auto set_offsets = [&]() {
+  const int64_t a_row0 = static_cast<int64_t>(f.tm) * BM;
+  const int64_t b_row0 = static_cast<int64_t>(f.tn) * BN;
 #pragma unroll
   for (int i = 0; i < AW; ++i) {
     const int r = (f.wave + 4 * i) * RPB + f.lane / KC;
@@ -430,7 +510,9 @@ void gemm_nt_kernel(Problem p, Epi epi) {
                       : static_cast<uint32_t>(((gr - b_row0) * p.b.ld + 8 * j) * 2);
     }
   }
+  };
   KPos<KB> kp;
+  TriWalk<KB> tw;
   // Loads of the next K tile into stage buffer s, one wave instruction at a
   // time (q < LPS) so that they can be spread between matrix-core ops.
   struct Issue {
@@ -439,9 +521,15 @@ void gemm_nt_kernel(Problem p, Epi epi) {
     int s;
   };
   auto issue_begin = [&](int s) {
-    Issue is{kp.ba.q0 + kp.offa, kp.bb.q0 + kp.offb, s};
-    kp.next(p);
-    return is;
+    if constexpr (PAIRED) {
+      Issue is{tw.ba + tw.offa, tw.bb + tw.offb, s};
+      tw.next();
+      return is;
+    } else {
+      Issue is{kp.ba.q0 + kp.offa, kp.bb.q0 + kp.offb, s};
+      kp.next(p);
+      return is;
+    }
   };
   auto issue_part = [&](const Issue& is, int q) {
     if (q < AW)
@@ -512,7 +600,7 @@ void gemm_nt_kernel(Problem p, Epi epi) {
     __builtin_amdgcn_sched_barrier(0);
   };
 
-  const int64_t nk = kt1 - kt0;
+  int64_t nk = 0;      // K tiles of the current job
   int64_t issued = 0;  // K tiles whose loads have been issued
   // Makes K tile `next` visible to every wave: wait for this wave's loads of
   // it (the STAGES - 3 tiles issued after it may stay in flight), then a bare
@@ -566,42 +654,82 @@ void gemm_nt_kernel(Problem p, Epi epi) {
     });
   };
 
-  if (nk > 0) {
-    const bool rev = p.krev != 0 && p.passes == 1 && p.segs == 1;
-    kp.init(p, rev ? kt1 - 1 : kt0, f.z, f.tm, f.tn, BM, BN, rev);
-    // tiles 0 .. STAGES - 3 up front, tile STAGES - 2 once tile 0 is visible
-    for (int q = 0; q < STAGES - 2 && issued < nk; ++q) {
-      issue(q);
-      ++issued;
+  for (int job = 0; job < njobs; ++job) {
+    if constexpr (PAIRED) {
+      // job 0: K tiles from the last one down to the diagonal block of its
+      // row tile.  job 1: K tiles from the block right of its diagonal block
+      // up to the last one, then its diagonal block downwards.  At any time
+      // the workgroups of one column tile then read at most two K blocks of
+      // B (block T - 1 - s in job 0, block s in job 1, s counted in blocks
+      // from the start), and every job ends on its diagonal block in
+      // descending order (the epilogue finds the last K tiles of that block
+      // still staged).
+      const int64_t kpb = BM / KB;  // K tiles per K block
+      if (job == 0) {
+        nk = ktiles - f.tm * kpb;
+        tw.init(p, f.z, f.tm, f.tn, BM, BN, ktiles - 1, false, -1, 0);
+      } else {
+        f.tm = tm1;
+        f.tn = tn1;
+        const int64_t lo = f.tm * kpb;
+        const int64_t hi = lo + kpb < ktiles ? lo + kpb : ktiles;
+        const int64_t up = ktiles - hi;
+        nk = up + (hi - lo);
+        if (up > 0)
+          tw.init(p, f.z, f.tm, f.tn, BM, BN, hi, true, up, hi - 1);
+        else
+          tw.init(p, f.z, f.tm, f.tn, BM, BN, hi - 1, false, -1, 0);
+      }
+    } else {
+      nk = kt1 - kt0;
     }
-    sync_tile(0, True());
-    if (issued < nk) {
-      issue(STAGES - 2);
-      ++issued;
+    f.row0 = f.tm * BM + f.wm * F::WM;
+    f.col0 = f.tn * BN + f.wn * F::WN;
+#pragma unroll
+    for (int mi = 0; mi < F::FM; ++mi)
+#pragma unroll
+      for (int ni = 0; ni < F::FN; ++ni)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) f.acc[mi][ni][r] = 0.0f;
+    set_offsets();
+    issued = 0;
+    if (nk > 0) {
+      if constexpr (!PAIRED) kp.init(p, kt0, f.z, f.tm, f.tn, BM, BN);
+      // tiles 0 .. STAGES - 3 up front, tile STAGES - 2 once tile 0 is visible
+      for (int q = 0; q < STAGES - 2 && issued < nk; ++q) {
+        issue(q);
+        ++issued;
+      }
+      sync_tile(0, True());
+      if (issued < nk) {
+        issue(STAGES - 2);
+        ++issued;
+      }
+      read_frags(Set0(), 0, 0);
+      int64_t i = 0;
+      for (; i + STAGES - 1 < nk; ++i) tile(i, True(), True(), False());
+      for (; i + 1 < nk; ++i) tile(i, True(), False(), True());
+      tile(i, False(), False(), True());
     }
-    read_frags(Set0(), 0, 0);
-    int64_t i = 0;
-    for (; i + STAGES - 1 < nk; ++i) tile(i, True(), True(), False());
-    for (; i + 1 < nk; ++i) tile(i, True(), False(), True());
-    tile(i, False(), False(), True());
+    // Pin the accumulators to AGPRs across the loop: otherwise an epilogue
+    // that feeds them to VALU instructions can pull part of them into VGPRs,
+    // which the loop then runs out of.
+#pragma unroll
+    for (int mi = 0; mi < F::FM; ++mi)
+#pragma unroll
+      for (int ni = 0; ni < F::FN; ++ni) asm volatile("" : "+a"(f.acc[mi][ni]));
+    wait_vmcnt<0>();
+    __syncthreads();  // epilogues may reuse the stage buffers
+    StageLds lds;
+    lds.a = As;
+    lds.b = Bs;
+    lds.a_elems = STAGES * ASZ;
+    lds.b_elems = STAGES * BSZ;
+    lds.nk = nk;
+    lds.stages = STAGES;
+    epi(f, lds);
+    if constexpr (PAIRED) __syncthreads();  // the next job refills the stage buffers
   }
-  // Pin the accumulators to AGPRs across the loop: otherwise an epilogue
-  // that feeds them to VALU instructions can pull part of them into VGPRs,
-  // which the loop then runs out of.
-#pragma unroll
-  for (int mi = 0; mi < F::FM; ++mi)
-#pragma unroll
-    for (int ni = 0; ni < F::FN; ++ni) asm volatile("" : "+a"(f.acc[mi][ni]));
-  wait_vmcnt<0>();
-  __syncthreads();  // epilogues may reuse the stage buffers
-  StageLds lds;
-  lds.a = As;
-  lds.b = Bs;
-  lds.a_elems = STAGES * ASZ;
-  lds.b_elems = STAGES * BSZ;
-  lds.nk = kt1 - kt0;
-  lds.stages = STAGES;
-  epi(f, lds);
 }
 
 }  // namespace gemm

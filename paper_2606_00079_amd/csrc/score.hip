@@ -394,6 +394,7 @@ extern "C" bitsmoe_status bitsmoe_score(const float* C_dev, int64_t units, int64
     return fail(BITSMOE_ERR_SHAPE, "score: group must be 32, 64, 128 or 256");
   if (d % 64 != 0 || d % group != 0)
     return fail(BITSMOE_ERR_SHAPE, "score: d must be a multiple of 64 and of the group");
+  if (d >= (int64_t{1} << 22)) return fail(BITSMOE_ERR_SHAPE, "score: d must be below 2^22");
   hipStream_t s = static_cast<hipStream_t>(stream);
   const int64_t R = units * nbits;
   const int tiles_m = static_cast<int>((d + SBM - 1) / SBM);
@@ -459,15 +460,18 @@ extern "C" bitsmoe_status bitsmoe_score(const float* C_dev, int64_t units, int64
   p.tiles_m = tiles_m;
   p.tiles_n = static_cast<int>(tiles_n);
   p.symmetric = 0;
-  p.group_n = std::max(1, 32 / tiles_m);  // ~one XCD's worth of workgroups per group
-  p.ktri = 1;  // H symmetric: upper block triangle of H_off only
-  p.krev = 1;  // all row tiles walk K down from the end, in step
+  // H symmetric: only the upper block triangle of H_off is visited, in the
+  // paired schedule, so that every workgroup does the same tiles_m + 1
+  // blocks of work
+  p.group_n = std::max(1, 32 / gemm::paired_unit_workgroups(tiles_m));  // ~one XCD's worth
   RowDot epi{D, part, R, d, tiles_m};
-  dim3 grid(static_cast<unsigned>(tiles_m * tiles_n), 1, 1);
+  const int64_t wgs = gemm::paired_workgroups(tiles_m, tiles_n);
+  if (wgs > INT32_MAX) return fail(BITSMOE_ERR_SHAPE, "score: too many units");
+  dim3 grid(static_cast<unsigned>(wgs), 1, 1);
   {
     KernelTimer timer("score_gemm", stream);
-    hipLaunchKernelGGL((gemm::gemm_nt_kernel<SBM, SBN, SKB, SSTAGES, RowDot, true>), grid,
-                       dim3(gemm::kThreads), 0, s, p, epi);
+    hipLaunchKernelGGL((gemm::gemm_nt_kernel<SBM, SBN, SKB, SSTAGES, RowDot, true, false, true>),
+                       grid, dim3(gemm::kThreads), 0, s, p, epi);
   }
   BITSMOE_LAUNCH_CHECK("score: gemm launch");
   hipLaunchKernelGGL(finalize_kernel, dim3(static_cast<unsigned>((R + 255) / 256)), dim3(256), 0, s,

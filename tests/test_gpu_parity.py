@@ -194,6 +194,11 @@ SCORE_CASES = [
     ("group32_bits8", 70, 256, 32, (1, 2, 3, 4, 8), False),
     ("group256", 40, 512, 256, (2, 4), True),
     ("one_width", 33, 128, 128, (3,), False),
+    # paired-triangle schedule: odd and even row-tile counts, partial last K
+    # block, an odd number of column tiles (the last unit is half empty)
+    ("odd_row_tiles", 130, 704, 64, (1, 2, 3, 4), True),
+    ("five_row_tiles", 70, 1280, 128, (2, 3, 4), False),
+    ("four_row_tiles_ragged", 64, 960, 64, (1, 2, 3, 4), False),
 ]
 
 
