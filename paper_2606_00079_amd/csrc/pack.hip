@@ -1,12 +1,16 @@
 // Step 5: pack every spectral unit at its assigned width as bit planes with
 // fp16 (scale, min) per group, and the inverse (dequantize) for checking.
 //
-// One wave per unit.  Word w of the row holds entries 64 w .. 64 w + 63, one
-// per lane, so the plane-t word of w is the wave ballot of bit t of the lane
-// codes.  Words are gathered in LDS and written out contiguously.  Codes
-// follow the fp64 quotient rule of the quantizer (decided in fp32 where that
-// provably gives the same integer), so they match an fp64 reference bit for
-// bit given the same fp32 row.
+// One wave per unit, four units per workgroup.  Lane l holds entries
+// [512 c + 8 l, 512 c + 8 l + 8) of chunk c (a group of G entries spans G/8
+// consecutive lanes).  For bit plane t the lane's eight code bits form one
+// byte: bit i of it is bit t of entry 8 l + i, which is exactly byte l of the
+// plane's 64-bit words 8 c .. 8 c + 7 (word w holds entries 64 w .. 64 w + 63,
+// bit j = entry 64 w + j, little-endian), so a plane of a chunk is one
+// coalesced 64-byte store.  The loads of chunk c + 1 are issued before chunk
+// c is packed.  Codes follow the fp64 quotient rule of the quantizer (decided
+// in fp32 where that provably gives the same integer), so they match an fp64
+// reference bit for bit given the same fp32 row.
 #include <algorithm>
 
 #include "bitsmoe.h"
@@ -17,50 +21,58 @@ namespace bitsmoe {
 namespace {
 
 template <int G>
-__global__ __launch_bounds__(64) void pack_kernel(const float* __restrict__ C, int64_t units,
-                                                  int64_t d, const uint8_t* __restrict__ bits,
-                                                  const int64_t* __restrict__ off,
-                                                  int64_t total_words,
-                                                  uint64_t* __restrict__ codes,
-                                                  uint32_t* __restrict__ params) {
-  extern __shared__ uint64_t smem[];  // [8 * nw] plane words, then [d/G] params
-  constexpr int WPB = G >= 64 ? G / 64 : 1;  // words per group batch
-  constexpr int RED = G >= 64 ? 64 : G;      // lanes sharing a group within a word
-  const int lane = threadIdx.x;
-  const int64_t u = blockIdx.x;
-  if (u >= units) return;
+__global__ __launch_bounds__(256) void pack_kernel(const float* __restrict__ C, int64_t units,
+                                                   int64_t d, const uint8_t* __restrict__ bits,
+                                                   const int64_t* __restrict__ off,
+                                                   int64_t total_words,
+                                                   uint64_t* __restrict__ codes,
+                                                   uint32_t* __restrict__ params) {
+  constexpr int GL = G / 8;  // lanes per group
+  const int lane = threadIdx.x & 63;
+  const int64_t u = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
+  if (u >= units) return;  // whole wave exits together
   const int b = bits[u];
   const int64_t nw = d / 64;
   const int64_t o0 = off[u], o1 = off[u + 1];
   if (b < 1 || b > BITSMOE_MAX_BITS || o1 - o0 != b * nw || o0 < 0 || o1 > total_words) return;
-  uint64_t* wbuf = smem;
-  uint32_t* pbuf = reinterpret_cast<uint32_t*>(smem + 8 * nw);
   const double qmax = static_cast<double>((1 << b) - 1);
   const float qmaxf = static_cast<float>((1 << b) - 1);
   const float* crow = C + u * d;
-  // words are processed in segments of kSegWords: every load of a segment is
-  // issued before any of its values is used
-  constexpr int kSegWords = 32;
-  static_assert(kSegWords % WPB == 0, "segments hold whole groups");
-  for (int64_t s0 = 0; s0 < nw; s0 += kSegWords) {
-    float cv[kSegWords];
+  uint8_t* ubytes = reinterpret_cast<uint8_t*>(codes + o0);  // plane t at byte t * d / 8
+  uint32_t* uparams = params + u * (d / G);
+
+  // lane's 8 entries of the chunk at k0 (zeros past the end)
+  auto load8 = [&](int64_t k0, float (&c)[8]) {
+    const int64_t k = k0 + 8 * lane;
+    if (k < d) {
+      const float4 v0 = *reinterpret_cast<const float4*>(crow + k);
+      const float4 v1 = *reinterpret_cast<const float4*>(crow + k + 4);
+      c[0] = v0.x; c[1] = v0.y; c[2] = v0.z; c[3] = v0.w;
+      c[4] = v1.x; c[5] = v1.y; c[6] = v1.z; c[7] = v1.w;
+    } else {
 #pragma unroll
-    for (int i = 0; i < kSegWords; ++i) cv[i] = (s0 + i < nw) ? crow[64 * (s0 + i) + lane] : 0.0f;
+      for (int i = 0; i < 8; ++i) c[i] = 0.0f;
+    }
+  };
+  float cur[8], nxt[8];
+  load8(0, cur);
+  for (int64_t k0 = 0; k0 < d; k0 += 512) {
+    if (k0 + 512 < d) load8(k0 + 512, nxt);
+    const int64_t k = k0 + 8 * lane;
+    float mn = cur[0], mx = cur[0];
 #pragma unroll
-    for (int g0 = 0; g0 < kSegWords; g0 += WPB) {
-      const int64_t w0 = s0 + g0;
-      if (w0 >= nw) break;
-      float mn = cv[g0], mx = cv[g0];
+    for (int i = 1; i < 8; ++i) {
+      mn = fminf(mn, cur[i]);
+      mx = fmaxf(mx, cur[i]);
+    }
 #pragma unroll
-      for (int i = 1; i < WPB; ++i) {
-        mn = fminf(mn, cv[g0 + i]);
-        mx = fmaxf(mx, cv[g0 + i]);
-      }
-#pragma unroll
-      for (int o = RED / 2; o > 0; o >>= 1) {
-        mn = fminf(mn, __shfl_xor(mn, o, 64));
-        mx = fmaxf(mx, __shfl_xor(mx, o, 64));
-      }
+    for (int o = 1; o < GL; o <<= 1) {
+      mn = fminf(mn, __shfl_xor(mn, o, 64));
+      mx = fmaxf(mx, __shfl_xor(mx, o, 64));
+    }
+    // d is a multiple of G, so a group is either wholly inside the row or
+    // wholly past its end
+    if (k < d) {
       const uint16_t m16 = f32_to_f16_bits(mn);
       const uint16_t s16 = f32_to_f16_bits((mx - mn) / qmaxf);
       const float mf = f16_bits_to_f32(m16);
@@ -71,40 +83,35 @@ __global__ __launch_bounds__(64) void pack_kernel(const float* __restrict__ C, i
       // codes from the fp32 quotient: it rounds the same way as the fp64 one
       // unless it lies within 1e-4 of a rounding boundary, and those (rare)
       // lanes decide in fp64
-      int q[WPB];
+      uint32_t q[8];
       bool near = false;
 #pragma unroll
-      for (int i = 0; i < WPB; ++i) {
-        const float t = (cv[g0 + i] - mf) * inv;
+      for (int i = 0; i < 8; ++i) {
+        const float t = (cur[i] - mf) * inv;
         const float r = rintf(t);
         near |= fabsf(t - r) > 0.4999f;
-        q[i] = static_cast<int>(__builtin_amdgcn_fmed3f(r, 0.0f, qmaxf));
+        q[i] = static_cast<uint32_t>(__builtin_amdgcn_fmed3f(r, 0.0f, qmaxf));
       }
       if (near && sf > 0.0f) {
         const double md = static_cast<double>(mf), sd = static_cast<double>(sf);
 #pragma unroll
-        for (int i = 0; i < WPB; ++i) {
-          const double t = (static_cast<double>(cv[g0 + i]) - md) / sd;
-          q[i] = static_cast<int>(fmin(fmax(rint(t), 0.0), qmax));
+        for (int i = 0; i < 8; ++i) {
+          const double t = (static_cast<double>(cur[i]) - md) / sd;
+          q[i] = static_cast<uint32_t>(fmin(fmax(rint(t), 0.0), qmax));
         }
       }
+      if ((lane % GL) == 0)
+        uparams[k / G] = static_cast<uint32_t>(s16) | (static_cast<uint32_t>(m16) << 16);
+      for (int t = 0; t < b; ++t) {
+        uint32_t byte = 0;
 #pragma unroll
-      for (int i = 0; i < WPB; ++i) {
-        for (int t = 0; t < b; ++t) {
-          const uint64_t word = __ballot((q[i] >> t) & 1);
-          if (lane == 0) wbuf[t * nw + w0 + i] = word;
-        }
-      }
-      if ((lane % RED) == 0) {
-        const int64_t g = (64 * w0 + lane) / G;
-        pbuf[g] = static_cast<uint32_t>(s16) | (static_cast<uint32_t>(m16) << 16);
+        for (int i = 0; i < 8; ++i) byte |= ((q[i] >> t) & 1u) << i;
+        ubytes[t * (d / 8) + k / 8] = static_cast<uint8_t>(byte);
       }
     }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) cur[i] = nxt[i];
   }
-  __syncthreads();
-  for (int64_t i = lane; i < b * nw; i += 64) codes[o0 + i] = wbuf[i];
-  const int64_t ng = d / G;
-  for (int64_t g = lane; g < ng; g += 64) params[u * ng + g] = pbuf[g];
 }
 
 __global__ __launch_bounds__(64) void unpack_kernel(const uint64_t* __restrict__ codes,
@@ -158,27 +165,25 @@ extern "C" bitsmoe_status bitsmoe_pack(const float* C_dev, int64_t units, int64_
   bitsmoe_status st = check_pack_args(units, d, group);
   if (st != BITSMOE_OK) return st;
   if (total_words < 0) return fail(BITSMOE_ERR_ARG, "pack: negative total_words");
-  const size_t lds = static_cast<size_t>(8 * (d / 64)) * 8 + static_cast<size_t>(d / group) * 4;
-  if (lds > 160 * 1024) return fail(BITSMOE_ERR_SHAPE, "pack: row too long");
   hipStream_t s = static_cast<hipStream_t>(stream);
   uint32_t* pr = reinterpret_cast<uint32_t*>(params_dev);
-  dim3 grid(static_cast<unsigned>(units));
+  dim3 grid(static_cast<unsigned>((units + 3) / 4));
   KernelTimer timer("pack", stream);
   switch (group) {
     case 32:
-      hipLaunchKernelGGL(pack_kernel<32>, grid, dim3(64), lds, s, C_dev, units, d, bits_dev,
+      hipLaunchKernelGGL(pack_kernel<32>, grid, dim3(256), 0, s, C_dev, units, d, bits_dev,
                          word_offsets_dev, total_words, codes_dev, pr);
       break;
     case 64:
-      hipLaunchKernelGGL(pack_kernel<64>, grid, dim3(64), lds, s, C_dev, units, d, bits_dev,
+      hipLaunchKernelGGL(pack_kernel<64>, grid, dim3(256), 0, s, C_dev, units, d, bits_dev,
                          word_offsets_dev, total_words, codes_dev, pr);
       break;
     case 128:
-      hipLaunchKernelGGL(pack_kernel<128>, grid, dim3(64), lds, s, C_dev, units, d, bits_dev,
+      hipLaunchKernelGGL(pack_kernel<128>, grid, dim3(256), 0, s, C_dev, units, d, bits_dev,
                          word_offsets_dev, total_words, codes_dev, pr);
       break;
     default:
-      hipLaunchKernelGGL(pack_kernel<256>, grid, dim3(64), lds, s, C_dev, units, d, bits_dev,
+      hipLaunchKernelGGL(pack_kernel<256>, grid, dim3(256), 0, s, C_dev, units, d, bits_dev,
                          word_offsets_dev, total_words, codes_dev, pr);
       break;
   }

@@ -129,7 +129,7 @@ struct QuantBits {
 // below 6.1e-5 for codes up to 255), in which case fp64 decides.
 // The row is read twice: once for max |c|, once to quantize (the second read
 // mostly hits in the caches; holding the row in registers instead costs more
-// in occupancy than it saves).
+// in occupancy than it saves); both passes keep several loads in flight.
 template <int NB>
 __global__ __launch_bounds__(256) void dgen_kernel(const float* __restrict__ C, int64_t units,
                                                    int64_t d, int G, QuantBits qb,
@@ -167,11 +167,20 @@ __global__ __launch_bounds__(256) void dgen_kernel(const float* __restrict__ C, 
   };
 
   // |delta| <= max - min <= 2 max |c| < 2^(e + 1): the error rows are stored
-  // as fp16(delta * 2^E) with E = kF16Top - 1 - e
-  float cc[8];
+  // as fp16(delta * 2^E) with E = kF16Top - 1 - e.  Four chunks' loads are
+  // issued before any is reduced.
   float amax = 0.0f;
-  for (int64_t k0 = 0; k0 < d; k0 += 512) {
-    load8(k0, cc);
+  int64_t ka = 0;
+  for (; ka + 4 * 512 <= d; ka += 4 * 512) {
+    float c4[4][8];
+#pragma unroll
+    for (int x = 0; x < 4; ++x) load8(ka + 512 * x, c4[x]);
+#pragma unroll
+    for (int x = 0; x < 4; ++x) amax = fmaxf(amax, absmax8(c4[x]));
+  }
+  for (; ka < d; ka += 512) {
+    float cc[8];
+    load8(ka, cc);
     amax = fmaxf(amax, absmax8(cc));
   }
 #pragma unroll
@@ -256,9 +265,14 @@ __global__ __launch_bounds__(256) void dgen_kernel(const float* __restrict__ C, 
       *reinterpret_cast<uint4*>(D + gemm::tiled_offset(u * nb + j, k, d, SBN)) = pk;
     }
   };
+  // the loads of chunk c + 1 are issued before chunk c is quantized
+  float cur[8], nxt[8];
+  load8(0, cur);
   for (int64_t k0 = 0; k0 < d; k0 += 512) {
-    load8(k0, cc);
-    chunk(k0, cc);
+    if (k0 + 512 < d) load8(k0 + 512, nxt);
+    chunk(k0, cur);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) cur[i] = nxt[i];
   }
 #pragma unroll
   for (int j = 0; j < NB; ++j) {
