@@ -1,0 +1,171 @@
+"""Pins of the oracle's piecewise surrogate cost and budget (App. B.3-B.5).
+
+Each check ties the oracle to something other than its own formula: the
+Gaussian closed form behind the printed kappa_b, the actual error of the
+paper's quantizers on random unit vectors, the brute-force activation loss
+of an evicted unit, a storage-accounting characterization of the budget,
+and exhaustive search for the ILP over the surrogate's widths.
+"""
+import math
+
+import numpy as np
+import pytest
+from scipy import optimize, stats
+
+import oracle
+from oracle import surrogate as sg
+
+
+def _unit_rows(n, d, seed, heavy=False):
+    g = np.random.default_rng(seed)
+    P = g.standard_t(4, size=(n, d)) if heavy else g.standard_normal((n, d))
+    return P / np.linalg.norm(P, axis=1, keepdims=True)
+
+
+def _gauss_sym_mse(s, b):
+    """E[(x - Q_b(x; s))^2] for x ~ N(0, 1) and levels s * {-2^(b-1) .. 2^(b-1) - 1},
+    summed cell by cell in closed form."""
+    lo, hi = -(1 << (b - 1)), (1 << (b - 1)) - 1
+    total = 0.0
+    for q in range(lo, hi + 1):
+        a = -np.inf if q == lo else (q - 0.5) * s
+        c = np.inf if q == hi else (q + 0.5) * s
+        lev = q * s
+        # int_a^c (x - lev)^2 phi(x) dx = [Phi](1 + lev^2) + [-phi](x + lev) ... in closed form
+        Pa, Pc = stats.norm.cdf(a), stats.norm.cdf(c)
+        fa = 0.0 if np.isinf(a) else stats.norm.pdf(a)
+        fc = 0.0 if np.isinf(c) else stats.norm.pdf(c)
+        xa = 0.0 if np.isinf(a) else a * fa
+        xc = 0.0 if np.isinf(c) else c * fc
+        m0 = Pc - Pa                      # int phi
+        m1 = fa - fc                      # int x phi
+        m2 = m0 + xa - xc                 # int x^2 phi
+        total += m2 - 2 * lev * m1 + lev * lev * m0
+    return total
+
+
+@pytest.mark.parametrize("b", [2, 3, 4])
+def test_kappa_is_the_gaussian_optimal_symmetric_distortion(b):
+    """The printed kappa_b (Table kappa_values) match the relative MSE of the
+    MSE-optimal symmetric quantizer for Gaussian coordinates -- the limit of
+    Eq. app_component_kappa_def for high-dimensional random directions."""
+    res = optimize.minimize_scalar(lambda s: _gauss_sym_mse(s, b), bounds=(0.05, 3.0),
+                                   method="bounded", options={"xatol": 1e-10})
+    kappa = res.fun
+    assert abs(kappa - sg.KAPPA_PRINTED[b]) / sg.KAPPA_PRINTED[b] < 5e-3, (b, kappa)
+
+
+@pytest.mark.parametrize("b", [2, 3, 4])
+def test_symmetric_quantizer_reproduces_kappa(b):
+    """Eq. app_kappa_def with the oracle's symmetric quantizer and a per-vector
+    MSE-optimal scale (grid search) lands on the printed kappa_b."""
+    d = 2048
+    P = _unit_rows(48, d, seed=10 + b)
+    grid = np.linspace(0.1, 1.6, 601) / math.sqrt(d)
+    ks = []
+    for p in P:
+        errs = [np.sum((p - sg.quant_symmetric(p, b, s)) ** 2) for s in grid]
+        ks.append(min(errs))
+    assert abs(np.mean(ks) - sg.KAPPA_PRINTED[b]) / sg.KAPPA_PRINTED[b] < 2e-2
+
+
+def test_sign_distortion_is_sin2_theta():
+    """Lemma one_bit_sign_distortion: ||p - mean|p| sign(p)||^2 = 1 - cos^2 theta,
+    cos theta = ||p||_1 / sqrt(d), exactly (any unit vector)."""
+    for d, heavy in ((64, False), (768, True), (2048, False)):
+        P = _unit_rows(16, d, seed=d, heavy=heavy)
+        a2, rho, cos = sg.unit_stats(P)
+        e_formula = sg.distortion(1, d, rho, cos)
+        e_direct = np.array([np.sum((p - sg.quant_sign(p)) ** 2) for p in P])
+        np.testing.assert_allclose(e_formula, e_direct, rtol=1e-12, atol=1e-15)
+        np.testing.assert_allclose(a2, 1.0, rtol=1e-12)
+
+
+@pytest.mark.parametrize("b", [6, 8])
+def test_high_bit_distortion_matches_uniform_noise(b):
+    """Lemma high_bit_distortion: with s = rho / q_max the measured error of the
+    symmetric quantizer is close to d s^2 / 12, and eta exp(-2 ln2 b) equals it
+    up to the q_max ~ 2^(b-1) step of the derivation."""
+    d = 2048
+    P = _unit_rows(64, d, seed=20 + b)
+    a2, rho, cos = sg.unit_stats(P)
+    qmax = (1 << (b - 1)) - 1
+    meas = np.array([np.sum((p - sg.quant_symmetric(p, b, r / qmax)) ** 2) for p, r in zip(P, rho)])
+    model = d * (rho / qmax) ** 2 / 12.0
+    assert abs(np.mean(meas / model) - 1.0) < 0.03
+    e = sg.distortion(b, d, rho, cos)
+    np.testing.assert_allclose(e, model * (qmax / 2 ** (b - 1)) ** 2, rtol=1e-12)
+
+
+def test_eviction_cost_is_the_exact_activation_loss():
+    """With gamma = 1 the b = 0 column is alpha^2 beta = c H c^T, which equals
+    ||X c^T||^2 / n computed from the calibration rows (App. B.2: exact only
+    under eviction)."""
+    g = np.random.default_rng(3)
+    n, d = 300, 48
+    X = g.standard_normal((n, d))
+    X[:, 5] *= 9.0
+    H = oracle.gram(X)
+    C = g.standard_normal((20, d)) * np.exp(g.standard_normal((20, 1)))
+    L = sg.surrogate_table(C, H, gamma=1.0)
+    brute = np.array([np.sum((X @ c) ** 2) / n for c in C])
+    np.testing.assert_allclose(L[:, sg.WIDTHS.index(0)], brute, rtol=1e-10)
+
+
+def test_gamma_zero_and_zero_rows():
+    g = np.random.default_rng(4)
+    d = 64
+    C = g.standard_normal((6, d))
+    C[2] = 0.0
+    H = oracle.gram(g.standard_normal((200, d)))
+    L0 = sg.surrogate_table(C, H, gamma=0.0)
+    a2, rho, cos = sg.unit_stats(C)
+    for j, b in enumerate(sg.WIDTHS):
+        np.testing.assert_allclose(L0[:, j], a2 * sg.distortion(b, d, rho, cos), rtol=1e-12)
+    L = sg.surrogate_table(C, H, gamma=0.7)
+    assert np.all(L[2] == 0.0)
+    assert np.all(np.isfinite(L))
+
+
+def test_surrogate_is_monotone_in_width_for_gaussian_directions():
+    """For random directions the surrogate prices wider codes lower at every
+    step of the candidate set (the ordering Sec. C reports)."""
+    P = _unit_rows(32, 2048, seed=5)
+    H = np.eye(2048)
+    L = sg.surrogate_table(P, H, gamma=0.5)
+    assert np.all(np.diff(L, axis=1) < 0)
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_budget_is_the_largest_that_fits_the_storage(seed):
+    """App. B.5: B is the largest integer with B m + 16 n_out r <= E m n_out b_eq
+    (vectors of length m at b bits cost b m bits; the basis is fp16)."""
+    g = np.random.default_rng(seed)
+    E = int(g.integers(1, 200))
+    n_out = int(g.integers(8, 4096))
+    m = int(g.integers(8, 8192))
+    r = int(g.integers(1, n_out + 1))
+    b_eq = float(g.choice([1.5, 2.0, 2.5, 3.0, 4.0]))
+    B = sg.budget_equivalent(E, n_out, m, b_eq, r)
+    total = E * m * n_out * b_eq
+    assert B * m + 16 * n_out * r <= total + 1e-6
+    assert (B + 1) * m + 16 * n_out * r > total - 1e-6
+
+
+def test_budget_full_basis_form():
+    """At r = n_out the budget is the paper's floor(E n b_eq - 16 n^2 / m)."""
+    assert sg.budget_equivalent(128, 2048, 768, 2.0) == math.floor(128 * 2048 * 2 - 16 * 2048 ** 2 / 768)
+    assert sg.budget_equivalent(128, 2048, 768, 2.0) == 436906
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_ilp_over_surrogate_widths_matches_exhaustive(seed):
+    """The ILP with eviction and fp16 among the candidates (widths 0..16)."""
+    g = np.random.default_rng(100 + seed)
+    C = g.standard_normal((5, 64)) * np.exp(g.standard_normal((5, 1)))
+    H = oracle.gram(g.standard_normal((256, 64)))
+    L = sg.surrogate_table(C, H, gamma=0.7)
+    for B in (0, 3, 9, 14, 30, 80):
+        b1, v1 = oracle.allocate_dp(L, sg.WIDTHS, B)
+        b2, v2 = oracle.allocate_exhaustive(L, sg.WIDTHS, B)
+        assert v1 == v2 and np.array_equal(b1, b2), (B, b1, b2)
