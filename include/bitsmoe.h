@@ -22,6 +22,13 @@
  *   bitsmoe_pack_layout   word offsets of the packed units   (host)
  *   bitsmoe_pack          bit-plane codes + fp16 params      (device)
  *
+ * The paper's own allocation prices widths by a closed-form surrogate
+ * instead of a measured loss (App. B.3-B.5); the library offers it too:
+ *   bitsmoe_surrogate         L[u][j] = alpha^2 beta^gamma E(b_j),
+ *                             widths {0,1,2,3,4,6,8,16}       (device)
+ *   bitsmoe_surrogate_budget  equivalent-bit budget           (host)
+ * and bitsmoe_allocate accepts those widths (0 = evicted, 16 = fp16).
+ *
  * Conventions shared by every call:
  *  - Pointers named *_dev are device memory on the current HIP device;
  *    *_host are host memory.  The caller allocates and owns every input and
@@ -73,6 +80,10 @@ typedef enum {
 /* Largest candidate width and group sizes accepted by score and pack. */
 #define BITSMOE_MAX_BITS 8
 #define BITSMOE_MAX_NBITS 8
+/* Widths bitsmoe_allocate accepts: 0 (evicted) .. 16 (fp16). */
+#define BITSMOE_ALLOC_MAX_BITS 16
+/* Columns of the surrogate table: widths 0, 1, 2, 3, 4, 6, 8, 16. */
+#define BITSMOE_SURROGATE_NWIDTHS 8
 
 /*
  * Step 1a -- calibration Gram.
@@ -171,7 +182,8 @@ bitsmoe_status bitsmoe_score(const float* C_dev, int64_t units, int64_t d, const
  * exact; among all optima the lexicographically smallest width vector (in
  * unit order) is returned.
  *   L_host         [units][nbits] fp32 (finite)
- *   bits_host      [nbits] strictly ascending widths, each in 1..8
+ *   bits_host      [nbits] strictly ascending widths, each in
+ *                  0..BITSMOE_ALLOC_MAX_BITS (0 = the unit is evicted)
  *   bits_out_host  [units] output: the chosen width of each unit
  *   objective_out  sum of the chosen L in fp64 (may be NULL)
  * ERR_INFEASIBLE if budget_bits < bits[0] * units; ERR_NUMERIC for a
@@ -195,6 +207,44 @@ bitsmoe_status bitsmoe_allocate_ex(const float* L_host, int64_t units, const int
                                    int nbits, int64_t budget_bits, uint8_t* bits_out_host,
                                    double* objective_out, int64_t full_dp_limit,
                                    int64_t* core_units_out);
+
+/*
+ * The paper's surrogate cost table (App. B.3-B.4, Theorem
+ * app_spectrum_loss; candidate widths of Eq. piecewise_error_surrogate).
+ * For unit row c (length d): alpha^2 = ||c||^2, p = c / alpha,
+ * beta = p^T H p (the output-space importance of Eq. app_down_beta_approx),
+ * rho = ||p||_inf, cos theta = ||p||_1 / sqrt(d), and
+ *     L[u][j] = alpha^2 beta^gamma E(b_j),  b = 0, 1, 2, 3, 4, 6, 8, 16:
+ *     E(0) = 1 (eviction), E(1) = sin^2 theta (sign quantizer),
+ *     E(2|3|4) = kappa_host[0|1|2], E(6|8|16) = (d rho^2 / 3) 4^-b.
+ * A zero row costs 0 at every width.
+ *   C_dev       [units][d] fp32
+ *   H_dev       [d][d] fp32 symmetric positive semidefinite (upper triangle
+ *               of 256 x 256 blocks and the diagonal are read)
+ *   gamma       smoothing exponent in [0, 1] (the paper: 0.7 for
+ *               Qwen3-30B-A3B, 0.5 for Mixtral-8x7B, 0.2 for DeepSeek-V2-Lite)
+ *   kappa_host  [3] low-bit coefficients for widths 2, 3, 4 (the paper's
+ *               Table kappa_values: 0.14949200, 0.04067890, 0.01184786)
+ *   L_dev       [units][BITSMOE_SURROGATE_NWIDTHS] fp32 output
+ *   stats_dev   [units][4] fp32 output {alpha^2, beta, rho, cos theta}, or NULL
+ * Shape rules: d % 64 == 0, d < 2^22.  beta comes from the same fp16
+ * matrix-core form as bitsmoe_score (relative error ~1e-4).
+ */
+bitsmoe_status bitsmoe_surrogate(const float* C_dev, int64_t units, int64_t d, const float* H_dev,
+                                 double gamma, const double* kappa_host, float* L_dev,
+                                 float* stats_dev, void* stream);
+
+/*
+ * ILP budget of one projection under the paper's equivalent bit-width
+ * (App. B.5, Eqs. app_projection_bit_budget, app_projection_normalized_budget):
+ * E experts of n_out x m weights at b_eq bits per weight, minus the fp16
+ * shared basis (n_out x r), divided by the spectral-vector length m:
+ *     budget = floor((E n_out m b_eq - 16 n_out r) / m)
+ * (the paper's floor(E n b_eq - 16 n^2 / m) at r = n_out).
+ * ERR_INFEASIBLE if the basis alone exceeds the storage.
+ */
+bitsmoe_status bitsmoe_surrogate_budget(int64_t E, int64_t n_out, int64_t m, int64_t r,
+                                        double b_eq, int64_t* budget_out);
 
 /*
  * Packed layout (host): unit u occupies bits[u] * d/64 uint64 words starting

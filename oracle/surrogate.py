@@ -41,6 +41,7 @@ agree at r = n_out).
 from __future__ import annotations
 
 import math
+from fractions import Fraction
 
 import numpy as np
 
@@ -75,8 +76,8 @@ def beta(C, H):
     if C.ndim == 1:
         C = C[None, :]
     H = np.asarray(H, dtype=np.float64)
-    q = np.einsum("ij,jk,ik->i", C, H, C)
-    a2 = np.einsum("ij,ij->i", C, C)
+    q = np.sum((C @ H) * C, axis=1)               # c H c^T per row
+    a2 = np.sum(C * C, axis=1)
     return np.where(a2 > 0, q / np.where(a2 > 0, a2, 1.0), 0.0)
 
 
@@ -114,7 +115,8 @@ def budget_equivalent(E: int, n_out: int, m: int, b_eq: float, r: int | None = N
     16 n_out r) / m), in bits per vector element; r defaults to n_out (the
     paper's full basis)."""
     r = n_out if r is None else r
-    return int(math.floor(E * n_out * b_eq - 16.0 * n_out * r / m))
+    total = Fraction(E) * n_out * m * Fraction(b_eq)   # exact (b_eq is a binary fraction)
+    return math.floor((total - 16 * n_out * r) / m)
 
 
 # --- the quantizers the surrogate is derived from (App. B.3) ---------------

@@ -39,7 +39,10 @@ EXPORTS = [
     "bitsmoe_score", "bitsmoe_allocate", "bitsmoe_allocate_ex", "bitsmoe_pack_layout",
     "bitsmoe_pack", "bitsmoe_unpack", "bitsmoe_set_lapack", "bitsmoe_last_error",
     "bitsmoe_release", "bitsmoe_version", "bitsmoe_timing", "bitsmoe_kernel_time",
+    "bitsmoe_surrogate", "bitsmoe_surrogate_budget",
 ]
+# Candidate widths of the surrogate table, in column order.
+SURROGATE_WIDTHS = (0, 1, 2, 3, 4, 6, 8, 16)
 
 
 class BitsmoeError(RuntimeError):
@@ -84,6 +87,8 @@ def lib() -> ctypes.CDLL:
     L.bitsmoe_pack_layout.argtypes = [vp, i64, i64, vp]
     L.bitsmoe_pack.argtypes = [vp, i64, i64, i32, vp, vp, i64, vp, vp, vp]
     L.bitsmoe_unpack.argtypes = [vp, vp, vp, vp, i64, i64, i64, i32, vp, vp]
+    L.bitsmoe_surrogate.argtypes = [vp, i64, i64, vp, ctypes.c_double, vp, vp, vp, vp]
+    L.bitsmoe_surrogate_budget.argtypes = [i64, i64, i64, i64, ctypes.c_double, vp]
     L.bitsmoe_set_lapack.argtypes = [ctypes.c_char_p]
     L.bitsmoe_timing.argtypes = [i32]
     L.bitsmoe_kernel_time.argtypes = [ctypes.c_char_p, vp, vp]
@@ -208,6 +213,36 @@ def score(C, H, bits: Sequence[int], group: int, out=None):
     _check(lib().bitsmoe_score(_dev(C, "C"), units, d, _dev(H, "H"), bp, len(b), group,
                                _dev(out, "L"), _stream()), "score")
     return out
+
+
+def surrogate(C, H, gamma: float, kappa: Sequence[float], out=None, stats=None):
+    """The paper's surrogate costs alpha^2 beta^gamma E(b) for the widths
+    SURROGATE_WIDTHS -> fp32 [units][8]; ``stats`` (optional, [units][4]) gets
+    {alpha^2, beta, rho, cos theta}."""
+    torch = _torch()
+    units, d = C.shape
+    if C.dtype != torch.float32 or H.dtype != torch.float32:
+        raise TypeError("C and H must be float32")
+    if tuple(H.shape) != (d, d):
+        raise ValueError("H must be [d][d]")
+    k = np.ascontiguousarray(np.asarray(kappa, dtype=np.float64))
+    if k.shape != (3,):
+        raise ValueError("kappa holds the coefficients of widths 2, 3, 4")
+    if out is None:
+        out = torch.empty((units, len(SURROGATE_WIDTHS)), dtype=torch.float32, device=C.device)
+    sp = _dev(stats, "stats") if stats is not None else None
+    _check(lib().bitsmoe_surrogate(_dev(C, "C"), units, d, _dev(H, "H"), float(gamma),
+                                   k.ctypes.data_as(ctypes.c_void_p), _dev(out, "L"), sp,
+                                   _stream()), "surrogate")
+    return out
+
+
+def surrogate_budget(E: int, n_out: int, m: int, r: int, b_eq: float) -> int:
+    """Equivalent-bit ILP budget of one projection (host)."""
+    b = ctypes.c_int64(0)
+    _check(lib().bitsmoe_surrogate_budget(E, n_out, m, r, float(b_eq), ctypes.byref(b)),
+           "surrogate_budget")
+    return b.value
 
 
 def allocate(L, bits: Sequence[int], budget: int, full_dp_limit: int = -1,

@@ -166,8 +166,8 @@ extern "C" bitsmoe_status bitsmoe_allocate_ex(const float* L_host, int64_t units
   if (units <= 0) return fail(BITSMOE_ERR_ARG, "allocate: units must be positive");
   if (nbits < 1 || nbits > BITSMOE_MAX_NBITS) return fail(BITSMOE_ERR_ARG, "allocate: nbits outside 1..8");
   for (int j = 0; j < nbits; ++j) {
-    if (bits_host[j] < 1 || bits_host[j] > BITSMOE_MAX_BITS)
-      return fail(BITSMOE_ERR_ARG, "allocate: width outside 1..8");
+    if (bits_host[j] < 0 || bits_host[j] > BITSMOE_ALLOC_MAX_BITS)
+      return fail(BITSMOE_ERR_ARG, "allocate: width outside 0..16");
     if (j > 0 && bits_host[j] <= bits_host[j - 1])
       return fail(BITSMOE_ERR_ARG, "allocate: widths must be strictly ascending");
   }

@@ -26,6 +26,8 @@
 //   4. finalize      L = diagonal term + the unscaled tile partials, in a fixed
 //                    order.
 #include <algorithm>
+#include <cmath>
+#include <string>
 
 #include "bitsmoe.h"
 #include "common.hpp"
@@ -382,6 +384,254 @@ __global__ __launch_bounds__(256) void finalize_kernel(const float* __restrict__
   L[row] = diag[row] + ldexpf(s, -(2 * uexp[row / nb] + *hexp));
 }
 
+// Raw rows for the surrogate's activation-aware importance (the eviction
+// case of the loss table, delta = c): one wave per unit writes fp16(c 2^E)
+// in the K-tiled layout of the loss-table GEMM, the diagonal term
+// sum_k H_kk c_k^2, and the fp32 row statistics sum c^2, max |c|, sum |c|.
+__global__ __launch_bounds__(256) void rowprep_kernel(const float* __restrict__ C, int64_t units,
+                                                      int64_t d, const float* __restrict__ hdiag,
+                                                      uint16_t* __restrict__ D,
+                                                      float* __restrict__ diag,
+                                                      int* __restrict__ uexp,
+                                                      float* __restrict__ rstats) {
+  const int lane = threadIdx.x & 63;
+  const int64_t u = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
+  if (u >= units) return;  // whole wave exits together
+  const float* crow = C + u * d;
+  auto load8 = [&](int64_t k0, float (&c)[8]) {
+    const int64_t k = k0 + 8 * lane;
+    if (k < d) {
+      const float4 v0 = *reinterpret_cast<const float4*>(crow + k);
+      const float4 v1 = *reinterpret_cast<const float4*>(crow + k + 4);
+      c[0] = v0.x; c[1] = v0.y; c[2] = v0.z; c[3] = v0.w;
+      c[4] = v1.x; c[5] = v1.y; c[6] = v1.z; c[7] = v1.w;
+    } else {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) c[i] = 0.0f;
+    }
+  };
+  // pass 1: max |c|, sum c^2, sum |c|, four chunks' loads in flight
+  float amax = 0.0f, s2 = 0.0f, s1 = 0.0f;
+  auto acc8 = [&](const float (&c)[8]) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      amax = fmaxf(amax, fabsf(c[i]));
+      s2 = fmaf(c[i], c[i], s2);
+      s1 += fabsf(c[i]);
+    }
+  };
+  int64_t ka = 0;
+  for (; ka + 4 * 512 <= d; ka += 4 * 512) {
+    float c4[4][8];
+#pragma unroll
+    for (int x = 0; x < 4; ++x) load8(ka + 512 * x, c4[x]);
+#pragma unroll
+    for (int x = 0; x < 4; ++x) acc8(c4[x]);
+  }
+  for (; ka < d; ka += 512) {
+    float cc[8];
+    load8(ka, cc);
+    acc8(cc);
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) amax = fmaxf(amax, __shfl_xor(amax, o, 64));
+  s2 = wave_sum(s2);
+  s1 = wave_sum(s1);
+  // |c| < 2^e: the rows are stored as fp16(c 2^E), E = kF16Top - 1 - e
+  const int E = kF16Top - 1 - exponent_above(amax);
+  // pass 2: scaled fp16 rows and the diagonal term
+  float dacc = 0.0f;
+  float cur[8], nxt[8];
+  load8(0, cur);
+  for (int64_t k0 = 0; k0 < d; k0 += 512) {
+    if (k0 + 512 < d) load8(k0 + 512, nxt);
+    const int64_t k = k0 + 8 * lane;
+    if (k < d) {
+      const float4 h0 = *reinterpret_cast<const float4*>(hdiag + k);
+      const float4 h1 = *reinterpret_cast<const float4*>(hdiag + k + 4);
+      const float hd[8] = {h0.x, h0.y, h0.z, h0.w, h1.x, h1.y, h1.z, h1.w};
+      uint16_t out[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const float cs = ldexpf(cur[i], E);
+        out[i] = f32_to_f16_bits(cs);
+        dacc = fmaf(hd[i] * cs, cs, dacc);
+      }
+      uint4 pk;
+      pk.x = static_cast<uint32_t>(out[0]) | (static_cast<uint32_t>(out[1]) << 16);
+      pk.y = static_cast<uint32_t>(out[2]) | (static_cast<uint32_t>(out[3]) << 16);
+      pk.z = static_cast<uint32_t>(out[4]) | (static_cast<uint32_t>(out[5]) << 16);
+      pk.w = static_cast<uint32_t>(out[6]) | (static_cast<uint32_t>(out[7]) << 16);
+      *reinterpret_cast<uint4*>(D + gemm::tiled_offset(u, k, d, SBN)) = pk;
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) cur[i] = nxt[i];
+  }
+  dacc = ldexpf(wave_sum(dacc), -2 * E);
+  if (lane == 0) {
+    uexp[u] = E;
+    diag[u] = dacc;
+    rstats[3 * u + 0] = s2;
+    rstats[3 * u + 1] = amax;
+    rstats[3 * u + 2] = s1;
+  }
+}
+
+// Low-bit distortion coefficients of the surrogate (widths 2, 3, 4).
+struct Kappa {
+  double k[3];
+};
+
+// The surrogate table of one unit (App. B.3-B.4): alpha^2 = sum c^2,
+// beta = c H c^T / alpha^2, rho = max |c| / alpha, cos theta =
+// sum |c| / (alpha sqrt(d)); L[u][j] = alpha^2 beta^gamma E(width j) over the
+// widths 0, 1, 2, 3, 4, 6, 8, 16.  A zero row costs 0 everywhere.
+__global__ __launch_bounds__(256) void surrogate_finalize_kernel(
+    const float* __restrict__ diag, const float* __restrict__ part, int64_t units, int tiles_m,
+    const int* __restrict__ uexp, const int* __restrict__ hexp, const float* __restrict__ rstats,
+    int64_t d, double gamma, Kappa kap, float* __restrict__ L, float* __restrict__ stats_out) {
+  const int64_t u = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (u >= units) return;
+  const float* p = part + u * tiles_m;
+  float s = 0.0f;
+  for (int t = 0; t < tiles_m; ++t) s += p[t];
+  const double q = static_cast<double>(diag[u] + ldexpf(s, -(2 * uexp[u] + *hexp)));  // c H c^T
+  const double a2 = static_cast<double>(rstats[3 * u + 0]);
+  double beta = 0.0, rho = 0.0, cs = 0.0, w = 0.0;
+  if (a2 > 0.0) {
+    const double alpha = sqrt(a2);
+    beta = q / a2;
+    rho = static_cast<double>(rstats[3 * u + 1]) / alpha;
+    cs = static_cast<double>(rstats[3 * u + 2]) / (alpha * sqrt(static_cast<double>(d)));
+    w = a2 * pow(fmax(beta, 0.0), gamma);
+  }
+  const double eta = static_cast<double>(d) * rho * rho / 3.0;
+  float* row = L + u * BITSMOE_SURROGATE_NWIDTHS;
+  row[0] = static_cast<float>(w);                       // b = 0: eviction, E = 1
+  row[1] = static_cast<float>(w * (1.0 - cs) * (1.0 + cs));  // b = 1: sin^2 theta
+  row[2] = static_cast<float>(w * kap.k[0]);            // b = 2
+  row[3] = static_cast<float>(w * kap.k[1]);            // b = 3
+  row[4] = static_cast<float>(w * kap.k[2]);            // b = 4
+  row[5] = static_cast<float>(w * eta * ldexp(1.0, -12));  // b = 6: eta 4^-6
+  row[6] = static_cast<float>(w * eta * ldexp(1.0, -16));  // b = 8
+  row[7] = static_cast<float>(w * eta * ldexp(1.0, -32));  // b = 16
+  if (stats_out) {
+    stats_out[4 * u + 0] = static_cast<float>(a2);
+    stats_out[4 * u + 1] = static_cast<float>(beta);
+    stats_out[4 * u + 2] = static_cast<float>(rho);
+    stats_out[4 * u + 3] = static_cast<float>(cs);
+  }
+}
+
+// Scratch and launch shape of one loss-table evaluation over R rows of D
+// (error rows for the score, raw rows for the surrogate) against H.
+struct LossTable {
+  int64_t d, R, units;
+  int tiles_m;
+  int64_t tiles_n, d_pad, R_pad;
+  uint16_t* Hoff;
+  uint16_t* D;
+  float* hdiag;  // [d]
+  float* diag;   // [R]
+  int* uexp;     // [units]
+  float* hpart;  // [kAbsMaxBlocks]
+  int* hexp;     // [1]
+  float* rstats; // [3 units] (surrogate only)
+  float* part;   // [R][tiles_m]
+};
+
+bitsmoe_status loss_table_setup(int64_t d, int64_t R, int64_t units, bool row_stats, void* stream,
+                                const char* who, LossTable* t) {
+  t->d = d;
+  t->R = R;
+  t->units = units;
+  t->tiles_m = static_cast<int>((d + SBM - 1) / SBM);
+  t->tiles_n = (R + SBN - 1) / SBN;
+  if (gemm::paired_workgroups(t->tiles_m, t->tiles_n) > INT32_MAX || (R + 255) / 256 > INT32_MAX)
+    return fail(BITSMOE_ERR_SHAPE, std::string(who) + ": too many units");
+  // H_off and D are K-tiled with 256-row tiles, rows padded to whole tiles
+  t->d_pad = t->tiles_m * static_cast<int64_t>(SBM);
+  t->R_pad = t->tiles_n * static_cast<int64_t>(SBN);
+  bitsmoe_status st;
+  t->Hoff = static_cast<uint16_t*>(scratch(kScratchA, t->d_pad * d * 2, stream, &st));
+  if (!t->Hoff) return st;
+  // small tables: diag(H) [d], diagonal terms [R], unit exponents [units],
+  // partial maxima of |H_off| [kAbsMaxBlocks], the H_off exponent [1],
+  // row statistics [3 units]
+  const int64_t small_words = d + R + units + kAbsMaxBlocks + 1 + (row_stats ? 3 * units : 0);
+  float* small = static_cast<float*>(scratch(kScratchMisc, small_words * sizeof(float), stream, &st));
+  if (!small) return st;
+  t->hdiag = small;
+  t->diag = t->hdiag + d;
+  t->uexp = reinterpret_cast<int*>(t->diag + R);
+  t->hpart = reinterpret_cast<float*>(t->uexp + units);
+  t->hexp = reinterpret_cast<int*>(t->hpart + kAbsMaxBlocks);
+  t->rstats = row_stats ? reinterpret_cast<float*>(t->hexp + 1) : nullptr;
+  t->D = static_cast<uint16_t*>(scratch(kScratchD, t->R_pad * d * 2, stream, &st));
+  if (!t->D) return st;
+  t->part = static_cast<float*>(scratch(kScratchPart, R * t->tiles_m * sizeof(float), stream, &st));
+  if (!t->part) return st;
+  return BITSMOE_OK;
+}
+
+// H -> scaled fp16 H_off and diag(H).
+bitsmoe_status loss_table_hoff(const float* H_dev, const LossTable& t, hipStream_t s, const char* who) {
+  hipLaunchKernelGGL(habsmax_kernel, dim3(kAbsMaxBlocks), dim3(256), 0, s, H_dev, t.d, t.hpart);
+  BITSMOE_LAUNCH_CHECK(who);
+  const unsigned hb = static_cast<unsigned>(std::min<int64_t>((t.d_pad * t.d + 255) / 256, 16384));
+  hipLaunchKernelGGL(hoff_kernel, dim3(hb), dim3(256), 0, s, H_dev, t.d, t.d_pad, t.hpart, t.Hoff,
+                     t.hdiag, t.hexp);
+  BITSMOE_LAUNCH_CHECK(who);
+  return BITSMOE_OK;
+}
+
+// part[row][tm] = sum over the 256-wide tile tm of H rows of the
+// off-diagonal form of row `row` of D (paired upper-triangle schedule).
+bitsmoe_status loss_table_gemm(const LossTable& t, void* stream, const char* timer, const char* who) {
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  gemm::Problem p{};
+  static_assert(SKB == gemm::kTileK, "the K-tiled operands need the kernel's K step");
+  p.a.pass[0] = t.Hoff;
+  p.a.rows = t.d_pad;
+  p.a.kstep = static_cast<int64_t>(SBM) * gemm::kTileK;
+  p.a.rtile = static_cast<int64_t>(SBM) * t.d;
+  p.b.pass[0] = t.D;
+  p.b.rows = t.R_pad;
+  p.b.kstep = static_cast<int64_t>(SBN) * gemm::kTileK;
+  p.b.rtile = static_cast<int64_t>(SBN) * t.d;
+  p.passes = 1;
+  p.segs = 1;
+  p.kseg = t.d;
+  p.ktiles = t.d / BK;
+  p.splits = 1;
+  p.tiles_m = t.tiles_m;
+  p.tiles_n = static_cast<int>(t.tiles_n);
+  p.symmetric = 0;
+  // H symmetric: only the upper block triangle of H_off is visited, in the
+  // paired schedule, so that every workgroup does the same tiles_m + 1
+  // blocks of work
+  p.group_n = std::max(1, 32 / gemm::paired_unit_workgroups(t.tiles_m));  // ~one XCD's worth
+  RowDot epi{t.D, t.part, t.R, t.d, t.tiles_m};
+  dim3 grid(static_cast<unsigned>(gemm::paired_workgroups(t.tiles_m, t.tiles_n)), 1, 1);
+  {
+    KernelTimer kt(timer, stream);
+    hipLaunchKernelGGL((gemm::gemm_nt_kernel<SBM, SBN, SKB, SSTAGES, RowDot, true, false, true>),
+                       grid, dim3(gemm::kThreads), 0, s, p, epi);
+  }
+  BITSMOE_LAUNCH_CHECK(who);
+  return BITSMOE_OK;
+}
+
+bitsmoe_status check_rows_args(const float* C_dev, const float* H_dev, int64_t units, int64_t d,
+                               const char* who) {
+  if (!aligned16({C_dev, H_dev}))
+    return fail(BITSMOE_ERR_ARG, std::string(who) + ": device pointers must be 16-byte aligned");
+  if (units <= 0 || d <= 0) return fail(BITSMOE_ERR_ARG, std::string(who) + ": non-positive size");
+  if (d % 64 != 0) return fail(BITSMOE_ERR_SHAPE, std::string(who) + ": d must be a multiple of 64");
+  if (d >= (int64_t{1} << 22)) return fail(BITSMOE_ERR_SHAPE, std::string(who) + ": d must be below 2^22");
+  return BITSMOE_OK;
+}
+
 }  // namespace
 }  // namespace bitsmoe
 
@@ -391,9 +641,9 @@ extern "C" bitsmoe_status bitsmoe_score(const float* C_dev, int64_t units, int64
                                         const float* H_dev, const int* bits_host, int nbits,
                                         int group, float* L_dev, void* stream) {
   if (!C_dev || !H_dev || !bits_host || !L_dev) return fail(BITSMOE_ERR_ARG, "score: null pointer");
-  if (!aligned16({C_dev, H_dev, L_dev}))
-    return fail(BITSMOE_ERR_ARG, "score: device pointers must be 16-byte aligned");
-  if (units <= 0 || d <= 0) return fail(BITSMOE_ERR_ARG, "score: non-positive size");
+  if (!aligned16({L_dev})) return fail(BITSMOE_ERR_ARG, "score: device pointers must be 16-byte aligned");
+  bitsmoe_status st = check_rows_args(C_dev, H_dev, units, d, "score");
+  if (st != BITSMOE_OK) return st;
   if (nbits < 1 || nbits > BITSMOE_MAX_NBITS) return fail(BITSMOE_ERR_ARG, "score: nbits outside 1..8");
   QuantBits qb{};
   qb.nb = nbits;
@@ -406,40 +656,14 @@ extern "C" bitsmoe_status bitsmoe_score(const float* C_dev, int64_t units, int64
   }
   if (!(group == 32 || group == 64 || group == 128 || group == 256))
     return fail(BITSMOE_ERR_SHAPE, "score: group must be 32, 64, 128 or 256");
-  if (d % 64 != 0 || d % group != 0)
-    return fail(BITSMOE_ERR_SHAPE, "score: d must be a multiple of 64 and of the group");
-  if (d >= (int64_t{1} << 22)) return fail(BITSMOE_ERR_SHAPE, "score: d must be below 2^22");
+  if (d % group != 0) return fail(BITSMOE_ERR_SHAPE, "score: d must be a multiple of the group");
   hipStream_t s = static_cast<hipStream_t>(stream);
   const int64_t R = units * nbits;
-  const int tiles_m = static_cast<int>((d + SBM - 1) / SBM);
-  const int64_t tiles_n = (R + SBN - 1) / SBN;
-  if (tiles_n * tiles_m > INT32_MAX) return fail(BITSMOE_ERR_SHAPE, "score: too many units");
-  bitsmoe_status st;
-  // H_off and D are K-tiled with 256-row tiles, rows padded to whole tiles
-  const int64_t d_pad = tiles_m * static_cast<int64_t>(SBM);
-  const int64_t R_pad = tiles_n * static_cast<int64_t>(SBN);
-  uint16_t* Hoff = static_cast<uint16_t*>(scratch(kScratchA, d_pad * d * 2, stream, &st));
-  if (!Hoff) return st;
-  // small tables: diag(H) [d], diagonal terms [R], unit exponents [units],
-  // partial maxima of |H_off| [kAbsMaxBlocks], the H_off exponent [1]
-  const int64_t small_words = d + R + units + kAbsMaxBlocks + 1;
-  float* small = static_cast<float*>(scratch(kScratchMisc, small_words * sizeof(float), stream, &st));
-  if (!small) return st;
-  float* hdiag = small;
-  float* diag = hdiag + d;
-  int* uexp = reinterpret_cast<int*>(diag + R);
-  float* hpart = reinterpret_cast<float*>(uexp + units);
-  int* hexp = reinterpret_cast<int*>(hpart + kAbsMaxBlocks);
-  uint16_t* D = static_cast<uint16_t*>(scratch(kScratchD, R_pad * d * 2, stream, &st));
-  if (!D) return st;
-  float* part = static_cast<float*>(scratch(kScratchPart, R * tiles_m * sizeof(float), stream, &st));
-  if (!part) return st;
-
-  hipLaunchKernelGGL(habsmax_kernel, dim3(kAbsMaxBlocks), dim3(256), 0, s, H_dev, d, hpart);
-  BITSMOE_LAUNCH_CHECK("score: habsmax launch");
-  const unsigned hb = static_cast<unsigned>(std::min<int64_t>((d_pad * d + 255) / 256, 16384));
-  hipLaunchKernelGGL(hoff_kernel, dim3(hb), dim3(256), 0, s, H_dev, d, d_pad, hpart, Hoff, hdiag, hexp);
-  BITSMOE_LAUNCH_CHECK("score: hoff launch");
+  LossTable t;
+  st = loss_table_setup(d, R, units, false, stream, "score", &t);
+  if (st != BITSMOE_OK) return st;
+  st = loss_table_hoff(H_dev, t, s, "score: H_off launch");
+  if (st != BITSMOE_OK) return st;
   const unsigned db = static_cast<unsigned>((units + 3) / 4);
   {
   KernelTimer dgen_timer("score_dgen", stream);
@@ -447,7 +671,7 @@ extern "C" bitsmoe_status bitsmoe_score(const float* C_dev, int64_t units, int64
 #define BITSMOE_DGEN(NB)                                                                       \
   case NB:                                                                                     \
     hipLaunchKernelGGL(dgen_kernel<NB>, dim3(db), dim3(256), 0, s, C_dev, units, d, group, qb, \
-                       hdiag, D, diag, uexp);                                                  \
+                       t.hdiag, t.D, t.diag, t.uexp);                                          \
     break;
     BITSMOE_DGEN(1) BITSMOE_DGEN(2) BITSMOE_DGEN(3) BITSMOE_DGEN(4)
     BITSMOE_DGEN(5) BITSMOE_DGEN(6) BITSMOE_DGEN(7) BITSMOE_DGEN(8)
@@ -455,41 +679,63 @@ extern "C" bitsmoe_status bitsmoe_score(const float* C_dev, int64_t units, int64
   }
   }
   BITSMOE_LAUNCH_CHECK("score: dgen launch");
-
-  gemm::Problem p{};
-  static_assert(SKB == gemm::kTileK, "the K-tiled operands need the kernel's K step");
-  p.a.pass[0] = Hoff;
-  p.a.rows = d_pad;
-  p.a.kstep = static_cast<int64_t>(SBM) * gemm::kTileK;
-  p.a.rtile = static_cast<int64_t>(SBM) * d;
-  p.b.pass[0] = D;
-  p.b.rows = R_pad;
-  p.b.kstep = static_cast<int64_t>(SBN) * gemm::kTileK;
-  p.b.rtile = static_cast<int64_t>(SBN) * d;
-  p.passes = 1;
-  p.segs = 1;
-  p.kseg = d;
-  p.ktiles = d / BK;
-  p.splits = 1;
-  p.tiles_m = tiles_m;
-  p.tiles_n = static_cast<int>(tiles_n);
-  p.symmetric = 0;
-  // H symmetric: only the upper block triangle of H_off is visited, in the
-  // paired schedule, so that every workgroup does the same tiles_m + 1
-  // blocks of work
-  p.group_n = std::max(1, 32 / gemm::paired_unit_workgroups(tiles_m));  // ~one XCD's worth
-  RowDot epi{D, part, R, d, tiles_m};
-  const int64_t wgs = gemm::paired_workgroups(tiles_m, tiles_n);
-  if (wgs > INT32_MAX) return fail(BITSMOE_ERR_SHAPE, "score: too many units");
-  dim3 grid(static_cast<unsigned>(wgs), 1, 1);
-  {
-    KernelTimer timer("score_gemm", stream);
-    hipLaunchKernelGGL((gemm::gemm_nt_kernel<SBM, SBN, SKB, SSTAGES, RowDot, true, false, true>),
-                       grid, dim3(gemm::kThreads), 0, s, p, epi);
-  }
-  BITSMOE_LAUNCH_CHECK("score: gemm launch");
+  st = loss_table_gemm(t, stream, "score_gemm", "score: gemm launch");
+  if (st != BITSMOE_OK) return st;
   hipLaunchKernelGGL(finalize_kernel, dim3(static_cast<unsigned>((R + 255) / 256)), dim3(256), 0, s,
-                     diag, part, R, tiles_m, nbits, uexp, hexp, L_dev);
+                     t.diag, t.part, R, t.tiles_m, nbits, t.uexp, t.hexp, L_dev);
   BITSMOE_LAUNCH_CHECK("score: finalize launch");
+  return ok();
+}
+
+extern "C" bitsmoe_status bitsmoe_surrogate(const float* C_dev, int64_t units, int64_t d,
+                                            const float* H_dev, double gamma,
+                                            const double* kappa_host, float* L_dev,
+                                            float* stats_dev, void* stream) {
+  if (!C_dev || !H_dev || !kappa_host || !L_dev) return fail(BITSMOE_ERR_ARG, "surrogate: null pointer");
+  if (!aligned16({L_dev, stats_dev}))
+    return fail(BITSMOE_ERR_ARG, "surrogate: device pointers must be 16-byte aligned");
+  bitsmoe_status st = check_rows_args(C_dev, H_dev, units, d, "surrogate");
+  if (st != BITSMOE_OK) return st;
+  if (!(gamma >= 0.0 && gamma <= 1.0)) return fail(BITSMOE_ERR_ARG, "surrogate: gamma outside [0, 1]");
+  Kappa kap{};
+  for (int j = 0; j < 3; ++j) {
+    if (!(kappa_host[j] >= 0.0) || !std::isfinite(kappa_host[j]))
+      return fail(BITSMOE_ERR_ARG, "surrogate: kappa must be finite and non-negative");
+    kap.k[j] = kappa_host[j];
+  }
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  LossTable t;
+  st = loss_table_setup(d, units, units, true, stream, "surrogate", &t);
+  if (st != BITSMOE_OK) return st;
+  st = loss_table_hoff(H_dev, t, s, "surrogate: H_off launch");
+  if (st != BITSMOE_OK) return st;
+  {
+    KernelTimer rt("surrogate_rows", stream);
+    hipLaunchKernelGGL(rowprep_kernel, dim3(static_cast<unsigned>((units + 3) / 4)), dim3(256), 0, s,
+                       C_dev, units, d, t.hdiag, t.D, t.diag, t.uexp, t.rstats);
+  }
+  BITSMOE_LAUNCH_CHECK("surrogate: row launch");
+  st = loss_table_gemm(t, stream, "surrogate_gemm", "surrogate: gemm launch");
+  if (st != BITSMOE_OK) return st;
+  hipLaunchKernelGGL(surrogate_finalize_kernel, dim3(static_cast<unsigned>((units + 255) / 256)),
+                     dim3(256), 0, s, t.diag, t.part, units, t.tiles_m, t.uexp, t.hexp, t.rstats, d,
+                     gamma, kap, L_dev, stats_dev);
+  BITSMOE_LAUNCH_CHECK("surrogate: finalize launch");
+  return ok();
+}
+
+extern "C" bitsmoe_status bitsmoe_surrogate_budget(int64_t E, int64_t n_out, int64_t m, int64_t r,
+                                                   double b_eq, int64_t* budget_out) {
+  if (!budget_out) return fail(BITSMOE_ERR_ARG, "surrogate_budget: null pointer");
+  if (E <= 0 || n_out <= 0 || m <= 0 || r <= 0 || r > n_out)
+    return fail(BITSMOE_ERR_ARG, "surrogate_budget: sizes must be positive with r <= n_out");
+  if (!(b_eq >= 0.0) || !std::isfinite(b_eq)) return fail(BITSMOE_ERR_ARG, "surrogate_budget: b_eq");
+  // storage of the projection at b_eq bits per weight minus the fp16 basis,
+  // divided by the length of a spectral vector
+  const long double total = static_cast<long double>(E) * n_out * m * b_eq;
+  const long double basis = 16.0L * n_out * r;
+  const long double B = floorl((total - basis) / m);
+  if (B < 0.0L) return fail(BITSMOE_ERR_INFEASIBLE, "surrogate_budget: the fp16 basis alone exceeds the budget");
+  *budget_out = static_cast<int64_t>(B);
   return ok();
 }

@@ -114,8 +114,48 @@ def test_allocate_errors(lib):
         pkg.allocate(L, [2, 1], 6)
     assert e.value.code == "ERR_ARG"
     with pytest.raises(pkg.BitsmoeError) as e:
-        pkg.allocate(L, [1, 9], 6)
+        pkg.allocate(L, [1, 17], 6)
     assert e.value.code == "ERR_ARG"
+    with pytest.raises(pkg.BitsmoeError) as e:
+        pkg.allocate(L, [-1, 2], 6)
+    assert e.value.code == "ERR_ARG"
+
+
+@pytest.mark.parametrize("seed,force_core", [(0, False), (1, True), (2, True)])
+def test_allocate_surrogate_widths_match_oracle(lib, seed, force_core):
+    """Widths 0 (eviction) .. 16 (fp16), as the surrogate mode uses them."""
+    from oracle import surrogate as sg
+    g = np.random.default_rng(50 + seed)
+    U = 300
+    C = (g.standard_normal((U, 64)) * np.exp(g.standard_normal((U, 1)))).astype(np.float32)
+    H = oracle.gram(g.standard_normal((256, 64)))
+    L = sg.surrogate_table(C.astype(np.float64), H, gamma=0.7).astype(np.float32)
+    for budget in (0, 150, 2 * U, 5 * U):
+        ref, _ = oracle.allocate_dp(L, sg.WIDTHS, budget)
+        got, _ = pkg.allocate(L, sg.WIDTHS, budget, full_dp_limit=0 if force_core else -1)
+        assert np.array_equal(got, ref), budget
+        assert int(got.astype(np.int64).sum()) <= budget
+
+
+def test_surrogate_budget_matches_oracle(lib):
+    from oracle import surrogate as sg
+    g = np.random.default_rng(8)
+    for _ in range(50):
+        E = int(g.integers(1, 300))
+        n_out = int(g.integers(8, 8192))
+        m = int(g.integers(8, 16384))
+        r = int(g.integers(1, n_out + 1))
+        b_eq = float(g.choice([1.5, 2.0, 2.5, 3.0, 4.0]))
+        ref = sg.budget_equivalent(E, n_out, m, b_eq, r)
+        if ref < 0:
+            with pytest.raises(pkg.BitsmoeError) as e:
+                pkg.surrogate_budget(E, n_out, m, r, b_eq)
+            assert e.value.code == "ERR_INFEASIBLE"
+        else:
+            assert pkg.surrogate_budget(E, n_out, m, r, b_eq) == ref
+    assert pkg.surrogate_budget(128, 2048, 768, 2048, 2.0) == 436906
+    with pytest.raises(pkg.BitsmoeError):
+        pkg.surrogate_budget(4, 64, 64, 65, 2.0)
 
 
 def test_pack_layout_matches_oracle(lib):
@@ -159,6 +199,13 @@ def test_device_entry_points_validate_before_launch(lib):
     assert "r > d_out" in pkg.last_error()
     assert lib.bitsmoe_shared_basis(null, 64, 4, fake, null, null, s) == 1
     assert lib.bitsmoe_set_lapack(b"/nonexistent/liblapack.so") == 8
+    kap = (ctypes.c_double * 3)(0.149492, 0.0406789, 0.01184786)
+    badk = (ctypes.c_double * 3)(0.149492, -1.0, 0.01184786)
+    assert lib.bitsmoe_surrogate(null, 10, 256, fake, 0.7, kap, fake, null, s) == 1
+    assert lib.bitsmoe_surrogate(fake, 10, 200, fake, 0.7, kap, fake, null, s) == 2
+    assert lib.bitsmoe_surrogate(fake, 0, 256, fake, 0.7, kap, fake, null, s) == 1
+    assert lib.bitsmoe_surrogate(fake, 10, 256, fake, 1.5, kap, fake, null, s) == 1
+    assert lib.bitsmoe_surrogate(fake, 10, 256, fake, 0.7, badk, fake, null, s) == 1
     # misaligned device pointers are refused before any launch
     odd = ctypes.c_void_p(0x1008)
     assert lib.bitsmoe_gram(odd, 1, 64, 64, fake, s) == 1
@@ -169,3 +216,5 @@ def test_device_entry_points_validate_before_launch(lib):
     assert lib.bitsmoe_pack(fake, 10, 256, 64, fake, odd, 10, fake, fake, s) == 1
     assert lib.bitsmoe_unpack(fake, fake, fake, fake, 10, 10, 256, 64, odd, s) == 1
     assert lib.bitsmoe_shared_basis(odd, 64, 4, fake, null, null, s) == 1
+    assert lib.bitsmoe_surrogate(fake, 10, 256, fake, 0.7, kap, odd, null, s) == 1
+    assert lib.bitsmoe_surrogate(fake, 10, 256, fake, 0.7, kap, fake, odd, s) == 1
