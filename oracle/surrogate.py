@@ -67,7 +67,9 @@ def unit_stats(C):
     safe = np.where(alpha > 0, alpha, 1.0)
     rho = np.where(alpha > 0, np.max(np.abs(C), axis=1) / safe, 0.0)
     cos = np.where(alpha > 0, np.sum(np.abs(C), axis=1) / (safe * math.sqrt(d)), 0.0)
-    return a2, rho, cos
+    # ||p||_1 <= sqrt(d) ||p||_2 (Cauchy-Schwarz): cos theta <= 1, attained by
+    # rows of equal magnitudes, where rounding may land just above 1
+    return a2, rho, np.minimum(cos, 1.0)
 
 
 def beta(C, H):

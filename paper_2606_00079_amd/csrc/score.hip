@@ -502,7 +502,8 @@ __global__ __launch_bounds__(256) void surrogate_finalize_kernel(
     const double alpha = sqrt(a2);
     beta = q / a2;
     rho = static_cast<double>(rstats[3 * u + 1]) / alpha;
-    cs = static_cast<double>(rstats[3 * u + 2]) / (alpha * sqrt(static_cast<double>(d)));
+    // ||p||_1 <= sqrt(d) (Cauchy-Schwarz); rows of equal magnitudes attain it
+    cs = fmin(static_cast<double>(rstats[3 * u + 2]) / (alpha * sqrt(static_cast<double>(d))), 1.0);
     w = a2 * pow(fmax(beta, 0.0), gamma);
   }
   const double eta = static_cast<double>(d) * rho * rho / 3.0;

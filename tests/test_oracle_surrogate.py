@@ -112,6 +112,19 @@ def test_eviction_cost_is_the_exact_activation_loss():
     np.testing.assert_allclose(L[:, sg.WIDTHS.index(0)], brute, rtol=1e-10)
 
 
+def test_equal_magnitude_row_has_zero_sign_distortion():
+    """A row whose entries share one magnitude is reproduced exactly by the
+    sign quantizer: cos theta = 1 and sin^2 theta = 0, not a rounding residue."""
+    for d in (64, 768, 2048):
+        p = np.full(d, 0.125)
+        p[::3] *= -1
+        a2, rho, cos = sg.unit_stats(p)
+        assert cos[0] <= 1.0
+        e = sg.distortion(1, d, rho, cos)
+        assert 0.0 <= e[0] < 1e-12
+        assert np.sum((p / np.sqrt(a2[0]) - sg.quant_sign(p / np.sqrt(a2[0]))) ** 2) < 1e-24
+
+
 def test_gamma_zero_and_zero_rows():
     g = np.random.default_rng(4)
     d = 64
