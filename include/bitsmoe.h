@@ -249,7 +249,8 @@ bitsmoe_status bitsmoe_surrogate_budget(int64_t E, int64_t n_out, int64_t m, int
 /*
  * Packed layout (host): unit u occupies bits[u] * d/64 uint64 words starting
  * at word_offsets_host[u]; word_offsets_host has units + 1 entries and the
- * last one is the total.  d % 64 == 0; each width in 1..8.
+ * last one is the total.  d % 64 == 0; each width is 1..8, or one of the
+ * surrogate's extra candidates 0 (evicted, no words) and 16 (fp16 row).
  */
 bitsmoe_status bitsmoe_pack_layout(const uint8_t* bits_host, int64_t units, int64_t d,
                                    int64_t* word_offsets_host);
@@ -261,13 +262,15 @@ bitsmoe_status bitsmoe_pack_layout(const uint8_t* bits_host, int64_t units, int6
  * (0 = least significant) of unit u is the word range
  * [off[u] + t*d/64, off[u] + (t+1)*d/64), and bit j of word w of a plane is
  * bit t of the code of entry 64*w + j.  params_dev[u][g] holds the fp16 bit
- * patterns {scale, min} of group g.
+ * patterns {scale, min} of group g.  The surrogate's extra widths: 16 stores
+ * the row in fp16 (round to nearest even), entry k in bits 16 (k % 4) of word
+ * k / 4 of the unit; 0 (eviction) stores no words.  Both get zero params.
  *   C_dev             [units][d] fp32
  *   bits_dev          [units] widths (device)
  *   word_offsets_dev  [units + 1] from bitsmoe_pack_layout (device)
  *   codes_dev         [total_words] uint64 output
  *   params_dev        [units][d/group][2] uint16 output
- * A unit whose width is outside 1..8, or whose offsets do not match its
+ * A unit whose width is not 0, 1..8 or 16, or whose offsets do not match its
  * width or exceed total_words, is left unwritten.
  */
 bitsmoe_status bitsmoe_pack(const float* C_dev, int64_t units, int64_t d, int group,
@@ -278,7 +281,8 @@ bitsmoe_status bitsmoe_pack(const float* C_dev, int64_t units, int64_t d, int gr
 /*
  * Inverse of bitsmoe_pack: x = m + q * s per entry, fp32 [units][d].  This
  * is the dequantized factor a decoder would use; it equals the fake-quant
- * value of bitsmoe_score's rule.
+ * value of bitsmoe_score's rule (the stored fp16 row at width 16, zeros at
+ * width 0).
  */
 bitsmoe_status bitsmoe_unpack(const uint64_t* codes_dev, const uint16_t* params_dev,
                               const uint8_t* bits_dev, const int64_t* word_offsets_dev,

@@ -133,6 +133,12 @@ def bit_planes(q: np.ndarray, b: int) -> np.ndarray:
 def pack(C, bits_u, G: int):
     """Pack every unit at its assigned width.
 
+    Widths 1..8 are codes of the group rule as bit planes.  The surrogate's
+    two extra widths (Sec. 3.3, candidate set {16, 8, 6, 4, 3, 2, 1, 0}):
+    16 stores the row itself in fp16 (round to nearest even), entry 4 w + i
+    in bits 16 i .. 16 i + 15 of word w; 0 (eviction) stores nothing.  Their
+    group parameters are zero.
+
     Returns (codes uint64 [total words], params uint16 [units][d/G][2] holding
     the fp16 bit patterns of (s16, m16), offsets int64 [units+1]).
     """
@@ -144,6 +150,14 @@ def pack(C, bits_u, G: int):
     params = np.zeros((units, d // G, 2), dtype=np.uint16)
     for b in np.unique(bits_u):
         us = np.nonzero(bits_u == b)[0]
+        if b == 0:
+            continue
+        if b == 16:
+            for u in us:
+                codes[off[u]:off[u + 1]] = C32[u].astype(np.float16).view(np.uint64)
+            continue
+        if not 1 <= b <= 8:
+            raise ValueError("pack: widths are 0, 1..8 or 16")
         q, s16, m16 = quant_group(C32[us], int(b), G)
         params[us, :, 0] = s16.view(np.uint16)
         params[us, :, 1] = m16.view(np.uint16)
@@ -154,7 +168,8 @@ def pack(C, bits_u, G: int):
 
 
 def unpack(codes, params, bits_u, d: int, G: int) -> np.ndarray:
-    """Dequantize packed units back to rows (fp64): m16 + q * s16."""
+    """Dequantize packed units back to rows (fp64): m16 + q * s16 (widths
+    1..8), the stored fp16 row (16), zeros (0)."""
     codes = np.asarray(codes, dtype=np.uint64)
     bits_u = np.asarray(bits_u, dtype=np.int64)
     off = pack_layout(bits_u, d)
@@ -165,6 +180,12 @@ def unpack(codes, params, bits_u, d: int, G: int) -> np.ndarray:
     m16 = params[:, :, 1].view(np.float16).astype(np.float64)
     for u in range(units):
         b = int(bits_u[u])
+        if b == 0:
+            out[u] = 0.0
+            continue
+        if b == 16:
+            out[u] = codes[off[u]:off[u + 1]].view(np.float16).astype(np.float64)
+            continue
         words = codes[off[u]:off[u + 1]].reshape(b, d // 64)
         q = np.zeros(d, dtype=np.uint64)
         for t in range(b):

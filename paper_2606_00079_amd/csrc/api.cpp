@@ -358,8 +358,8 @@ bitsmoe_status bitsmoe_pack_layout(const uint8_t* bits_host, int64_t units, int6
   word_offsets_host[0] = 0;
   for (int64_t u = 0; u < units; ++u) {
     const int b = bits_host[u];
-    if (b < 1 || b > BITSMOE_MAX_BITS)
-      return fail(BITSMOE_ERR_ARG, "pack_layout: width outside 1..8 at unit " + std::to_string(u));
+    if (!(b == 0 || b == 16 || (b >= 1 && b <= BITSMOE_MAX_BITS)))
+      return fail(BITSMOE_ERR_ARG, "pack_layout: width other than 0, 1..8, 16 at unit " + std::to_string(u));
     off += b * wpp;
     word_offsets_host[u + 1] = off;
   }

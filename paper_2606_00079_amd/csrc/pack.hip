@@ -20,6 +20,11 @@
 namespace bitsmoe {
 namespace {
 
+// Widths a unit may be packed at: codes of 1..8 bits, 16 (fp16 row), 0 (evicted).
+__host__ __device__ __forceinline__ bool width_ok(int b) {
+  return b == 0 || b == 16 || (b >= 1 && b <= BITSMOE_MAX_BITS);
+}
+
 template <int G>
 __global__ __launch_bounds__(256) void pack_kernel(const float* __restrict__ C, int64_t units,
                                                    int64_t d, const uint8_t* __restrict__ bits,
@@ -34,12 +39,28 @@ __global__ __launch_bounds__(256) void pack_kernel(const float* __restrict__ C, 
   const int b = bits[u];
   const int64_t nw = d / 64;
   const int64_t o0 = off[u], o1 = off[u + 1];
-  if (b < 1 || b > BITSMOE_MAX_BITS || o1 - o0 != b * nw || o0 < 0 || o1 > total_words) return;
+  if (!width_ok(b) || o1 - o0 != b * nw || o0 < 0 || o1 > total_words) return;
+  const float* crow = C + u * d;
+  uint32_t* uparams = params + u * (d / G);
+  if (b == 0 || b == 16) {
+    // eviction stores nothing; width 16 stores the row in fp16, entry k at
+    // bits 16 (k % 4) of word k / 4; neither has group parameters
+    for (int64_t g = lane; g < d / G; g += 64) uparams[g] = 0u;
+    if (b == 16) {
+      uint2* w = reinterpret_cast<uint2*>(codes + o0);  // 8-byte aligned words
+      for (int64_t k = 4 * lane; k < d; k += 256) {
+        const float4 v = *reinterpret_cast<const float4*>(crow + k);
+        uint2 h;
+        h.x = static_cast<uint32_t>(f32_to_f16_bits(v.x)) | (static_cast<uint32_t>(f32_to_f16_bits(v.y)) << 16);
+        h.y = static_cast<uint32_t>(f32_to_f16_bits(v.z)) | (static_cast<uint32_t>(f32_to_f16_bits(v.w)) << 16);
+        w[k / 4] = h;
+      }
+    }
+    return;
+  }
   const double qmax = static_cast<double>((1 << b) - 1);
   const float qmaxf = static_cast<float>((1 << b) - 1);
-  const float* crow = C + u * d;
   uint8_t* ubytes = reinterpret_cast<uint8_t*>(codes + o0);  // plane t at byte t * d / 8
-  uint32_t* uparams = params + u * (d / G);
 
   // lane's 8 entries of the chunk at k0 (zeros past the end)
   auto load8 = [&](int64_t k0, float (&c)[8]) {
@@ -126,7 +147,12 @@ __global__ __launch_bounds__(64) void unpack_kernel(const uint64_t* __restrict__
   const int b = bits[u];
   const int64_t nw = d / 64;
   const int64_t o0 = off[u], o1 = off[u + 1];
-  if (b < 1 || b > BITSMOE_MAX_BITS || o1 - o0 != b * nw || o0 < 0 || o1 > total_words) return;
+  if (!width_ok(b) || o1 - o0 != b * nw || o0 < 0 || o1 > total_words) return;
+  if (b == 0 || b == 16) {
+    const uint16_t* h = reinterpret_cast<const uint16_t*>(codes + o0);
+    for (int64_t k = lane; k < d; k += 64) out[u * d + k] = b == 0 ? 0.0f : f16_bits_to_f32(h[k]);
+    return;
+  }
   const int64_t ng = d / G;
   for (int64_t w = 0; w < nw; ++w) {
     uint32_t q = 0;

@@ -11,6 +11,10 @@ A projection runs three device segments separated by the two host steps:
 Device segments are timed with HIP events on the current stream; the host
 steps with a wall clock.  Gate and up projections of a layer read the same
 calibration input, so their H is computed once.
+
+``surrogate_allocation`` runs the paper's own allocation on the same spectral
+units: the closed-form surrogate costs on the device, then the ILP over the
+widths {0, 1, 2, 3, 4, 6, 8, 16} under the equivalent-bit budget.
 """
 from __future__ import annotations
 
@@ -20,7 +24,8 @@ from typing import Dict, List, Optional, Sequence
 
 import numpy as np
 
-from . import (allocate, gram, gram_experts, pack, pack_layout, project, score, shared_basis)
+from . import (SURROGATE_WIDTHS, allocate, gram, gram_experts, pack, pack_layout, project, score,
+               shared_basis, surrogate, surrogate_budget)
 
 
 @dataclasses.dataclass
@@ -116,3 +121,47 @@ def quantize_layer(projs: List[dict]) -> List[ProjectionResult]:
         cache[key] = res.H
         out.append(res)
     return out
+
+
+@dataclasses.dataclass
+class SurrogateResult:
+    L: object            # device [units][8] surrogate costs
+    stats: object        # device [units][4] {alpha^2, beta, rho, cos theta}
+    bits_u: np.ndarray   # chosen widths (0 = evicted, 16 = fp16)
+    budget: int
+    objective: float
+    offsets: np.ndarray
+    codes: object
+    params: object
+    times: Dict[str, float]
+
+
+def surrogate_allocation(C, H, gamma: float, kappa: Sequence[float], E: int, n_out: int, r: int,
+                         b_eq: float, group: int) -> SurrogateResult:
+    """Surrogate costs of the units C (rows of U^T W_e), the ILP over the
+    widths {0..16} under the equivalent-bit budget, and the packed units."""
+    import torch
+    units, d = C.shape
+    dev = C.device
+    L = torch.empty((units, len(SURROGATE_WIDTHS)), dtype=torch.float32, device=dev)
+    st = torch.empty((units, 4), dtype=torch.float32, device=dev)
+    budget = surrogate_budget(E, n_out, d, r, b_eq)
+    seg = _Seg()
+    with seg:
+        surrogate(C, H, gamma, kappa, out=L, stats=st)
+    t0 = time.perf_counter()
+    Lh = L.cpu().numpy()
+    bits_u, obj = allocate(Lh, SURROGATE_WIDTHS, budget)
+    off = pack_layout(bits_u, d)
+    times = {"gpu_cost_ms": seg.ms()}
+    bits_d = torch.from_numpy(bits_u).to(dev)
+    off_d = torch.from_numpy(off).to(dev)
+    times["host_ilp_ms"] = (time.perf_counter() - t0) * 1e3
+    codes = torch.empty((max(int(off[-1]), 1),), dtype=torch.int64, device=dev)
+    params = torch.empty((units, d // group, 2), dtype=torch.int16, device=dev)
+    sp = _Seg()
+    with sp:
+        pack(C, bits_d, off_d, group, int(off[-1]), codes=codes, params=params)
+    times["gpu_pack_ms"] = sp.ms()
+    times["gpu_ms"] = times["gpu_cost_ms"] + times["gpu_pack_ms"]
+    return SurrogateResult(L, st, bits_u, budget, obj, off, codes, params, times)

@@ -167,9 +167,11 @@ def test_pack_layout_matches_oracle(lib):
         pkg.pack_layout(bits_u, 100)
     assert e.value.code == "ERR_SHAPE"
     bad = bits_u.copy()
-    bad[5] = 0
+    bad[5] = 9
     with pytest.raises(pkg.BitsmoeError):
         pkg.pack_layout(bad, 64)
+    surr = g.choice([0, 1, 2, 3, 4, 6, 8, 16], size=77).astype(np.uint8)
+    assert np.array_equal(pkg.pack_layout(surr, 128), oracle.pack_layout(surr, 128))
 
 
 # ------------------------------------------------- device calls, rejected early

@@ -273,6 +273,29 @@ def test_pack_bit_exact(group, d, units):
     assert np.array_equal(xh.astype(np.float64), ref)
 
 
+@pytest.mark.parametrize("group,d", [(128, 2048), (64, 192)])
+def test_pack_surrogate_widths_bit_exact(group, d):
+    """Widths of the surrogate's candidate set, eviction (0) and fp16 rows
+    (16) included, packed and unpacked bit for bit as the oracle does."""
+    say("pack surrogate widths", group, d)
+    units = 211
+    g = np.random.default_rng(group + d + 1)
+    C = synth.random_rows(units, d, seed=units + d, scale=0.04, heavy=True)
+    C[0] = 0.0
+    bits_u = g.choice([0, 1, 2, 3, 4, 6, 8, 16], size=units).astype(np.uint8)
+    bits_u[:3] = [16, 0, 16]
+    off = bm.pack_layout(bits_u, d)
+    bd = torch.from_numpy(bits_u).to(DEV)
+    od = torch.from_numpy(off).to(DEV)
+    codes, params = bm.pack(dev(C, "f32"), bd, od, group, int(off[-1]))
+    rc, rp, roff = oracle.pack(C, bits_u, group)
+    assert np.array_equal(off, roff)
+    assert np.array_equal(codes.cpu().numpy().view(np.uint64)[: len(rc)], rc)
+    assert np.array_equal(params.cpu().numpy().view(np.uint16), rp)
+    xh = bm.unpack(codes, params, bd, od, units, d, group, int(off[-1])).cpu().numpy()
+    assert np.array_equal(xh.astype(np.float64), oracle.unpack(rc, rp, bits_u, d, group))
+
+
 # -------------------------------------------------------------- end to end
 def _stagewise(proj, sample_rows=None, check_ilp=True):
     """Run the pipeline and check each stage on the device's own inputs."""

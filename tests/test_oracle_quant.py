@@ -175,3 +175,22 @@ def test_pack_roundtrip_and_size():
         q, _, _ = oracle.quant_group(c[u], b, G)
         planes = codes[off[u]:off[u + 1]].reshape(b, d // 64)
         assert np.array_equal(planes, oracle.bit_planes(q[0], b))
+
+
+def test_pack_eviction_and_fp16_widths():
+    """Widths 0 (evicted) and 16 (fp16 row) of the surrogate's candidate set:
+    sizes b d / 8 bytes, fp16 entries four to a little-endian word (hand-made
+    words: 1.0 = 0x3C00, -2.0 = 0xC000, 0.5 = 0x3800, 65504 = 0x7BFF)."""
+    d, G = 64, 32
+    c = np.zeros((3, d), dtype=np.float32)
+    c[:, :4] = [1.0, -2.0, 0.5, 65504.0]
+    c[:, 4:] = np.linspace(-1, 1, d - 4, dtype=np.float32)
+    bits_u = np.array([16, 0, 2], dtype=np.uint8)
+    codes, params, off = oracle.pack(c, bits_u, G)
+    assert list(off) == [0, 16, 16, 18]
+    assert int(codes[0]) == 0x7BFF3800C0003C00
+    assert np.all(params[:2] == 0)
+    xh = oracle.unpack(codes, params, bits_u, d, G)
+    assert np.array_equal(xh[0], c[0].astype(np.float16).astype(np.float64))
+    assert np.all(xh[1] == 0.0)
+    assert np.array_equal(xh[2], oracle.fake_quant(c[2], 2, G)[0])
