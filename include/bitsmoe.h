@@ -29,6 +29,13 @@
  *   bitsmoe_surrogate_budget  equivalent-bit budget           (host)
  * and bitsmoe_allocate accepts those widths (0 = evicted, 16 = fp16).
  *
+ * The paper builds the gate/up bases in the shared *input* space instead
+ * (Sec. 3.2); that construction is available as well:
+ *   bitsmoe_gram_experts_in   M_in = sum_e W_e^T W_e               (device)
+ *   bitsmoe_project_in        C_e = Phi_r^T W_e^T (units W_e phi_k) (device)
+ *   bitsmoe_basis_importance  beta_k = phi_k^T H phi_k             (device)
+ *   bitsmoe_score_diag        L = beta_k ||c - Q_b(c)||^2          (device)
+ *
  * Conventions shared by every call:
  *  - Pointers named *_dev are device memory on the current HIP device;
  *    *_host are host memory.  The caller allocates and owns every input and
@@ -207,6 +214,63 @@ bitsmoe_status bitsmoe_allocate_ex(const float* L_host, int64_t units, const int
                                    int nbits, int64_t budget_bits, uint8_t* bits_out_host,
                                    double* objective_out, int64_t full_dp_limit,
                                    int64_t* core_units_out);
+
+/*
+ * Input-space basis of a gate/up projection (Sec. 3.2, Eq.
+ * shared_basis_input_proj): the experts are stacked along their output
+ * channels, W_cat = [W_1; ...; W_E] = P~_cat Phi^T, so Phi holds the
+ * eigenvectors of
+ *     M_in = W_cat^T W_cat = sum_e W_e^T W_e,
+ * computed here in fp64 (same engine and fixed-order reduction as
+ * bitsmoe_gram, over the E * d_out stacked rows).  The basis itself comes
+ * from bitsmoe_shared_basis(M_in, d_in, r).
+ *   W_dev  [E][d_out][d_in] of type wt
+ *   M_dev  [d_in][d_in] fp64 output, full symmetric
+ * Shape rules: d_out % 64 == 0, d_in % 64 == 0.
+ */
+bitsmoe_status bitsmoe_gram_experts_in(const void* W_dev, bitsmoe_dtype wt, int64_t E,
+                                       int64_t d_out, int64_t d_in, double* M_dev, void* stream);
+
+/*
+ * Input-space spectral units: C_e = Phi_r^T W_e^T, so row k of C_e is the
+ * column p~_{e,k} = W_e phi_k of P~_e = W_e Phi (Definitions
+ * spectral_energy_matrix and spectral_matrix); unit u = e*r + k, length d_out.
+ * As in bitsmoe_project, the fp32 basis is split into bf16 hi + lo terms.
+ *   Vt_dev  [r][d_in] fp32 (row k = phi_k, e.g. from bitsmoe_shared_basis)
+ *   W_dev   [E][d_out][d_in] of type wt
+ *   C_dev   [E][r][d_out] fp32 output
+ * Shape rules: d_out % 64 == 0, d_in % 64 == 0, 1 <= r <= d_in.
+ */
+bitsmoe_status bitsmoe_project_in(const float* Vt_dev, const void* W_dev, bitsmoe_dtype wt,
+                                  int64_t E, int64_t d_out, int64_t d_in, int64_t r,
+                                  float* C_dev, void* stream);
+
+/*
+ * Activation-aware importance of each input-space basis vector (Eq.
+ * beta_def): beta[k] = phi_k^T H phi_k for the rows phi_k of Vt, through the
+ * same fp16 matrix-core form as bitsmoe_score (relative error ~1e-4).
+ *   Vt_dev    [r][d] fp32;  H_dev [d][d] fp32 symmetric (as bitsmoe_score)
+ *   beta_dev  [r] fp32 output
+ * Shape rules: d % 64 == 0, d < 2^22.
+ */
+bitsmoe_status bitsmoe_basis_importance(const float* Vt_dev, int64_t r, int64_t d,
+                                        const float* H_dev, float* beta_dev, void* stream);
+
+/*
+ * Loss table of the input-space units under the paper's diagonal
+ * approximation (the cross terms phi_k^T H phi_l, k != l, of Lemma
+ * spectrum_wise_error_decomp dropped; Corollary additive_spectrum_wise_loss):
+ *     L[u][j] = beta[u % r] * ||c_u - Q_{bits[j]}(c_u)||^2
+ * with the group-wise quantizer of bitsmoe_score (so widths and codes match
+ * bitsmoe_pack).  The error norms are summed in fp32.
+ *   C_dev     [units][d] fp32 (from bitsmoe_project_in)
+ *   beta_dev  [r] fp32 (from bitsmoe_basis_importance)
+ *   L_dev     [units][nbits] fp32 output
+ * Shape rules as bitsmoe_score.
+ */
+bitsmoe_status bitsmoe_score_diag(const float* C_dev, int64_t units, int64_t d,
+                                  const float* beta_dev, int64_t r, const int* bits_host, int nbits,
+                                  int group, float* L_dev, void* stream);
 
 /*
  * The paper's surrogate cost table (App. B.3-B.4, Theorem

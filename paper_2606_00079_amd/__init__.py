@@ -39,7 +39,8 @@ EXPORTS = [
     "bitsmoe_score", "bitsmoe_allocate", "bitsmoe_allocate_ex", "bitsmoe_pack_layout",
     "bitsmoe_pack", "bitsmoe_unpack", "bitsmoe_set_lapack", "bitsmoe_last_error",
     "bitsmoe_release", "bitsmoe_version", "bitsmoe_timing", "bitsmoe_kernel_time",
-    "bitsmoe_surrogate", "bitsmoe_surrogate_budget",
+    "bitsmoe_surrogate", "bitsmoe_surrogate_budget", "bitsmoe_gram_experts_in",
+    "bitsmoe_project_in", "bitsmoe_basis_importance", "bitsmoe_score_diag",
 ]
 # Candidate widths of the surrogate table, in column order.
 SURROGATE_WIDTHS = (0, 1, 2, 3, 4, 6, 8, 16)
@@ -89,6 +90,10 @@ def lib() -> ctypes.CDLL:
     L.bitsmoe_unpack.argtypes = [vp, vp, vp, vp, i64, i64, i64, i32, vp, vp]
     L.bitsmoe_surrogate.argtypes = [vp, i64, i64, vp, ctypes.c_double, vp, vp, vp, vp]
     L.bitsmoe_surrogate_budget.argtypes = [i64, i64, i64, i64, ctypes.c_double, vp]
+    L.bitsmoe_gram_experts_in.argtypes = [vp, i32, i64, i64, i64, vp, vp]
+    L.bitsmoe_project_in.argtypes = [vp, vp, i32, i64, i64, i64, i64, vp, vp]
+    L.bitsmoe_basis_importance.argtypes = [vp, i64, i64, vp, vp, vp]
+    L.bitsmoe_score_diag.argtypes = [vp, i64, i64, vp, i64, vp, i32, i32, vp, vp]
     L.bitsmoe_set_lapack.argtypes = [ctypes.c_char_p]
     L.bitsmoe_timing.argtypes = [i32]
     L.bitsmoe_kernel_time.argtypes = [ctypes.c_char_p, vp, vp]
@@ -212,6 +217,62 @@ def score(C, H, bits: Sequence[int], group: int, out=None):
         out = torch.empty((units, len(b)), dtype=torch.float32, device=C.device)
     _check(lib().bitsmoe_score(_dev(C, "C"), units, d, _dev(H, "H"), bp, len(b), group,
                                _dev(out, "L"), _stream()), "score")
+    return out
+
+
+def gram_experts_in(W, out=None):
+    """M_in = sum_e W_e^T W_e for W [E][d_out][d_in] -> fp64 [d_in][d_in] (input-space basis)."""
+    torch = _torch()
+    E, d_out, d_in = W.shape
+    if out is None:
+        out = torch.empty((d_in, d_in), dtype=torch.float64, device=W.device)
+    _check(lib().bitsmoe_gram_experts_in(_dev(W, "W"), _dtype_code(W, "W"), E, d_out, d_in,
+                                         _dev(out, "M_in"), _stream()), "gram_experts_in")
+    return out
+
+
+def project_in(Vt, W, out=None):
+    """C_e = Phi_r^T W_e^T -> fp32 [E*r][d_out] (unit u = e*r + k is the column W_e phi_k)."""
+    torch = _torch()
+    r, d_in = Vt.shape
+    E, d_out, d_in2 = W.shape
+    if d_in2 != d_in:
+        raise ValueError("Vt and W disagree on d_in")
+    if Vt.dtype != torch.float32:
+        raise TypeError("Vt must be float32")
+    if out is None:
+        out = torch.empty((E * r, d_out), dtype=torch.float32, device=W.device)
+    _check(lib().bitsmoe_project_in(_dev(Vt, "Vt"), _dev(W, "W"), _dtype_code(W, "W"), E, d_out,
+                                    d_in, r, _dev(out, "C"), _stream()), "project_in")
+    return out
+
+
+def basis_importance(Vt, H, out=None):
+    """beta_k = phi_k^T H phi_k for the rows of Vt -> fp32 [r]."""
+    torch = _torch()
+    r, d = Vt.shape
+    if Vt.dtype != torch.float32 or H.dtype != torch.float32:
+        raise TypeError("Vt and H must be float32")
+    if tuple(H.shape) != (d, d):
+        raise ValueError("H must be [d][d]")
+    if out is None:
+        out = torch.empty((r,), dtype=torch.float32, device=Vt.device)
+    _check(lib().bitsmoe_basis_importance(_dev(Vt, "Vt"), r, d, _dev(H, "H"), _dev(out, "beta"),
+                                          _stream()), "basis_importance")
+    return out
+
+
+def score_diag(C, beta, bits: Sequence[int], group: int, out=None):
+    """L[u][j] = beta[u % r] ||c_u - Q_{bits[j]}(c_u)||^2 -> fp32 [units][len(bits)]."""
+    torch = _torch()
+    units, d = C.shape
+    if C.dtype != torch.float32 or beta.dtype != torch.float32:
+        raise TypeError("C and beta must be float32")
+    b, bp = _bits_arr(bits)
+    if out is None:
+        out = torch.empty((units, len(b)), dtype=torch.float32, device=C.device)
+    _check(lib().bitsmoe_score_diag(_dev(C, "C"), units, d, _dev(beta, "beta"), beta.shape[0], bp,
+                                    len(b), group, _dev(out, "L"), _stream()), "score_diag")
     return out
 
 

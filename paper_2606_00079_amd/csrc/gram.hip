@@ -3,6 +3,7 @@
 // partial tiles are added in fp64 in a fixed order (deterministic).
 #include <algorithm>
 #include <cstdio>
+#include <string>
 
 #include "bitsmoe.h"
 #include "common.hpp"
@@ -201,17 +202,18 @@ bitsmoe_status run_symmetric(gemm::Problem p, int64_t d, double scale, OutT* out
 
 using namespace bitsmoe;
 
-extern "C" bitsmoe_status bitsmoe_gram(const void* X_dev, bitsmoe_dtype xt, int64_t n, int64_t d,
-                                       float* H_dev, void* stream) {
-  if (!X_dev || !H_dev) return fail(BITSMOE_ERR_ARG, "gram: null pointer");
-  if (!aligned16({X_dev, H_dev})) return fail(BITSMOE_ERR_ARG, "gram: device pointers must be 16-byte aligned");
-  if (n <= 0 || d <= 0) return fail(BITSMOE_ERR_ARG, "gram: non-positive size");
-  if (xt != BITSMOE_F32 && xt != BITSMOE_BF16) return fail(BITSMOE_ERR_DTYPE, "gram: dtype");
-  if (d % 64 != 0) return fail(BITSMOE_ERR_SHAPE, "gram: d must be a multiple of 64");
+namespace bitsmoe {
+namespace {
+
+// scale * R^T R for rows R [n][d] (bf16 or fp32): R is transposed into the
+// K-tiled layout (K = rows, zero-padded to the engine's K alignment; fp32
+// split into hi + lo) and multiplied by the symmetric split-K GEMM.
+template <typename OutT>
+bitsmoe_status gram_rows(const void* R_dev, bitsmoe_dtype rt, int64_t n, int64_t d, double scale,
+                         OutT* out_dev, void* stream, const char* who) {
   hipStream_t s = static_cast<hipStream_t>(stream);
-  // K padded with zero rows to a multiple of the engine's K alignment
   const int64_t npad = (n + gemm::kKAlign - 1) / gemm::kKAlign * gemm::kKAlign;
-  const bool f32 = xt == BITSMOE_F32;
+  const bool f32 = rt == BITSMOE_F32;
   bitsmoe_status st;
   const int64_t d_pad = (d + GT - 1) / GT * GT;  // whole K-tiled row tiles
   uint16_t* hi = static_cast<uint16_t*>(scratch(kScratchA, d_pad * npad * 2, stream, &st));
@@ -221,12 +223,13 @@ extern "C" bitsmoe_status bitsmoe_gram(const void* X_dev, bitsmoe_dtype xt, int6
     lo = static_cast<uint16_t*>(scratch(kScratchB, d_pad * npad * 2, stream, &st));
     if (!lo) return st;
   }
+  if ((npad + 63) / 64 > INT32_MAX) return fail(BITSMOE_ERR_SHAPE, std::string(who) + ": too many rows");
   dim3 tg(static_cast<unsigned>((npad + 63) / 64), static_cast<unsigned>((d + 63) / 64));
   if (f32)
-    hipLaunchKernelGGL(transpose_split_kernel<true>, tg, dim3(256), 0, s, X_dev, n, d, npad, hi, lo);
+    hipLaunchKernelGGL(transpose_split_kernel<true>, tg, dim3(256), 0, s, R_dev, n, d, npad, hi, lo);
   else
-    hipLaunchKernelGGL(transpose_split_kernel<false>, tg, dim3(256), 0, s, X_dev, n, d, npad, hi, lo);
-  BITSMOE_LAUNCH_CHECK("gram: transpose launch");
+    hipLaunchKernelGGL(transpose_split_kernel<false>, tg, dim3(256), 0, s, R_dev, n, d, npad, hi, lo);
+  BITSMOE_LAUNCH_CHECK(who);
   gemm::Problem p{};
   static_assert(BK == gemm::kTileK, "the K-tiled operands need the kernel's K step");
   p.a.rows = p.b.rows = d_pad;
@@ -244,7 +247,42 @@ extern "C" bitsmoe_status bitsmoe_gram(const void* X_dev, bitsmoe_dtype xt, int6
     p.a.pass[0] = p.b.pass[0] = hi;
   }
   p.ktiles = p.passes * npad / BK;
-  st = run_symmetric<float>(p, d, 1.0 / static_cast<double>(n), H_dev, stream, "gram");
+  return run_symmetric<OutT>(p, d, scale, out_dev, stream, who);
+}
+
+bitsmoe_status check_rows(const void* R_dev, const void* out_dev, bitsmoe_dtype rt, int64_t n,
+                          int64_t d, const char* who) {
+  if (!R_dev || !out_dev) return fail(BITSMOE_ERR_ARG, std::string(who) + ": null pointer");
+  if (!aligned16({R_dev, out_dev}))
+    return fail(BITSMOE_ERR_ARG, std::string(who) + ": device pointers must be 16-byte aligned");
+  if (n <= 0 || d <= 0) return fail(BITSMOE_ERR_ARG, std::string(who) + ": non-positive size");
+  if (rt != BITSMOE_F32 && rt != BITSMOE_BF16) return fail(BITSMOE_ERR_DTYPE, std::string(who) + ": dtype");
+  if (d % 64 != 0) return fail(BITSMOE_ERR_SHAPE, std::string(who) + ": d must be a multiple of 64");
+  return BITSMOE_OK;
+}
+
+}  // namespace
+}  // namespace bitsmoe
+
+extern "C" bitsmoe_status bitsmoe_gram(const void* X_dev, bitsmoe_dtype xt, int64_t n, int64_t d,
+                                       float* H_dev, void* stream) {
+  bitsmoe_status st = check_rows(X_dev, H_dev, xt, n, d, "gram");
+  if (st != BITSMOE_OK) return st;
+  st = gram_rows<float>(X_dev, xt, n, d, 1.0 / static_cast<double>(n), H_dev, stream, "gram");
+  if (st != BITSMOE_OK) return st;
+  return ok();
+}
+
+extern "C" bitsmoe_status bitsmoe_gram_experts_in(const void* W_dev, bitsmoe_dtype wt, int64_t E,
+                                                  int64_t d_out, int64_t d_in, double* M_dev,
+                                                  void* stream) {
+  if (E <= 0 || d_out <= 0) return fail(BITSMOE_ERR_ARG, "gram_experts_in: non-positive size");
+  if (d_out % 64 != 0)
+    return fail(BITSMOE_ERR_SHAPE, "gram_experts_in: d_out and d_in must be multiples of 64");
+  // the stacked expert rows W_cat = [W_1; ...; W_E] are [E * d_out][d_in]
+  bitsmoe_status st = check_rows(W_dev, M_dev, wt, E * d_out, d_in, "gram_experts_in");
+  if (st != BITSMOE_OK) return st;
+  st = gram_rows<double>(W_dev, wt, E * d_out, d_in, 1.0, M_dev, stream, "gram_experts_in");
   if (st != BITSMOE_OK) return st;
   return ok();
 }

@@ -78,23 +78,36 @@ __global__ __launch_bounds__(256) void batched_transpose_kernel(const void* __re
   }
 }
 
-// C[z][row][col] = acc for row < r, col < d_in.
+// fp32 x -> (hi, lo) bf16, element by element (row-major operands).
+__global__ __launch_bounds__(256) void split_rows_kernel(const float* __restrict__ x, int64_t count,
+                                                         uint16_t* __restrict__ hi,
+                                                         uint16_t* __restrict__ lo) {
+  for (int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; i < count;
+       i += static_cast<int64_t>(gridDim.x) * 256) {
+    const float v = x[i];
+    const uint16_t h = f32_to_bf16(v);
+    hi[i] = h;
+    lo[i] = f32_to_bf16(v - bf16_to_f32(h));
+  }
+}
+
+// C[z][row][col] = acc for row < r, col < cols.
 struct FactorStore {
   float* C;
-  int64_t r, d_in;
+  int64_t r, cols;
   template <class F>
   __device__ void operator()(F& f, const gemm::StageLds&) const {
-    float* base = C + f.z * r * d_in;
+    float* base = C + f.z * r * cols;
 #pragma unroll
     for (int mi = 0; mi < F::FM; ++mi)
 #pragma unroll
       for (int ni = 0; ni < F::FN; ++ni) {
         const int col = f.col(ni);
-        if (col >= d_in) continue;
+        if (col >= cols) continue;
 #pragma unroll
         for (int q = 0; q < 16; ++q) {
           const int row = f.row(mi, q);
-          if (row < r) base[static_cast<int64_t>(row) * d_in + col] = f.acc[mi][ni][q];
+          if (row < r) base[static_cast<int64_t>(row) * cols + col] = f.acc[mi][ni][q];
         }
       }
   }
@@ -199,5 +212,93 @@ extern "C" bitsmoe_status bitsmoe_project(const float* Ut_dev, const void* W_dev
 #undef BITSMOE_PROJECT
   }
   BITSMOE_LAUNCH_CHECK("project: gemm launch");
+  return ok();
+}
+
+// Input-space factors of the gate/up projections: C_e = Phi_r^T W_e^T, i.e.
+// acc[k][j] = sum_i Vt[k][i] W_e[j][i]; both operands are contiguous along
+// K = d_in, so W is read row-major where it lies (fp32 W split into hi/lo).
+extern "C" bitsmoe_status bitsmoe_project_in(const float* Vt_dev, const void* W_dev,
+                                             bitsmoe_dtype wt, int64_t E, int64_t d_out,
+                                             int64_t d_in, int64_t r, float* C_dev, void* stream) {
+  if (!Vt_dev || !W_dev || !C_dev) return fail(BITSMOE_ERR_ARG, "project_in: null pointer");
+  if (!aligned16({Vt_dev, W_dev, C_dev}))
+    return fail(BITSMOE_ERR_ARG, "project_in: device pointers must be 16-byte aligned");
+  if (E <= 0 || d_out <= 0 || d_in <= 0 || r <= 0)
+    return fail(BITSMOE_ERR_ARG, "project_in: non-positive size");
+  if (wt != BITSMOE_F32 && wt != BITSMOE_BF16) return fail(BITSMOE_ERR_DTYPE, "project_in: dtype");
+  if (d_out % 64 != 0 || d_in % 64 != 0)
+    return fail(BITSMOE_ERR_SHAPE, "project_in: d_out and d_in must be multiples of 64");
+  if (r > d_in) return fail(BITSMOE_ERR_SHAPE, "project_in: r > d_in");
+  if (E > 65535) return fail(BITSMOE_ERR_SHAPE, "project_in: too many experts");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const bool f32 = wt == BITSMOE_F32;
+  bitsmoe_status st;
+  int PM = 256;
+  for (int t : {192, 128})
+    if ((r + t - 1) / t * t < (r + PM - 1) / PM * PM) PM = t;
+  const int64_t r_pad = (r + PM - 1) / PM * PM;
+  uint16_t* V2 = static_cast<uint16_t*>(scratch(kScratchMisc, 2 * r_pad * d_in * 2, stream, &st));
+  if (!V2) return st;
+  {
+    const int64_t count = r_pad * d_in;
+    const unsigned blocks = static_cast<unsigned>(std::min<int64_t>((count + 255) / 256, 65536));
+    hipLaunchKernelGGL(split_f32_kernel, dim3(blocks), dim3(256), 0, s, Vt_dev, r, r_pad, d_in, PM,
+                       V2, V2 + count);
+    BITSMOE_LAUNCH_CHECK("project_in: split launch");
+  }
+  gemm::Problem p{};
+  const uint16_t* Vhi = V2;
+  const uint16_t* Vlo = V2 + r_pad * d_in;
+  p.a.rows = r_pad;
+  p.a.kstep = static_cast<int64_t>(PM) * gemm::kTileK;
+  p.a.rtile = static_cast<int64_t>(PM) * d_in;
+  p.a.bstride = 0;
+  p.b.ld = d_in;
+  p.b.rows = d_out;  // rows past it are clamped
+  p.b.kstep = 0;     // row-major
+  p.b.bstride = d_out * d_in;
+  p.segs = 1;
+  p.kseg = d_in;
+  const uint16_t* Wb = static_cast<const uint16_t*>(W_dev);
+  if (f32) {
+    const int64_t wcount = E * d_out * d_in;
+    uint16_t* W2 = static_cast<uint16_t*>(scratch(kScratchB, 2 * wcount * 2, stream, &st));
+    if (!W2) return st;
+    const unsigned blocks = static_cast<unsigned>(std::min<int64_t>((wcount + 255) / 256, 65536));
+    hipLaunchKernelGGL(split_rows_kernel, dim3(blocks), dim3(256), 0, s,
+                       static_cast<const float*>(W_dev), wcount, W2, W2 + wcount);
+    BITSMOE_LAUNCH_CHECK("project_in: W split launch");
+    p.passes = 3;  // Vhi*Whi + Vhi*Wlo + Vlo*Whi
+    p.a.pass[0] = Vhi; p.b.pass[0] = W2;
+    p.a.pass[1] = Vhi; p.b.pass[1] = W2 + wcount;
+    p.a.pass[2] = Vlo; p.b.pass[2] = W2;
+  } else {
+    p.passes = 2;  // Vhi*W + Vlo*W
+    p.a.pass[0] = Vhi; p.b.pass[0] = Wb;
+    p.a.pass[1] = Vlo; p.b.pass[1] = Wb;
+  }
+  p.ktiles = static_cast<int64_t>(p.passes) * d_in / BK;
+  p.splits = 1;
+  p.tiles_m = static_cast<int>((r + PM - 1) / PM);
+  p.tiles_n = static_cast<int>((d_out + PN - 1) / PN);
+  p.symmetric = 0;
+  p.group_n = p.tiles_n;
+  FactorStore epi{C_dev, r, d_out};
+  dim3 grid(static_cast<unsigned>(p.tiles_m * p.tiles_n), 1, static_cast<unsigned>(E));
+  {
+    KernelTimer timer("project_in", stream);
+#define BITSMOE_PROJECT_IN(TM)                                                                \
+  hipLaunchKernelGGL((gemm::gemm_nt_kernel<TM, PN, 32, 4, FactorStore>), grid,                \
+                     dim3(gemm::kThreads), 0, s, p, epi)
+    if (PM == 256)
+      BITSMOE_PROJECT_IN(256);
+    else if (PM == 192)
+      BITSMOE_PROJECT_IN(192);
+    else
+      BITSMOE_PROJECT_IN(128);
+#undef BITSMOE_PROJECT_IN
+  }
+  BITSMOE_LAUNCH_CHECK("project_in: gemm launch");
   return ok();
 }

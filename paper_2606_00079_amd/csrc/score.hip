@@ -132,12 +132,19 @@ struct QuantBits {
 // The row is read twice: once for max |c|, once to quantize (the second read
 // mostly hits in the caches; holding the row in registers instead costs more
 // in occupancy than it saves); both passes keep several loads in flight.
-template <int NB>
+//
+// NORM: only the error norms are wanted (the input-space table
+// beta_k ||delta||^2 of the diagonal approximation): no error rows are
+// written, H's diagonal is taken as 1, the errors are not rescaled (E = 0),
+// and diag[u * nb + j] = w[u % wperiod] * sum delta^2.
+template <int NB, bool NORM = false>
 __global__ __launch_bounds__(256) void dgen_kernel(const float* __restrict__ C, int64_t units,
                                                    int64_t d, int G, QuantBits qb,
                                                    const float* __restrict__ hdiag,
                                                    uint16_t* __restrict__ D,
-                                                   float* __restrict__ diag, int* __restrict__ uexp) {
+                                                   float* __restrict__ diag, int* __restrict__ uexp,
+                                                   const float* __restrict__ w = nullptr,
+                                                   int64_t wperiod = 1) {
   const int lane = threadIdx.x & 63;
   const int64_t u = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
   if (u >= units) return;  // whole wave exits together
@@ -171,24 +178,27 @@ __global__ __launch_bounds__(256) void dgen_kernel(const float* __restrict__ C, 
   // |delta| <= max - min <= 2 max |c| < 2^(e + 1): the error rows are stored
   // as fp16(delta * 2^E) with E = kF16Top - 1 - e.  Four chunks' loads are
   // issued before any is reduced.
-  float amax = 0.0f;
-  int64_t ka = 0;
-  for (; ka + 4 * 512 <= d; ka += 4 * 512) {
-    float c4[4][8];
+  int E = 0;
+  if constexpr (!NORM) {
+    float amax = 0.0f;
+    int64_t ka = 0;
+    for (; ka + 4 * 512 <= d; ka += 4 * 512) {
+      float c4[4][8];
 #pragma unroll
-    for (int x = 0; x < 4; ++x) load8(ka + 512 * x, c4[x]);
+      for (int x = 0; x < 4; ++x) load8(ka + 512 * x, c4[x]);
 #pragma unroll
-    for (int x = 0; x < 4; ++x) amax = fmaxf(amax, absmax8(c4[x]));
+      for (int x = 0; x < 4; ++x) amax = fmaxf(amax, absmax8(c4[x]));
+    }
+    for (; ka < d; ka += 512) {
+      float cc[8];
+      load8(ka, cc);
+      amax = fmaxf(amax, absmax8(cc));
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) amax = fmaxf(amax, __shfl_xor(amax, o, 64));
+    E = kF16Top - 1 - exponent_above(amax);
+    if (lane == 0) uexp[u] = E;
   }
-  for (; ka < d; ka += 512) {
-    float cc[8];
-    load8(ka, cc);
-    amax = fmaxf(amax, absmax8(cc));
-  }
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) amax = fmaxf(amax, __shfl_xor(amax, o, 64));
-  const int E = kF16Top - 1 - exponent_above(amax);
-  if (lane == 0) uexp[u] = E;
 
   // quantize one 512-entry chunk at every width
   auto chunk = [&](int64_t k0, const float (&c)[8]) {
@@ -206,10 +216,15 @@ __global__ __launch_bounds__(256) void dgen_kernel(const float* __restrict__ C, 
     }
     if (!active) return;
     float hd[8];
-    const float4 h0 = *reinterpret_cast<const float4*>(hdiag + k);
-    const float4 h1 = *reinterpret_cast<const float4*>(hdiag + k + 4);
-    hd[0] = h0.x; hd[1] = h0.y; hd[2] = h0.z; hd[3] = h0.w;
-    hd[4] = h1.x; hd[5] = h1.y; hd[6] = h1.z; hd[7] = h1.w;
+    if constexpr (NORM) {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) hd[i] = 1.0f;
+    } else {
+      const float4 h0 = *reinterpret_cast<const float4*>(hdiag + k);
+      const float4 h1 = *reinterpret_cast<const float4*>(hdiag + k + 4);
+      hd[0] = h0.x; hd[1] = h0.y; hd[2] = h0.z; hd[3] = h0.w;
+      hd[4] = h1.x; hd[5] = h1.y; hd[6] = h1.z; hd[7] = h1.w;
+    }
     const float mf = f16_bits_to_f32(f32_to_f16_bits(mn));
     const float range = mx - mn;
     // c - m16 once per entry, and its image scaled by 2^E (exact)
@@ -259,12 +274,14 @@ __global__ __launch_bounds__(256) void dgen_kernel(const float* __restrict__ C, 
         out[i] = f32_to_f16_bits(dls);
         dacc[j] = fmaf(hd[i] * dls, dls, dacc[j]);
       }
-      uint4 pk;
-      pk.x = static_cast<uint32_t>(out[0]) | (static_cast<uint32_t>(out[1]) << 16);
-      pk.y = static_cast<uint32_t>(out[2]) | (static_cast<uint32_t>(out[3]) << 16);
-      pk.z = static_cast<uint32_t>(out[4]) | (static_cast<uint32_t>(out[5]) << 16);
-      pk.w = static_cast<uint32_t>(out[6]) | (static_cast<uint32_t>(out[7]) << 16);
-      *reinterpret_cast<uint4*>(D + gemm::tiled_offset(u * nb + j, k, d, SBN)) = pk;
+      if constexpr (!NORM) {
+        uint4 pk;
+        pk.x = static_cast<uint32_t>(out[0]) | (static_cast<uint32_t>(out[1]) << 16);
+        pk.y = static_cast<uint32_t>(out[2]) | (static_cast<uint32_t>(out[3]) << 16);
+        pk.z = static_cast<uint32_t>(out[4]) | (static_cast<uint32_t>(out[5]) << 16);
+        pk.w = static_cast<uint32_t>(out[6]) | (static_cast<uint32_t>(out[7]) << 16);
+        *reinterpret_cast<uint4*>(D + gemm::tiled_offset(u * nb + j, k, d, SBN)) = pk;
+      }
     }
   };
   // the loads of chunk c + 1 are issued before chunk c is quantized
@@ -276,10 +293,11 @@ __global__ __launch_bounds__(256) void dgen_kernel(const float* __restrict__ C, 
 #pragma unroll
     for (int i = 0; i < 8; ++i) cur[i] = nxt[i];
   }
+  const float wu = NORM ? w[u % wperiod] : 1.0f;
 #pragma unroll
   for (int j = 0; j < NB; ++j) {
     const float v = ldexpf(wave_sum(dacc[j]), -2 * E);
-    if (lane == 0) diag[u * nb + j] = v;
+    if (lane == 0) diag[u * nb + j] = NORM ? wu * v : v;
   }
 }
 
@@ -524,6 +542,21 @@ __global__ __launch_bounds__(256) void surrogate_finalize_kernel(
   }
 }
 
+// q[row] = c H c^T for the raw rows prepared by rowprep_kernel.
+__global__ __launch_bounds__(256) void quadform_finalize_kernel(const float* __restrict__ diag,
+                                                                const float* __restrict__ part,
+                                                                int64_t rows, int tiles_m,
+                                                                const int* __restrict__ uexp,
+                                                                const int* __restrict__ hexp,
+                                                                float* __restrict__ q) {
+  const int64_t row = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (row >= rows) return;
+  const float* p = part + row * tiles_m;
+  float s = 0.0f;
+  for (int t = 0; t < tiles_m; ++t) s += p[t];
+  q[row] = diag[row] + ldexpf(s, -(2 * uexp[row] + *hexp));
+}
+
 // Scratch and launch shape of one loss-table evaluation over R rows of D
 // (error rows for the score, raw rows for the surrogate) against H.
 struct LossTable {
@@ -738,5 +771,72 @@ extern "C" bitsmoe_status bitsmoe_surrogate_budget(int64_t E, int64_t n_out, int
   const long double B = floorl((total - basis) / m);
   if (B < 0.0L) return fail(BITSMOE_ERR_INFEASIBLE, "surrogate_budget: the fp16 basis alone exceeds the budget");
   *budget_out = static_cast<int64_t>(B);
+  return ok();
+}
+
+extern "C" bitsmoe_status bitsmoe_basis_importance(const float* Vt_dev, int64_t r, int64_t d,
+                                                   const float* H_dev, float* beta_dev,
+                                                   void* stream) {
+  if (!Vt_dev || !H_dev || !beta_dev) return fail(BITSMOE_ERR_ARG, "basis_importance: null pointer");
+  if (!aligned16({beta_dev}))
+    return fail(BITSMOE_ERR_ARG, "basis_importance: device pointers must be 16-byte aligned");
+  bitsmoe_status st = check_rows_args(Vt_dev, H_dev, r, d, "basis_importance");
+  if (st != BITSMOE_OK) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  LossTable t;
+  st = loss_table_setup(d, r, r, true, stream, "basis_importance", &t);
+  if (st != BITSMOE_OK) return st;
+  st = loss_table_hoff(H_dev, t, s, "basis_importance: H_off launch");
+  if (st != BITSMOE_OK) return st;
+  hipLaunchKernelGGL(rowprep_kernel, dim3(static_cast<unsigned>((r + 3) / 4)), dim3(256), 0, s,
+                     Vt_dev, r, d, t.hdiag, t.D, t.diag, t.uexp, t.rstats);
+  BITSMOE_LAUNCH_CHECK("basis_importance: row launch");
+  st = loss_table_gemm(t, stream, "basis_importance", "basis_importance: gemm launch");
+  if (st != BITSMOE_OK) return st;
+  hipLaunchKernelGGL(quadform_finalize_kernel, dim3(static_cast<unsigned>((r + 255) / 256)),
+                     dim3(256), 0, s, t.diag, t.part, r, t.tiles_m, t.uexp, t.hexp, beta_dev);
+  BITSMOE_LAUNCH_CHECK("basis_importance: finalize launch");
+  return ok();
+}
+
+extern "C" bitsmoe_status bitsmoe_score_diag(const float* C_dev, int64_t units, int64_t d,
+                                             const float* beta_dev, int64_t r,
+                                             const int* bits_host, int nbits, int group,
+                                             float* L_dev, void* stream) {
+  if (!C_dev || !beta_dev || !bits_host || !L_dev) return fail(BITSMOE_ERR_ARG, "score_diag: null pointer");
+  if (!aligned16({C_dev, beta_dev, L_dev}))
+    return fail(BITSMOE_ERR_ARG, "score_diag: device pointers must be 16-byte aligned");
+  if (units <= 0 || d <= 0 || r <= 0) return fail(BITSMOE_ERR_ARG, "score_diag: non-positive size");
+  if (nbits < 1 || nbits > BITSMOE_MAX_NBITS) return fail(BITSMOE_ERR_ARG, "score_diag: nbits outside 1..8");
+  QuantBits qb{};
+  qb.nb = nbits;
+  for (int j = 0; j < nbits; ++j) {
+    if (bits_host[j] < 1 || bits_host[j] > BITSMOE_MAX_BITS)
+      return fail(BITSMOE_ERR_ARG, "score_diag: width outside 1..8");
+    if (j > 0 && bits_host[j] <= bits_host[j - 1])
+      return fail(BITSMOE_ERR_ARG, "score_diag: widths must be strictly ascending");
+    qb.b[j] = bits_host[j];
+  }
+  if (!(group == 32 || group == 64 || group == 128 || group == 256))
+    return fail(BITSMOE_ERR_SHAPE, "score_diag: group must be 32, 64, 128 or 256");
+  if (d % 64 != 0 || d % group != 0)
+    return fail(BITSMOE_ERR_SHAPE, "score_diag: d must be a multiple of 64 and of the group");
+  if ((units + 3) / 4 > INT32_MAX) return fail(BITSMOE_ERR_SHAPE, "score_diag: too many units");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const unsigned db = static_cast<unsigned>((units + 3) / 4);
+  {
+    KernelTimer timer("score_diag", stream);
+    switch (nbits) {
+#define BITSMOE_DNORM(NB)                                                                        \
+  case NB:                                                                                       \
+    hipLaunchKernelGGL((dgen_kernel<NB, true>), dim3(db), dim3(256), 0, s, C_dev, units, d, group, \
+                       qb, nullptr, nullptr, L_dev, nullptr, beta_dev, r);                      \
+    break;
+      BITSMOE_DNORM(1) BITSMOE_DNORM(2) BITSMOE_DNORM(3) BITSMOE_DNORM(4)
+      BITSMOE_DNORM(5) BITSMOE_DNORM(6) BITSMOE_DNORM(7) BITSMOE_DNORM(8)
+#undef BITSMOE_DNORM
+    }
+  }
+  BITSMOE_LAUNCH_CHECK("score_diag: launch");
   return ok();
 }

@@ -24,8 +24,9 @@ from typing import Dict, List, Optional, Sequence
 
 import numpy as np
 
-from . import (SURROGATE_WIDTHS, allocate, gram, gram_experts, pack, pack_layout, project, score,
-               shared_basis, surrogate, surrogate_budget)
+from . import (SURROGATE_WIDTHS, allocate, basis_importance, gram, gram_experts, gram_experts_in,
+               pack, pack_layout, project, project_in, score, score_diag, shared_basis, surrogate,
+               surrogate_budget)
 
 
 @dataclasses.dataclass
@@ -107,6 +108,56 @@ def quantize_projection(W, X, r: int, bits: Sequence[int], group: int, budget: i
     times["gpu_pack_ms"] = s3.ms()
     times["gpu_ms"] = times["gpu_gram_ms"] + times["gpu_score_ms"] + times["gpu_pack_ms"]
     return ProjectionResult(H, M, Ut, ev, C, L, bits_u, obj, off, codes, params, times)
+
+
+def quantize_projection_in(W, X, r: int, bits: Sequence[int], group: int, budget: int,
+                           H=None) -> ProjectionResult:
+    """The paper's input-space construction of a gate/up projection (Sec. 3.2):
+    basis Phi from M_in = sum W_e^T W_e, units W_e phi_k (rows of C, length
+    d_out), loss beta_k ||c - Q_b(c)||^2 (diagonal approximation), exact ILP,
+    pack.  ``Ut`` of the result holds Phi_r^T and ``M`` holds M_in."""
+    import torch
+    times: Dict[str, float] = {}
+    dev = W.device
+    E, d_out, d_in = W.shape
+    Hbuf = None
+    if H is None:
+        Hbuf = torch.empty((d_in, d_in), dtype=torch.float32, device=dev)
+    M = torch.empty((d_in, d_in), dtype=torch.float64, device=dev)
+    s1 = _Seg()
+    with s1:
+        if H is None:
+            H = gram(X, out=Hbuf)
+        gram_experts_in(W, out=M)
+    Vt, ev, eig_ms = shared_basis(M, r)
+    times["gpu_gram_ms"] = s1.ms()
+    times["host_eig_ms"] = eig_ms
+    C = torch.empty((E * r, d_out), dtype=torch.float32, device=dev)
+    beta = torch.empty((r,), dtype=torch.float32, device=dev)
+    L = torch.empty((E * r, len(bits)), dtype=torch.float32, device=dev)
+    s2 = _Seg()
+    with s2:
+        project_in(Vt, W, out=C)
+        basis_importance(Vt, H, out=beta)
+        score_diag(C, beta, bits, group, out=L)
+    t0 = time.perf_counter()
+    Lh = L.cpu().numpy()
+    bits_u, obj = allocate(Lh, bits, budget)
+    off = pack_layout(bits_u, d_out)
+    times["gpu_score_ms"] = s2.ms()
+    bits_d = torch.from_numpy(bits_u).to(dev, non_blocking=False)
+    off_d = torch.from_numpy(off).to(dev, non_blocking=False)
+    times["host_ilp_ms"] = (time.perf_counter() - t0) * 1e3
+    codes = torch.empty((max(int(off[-1]), 1),), dtype=torch.int64, device=dev)
+    params = torch.empty((C.shape[0], d_out // group, 2), dtype=torch.int16, device=dev)
+    s3 = _Seg()
+    with s3:
+        pack(C, bits_d, off_d, group, int(off[-1]), codes=codes, params=params)
+    times["gpu_pack_ms"] = s3.ms()
+    times["gpu_ms"] = times["gpu_gram_ms"] + times["gpu_score_ms"] + times["gpu_pack_ms"]
+    res = ProjectionResult(H, M, Vt, ev, C, L, bits_u, obj, off, codes, params, times)
+    res.beta = beta
+    return res
 
 
 def quantize_layer(projs: List[dict]) -> List[ProjectionResult]:

@@ -208,6 +208,16 @@ def test_device_entry_points_validate_before_launch(lib):
     assert lib.bitsmoe_surrogate(fake, 0, 256, fake, 0.7, kap, fake, null, s) == 1
     assert lib.bitsmoe_surrogate(fake, 10, 256, fake, 1.5, kap, fake, null, s) == 1
     assert lib.bitsmoe_surrogate(fake, 10, 256, fake, 0.7, badk, fake, null, s) == 1
+    assert lib.bitsmoe_gram_experts_in(fake, 1, 2, 96, 64, fake, s) == 2
+    assert lib.bitsmoe_gram_experts_in(null, 1, 2, 64, 64, fake, s) == 1
+    assert lib.bitsmoe_gram_experts_in(fake, 5, 2, 64, 64, fake, s) == 3
+    assert lib.bitsmoe_project_in(fake, fake, 1, 2, 64, 64, 65, fake, s) == 2
+    assert lib.bitsmoe_project_in(fake, fake, 1, 2, 100, 64, 8, fake, s) == 2
+    assert lib.bitsmoe_basis_importance(fake, 8, 100, fake, fake, s) == 2
+    assert lib.bitsmoe_basis_importance(null, 8, 64, fake, fake, s) == 1
+    assert lib.bitsmoe_score_diag(fake, 10, 256, fake, 0, bits, 4, 64, fake, s) == 1
+    assert lib.bitsmoe_score_diag(fake, 10, 256, fake, 4, bits, 4, 48, fake, s) == 2
+    assert lib.bitsmoe_score_diag(fake, 10, 256, fake, 4, bad_bits, 2, 64, fake, s) == 1
     # misaligned device pointers are refused before any launch
     odd = ctypes.c_void_p(0x1008)
     assert lib.bitsmoe_gram(odd, 1, 64, 64, fake, s) == 1
