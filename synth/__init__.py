@@ -36,7 +36,7 @@ import numpy as np
 __all__ = [
     "ProjSpec", "ConfigSpec", "CONFIGS", "Projection", "make_projection",
     "make_layer", "expert_weights", "calibration_input", "f32_to_bf16_bits",
-    "bf16_bits_to_f32", "as_f64", "random_rows",
+    "bf16_bits_to_f32", "as_f64", "random_rows", "TOP_K", "routing",
 ]
 
 
@@ -216,6 +216,42 @@ def _layer_input_f32(cfg: ConfigSpec, seed: int) -> np.ndarray:
         cols = np.sort(g.choice(d_in, size=n_out, replace=False))
         X[:, cols] *= np.float32(cfg.outlier_scale)
     return X
+
+
+# Routed experts per token of the model families the configurations stand in
+# for (Qwen3-30B-A3B: 8 of 128; Mixtral-8x7B: 2 of 8; DeepSeek-V3: 8 of 256).
+TOP_K = {"tiny": 2, "qwen_gate": 8, "qwen_layer": 8, "mixtral": 2, "dsv3": 8}
+
+
+def routing(cfg: ConfigSpec, X: Optional[np.ndarray] = None, seed: int = 0):
+    """Synthetic top-k routing of the calibration tokens of a layer.
+
+    A random linear router R ~ N(0, 1/d_in) [d_in][E] scores every token of
+    the layer input (logits = X R in fp32); each token goes to its TOP_K
+    highest-scoring experts with weights softmax-normalized over those k.
+    Returned grouped by expert, tokens ascending within an expert:
+    (offsets int64 [E+1], tokens int32 [n k], weights float32 [n k]).
+    """
+    if X is None:
+        X = _decode32(_encode(_layer_input_f32(cfg, seed), cfg.dtype), cfg.dtype)
+    else:
+        X = _decode32(X, cfg.dtype)
+    n, d_in = X.shape
+    E, k = cfg.E, TOP_K[cfg.name]
+    g = _rng(seed, cfg.config_id, 98, 0)
+    R = (g.standard_normal((d_in, E), dtype=np.float32) / np.float32(math.sqrt(d_in)))
+    logits = X @ R
+    top = np.argsort(-logits, axis=1, kind="stable")[:, :k]
+    z = np.take_along_axis(logits, top, axis=1).astype(np.float64)
+    w = np.exp(z - z.max(axis=1, keepdims=True))
+    w = (w / w.sum(axis=1, keepdims=True)).astype(np.float32)
+    tok = np.repeat(np.arange(n, dtype=np.int32), k)
+    ex = top.reshape(-1)
+    order = np.lexsort((tok, ex))
+    counts = np.bincount(ex, minlength=E)
+    offsets = np.zeros(E + 1, dtype=np.int64)
+    offsets[1:] = np.cumsum(counts)
+    return offsets, tok[order], w.reshape(-1)[order]
 
 
 def calibration_input(cfg: ConfigSpec, pname: str, seed: int = 0) -> np.ndarray:
