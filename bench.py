@@ -202,6 +202,36 @@ def surrogate_report(cfg, layer, res, dev_inputs, bm, pipeline) -> dict:
             "widths_chosen": {str(k): v for k, v in hist.items()}, "projections": parts}
 
 
+def routed_report(cfg, layer, dev_inputs, bm, pipeline) -> dict:
+    """The hot path with routed per-expert calibration Grams (synthetic top-k
+    router) for the projections that read the layer input, once each."""
+    import numpy as np
+    import torch
+    import synth
+    names = ("gram_routed", "score_routed_dgen", "score_routed_gemm")
+    for n in names:
+        bm.kernel_time(n)
+    parts, Hs = [], None
+    for p, inp in zip(layer, dev_inputs):
+        if p.spec.input != "x":
+            continue
+        if Hs is None:
+            Xh = inp["X"].view(torch.int16).cpu().numpy().view(np.uint16) if cfg.dtype == "bf16" \
+                else inp["X"].cpu().numpy()
+            routing = synth.routing(cfg, Xh)
+        bm.timing(True)
+        rr = pipeline.quantize_projection_routed(inp["W"], inp["X"], routing, inp["r"], inp["bits"],
+                                                 inp["group"], inp["budget"], Hs=Hs)
+        torch.cuda.synchronize()
+        bm.timing(False)
+        Hs = rr.H
+        parts.append({"projection": p.spec.name, "gpu_ms": round(rr.times["gpu_ms"], 4),
+                      "host_eig_ms": round(rr.times["host_eig_ms"], 2),
+                      "host_ilp_ms": round(rr.times["host_ilp_ms"], 2)})
+    kt = {n: round(bm.kernel_time(n)[0], 4) for n in names}
+    return {"top_k": synth.TOP_K.get(cfg.name), "projections": parts, "kernel_ms": kt}
+
+
 def inspace_report(layer, res, dev_inputs, bm, pipeline) -> dict:
     """The paper's input-space construction of the gate/up projections (basis
     from M_in = sum W_e^T W_e, diagonal-approximation loss), once each, on the
@@ -365,6 +395,7 @@ def main(argv=None) -> int:
     # reported beside the exact path with its agreement with the exact costs.
     sur = surrogate_report(cfg, layer, res, dev_inputs, bm, pipeline)
     insp = inspace_report(layer, res, dev_inputs, bm, pipeline)
+    rout = routed_report(cfg, layer, dev_inputs, bm, pipeline)
 
     value = float(np.median(gpu_ms))
     traffic = measured_traffic(args.config)
@@ -402,6 +433,7 @@ def main(argv=None) -> int:
     }
     out["surrogate"] = sur
     out["inspace"] = insp
+    out["routed"] = rout
     if not args.no_cpu_baseline and not args.device_inputs:
         log("timing the fp64 oracle on a sample")
         out["cpu_baseline"] = cpu_baseline(cfg, layer)

@@ -35,6 +35,9 @@
  *   bitsmoe_project_in        C_e = Phi_r^T W_e^T (units W_e phi_k) (device)
  *   bitsmoe_basis_importance  beta_k = phi_k^T H phi_k             (device)
  *   bitsmoe_score_diag        L = beta_k ||c - Q_b(c)||^2          (device)
+ * and the paper's per-expert, routing-weighted calibration Grams:
+ *   bitsmoe_gram_routed       H_e = (1/n) sum_t g_te x_t x_t^T     (device)
+ *   bitsmoe_score_routed      L = delta H_e delta^T                (device)
  *
  * Conventions shared by every call:
  *  - Pointers named *_dev are device memory on the current HIP device;
@@ -271,6 +274,41 @@ bitsmoe_status bitsmoe_basis_importance(const float* Vt_dev, int64_t r, int64_t 
 bitsmoe_status bitsmoe_score_diag(const float* C_dev, int64_t units, int64_t d,
                                   const float* beta_dev, int64_t r, const int* bits_host, int nbits,
                                   int group, float* L_dev, void* stream);
+
+/*
+ * Routing-affinity-weighted calibration Gram of every expert (App. B.2, Eq.
+ * app_affinity_gram: H = X Diag(g) X^T over the tokens routed to the expert):
+ *     H_e = (1/n) sum_{i in [offsets[e], offsets[e+1])} w_i x_{rows[i]} x_{rows[i]}^T
+ * with the same 1/n as bitsmoe_gram (so, with every token's weights summing
+ * to 1, sum_e H_e is the shared Gram).  The routed rows are gathered on the
+ * device (the weighted side split into bf16 hi + lo) and all experts' Grams
+ * run in one batched symmetric matrix-core launch, reduced in fp64 in a
+ * fixed order.
+ *   X_dev         [n][d] of type xt (calibration rows)
+ *   offsets_host  [E + 1] non-decreasing, offsets[0] = 0 (host)
+ *   rows_host     [offsets[E]] row of X of each routed entry, in [0, n) (host)
+ *   weights_host  [offsets[E]] routing weight of each entry, finite, >= 0 (host)
+ *   H_dev         [E][d][d] fp32 output, full symmetric
+ * The host tables are copied to the device before the call returns (the
+ * call synchronizes `stream` for that).  Shape rules: d % 64 == 0,
+ * 1 <= E <= 65535.
+ */
+bitsmoe_status bitsmoe_gram_routed(const void* X_dev, bitsmoe_dtype xt, int64_t n, int64_t d,
+                                   int64_t E, const int64_t* offsets_host, const int32_t* rows_host,
+                                   const float* weights_host, float* H_dev, void* stream);
+
+/*
+ * bitsmoe_score with one H per expert: the units are grouped by expert,
+ * units_per_h consecutive units per H, and unit u is scored against
+ * H_dev[u / units_per_h] (the routed Grams of bitsmoe_gram_routed).
+ *   H_dev  [units / units_per_h][d][d] fp32 symmetric
+ * Shape rules as bitsmoe_score, plus units % units_per_h == 0 and
+ * units_per_h * nbits % 256 == 0 (every 256-row tile of error rows belongs
+ * to one expert).
+ */
+bitsmoe_status bitsmoe_score_routed(const float* C_dev, int64_t units, int64_t d, const float* H_dev,
+                                    int64_t units_per_h, const int* bits_host, int nbits, int group,
+                                    float* L_dev, void* stream);
 
 /*
  * The paper's surrogate cost table (App. B.3-B.4, Theorem

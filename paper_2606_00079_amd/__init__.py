@@ -41,6 +41,7 @@ EXPORTS = [
     "bitsmoe_release", "bitsmoe_version", "bitsmoe_timing", "bitsmoe_kernel_time",
     "bitsmoe_surrogate", "bitsmoe_surrogate_budget", "bitsmoe_gram_experts_in",
     "bitsmoe_project_in", "bitsmoe_basis_importance", "bitsmoe_score_diag",
+    "bitsmoe_gram_routed", "bitsmoe_score_routed",
 ]
 # Candidate widths of the surrogate table, in column order.
 SURROGATE_WIDTHS = (0, 1, 2, 3, 4, 6, 8, 16)
@@ -94,6 +95,8 @@ def lib() -> ctypes.CDLL:
     L.bitsmoe_project_in.argtypes = [vp, vp, i32, i64, i64, i64, i64, vp, vp]
     L.bitsmoe_basis_importance.argtypes = [vp, i64, i64, vp, vp, vp]
     L.bitsmoe_score_diag.argtypes = [vp, i64, i64, vp, i64, vp, i32, i32, vp, vp]
+    L.bitsmoe_gram_routed.argtypes = [vp, i32, i64, i64, i64, vp, vp, vp, vp, vp]
+    L.bitsmoe_score_routed.argtypes = [vp, i64, i64, vp, i64, vp, i32, i32, vp, vp]
     L.bitsmoe_set_lapack.argtypes = [ctypes.c_char_p]
     L.bitsmoe_timing.argtypes = [i32]
     L.bitsmoe_kernel_time.argtypes = [ctypes.c_char_p, vp, vp]
@@ -273,6 +276,43 @@ def score_diag(C, beta, bits: Sequence[int], group: int, out=None):
         out = torch.empty((units, len(b)), dtype=torch.float32, device=C.device)
     _check(lib().bitsmoe_score_diag(_dev(C, "C"), units, d, _dev(beta, "beta"), beta.shape[0], bp,
                                     len(b), group, _dev(out, "L"), _stream()), "score_diag")
+    return out
+
+
+def gram_routed(X, offsets, rows, weights, out=None):
+    """Per-expert routed Grams H_e = (1/n) sum w x x^T -> fp32 [E][d][d]; the
+    routing tables (offsets [E+1], rows [nnz], weights [nnz]) are host arrays."""
+    torch = _torch()
+    n, d = X.shape
+    off = np.ascontiguousarray(np.asarray(offsets, dtype=np.int64))
+    rw = np.ascontiguousarray(np.asarray(rows, dtype=np.int32))
+    wt = np.ascontiguousarray(np.asarray(weights, dtype=np.float32))
+    E = off.shape[0] - 1
+    if rw.shape[0] < off[-1] or wt.shape[0] < off[-1]:
+        raise ValueError("rows and weights need offsets[-1] entries")
+    if out is None:
+        out = torch.empty((E, d, d), dtype=torch.float32, device=X.device)
+    _check(lib().bitsmoe_gram_routed(_dev(X, "X"), _dtype_code(X, "X"), n, d, E,
+                                     off.ctypes.data_as(ctypes.c_void_p),
+                                     rw.ctypes.data_as(ctypes.c_void_p),
+                                     wt.ctypes.data_as(ctypes.c_void_p), _dev(out, "H"),
+                                     _stream()), "gram_routed")
+    return out
+
+
+def score_routed(C, Hs, units_per_h: int, bits: Sequence[int], group: int, out=None):
+    """Loss table with one H per block of units_per_h units -> fp32 [units][len(bits)]."""
+    torch = _torch()
+    units, d = C.shape
+    if C.dtype != torch.float32 or Hs.dtype != torch.float32:
+        raise TypeError("C and H must be float32")
+    if Hs.dim() != 3 or tuple(Hs.shape[1:]) != (d, d) or Hs.shape[0] * units_per_h != units:
+        raise ValueError("Hs must be [units / units_per_h][d][d]")
+    b, bp = _bits_arr(bits)
+    if out is None:
+        out = torch.empty((units, len(b)), dtype=torch.float32, device=C.device)
+    _check(lib().bitsmoe_score_routed(_dev(C, "C"), units, d, _dev(Hs, "H"), units_per_h, bp, len(b),
+                                      group, _dev(out, "L"), _stream()), "score_routed")
     return out
 
 

@@ -102,6 +102,9 @@ struct Problem {
   int symmetric;     // 1: only tiles with tm <= tn are launched (gridDim.x = T(T+1)/2)
   int group_n;       // column tiles per ordering group (non-symmetric; paired: per
                      // group_n column tiles, all pairs of each)
+  int64_t a_batch_rows;  // paired only: if > 0, the A operand of column tile tn is
+                         // batch (tn * BN) / a_batch_rows (stride a.bstride): one A per
+                         // block of B rows (a multiple of BN)
 };
 
 // XCD-contiguous logical id of the linear workgroup id t (of n in total).
@@ -287,7 +290,8 @@ struct TriWalk {
   __device__ __forceinline__ void init(const Problem& p, int64_t z, int tm, int tn, int BM, int BN,
                                        int64_t q0, bool up, int64_t turn_at, int64_t qt) {
     PassBases a, b;
-    a.init(p.a, z, tm, BM);
+    const int64_t za = p.a_batch_rows > 0 ? static_cast<int64_t>(tn) * BN / p.a_batch_rows : z;
+    a.init(p.a, za, tm, BM);
     b.init(p.b, z, tn, BN);
     ba = reinterpret_cast<const uint16_t*>(uniform64(reinterpret_cast<int64_t>(a.q0)));
     bb = reinterpret_cast<const uint16_t*>(uniform64(reinterpret_cast<int64_t>(b.q0)));

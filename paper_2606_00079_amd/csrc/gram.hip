@@ -2,6 +2,7 @@
 // M = sum_e W_e W_e^T, both as symmetric split-K matrix-core GEMMs whose fp32
 // partial tiles are added in fp64 in a fixed order (deterministic).
 #include <algorithm>
+#include <cmath>
 #include <cstdio>
 #include <string>
 
@@ -65,15 +66,65 @@ __global__ __launch_bounds__(256) void split_kernel(const float* __restrict__ W,
   }
 }
 
-// Stores each wave's fp32 accumulators into partials[split][tile][GT][GT].
+// Routed rows of expert e = blockIdx.z, in the K-tiled layout of the
+// symmetric GEMM (rows = channels, K = the expert's tokens, zero-padded to
+// npad): the A side holds x_{rows[i]} (fp32 input split into bf16 hi + lo),
+// the B side w_i x_{rows[i]} split into hi + lo.  Routing entries are
+// checked on the host (rows in [0, n)).
+template <bool F32>
+__global__ __launch_bounds__(256) void routed_gather_kernel(
+    const void* __restrict__ X, int64_t d, const int64_t* __restrict__ off,
+    const int32_t* __restrict__ rows, const float* __restrict__ w, int64_t npad, int64_t d_pad,
+    uint16_t* __restrict__ a_hi, uint16_t* __restrict__ a_lo, uint16_t* __restrict__ b_hi,
+    uint16_t* __restrict__ b_lo) {
+  __shared__ float tile[64][65];
+  __shared__ float wt[64];
+  const int64_t e = blockIdx.z;
+  const int64_t i0 = static_cast<int64_t>(blockIdx.x) * 64;  // token block of the expert
+  const int64_t c0 = static_cast<int64_t>(blockIdx.y) * 64;  // channel block
+  const int64_t o0 = off[e], ne = off[e + 1] - o0;
+  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+  if (ty == 0) wt[tx] = (i0 + tx < ne) ? w[o0 + i0 + tx] : 0.0f;
+  for (int i = ty; i < 64; i += 4) {
+    const int64_t t = i0 + i, c = c0 + tx;
+    float v = 0.0f;
+    if (t < ne && c < d) {
+      const int64_t row = rows[o0 + t];
+      if (F32)
+        v = static_cast<const float*>(X)[row * d + c];
+      else
+        v = bf16_to_f32(static_cast<const uint16_t*>(X)[row * d + c]);
+    }
+    tile[i][tx] = v;
+  }
+  __syncthreads();
+  const int64_t base = e * d_pad * npad;
+  for (int i = ty; i < 64; i += 4) {
+    const int64_t c = c0 + i, t = i0 + tx;
+    if (c < d) {
+      const float v = tile[tx][i];
+      const int64_t o = base + gemm::tiled_offset(c, t, npad, GT);
+      const uint16_t h = f32_to_bf16(v);
+      a_hi[o] = h;
+      if (F32) a_lo[o] = f32_to_bf16(v - bf16_to_f32(h));
+      const float wv = wt[tx] * v;
+      const uint16_t hb = f32_to_bf16(wv);
+      b_hi[o] = hb;
+      b_lo[o] = f32_to_bf16(wv - bf16_to_f32(hb));
+    }
+  }
+}
+
+// Stores each wave's fp32 accumulators into partials[batch][split][tile][GT][GT].
 struct PartialStore {
   float* part;
   int64_t ntiles;     // tiles in the upper triangle
   int ntiles_side;    // tiles per side
+  int64_t zstride;    // elements per batch (splits * ntiles * GT * GT)
   template <class F>
   __device__ void operator()(F& f, const gemm::StageLds&) const {
     const int64_t t = (static_cast<int64_t>(f.tm) * (2 * ntiles_side - f.tm + 1)) / 2 + (f.tn - f.tm);
-    float* base = part + (static_cast<int64_t>(f.ks) * ntiles + t) * GT * GT;
+    float* base = part + f.z * zstride + (static_cast<int64_t>(f.ks) * ntiles + t) * GT * GT;
 #pragma unroll
     for (int mi = 0; mi < F::FM; ++mi)
 #pragma unroll
@@ -110,6 +161,9 @@ __global__ __launch_bounds__(256) void sym_reduce_kernel(const float* __restrict
                                                          int64_t ntiles, int T, int64_t d,
                                                          double scale, OutT* __restrict__ out) {
   __shared__ double tile[RB_ROWS][RB_COLS + 1];
+  // batch blockIdx.y: its own partials and output matrix
+  part += static_cast<int64_t>(blockIdx.y) * splits * ntiles * GT * GT;
+  out += static_cast<int64_t>(blockIdx.y) * d * d;
   constexpr int SR = GT / RB_ROWS, SC = GT / RB_COLS;  // blocks per tile edge
   const int64_t t = blockIdx.x / (SR * SC);            // upper-triangle tile
   const int sb = static_cast<int>(blockIdx.x % (SR * SC));
@@ -150,8 +204,20 @@ __global__ __launch_bounds__(256) void sym_reduce_kernel(const float* __restrict
   }
 #pragma unroll
   for (int j = 0; j < 4; ++j) acc[j] *= scale;
+  if (tm == tn) {
+    // a diagonal tile holds both triangles; its upper one is written and
+    // mirrored, so the output is exactly symmetric even when the two GEMM
+    // operands differ in rounding (the routed Gram's weighted side)
+    const int64_t row = gi0 + r;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int64_t col = gj0 + 4 * cq + j;
+      if (col >= row) out[row * d + col] = static_cast<OutT>(acc[j]);
+      if (col > row) out[col * d + row] = static_cast<OutT>(acc[j]);
+    }
+    return;
+  }
   store4(out + (gi0 + r) * d + gj0 + 4 * cq, acc);
-  if (tm == tn) return;  // a diagonal tile holds both triangles itself
 #pragma unroll
   for (int j = 0; j < 4; ++j) tile[r][4 * cq + j] = acc[j];
   __syncthreads();
@@ -163,9 +229,11 @@ __global__ __launch_bounds__(256) void sym_reduce_kernel(const float* __restrict
 
 // Launches the symmetric split-K GEMM of p (tiles/splits already set) and
 // reduces it into out.
+// `batches` independent problems (blockIdx.z, operand strides bstride) write
+// batches consecutive d x d outputs.
 template <typename OutT>
 bitsmoe_status run_symmetric(gemm::Problem p, int64_t d, double scale, OutT* out, void* stream,
-                             const char* name) {
+                             const char* name, int64_t batches = 1) {
   hipStream_t s = static_cast<hipStream_t>(stream);
   const int T = static_cast<int>((d + GT - 1) / GT);
   const int64_t ntiles = static_cast<int64_t>(T) * (T + 1) / 2;
@@ -175,15 +243,18 @@ bitsmoe_status run_symmetric(gemm::Problem p, int64_t d, double scale, OutT* out
   // least four K tiles per workgroup.
   const int64_t kt = p.ktiles;  // in units of gemm::BK
   int64_t splits = (kt * BK + 4095) / 4096;
-  splits = std::max<int64_t>(splits, (768 + ntiles - 1) / ntiles);
+  splits = std::max<int64_t>(splits, (768 + ntiles * batches - 1) / (ntiles * batches));
   splits = std::min<int64_t>(splits, std::max<int64_t>(1, kt / 4));
   p.splits = static_cast<int>(splits);
+  if (batches > 65535) return fail(BITSMOE_ERR_SHAPE, std::string(name) + ": too many batches");
   bitsmoe_status st;
+  const int64_t zstride = splits * ntiles * GT * GT;
   float* part = static_cast<float*>(
-      scratch(kScratchPart, static_cast<size_t>(splits) * ntiles * GT * GT * sizeof(float), stream, &st));
+      scratch(kScratchPart, static_cast<size_t>(batches * zstride) * sizeof(float), stream, &st));
   if (!part) return st;
-  PartialStore epi{part, ntiles, T};
-  dim3 grid(static_cast<unsigned>(ntiles), static_cast<unsigned>(splits), 1);
+  PartialStore epi{part, ntiles, T, zstride};
+  dim3 grid(static_cast<unsigned>(ntiles), static_cast<unsigned>(splits),
+            static_cast<unsigned>(batches));
   {
     KernelTimer timer(name, stream);
     hipLaunchKernelGGL((gemm::gemm_nt_kernel<GT, GT, 32, 4, PartialStore>), grid,
@@ -191,7 +262,8 @@ bitsmoe_status run_symmetric(gemm::Problem p, int64_t d, double scale, OutT* out
   }
   BITSMOE_LAUNCH_CHECK("gram: gemm launch");
   constexpr int NB = (GT / RB_ROWS) * (GT / RB_COLS);
-  hipLaunchKernelGGL((sym_reduce_kernel<OutT>), dim3(static_cast<unsigned>(ntiles * NB)),
+  hipLaunchKernelGGL((sym_reduce_kernel<OutT>),
+                     dim3(static_cast<unsigned>(ntiles * NB), static_cast<unsigned>(batches)),
                      dim3(256), 0, s, part, p.splits, ntiles, T, d, scale, out);
   BITSMOE_LAUNCH_CHECK("gram: reduce launch");
   return BITSMOE_OK;
@@ -325,6 +397,87 @@ extern "C" bitsmoe_status bitsmoe_gram_experts(const void* W_dev, bitsmoe_dtype 
   }
   p.ktiles = static_cast<int64_t>(p.passes) * E * d_in / BK;
   bitsmoe_status st = run_symmetric<double>(p, d_out, 1.0, M_dev, stream, "gram_experts");
+  if (st != BITSMOE_OK) return st;
+  return ok();
+}
+
+extern "C" bitsmoe_status bitsmoe_gram_routed(const void* X_dev, bitsmoe_dtype xt, int64_t n,
+                                              int64_t d, int64_t E, const int64_t* offsets_host,
+                                              const int32_t* rows_host, const float* weights_host,
+                                              float* H_dev, void* stream) {
+  bitsmoe_status st = check_rows(X_dev, H_dev, xt, n, d, "gram_routed");
+  if (st != BITSMOE_OK) return st;
+  if (!offsets_host || !rows_host || !weights_host)
+    return fail(BITSMOE_ERR_ARG, "gram_routed: null pointer");
+  if (E <= 0 || E > 65535) return fail(BITSMOE_ERR_ARG, "gram_routed: experts outside 1..65535");
+  if (offsets_host[0] != 0) return fail(BITSMOE_ERR_ARG, "gram_routed: offsets[0] must be 0");
+  int64_t nmax = 0;
+  for (int64_t e = 0; e < E; ++e) {
+    const int64_t c = offsets_host[e + 1] - offsets_host[e];
+    if (c < 0) return fail(BITSMOE_ERR_ARG, "gram_routed: offsets must not decrease");
+    nmax = std::max(nmax, c);
+  }
+  const int64_t total = offsets_host[E];
+  for (int64_t i = 0; i < total; ++i) {
+    if (rows_host[i] < 0 || rows_host[i] >= n)
+      return fail(BITSMOE_ERR_ARG, "gram_routed: row index outside [0, n)");
+    if (!(weights_host[i] >= 0.0f) || !std::isfinite(weights_host[i]))
+      return fail(BITSMOE_ERR_ARG, "gram_routed: weights must be finite and non-negative");
+  }
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const bool f32 = xt == BITSMOE_F32;
+  const int64_t npad = std::max<int64_t>(gemm::kKAlign,
+                                         (nmax + gemm::kKAlign - 1) / gemm::kKAlign * gemm::kKAlign);
+  const int64_t d_pad = (d + GT - 1) / GT * GT;
+  const int64_t per = d_pad * npad;  // elements per expert and operand
+  // routing tables on the device: offsets [E+1], rows [total], weights [total]
+  const size_t tbytes = static_cast<size_t>(E + 1) * 8 + static_cast<size_t>(total) * 8 + 16;
+  char* tab = static_cast<char*>(scratch(kScratchMisc, tbytes, stream, &st));
+  if (!tab) return st;
+  int64_t* off_d = reinterpret_cast<int64_t*>(tab);
+  int32_t* rows_d = reinterpret_cast<int32_t*>(off_d + E + 1);
+  float* w_d = reinterpret_cast<float*>(rows_d + total + (total & 1));
+  hipError_t he = hipMemcpyAsync(off_d, offsets_host, (E + 1) * 8, hipMemcpyHostToDevice, s);
+  if (he == hipSuccess && total > 0)
+    he = hipMemcpyAsync(rows_d, rows_host, total * 4, hipMemcpyHostToDevice, s);
+  if (he == hipSuccess && total > 0)
+    he = hipMemcpyAsync(w_d, weights_host, total * 4, hipMemcpyHostToDevice, s);
+  if (he == hipSuccess) he = hipStreamSynchronize(s);  // the host tables may go away after return
+  if (he != hipSuccess) return device_error("gram_routed: routing table copy", he);
+  uint16_t* A = static_cast<uint16_t*>(scratch(kScratchA, (f32 ? 2 : 1) * E * per * 2, stream, &st));
+  if (!A) return st;
+  uint16_t* B = static_cast<uint16_t*>(scratch(kScratchB, 2 * E * per * 2, stream, &st));
+  if (!B) return st;
+  uint16_t* a_lo = f32 ? A + E * per : nullptr;
+  uint16_t* b_lo = B + E * per;
+  dim3 tg(static_cast<unsigned>(npad / 64), static_cast<unsigned>((d + 63) / 64),
+          static_cast<unsigned>(E));
+  if (f32)
+    hipLaunchKernelGGL(routed_gather_kernel<true>, tg, dim3(256), 0, s, X_dev, d, off_d, rows_d, w_d,
+                       npad, d_pad, A, a_lo, B, b_lo);
+  else
+    hipLaunchKernelGGL(routed_gather_kernel<false>, tg, dim3(256), 0, s, X_dev, d, off_d, rows_d,
+                       w_d, npad, d_pad, A, a_lo, B, b_lo);
+  BITSMOE_LAUNCH_CHECK("gram_routed: gather launch");
+  gemm::Problem p{};
+  p.a.rows = p.b.rows = d_pad;
+  p.a.kstep = p.b.kstep = static_cast<int64_t>(GT) * gemm::kTileK;
+  p.a.rtile = p.b.rtile = static_cast<int64_t>(GT) * npad;
+  p.a.bstride = p.b.bstride = per;
+  p.segs = 1;
+  p.kseg = npad;
+  if (f32) {
+    p.passes = 3;  // x_hi (wx)_hi + x_hi (wx)_lo + x_lo (wx)_hi
+    p.a.pass[0] = A;    p.b.pass[0] = B;
+    p.a.pass[1] = A;    p.b.pass[1] = b_lo;
+    p.a.pass[2] = a_lo; p.b.pass[2] = B;
+  } else {
+    p.passes = 2;  // x (wx)_hi + x (wx)_lo, x exact in bf16
+    p.a.pass[0] = A; p.b.pass[0] = B;
+    p.a.pass[1] = A; p.b.pass[1] = b_lo;
+  }
+  p.ktiles = p.passes * npad / BK;
+  st = run_symmetric<float>(p, d, 1.0 / static_cast<double>(n), H_dev, stream, "gram_routed", E);
   if (st != BITSMOE_OK) return st;
   return ok();
 }

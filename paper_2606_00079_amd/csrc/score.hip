@@ -58,6 +58,8 @@ __device__ __forceinline__ int exponent_above(float v) {
 __global__ __launch_bounds__(256) void habsmax_kernel(const float* __restrict__ H, int64_t d,
                                                       float* __restrict__ partial) {
   __shared__ float red[256];
+  H += static_cast<int64_t>(blockIdx.y) * d * d;  // one H per blockIdx.y
+  partial += static_cast<int64_t>(blockIdx.y) * kAbsMaxBlocks;
   float m = 0.0f;
   const int64_t n4 = d * d / 4;
   for (int64_t idx = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; idx < n4;
@@ -86,6 +88,14 @@ __global__ __launch_bounds__(256) void hoff_kernel(const float* __restrict__ H, 
                                                    uint16_t* __restrict__ Hoff,
                                                    float* __restrict__ hdiag, int* __restrict__ hexp) {
   __shared__ int sF;
+  {  // one H per blockIdx.y
+    const int64_t z = blockIdx.y;
+    H += z * d * d;
+    partial += z * kAbsMaxBlocks;
+    Hoff += z * d_pad * d;
+    hdiag += z * d;
+    hexp += z;
+  }
   if (threadIdx.x < 64) {  // wave 0 reduces the partial maxima
     float m = 0.0f;
     for (int b = threadIdx.x; b < kAbsMaxBlocks; b += 64) m = fmaxf(m, partial[b]);
@@ -144,7 +154,7 @@ __global__ __launch_bounds__(256) void dgen_kernel(const float* __restrict__ C, 
                                                    uint16_t* __restrict__ D,
                                                    float* __restrict__ diag, int* __restrict__ uexp,
                                                    const float* __restrict__ w = nullptr,
-                                                   int64_t wperiod = 1) {
+                                                   int64_t wperiod = 1, int64_t hd_upe = 0) {
   const int lane = threadIdx.x & 63;
   const int64_t u = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
   if (u >= units) return;  // whole wave exits together
@@ -154,6 +164,7 @@ __global__ __launch_bounds__(256) void dgen_kernel(const float* __restrict__ C, 
 #pragma unroll
   for (int j = 0; j < NB; ++j) dacc[j] = 0.0f;
   const float* crow = C + u * d;
+  if (hd_upe > 0) hdiag += (u / hd_upe) * d;  // one H per block of hd_upe units
 
   // lane's 8 entries of the 512-entry chunk at k0 (zeros past the end)
   auto load8 = [&](int64_t k0, float (&c)[8]) {
@@ -388,18 +399,21 @@ struct RowDot {
 };
 
 // L = diagonal term + (sum of the tile partials, in tile order) * 2^-(2 E_u + F).
+// With one H per block of upe units (upe > 0), the H exponent is that H's.
 __global__ __launch_bounds__(256) void finalize_kernel(const float* __restrict__ diag,
                                                        const float* __restrict__ part, int64_t R,
                                                        int tiles_m, int nb,
                                                        const int* __restrict__ uexp,
                                                        const int* __restrict__ hexp,
-                                                       float* __restrict__ L) {
+                                                       float* __restrict__ L, int64_t upe = 0) {
   const int64_t row = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
   if (row >= R) return;
   const float* p = part + row * tiles_m;
   float s = 0.0f;
   for (int t = 0; t < tiles_m; ++t) s += p[t];
-  L[row] = diag[row] + ldexpf(s, -(2 * uexp[row / nb] + *hexp));
+  const int64_t u = row / nb;
+  const int F = hexp[upe > 0 ? u / upe : 0];
+  L[row] = diag[row] + ldexpf(s, -(2 * uexp[u] + F));
 }
 
 // Raw rows for the surrogate's activation-aware importance (the eviction
@@ -561,6 +575,7 @@ __global__ __launch_bounds__(256) void quadform_finalize_kernel(const float* __r
 // (error rows for the score, raw rows for the surrogate) against H.
 struct LossTable {
   int64_t d, R, units;
+  int64_t nh;        // number of H matrices (one per block of units / nh units)
   int tiles_m;
   int64_t tiles_n, d_pad, R_pad;
   uint16_t* Hoff;
@@ -569,16 +584,17 @@ struct LossTable {
   float* diag;   // [R]
   int* uexp;     // [units]
   float* hpart;  // [kAbsMaxBlocks]
-  int* hexp;     // [1]
+  int* hexp;     // [nh]
   float* rstats; // [3 units] (surrogate only)
   float* part;   // [R][tiles_m]
 };
 
 bitsmoe_status loss_table_setup(int64_t d, int64_t R, int64_t units, bool row_stats, void* stream,
-                                const char* who, LossTable* t) {
+                                const char* who, LossTable* t, int64_t nh = 1) {
   t->d = d;
   t->R = R;
   t->units = units;
+  t->nh = nh;
   t->tiles_m = static_cast<int>((d + SBM - 1) / SBM);
   t->tiles_n = (R + SBN - 1) / SBN;
   if (gemm::paired_workgroups(t->tiles_m, t->tiles_n) > INT32_MAX || (R + 255) / 256 > INT32_MAX)
@@ -587,20 +603,21 @@ bitsmoe_status loss_table_setup(int64_t d, int64_t R, int64_t units, bool row_st
   t->d_pad = t->tiles_m * static_cast<int64_t>(SBM);
   t->R_pad = t->tiles_n * static_cast<int64_t>(SBN);
   bitsmoe_status st;
-  t->Hoff = static_cast<uint16_t*>(scratch(kScratchA, t->d_pad * d * 2, stream, &st));
+  t->Hoff = static_cast<uint16_t*>(scratch(kScratchA, nh * t->d_pad * d * 2, stream, &st));
   if (!t->Hoff) return st;
-  // small tables: diag(H) [d], diagonal terms [R], unit exponents [units],
-  // partial maxima of |H_off| [kAbsMaxBlocks], the H_off exponent [1],
-  // row statistics [3 units]
-  const int64_t small_words = d + R + units + kAbsMaxBlocks + 1 + (row_stats ? 3 * units : 0);
+  // small tables: diag(H) [nh][d], diagonal terms [R], unit exponents
+  // [units], partial maxima of |H_off| [nh][kAbsMaxBlocks], the H_off
+  // exponents [nh], row statistics [3 units]
+  const int64_t small_words =
+      nh * d + R + units + nh * kAbsMaxBlocks + nh + (row_stats ? 3 * units : 0);
   float* small = static_cast<float*>(scratch(kScratchMisc, small_words * sizeof(float), stream, &st));
   if (!small) return st;
   t->hdiag = small;
-  t->diag = t->hdiag + d;
+  t->diag = t->hdiag + nh * d;
   t->uexp = reinterpret_cast<int*>(t->diag + R);
   t->hpart = reinterpret_cast<float*>(t->uexp + units);
-  t->hexp = reinterpret_cast<int*>(t->hpart + kAbsMaxBlocks);
-  t->rstats = row_stats ? reinterpret_cast<float*>(t->hexp + 1) : nullptr;
+  t->hexp = reinterpret_cast<int*>(t->hpart + nh * kAbsMaxBlocks);
+  t->rstats = row_stats ? reinterpret_cast<float*>(t->hexp + nh) : nullptr;
   t->D = static_cast<uint16_t*>(scratch(kScratchD, t->R_pad * d * 2, stream, &st));
   if (!t->D) return st;
   t->part = static_cast<float*>(scratch(kScratchPart, R * t->tiles_m * sizeof(float), stream, &st));
@@ -610,10 +627,11 @@ bitsmoe_status loss_table_setup(int64_t d, int64_t R, int64_t units, bool row_st
 
 // H -> scaled fp16 H_off and diag(H).
 bitsmoe_status loss_table_hoff(const float* H_dev, const LossTable& t, hipStream_t s, const char* who) {
-  hipLaunchKernelGGL(habsmax_kernel, dim3(kAbsMaxBlocks), dim3(256), 0, s, H_dev, t.d, t.hpart);
+  const unsigned nh = static_cast<unsigned>(t.nh);
+  hipLaunchKernelGGL(habsmax_kernel, dim3(kAbsMaxBlocks, nh), dim3(256), 0, s, H_dev, t.d, t.hpart);
   BITSMOE_LAUNCH_CHECK(who);
   const unsigned hb = static_cast<unsigned>(std::min<int64_t>((t.d_pad * t.d + 255) / 256, 16384));
-  hipLaunchKernelGGL(hoff_kernel, dim3(hb), dim3(256), 0, s, H_dev, t.d, t.d_pad, t.hpart, t.Hoff,
+  hipLaunchKernelGGL(hoff_kernel, dim3(hb, nh), dim3(256), 0, s, H_dev, t.d, t.d_pad, t.hpart, t.Hoff,
                      t.hdiag, t.hexp);
   BITSMOE_LAUNCH_CHECK(who);
   return BITSMOE_OK;
@@ -621,7 +639,10 @@ bitsmoe_status loss_table_hoff(const float* H_dev, const LossTable& t, hipStream
 
 // part[row][tm] = sum over the 256-wide tile tm of H rows of the
 // off-diagonal form of row `row` of D (paired upper-triangle schedule).
-bitsmoe_status loss_table_gemm(const LossTable& t, void* stream, const char* timer, const char* who) {
+// With t.nh > 1, column tile tn of D multiplies H number (tn * 256) /
+// a_batch_rows (every block of a_batch_rows rows of D belongs to one H).
+bitsmoe_status loss_table_gemm(const LossTable& t, void* stream, const char* timer, const char* who,
+                               int64_t a_batch_rows = 0) {
   hipStream_t s = static_cast<hipStream_t>(stream);
   gemm::Problem p{};
   static_assert(SKB == gemm::kTileK, "the K-tiled operands need the kernel's K step");
@@ -629,6 +650,8 @@ bitsmoe_status loss_table_gemm(const LossTable& t, void* stream, const char* tim
   p.a.rows = t.d_pad;
   p.a.kstep = static_cast<int64_t>(SBM) * gemm::kTileK;
   p.a.rtile = static_cast<int64_t>(SBM) * t.d;
+  p.a.bstride = t.d_pad * t.d;
+  p.a_batch_rows = a_batch_rows;
   p.b.pass[0] = t.D;
   p.b.rows = t.R_pad;
   p.b.kstep = static_cast<int64_t>(SBN) * gemm::kTileK;
@@ -838,5 +861,63 @@ extern "C" bitsmoe_status bitsmoe_score_diag(const float* C_dev, int64_t units, 
     }
   }
   BITSMOE_LAUNCH_CHECK("score_diag: launch");
+  return ok();
+}
+
+extern "C" bitsmoe_status bitsmoe_score_routed(const float* C_dev, int64_t units, int64_t d,
+                                               const float* H_dev, int64_t units_per_h,
+                                               const int* bits_host, int nbits, int group,
+                                               float* L_dev, void* stream) {
+  if (!C_dev || !H_dev || !bits_host || !L_dev) return fail(BITSMOE_ERR_ARG, "score_routed: null pointer");
+  if (!aligned16({L_dev})) return fail(BITSMOE_ERR_ARG, "score_routed: device pointers must be 16-byte aligned");
+  bitsmoe_status st = check_rows_args(C_dev, H_dev, units, d, "score_routed");
+  if (st != BITSMOE_OK) return st;
+  if (nbits < 1 || nbits > BITSMOE_MAX_NBITS) return fail(BITSMOE_ERR_ARG, "score_routed: nbits outside 1..8");
+  QuantBits qb{};
+  qb.nb = nbits;
+  for (int j = 0; j < nbits; ++j) {
+    if (bits_host[j] < 1 || bits_host[j] > BITSMOE_MAX_BITS)
+      return fail(BITSMOE_ERR_ARG, "score_routed: width outside 1..8");
+    if (j > 0 && bits_host[j] <= bits_host[j - 1])
+      return fail(BITSMOE_ERR_ARG, "score_routed: widths must be strictly ascending");
+    qb.b[j] = bits_host[j];
+  }
+  if (!(group == 32 || group == 64 || group == 128 || group == 256))
+    return fail(BITSMOE_ERR_SHAPE, "score_routed: group must be 32, 64, 128 or 256");
+  if (d % group != 0) return fail(BITSMOE_ERR_SHAPE, "score_routed: d must be a multiple of the group");
+  if (units_per_h <= 0 || units % units_per_h != 0)
+    return fail(BITSMOE_ERR_SHAPE, "score_routed: units must be a multiple of units_per_h");
+  if ((units_per_h * nbits) % SBN != 0)
+    return fail(BITSMOE_ERR_SHAPE, "score_routed: units_per_h * nbits must be a multiple of 256");
+  const int64_t nh = units / units_per_h;
+  if (nh > 65535) return fail(BITSMOE_ERR_SHAPE, "score_routed: too many H matrices");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int64_t R = units * nbits;
+  LossTable t;
+  st = loss_table_setup(d, R, units, false, stream, "score_routed", &t, nh);
+  if (st != BITSMOE_OK) return st;
+  st = loss_table_hoff(H_dev, t, s, "score_routed: H_off launch");
+  if (st != BITSMOE_OK) return st;
+  const unsigned db = static_cast<unsigned>((units + 3) / 4);
+  {
+    KernelTimer dgen_timer("score_routed_dgen", stream);
+    switch (nbits) {
+#define BITSMOE_DGEN_R(NB)                                                                        \
+  case NB:                                                                                        \
+    hipLaunchKernelGGL((dgen_kernel<NB, false>), dim3(db), dim3(256), 0, s, C_dev, units, d, group, \
+                       qb, t.hdiag, t.D, t.diag, t.uexp, nullptr, 1, units_per_h);             \
+    break;
+      BITSMOE_DGEN_R(1) BITSMOE_DGEN_R(2) BITSMOE_DGEN_R(3) BITSMOE_DGEN_R(4)
+      BITSMOE_DGEN_R(5) BITSMOE_DGEN_R(6) BITSMOE_DGEN_R(7) BITSMOE_DGEN_R(8)
+#undef BITSMOE_DGEN_R
+    }
+  }
+  BITSMOE_LAUNCH_CHECK("score_routed: dgen launch");
+  st = loss_table_gemm(t, stream, "score_routed_gemm", "score_routed: gemm launch",
+                       units_per_h * nbits);
+  if (st != BITSMOE_OK) return st;
+  hipLaunchKernelGGL(finalize_kernel, dim3(static_cast<unsigned>((R + 255) / 256)), dim3(256), 0, s,
+                     t.diag, t.part, R, t.tiles_m, nbits, t.uexp, t.hexp, L_dev, units_per_h);
+  BITSMOE_LAUNCH_CHECK("score_routed: finalize launch");
   return ok();
 }

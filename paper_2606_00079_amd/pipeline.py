@@ -25,8 +25,8 @@ from typing import Dict, List, Optional, Sequence
 import numpy as np
 
 from . import (SURROGATE_WIDTHS, allocate, basis_importance, gram, gram_experts, gram_experts_in,
-               pack, pack_layout, project, project_in, score, score_diag, shared_basis, surrogate,
-               surrogate_budget)
+               gram_routed, pack, pack_layout, project, project_in, score, score_diag,
+               score_routed, shared_basis, surrogate, surrogate_budget)
 
 
 @dataclasses.dataclass
@@ -158,6 +158,54 @@ def quantize_projection_in(W, X, r: int, bits: Sequence[int], group: int, budget
     res = ProjectionResult(H, M, Vt, ev, C, L, bits_u, obj, off, codes, params, times)
     res.beta = beta
     return res
+
+
+def quantize_projection_routed(W, X, routing, r: int, bits: Sequence[int], group: int,
+                               budget: int, Hs=None) -> ProjectionResult:
+    """The hot path with the paper's routed calibration: one affinity-weighted
+    Gram H_e per expert (App. B.2, Eq. app_affinity_gram) from ``routing`` =
+    (offsets, rows, weights) over the rows of X, and every unit scored
+    against its own expert's H_e.  ``H`` of the result holds the [E][d][d]
+    Grams."""
+    import torch
+    times: Dict[str, float] = {}
+    dev = W.device
+    E, d_out, d_in = W.shape
+    offsets, rows, weights = routing
+    Hbuf = None
+    if Hs is None:
+        Hbuf = torch.empty((E, d_in, d_in), dtype=torch.float32, device=dev)
+    M = torch.empty((d_out, d_out), dtype=torch.float64, device=dev)
+    s1 = _Seg()
+    with s1:
+        if Hs is None:
+            Hs = gram_routed(X, offsets, rows, weights, out=Hbuf)
+        gram_experts(W, out=M)
+    Ut, ev, eig_ms = shared_basis(M, r)
+    times["gpu_gram_ms"] = s1.ms()
+    times["host_eig_ms"] = eig_ms
+    C = torch.empty((E * r, d_in), dtype=torch.float32, device=dev)
+    L = torch.empty((E * r, len(bits)), dtype=torch.float32, device=dev)
+    s2 = _Seg()
+    with s2:
+        project(Ut, W, out=C)
+        score_routed(C, Hs, r, bits, group, out=L)
+    t0 = time.perf_counter()
+    Lh = L.cpu().numpy()
+    bits_u, obj = allocate(Lh, bits, budget)
+    off = pack_layout(bits_u, d_in)
+    times["gpu_score_ms"] = s2.ms()
+    bits_d = torch.from_numpy(bits_u).to(dev, non_blocking=False)
+    off_d = torch.from_numpy(off).to(dev, non_blocking=False)
+    times["host_ilp_ms"] = (time.perf_counter() - t0) * 1e3
+    codes = torch.empty((max(int(off[-1]), 1),), dtype=torch.int64, device=dev)
+    params = torch.empty((C.shape[0], d_in // group, 2), dtype=torch.int16, device=dev)
+    s3 = _Seg()
+    with s3:
+        pack(C, bits_d, off_d, group, int(off[-1]), codes=codes, params=params)
+    times["gpu_pack_ms"] = s3.ms()
+    times["gpu_ms"] = times["gpu_gram_ms"] + times["gpu_score_ms"] + times["gpu_pack_ms"]
+    return ProjectionResult(Hs, M, Ut, ev, C, L, bits_u, obj, off, codes, params, times)
 
 
 def quantize_layer(projs: List[dict]) -> List[ProjectionResult]:

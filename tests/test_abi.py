@@ -218,6 +218,19 @@ def test_device_entry_points_validate_before_launch(lib):
     assert lib.bitsmoe_score_diag(fake, 10, 256, fake, 0, bits, 4, 64, fake, s) == 1
     assert lib.bitsmoe_score_diag(fake, 10, 256, fake, 4, bits, 4, 48, fake, s) == 2
     assert lib.bitsmoe_score_diag(fake, 10, 256, fake, 4, bad_bits, 2, 64, fake, s) == 1
+    off = (ctypes.c_int64 * 3)(0, 2, 3)
+    badoff = (ctypes.c_int64 * 3)(0, 2, 1)
+    rows = (ctypes.c_int32 * 3)(0, 5, 9)
+    badrows = (ctypes.c_int32 * 3)(0, 5, 10)
+    wts = (ctypes.c_float * 3)(0.5, 0.5, 1.0)
+    badw = (ctypes.c_float * 3)(0.5, -0.5, 1.0)
+    assert lib.bitsmoe_gram_routed(fake, 1, 10, 64, 2, badoff, rows, wts, fake, s) == 1
+    assert lib.bitsmoe_gram_routed(fake, 1, 10, 64, 2, off, badrows, wts, fake, s) == 1
+    assert lib.bitsmoe_gram_routed(fake, 1, 10, 64, 2, off, rows, badw, fake, s) == 1
+    assert lib.bitsmoe_gram_routed(fake, 1, 10, 100, 2, off, rows, wts, fake, s) == 2
+    assert lib.bitsmoe_score_routed(fake, 10, 256, fake, 3, bits, 4, 64, fake, s) == 2
+    assert lib.bitsmoe_score_routed(fake, 128, 256, fake, 32, bits, 4, 64, fake, s) == 2
+    assert lib.bitsmoe_score_routed(fake, 128, 256, fake, 0, bits, 4, 64, fake, s) == 2
     # misaligned device pointers are refused before any launch
     odd = ctypes.c_void_p(0x1008)
     assert lib.bitsmoe_gram(odd, 1, 64, 64, fake, s) == 1
