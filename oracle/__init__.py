@@ -23,6 +23,8 @@ definition from the paper (arXiv 2606.00079, "BitsMoE"), in fp64:
                      loss beta_k ||c - Q_b(c)||^2
 * ``routed``         routing-affinity-weighted calibration Grams H_e per expert
                      (App. B.2, Eq. app_affinity_gram) and their loss table
+* ``decode``         stage-3 inference from the packed factors: y = U sum_j g_j C^_e x
+                     (Sec. 4.4)
 * ``surrogate``      the paper's piecewise surrogate cost alpha^2 beta^gamma E(b) over the
                      widths {0,1,2,3,4,6,8,16}, its quantizers and the equivalent-bit
                      budget (App. B.3-B.5, Theorem app_spectrum_loss)
@@ -35,12 +37,12 @@ from .spectral import gram, gram_experts, shared_basis, project, unit_energy, tr
 from .quant import (quant_group, fake_quant, score, score_rows, pack_layout, pack, unpack,
                     bit_planes)
 from .ilp import integerize, allocate_dp, allocate_exhaustive, objective, budget_from_avg
-from . import surrogate, inspace, routed
+from . import surrogate, inspace, routed, decode
 from .surrogate import surrogate_table, budget_equivalent
 
 __all__ = [
     "gram", "gram_experts", "shared_basis", "project", "unit_energy", "truncation_loss",
     "quant_group", "fake_quant", "score", "score_rows", "pack_layout", "pack", "unpack",
     "bit_planes", "integerize", "allocate_dp", "allocate_exhaustive", "objective",
-    "budget_from_avg", "surrogate", "surrogate_table", "budget_equivalent", "inspace", "routed",
+    "budget_from_avg", "surrogate", "surrogate_table", "budget_equivalent", "inspace", "routed", "decode",
 ]
