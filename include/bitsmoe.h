@@ -38,6 +38,8 @@
  * and the paper's per-expert, routing-weighted calibration Grams:
  *   bitsmoe_gram_routed       H_e = (1/n) sum_t g_te x_t x_t^T     (device)
  *   bitsmoe_score_routed      L = delta H_e delta^T                (device)
+ * and serving a projection from its packed factors:
+ *   bitsmoe_moe_decode        y = U sum_j g_j C^_{e_j} x           (device)
  *
  * Conventions shared by every call:
  *  - Pointers named *_dev are device memory on the current HIP device;
@@ -309,6 +311,37 @@ bitsmoe_status bitsmoe_gram_routed(const void* X_dev, bitsmoe_dtype xt, int64_t 
 bitsmoe_status bitsmoe_score_routed(const float* C_dev, int64_t units, int64_t d, const float* H_dev,
                                     int64_t units_per_h, const int* bits_host, int nbits, int group,
                                     float* L_dev, void* stream);
+
+/*
+ * Stage-3 inference of one projection from its packed factors (Sec. 4.4:
+ * the packed expert-specific factors are dequantized inside the expert
+ * kernels).  With the output-space basis W_e ~ U C^_e, every token b gets
+ *     y_b = U z_b,   z_b = sum over token b's routing entries i of
+ *                          weights[i] C^_{e(i)} x_b,
+ * where e(i) is the expert whose range [offsets[e], offsets[e+1]) holds i and
+ * C^_e is expert e's r packed units decoded exactly as bitsmoe_unpack does
+ * (widths 0..8 and 16).  Each unit row is decoded once per chunk of its
+ * expert's tokens; the basis is applied once per token.
+ *   codes_dev, params_dev, bits_dev, word_offsets_dev, total_words
+ *               the packed units of all E * r units (as from bitsmoe_pack;
+ *               bits and offsets must cover E * r units)
+ *   Ut_dev      [r][d_out] fp32 shared basis (bitsmoe_shared_basis)
+ *   X_dev       [B][d_in] fp32 tokens
+ *   offsets_host, tokens_host, weights_host
+ *               the routing, grouped by expert as for bitsmoe_gram_routed
+ *               (tokens in [0, B), finite weights); copied to the device
+ *               before the call returns
+ *   Y_dev       [B][d_out] fp32 output (a token without entries gets 0)
+ * Shape rules: d_in % 64 == 0, group in {32, 64, 128, 256}, d_in % group == 0,
+ * r <= 8192, E and B <= 65535.  A unit whose width or offsets are
+ * inconsistent contributes nothing.
+ */
+bitsmoe_status bitsmoe_moe_decode(const uint64_t* codes_dev, const uint16_t* params_dev,
+                                  const uint8_t* bits_dev, const int64_t* word_offsets_dev,
+                                  int64_t total_words, int64_t E, int64_t r, int64_t d_in, int group,
+                                  const float* Ut_dev, int64_t d_out, const float* X_dev, int64_t B,
+                                  const int64_t* offsets_host, const int32_t* tokens_host,
+                                  const float* weights_host, float* Y_dev, void* stream);
 
 /*
  * The paper's surrogate cost table (App. B.3-B.4, Theorem

@@ -41,7 +41,7 @@ EXPORTS = [
     "bitsmoe_release", "bitsmoe_version", "bitsmoe_timing", "bitsmoe_kernel_time",
     "bitsmoe_surrogate", "bitsmoe_surrogate_budget", "bitsmoe_gram_experts_in",
     "bitsmoe_project_in", "bitsmoe_basis_importance", "bitsmoe_score_diag",
-    "bitsmoe_gram_routed", "bitsmoe_score_routed",
+    "bitsmoe_gram_routed", "bitsmoe_score_routed", "bitsmoe_moe_decode",
 ]
 # Candidate widths of the surrogate table, in column order.
 SURROGATE_WIDTHS = (0, 1, 2, 3, 4, 6, 8, 16)
@@ -97,6 +97,8 @@ def lib() -> ctypes.CDLL:
     L.bitsmoe_score_diag.argtypes = [vp, i64, i64, vp, i64, vp, i32, i32, vp, vp]
     L.bitsmoe_gram_routed.argtypes = [vp, i32, i64, i64, i64, vp, vp, vp, vp, vp]
     L.bitsmoe_score_routed.argtypes = [vp, i64, i64, vp, i64, vp, i32, i32, vp, vp]
+    L.bitsmoe_moe_decode.argtypes = [vp, vp, vp, vp, i64, i64, i64, i64, i32, vp, i64, vp, i64,
+                                     vp, vp, vp, vp, vp]
     L.bitsmoe_set_lapack.argtypes = [ctypes.c_char_p]
     L.bitsmoe_timing.argtypes = [i32]
     L.bitsmoe_kernel_time.argtypes = [ctypes.c_char_p, vp, vp]
@@ -313,6 +315,34 @@ def score_routed(C, Hs, units_per_h: int, bits: Sequence[int], group: int, out=N
         out = torch.empty((units, len(b)), dtype=torch.float32, device=C.device)
     _check(lib().bitsmoe_score_routed(_dev(C, "C"), units, d, _dev(Hs, "H"), units_per_h, bp, len(b),
                                       group, _dev(out, "L"), _stream()), "score_routed")
+    return out
+
+
+def moe_decode(codes, params, bits_dev, offsets_dev, total_words: int, E: int, r: int, d_in: int,
+               group: int, Ut, X, routing, out=None):
+    """y = U sum_j g_j C^_e x for every token of X [B][d_in] (fp32) from the packed
+    units; routing = (offsets [E+1], tokens, weights) host arrays -> fp32 [B][d_out]."""
+    torch = _torch()
+    B = X.shape[0]
+    d_out = Ut.shape[1]
+    if X.dtype != torch.float32 or Ut.dtype != torch.float32:
+        raise TypeError("X and Ut must be float32")
+    if X.dim() != 2 or X.shape[1] != d_in or Ut.dim() != 2 or Ut.shape[0] != r:
+        raise ValueError("X must be [B][d_in] and Ut [r][d_out]")
+    off = np.ascontiguousarray(np.asarray(routing[0], dtype=np.int64))
+    tok = np.ascontiguousarray(np.asarray(routing[1], dtype=np.int32))
+    wt = np.ascontiguousarray(np.asarray(routing[2], dtype=np.float32))
+    if off.shape[0] != E + 1 or tok.shape[0] < off[-1] or wt.shape[0] < off[-1]:
+        raise ValueError("routing tables do not match E")
+    if out is None:
+        out = torch.empty((B, d_out), dtype=torch.float32, device=X.device)
+    _check(lib().bitsmoe_moe_decode(_dev(codes, "codes"), _dev(params, "params"),
+                                    _dev(bits_dev, "bits"), _dev(offsets_dev, "offsets"),
+                                    int(total_words), E, r, d_in, group, _dev(Ut, "Ut"), d_out,
+                                    _dev(X, "X"), B, off.ctypes.data_as(ctypes.c_void_p),
+                                    tok.ctypes.data_as(ctypes.c_void_p),
+                                    wt.ctypes.data_as(ctypes.c_void_p), _dev(out, "Y"), _stream()),
+           "moe_decode")
     return out
 
 

@@ -231,8 +231,23 @@ def test_device_entry_points_validate_before_launch(lib):
     assert lib.bitsmoe_score_routed(fake, 10, 256, fake, 3, bits, 4, 64, fake, s) == 2
     assert lib.bitsmoe_score_routed(fake, 128, 256, fake, 32, bits, 4, 64, fake, s) == 2
     assert lib.bitsmoe_score_routed(fake, 128, 256, fake, 0, bits, 4, 64, fake, s) == 2
+    dtok = (ctypes.c_int32 * 3)(0, 1, 1)
+    dbad = (ctypes.c_int32 * 3)(0, 1, 2)
+    dw = (ctypes.c_float * 3)(0.5, 0.5, 1.0)
+    assert lib.bitsmoe_moe_decode(fake, fake, fake, fake, 10, 2, 8, 100, 64, fake, 64, fake, 2,
+                                  off, dtok, dw, fake, s) == 2
+    assert lib.bitsmoe_moe_decode(fake, fake, fake, fake, 10, 2, 8, 128, 48, fake, 64, fake, 2,
+                                  off, dtok, dw, fake, s) == 2
+    assert lib.bitsmoe_moe_decode(fake, fake, fake, fake, 10, 2, 8, 128, 64, fake, 64, fake, 2,
+                                  off, dbad, dw, fake, s) == 1
+    assert lib.bitsmoe_moe_decode(fake, fake, fake, fake, 10, 2, 8, 128, 64, fake, 64, fake, 2,
+                                  badoff, dtok, dw, fake, s) == 1
+    assert lib.bitsmoe_moe_decode(null, fake, fake, fake, 10, 2, 8, 128, 64, fake, 64, fake, 2,
+                                  off, dtok, dw, fake, s) == 1
     # misaligned device pointers are refused before any launch
     odd = ctypes.c_void_p(0x1008)
+    assert lib.bitsmoe_moe_decode(fake, fake, fake, fake, 10, 2, 8, 128, 64, fake, 64, odd, 2,
+                                  off, dtok, dw, fake, s) == 1
     assert lib.bitsmoe_gram(odd, 1, 64, 64, fake, s) == 1
     assert "aligned" in pkg.last_error()
     assert lib.bitsmoe_gram_experts(fake, 1, 2, 64, 64, odd, s) == 1
