@@ -258,6 +258,109 @@ def inspace_report(layer, res, dev_inputs, bm, pipeline) -> dict:
             "gpu_ms_gate_up": round(sum(q["gpu_ms"] for q in parts), 4)}
 
 
+def _decode_case(p, r, inp, routing, Xdec, bm, reps):
+    """One projection, one decode batch: the packed-factor decode and a dense
+    bf16 batched GEMV/GEMM over the same routed experts."""
+    import numpy as np
+    import torch
+    E, d_out, d_in, G = p.E, p.spec.d_out, p.spec.d_in, p.group
+    offs, tok, w = routing
+    B = Xdec.shape[0]
+    nnz = int(offs[-1])
+    bits_d = torch.from_numpy(np.ascontiguousarray(r.bits_u)).cuda()
+    off_d = torch.from_numpy(np.ascontiguousarray(r.offsets)).cuda()
+    Y = torch.empty((B, d_out), dtype=torch.float32, device="cuda")
+    for _ in range(3):
+        bm.moe_decode(r.codes, r.params, bits_d, off_d, int(r.offsets[-1]), E, p.r, d_in, G, r.Ut,
+                      Xdec, routing, out=Y)
+    torch.cuda.synchronize()
+    bm.timing(True)
+    bm.kernel_time("moe_decode_z")
+    bm.kernel_time("moe_decode_y")
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        bm.moe_decode(r.codes, r.params, bits_d, off_d, int(r.offsets[-1]), E, p.r, d_in, G, r.Ut,
+                      Xdec, routing, out=Y)
+    torch.cuda.synchronize()
+    call_ms = (time.perf_counter() - t0) * 1e3 / reps
+    zms = bm.kernel_time("moe_decode_z")[0] / reps
+    yms = bm.kernel_time("moe_decode_y")[0] / reps
+    bm.timing(False)
+    # algorithmic bytes: the touched experts' packed units (bit planes, group
+    # parameters, fp16 rows), U^T in fp32, X and Y
+    touched = [e for e in range(E) if offs[e + 1] > offs[e]]
+    bu = r.bits_u.reshape(E, p.r)[touched].astype(np.int64)
+    packed = int(np.sum(np.where(bu == 16, 2 * d_in,
+                                 np.where(bu == 0, 0, bu * d_in // 8 + 4 * (d_in // G)))))
+    dec_bytes = packed + p.r * d_out * 4 + B * d_in * 4 + B * d_out * 4
+    # dense bf16 baseline: the touched experts' weights gathered contiguous
+    # (outside the timed region), one batched product, weighted combine
+    W = inp["W"]
+    Wt = W[torch.as_tensor(touched, device=W.device)].contiguous()
+    counts = np.diff(offs)[touched]
+    tmax = int(counts.max())
+    Xp = torch.zeros((len(touched), tmax, d_in), dtype=W.dtype, device="cuda")
+    row = np.concatenate([np.full(c, j) for j, c in enumerate(counts)])
+    col = np.concatenate([np.arange(c) for c in counts])
+    Xb = Xdec.to(W.dtype)
+    Xp[torch.as_tensor(row, device="cuda"), torch.as_tensor(col, device="cuda")] = \
+        Xb[torch.as_tensor(tok.astype(np.int64), device="cuda")]
+    Xpt = Xp.transpose(1, 2).contiguous()                     # [T][d_in][tmax]
+    slot = torch.as_tensor(row * tmax + col, device="cuda")
+    tok_d = torch.as_tensor(tok.astype(np.int64), device="cuda")
+    w_d = torch.as_tensor(w, device="cuda")
+    Yd = torch.zeros((B, d_out), dtype=torch.float32, device="cuda")
+
+    def dense():
+        Z = torch.bmm(Wt, Xpt)                                # [T][d_out][tmax]
+        Zr = Z.transpose(1, 2).reshape(-1, d_out)[slot].float()
+        Yd.zero_()
+        Yd.index_add_(0, tok_d, Zr * w_d[:, None])
+    for _ in range(3):
+        dense()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    a.record()
+    for _ in range(reps):
+        dense()
+    b.record()
+    torch.cuda.synchronize()
+    dense_ms = a.elapsed_time(b) / reps
+    dense_bytes = len(touched) * d_out * d_in * W.element_size() + B * d_in * 2 + B * d_out * 4
+    dev_ms = zms + yms
+    return {"tokens": B, "experts_touched": len(touched), "routing_entries": nnz,
+            "z_kernel_ms": round(zms, 5), "y_kernel_ms": round(yms, 5),
+            "device_ms": round(dev_ms, 5), "call_ms_incl_host_routing": round(call_ms, 4),
+            "bytes": dec_bytes, "gbs": round(dec_bytes / (dev_ms * 1e-3) / 1e9, 1),
+            "hbm_floor_ms": round(dec_bytes / (PEAK_HBM_GBS * 1e9) * 1e3, 5),
+            "dense_bf16_ms": round(dense_ms, 5), "dense_bf16_bytes": dense_bytes,
+            "dense_bf16_gbs": round(dense_bytes / (dense_ms * 1e-3) / 1e9, 1),
+            "speedup_vs_dense_bf16": round(dense_ms / dev_ms, 2)}
+
+
+def decode_report(cfg, layer, res, dev_inputs, bm, reps=50) -> dict:
+    """Stage-3 decode of every projection of the layer from its packed factors
+    (y = U sum_j g_j C^_e x, output-space form) for a batch of 1 token and of
+    64 tokens routed by the synthetic top-k router, beside a dense bf16
+    batched product over the same routed experts' weights."""
+    import numpy as np
+    import torch
+    import synth
+    xin = next(inp["X"] for p, inp in zip(layer, dev_inputs) if p.spec.input == "x")
+    cases = []
+    for B in (1, 64):
+        Xh = xin[:B].float().cpu().numpy()
+        routing = synth.routing(cfg, Xh if cfg.dtype == "f32" else synth.f32_to_bf16_bits(Xh))
+        for p, r, inp in zip(layer, res, dev_inputs):
+            Xdec = inp["X"][:B].float().contiguous()
+            c = _decode_case(p, r, inp, routing, Xdec, bm, reps)
+            c["projection"] = p.spec.name
+            cases.append(c)
+            torch.cuda.synchronize()
+    return {"top_k": synth.TOP_K.get(cfg.name), "format": "bit planes + fp16 group params; U^T fp32",
+            "cases": cases}
+
+
 def main(argv=None) -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -396,6 +499,7 @@ def main(argv=None) -> int:
     sur = surrogate_report(cfg, layer, res, dev_inputs, bm, pipeline)
     insp = inspace_report(layer, res, dev_inputs, bm, pipeline)
     rout = routed_report(cfg, layer, dev_inputs, bm, pipeline)
+    dec = decode_report(cfg, layer, res, dev_inputs, bm)
 
     value = float(np.median(gpu_ms))
     traffic = measured_traffic(args.config)
@@ -434,6 +538,7 @@ def main(argv=None) -> int:
     out["surrogate"] = sur
     out["inspace"] = insp
     out["routed"] = rout
+    out["decode"] = dec
     if not args.no_cpu_baseline and not args.device_inputs:
         log("timing the fp64 oracle on a sample")
         out["cpu_baseline"] = cpu_baseline(cfg, layer)

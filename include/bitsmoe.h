@@ -40,6 +40,7 @@
  *   bitsmoe_score_routed      L = delta H_e delta^T                (device)
  * and serving a projection from its packed factors:
  *   bitsmoe_moe_decode        y = U sum_j g_j C^_{e_j} x           (device)
+ *   bitsmoe_moe_decode_topk   the same from a device top-k table   (device)
  *
  * Conventions shared by every call:
  *  - Pointers named *_dev are device memory on the current HIP device;
@@ -332,9 +333,11 @@ bitsmoe_status bitsmoe_score_routed(const float* C_dev, int64_t units, int64_t d
  *               (tokens in [0, B), finite weights); copied to the device
  *               before the call returns
  *   Y_dev       [B][d_out] fp32 output (a token without entries gets 0)
- * Shape rules: d_in % 64 == 0, group in {32, 64, 128, 256}, d_in % group == 0,
- * r <= 8192, E and B <= 65535.  A unit whose width or offsets are
- * inconsistent contributes nothing.
+ * Shape rules: d_in % 64 == 0, d_in <= 2^20, group in {32, 64, 128, 256},
+ * d_in % group == 0, r <= 8192, E and B <= 65535, and at most 65535 chunks
+ * of four routing entries of one expert.  A unit whose width or offsets are
+ * inconsistent contributes nothing.  The call waits for the stream once
+ * (after copying the routing tables) before it enqueues the kernels.
  */
 bitsmoe_status bitsmoe_moe_decode(const uint64_t* codes_dev, const uint16_t* params_dev,
                                   const uint8_t* bits_dev, const int64_t* word_offsets_dev,
@@ -342,6 +345,28 @@ bitsmoe_status bitsmoe_moe_decode(const uint64_t* codes_dev, const uint16_t* par
                                   const float* Ut_dev, int64_t d_out, const float* X_dev, int64_t B,
                                   const int64_t* offsets_host, const int32_t* tokens_host,
                                   const float* weights_host, float* Y_dev, void* stream);
+
+/*
+ * bitsmoe_moe_decode with the router's top-k table on the device, for
+ * decode loops: token b's routing entries are the k slots
+ * topk_experts_dev[b][0..k) with weights topk_weights_dev[b][0..k), summed
+ * in slot order.  Nothing is read back to the host and the call does not
+ * wait for the stream (after the first call on a device, which allocates
+ * the partial sums).  Each slot's expert row is decoded for that token
+ * alone; bitsmoe_moe_decode, which groups each expert's tokens, suits
+ * larger batches.
+ *   topk_experts_dev  [B][k] int32; a slot whose expert is outside [0, E)
+ *                     contributes nothing
+ *   topk_weights_dev  [B][k] fp32, used as given
+ * Shape rules as bitsmoe_moe_decode, plus 1 <= k <= E and B * k <= 65535.
+ */
+bitsmoe_status bitsmoe_moe_decode_topk(const uint64_t* codes_dev, const uint16_t* params_dev,
+                                       const uint8_t* bits_dev, const int64_t* word_offsets_dev,
+                                       int64_t total_words, int64_t E, int64_t r, int64_t d_in,
+                                       int group, const float* Ut_dev, int64_t d_out,
+                                       const float* X_dev, int64_t B, int64_t k,
+                                       const int32_t* topk_experts_dev,
+                                       const float* topk_weights_dev, float* Y_dev, void* stream);
 
 /*
  * The paper's surrogate cost table (App. B.3-B.4, Theorem

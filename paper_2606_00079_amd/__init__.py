@@ -42,6 +42,7 @@ EXPORTS = [
     "bitsmoe_surrogate", "bitsmoe_surrogate_budget", "bitsmoe_gram_experts_in",
     "bitsmoe_project_in", "bitsmoe_basis_importance", "bitsmoe_score_diag",
     "bitsmoe_gram_routed", "bitsmoe_score_routed", "bitsmoe_moe_decode",
+    "bitsmoe_moe_decode_topk",
 ]
 # Candidate widths of the surrogate table, in column order.
 SURROGATE_WIDTHS = (0, 1, 2, 3, 4, 6, 8, 16)
@@ -99,6 +100,8 @@ def lib() -> ctypes.CDLL:
     L.bitsmoe_score_routed.argtypes = [vp, i64, i64, vp, i64, vp, i32, i32, vp, vp]
     L.bitsmoe_moe_decode.argtypes = [vp, vp, vp, vp, i64, i64, i64, i64, i32, vp, i64, vp, i64,
                                      vp, vp, vp, vp, vp]
+    L.bitsmoe_moe_decode_topk.argtypes = [vp, vp, vp, vp, i64, i64, i64, i64, i32, vp, i64, vp,
+                                          i64, i64, vp, vp, vp, vp]
     L.bitsmoe_set_lapack.argtypes = [ctypes.c_char_p]
     L.bitsmoe_timing.argtypes = [i32]
     L.bitsmoe_kernel_time.argtypes = [ctypes.c_char_p, vp, vp]
@@ -343,6 +346,34 @@ def moe_decode(codes, params, bits_dev, offsets_dev, total_words: int, E: int, r
                                     tok.ctypes.data_as(ctypes.c_void_p),
                                     wt.ctypes.data_as(ctypes.c_void_p), _dev(out, "Y"), _stream()),
            "moe_decode")
+    return out
+
+
+def moe_decode_topk(codes, params, bits_dev, offsets_dev, total_words: int, E: int, r: int,
+                    d_in: int, group: int, Ut, X, topk_experts, topk_weights, out=None):
+    """moe_decode from the router's device top-k table: topk_experts int32
+    [B][k], topk_weights fp32 [B][k] (both on the device) -> fp32 [B][d_out]."""
+    torch = _torch()
+    B = X.shape[0]
+    d_out = Ut.shape[1]
+    if X.dtype != torch.float32 or Ut.dtype != torch.float32 or topk_weights.dtype != torch.float32:
+        raise TypeError("X, Ut and topk_weights must be float32")
+    if topk_experts.dtype != torch.int32:
+        raise TypeError("topk_experts must be int32")
+    if X.dim() != 2 or X.shape[1] != d_in or Ut.dim() != 2 or Ut.shape[0] != r:
+        raise ValueError("X must be [B][d_in] and Ut [r][d_out]")
+    if topk_experts.dim() != 2 or topk_experts.shape[0] != B or \
+            tuple(topk_weights.shape) != tuple(topk_experts.shape):
+        raise ValueError("topk_experts and topk_weights must both be [B][k]")
+    k = topk_experts.shape[1]
+    if out is None:
+        out = torch.empty((B, d_out), dtype=torch.float32, device=X.device)
+    _check(lib().bitsmoe_moe_decode_topk(_dev(codes, "codes"), _dev(params, "params"),
+                                         _dev(bits_dev, "bits"), _dev(offsets_dev, "offsets"),
+                                         int(total_words), E, r, d_in, group, _dev(Ut, "Ut"), d_out,
+                                         _dev(X, "X"), B, k, _dev(topk_experts, "topk_experts"),
+                                         _dev(topk_weights, "topk_weights"), _dev(out, "Y"),
+                                         _stream()), "moe_decode_topk")
     return out
 
 

@@ -6,13 +6,22 @@
 //     y = U z,   z = sum_j g_j C^_{e_j} x,
 // the shared basis applied once per token whatever the number of routed
 // experts.
-//   1. decode_z_kernel  one wave per (expert, unit row): the row is decoded
-//                       from its bit planes (or fp16 / evicted widths) once
-//                       per chunk of the expert's tokens and dotted with
-//                       each token's x: zp[i][k] = w_i (c^_{e,k} . x_{tok_i})
-//                       for every routing entry i.
-//   2. decode_y_kernel  per token: z = sum of its entries' zp (fixed order),
-//                       y = U z with the basis rows read coalesced.
+//   1. decode_z_kernel  a job is (expert, up to T of its routing entries);
+//                       each lane owns 32-entry segments of a unit row (one
+//                       32-bit word of every bit plane, one group parameter)
+//                       and holds the jobs' token values of its segment in
+//                       registers across the rows its wave walks:
+//                       zp[i][k] = w_i (c^_{e,k} . x_{tok_i}).
+//   2. decode_y_kernel  per token tile: z = sum of each token's partials
+//                       (fixed order) staged in LDS, y = U z with 16 waves
+//                       splitting r and one lane per output column.
+//
+// Decoding a segment: entry j of the segment is bit j of each plane word, so
+// four entries at a time the planes' nibbles are spread to one byte per
+// entry (nibble * 0x204081 places bit i at bit 8i with no carries) and
+// or-ed, plane t shifted by t; the bytes convert to floats exactly.  The
+// group's affine step is applied once per segment:
+//     sum_j (q_j s + m) x_j = s sum_j q_j x_j + m sum_j x_j.
 #include <algorithm>
 #include <cmath>
 #include <string>
@@ -25,91 +34,422 @@
 namespace bitsmoe {
 namespace {
 
-constexpr int kTok = 8;  // tokens per pass over a unit row
+constexpr int kWaves = 4;      // waves per decode_z workgroup
+constexpr int kSeg = 32;       // entries per lane segment
+constexpr int kYWaves = 16;    // waves per decode_y workgroup
 
 __device__ __forceinline__ bool width_ok(int b) {
   return b == 0 || b == 16 || (b >= 1 && b <= BITSMOE_MAX_BITS);
 }
 
-template <int G>
+// bits 0..3 of v -> bit 0 of bytes 0..3
+__device__ __forceinline__ uint32_t spread4(uint32_t v) {
+  return __umul24(v & 15u, 0x204081u) & 0x01010101u;
+}
+
+// A row's packed state as one lane sees it: width (0 when the unit is
+// evicted or inconsistent), first word, its segment's plane words and group
+// parameter.
+struct RowFetch {
+  int b;
+  int64_t o0;
+  uint32_t pw[BITSMOE_MAX_BITS];
+  uint32_t prm;
+};
+
+// One job per blockIdx.y: jobs[2j] = {expert, first routing entry, entries
+// (1..T), 0}, jobs[2j+1] = the entries' tokens.  Each wave walks `passes`
+// passes of R = 64 / L rows (L lanes per row, a power of two); a row of
+// nseg = d / 32 segments takes ceil(nseg / L) slices.  ONE_SLICE
+// (nseg <= L) keeps the token values in registers for all the wave's rows
+// and fetches the next row's plane words while the current one is summed.
+// The row descriptors (width, offsets) of the wave's rows are loaded once,
+// lane sub * L + p holding pass p of row group sub (passes <= L).
+// TOPK (T = 1): job j is routing slot j of a [B][kk] top-k table instead,
+// expert topk[j], token j / kk, weight ew[j]; an expert outside [0, E)
+// gives a zero partial.
+template <int T, bool ONE_SLICE, bool TOPK>
 __global__ __launch_bounds__(256) void decode_z_kernel(
-    const uint64_t* __restrict__ codes, const uint32_t* __restrict__ params,
+    const uint32_t* __restrict__ codes32, const uint32_t* __restrict__ params,
     const uint8_t* __restrict__ bits, const int64_t* __restrict__ off, int64_t total_words,
-    int64_t r, int64_t d, const float* __restrict__ X, const int64_t* __restrict__ eoff,
-    const int32_t* __restrict__ etok, const float* __restrict__ ew, float* __restrict__ zp) {
+    int r, int d, int G, int L, int passes, const float* __restrict__ X,
+    const int4* __restrict__ jobs, const int32_t* __restrict__ topk, int kk, int E,
+    const float* __restrict__ ew, float* __restrict__ zp) {
+  static_assert(!TOPK || T == 1, "top-k jobs hold one routing entry");
   const int lane = threadIdx.x & 63;
-  const int64_t k = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);  // unit of the expert
-  const int64_t e = blockIdx.y;
-  if (k >= r) return;  // whole wave
-  const int64_t i0 = eoff[e], i1 = eoff[e + 1];
-  if (i0 >= i1) return;
-  const int64_t u = e * r + k;
-  const int b = bits[u];
+  const int wave = threadIdx.x >> 6;
+  int e, nt;
+  int64_t i0;
+  int4 jt;
+  bool dead = false;
+  if (TOPK) {
+    e = topk[blockIdx.y];
+    dead = e < 0 || e >= E;
+    if (dead) e = 0;
+    i0 = blockIdx.y;
+    nt = 1;
+    jt = make_int4(static_cast<int>(blockIdx.y) / kk, 0, 0, 0);
+  } else {
+    const int4 job = jobs[2 * blockIdx.y];
+    jt = jobs[2 * blockIdx.y + 1];
+    e = job.x;
+    i0 = job.y;
+    nt = job.z;
+  }
+  const int R = 64 / L;
+  const int sub = lane / L, sl = lane % L;
+  const int nseg = d / kSeg;
+  const int ns = (nseg + L - 1) / L;
   const int64_t nw = d / 64;
-  const int64_t o0 = off[u], o1 = off[u + 1];
-  // a unit whose width or offsets are inconsistent contributes nothing (as
-  // bitsmoe_pack leaves it unwritten)
-  const bool valid = width_ok(b) && b != 0 && o1 - o0 == b * nw && o0 >= 0 && o1 <= total_words;
-  const uint32_t* pr = params + u * (d / G);
-  const uint16_t* h16 = reinterpret_cast<const uint16_t*>(codes + o0);
-  for (int64_t c0 = i0; c0 < i1; c0 += kTok) {
-    const int nt = static_cast<int>(std::min<int64_t>(kTok, i1 - c0));
-    const float* xs[kTok];
+  const int kbase = (static_cast<int>(blockIdx.x) * kWaves + wave) * passes * R;
+  if (kbase >= r) return;  // whole wave
+  // row descriptors
+  int db = 0;
+  int64_t do0 = 0;
+  {
+    const int k = kbase + sl * R + sub;
+    if (sl < passes && k < r) {
+      const int64_t u = static_cast<int64_t>(e) * r + k;
+      const int b = bits[u];
+      const int64_t o0 = off[u], o1 = off[u + 1];
+      // a unit whose width or offsets are inconsistent contributes nothing
+      // (as bitsmoe_pack leaves it unwritten); width 0 is evicted
+      const bool valid = width_ok(b) && b != 0 && o1 - o0 == b * nw && o0 >= 0 && o1 <= total_words;
+      db = valid && !dead ? b : 0;
+      do0 = valid && !dead ? o0 : 0;
+    }
+  }
+  const int tk[4] = {jt.x, jt.y, jt.z, jt.w};
+  const float* xrow[T];
 #pragma unroll
-    for (int t = 0; t < kTok; ++t) xs[t] = X + static_cast<int64_t>(etok[c0 + (t < nt ? t : nt - 1)]) * d;
-    float acc[kTok];
+  for (int t = 0; t < T; ++t) xrow[t] = X + static_cast<int64_t>(tk[t < nt ? t : 0]) * d;
+  float x[T][kSeg], xs[T];
+  auto load_x = [&](int seg) {
 #pragma unroll
-    for (int t = 0; t < kTok; ++t) acc[t] = 0.0f;
-    if (valid) {
-      for (int64_t w = 0; w < nw; ++w) {
-        const int64_t j = 64 * w + lane;
-        float xh;
-        if (b == 16) {
-          xh = f16_bits_to_f32(h16[j]);
-        } else {
-          uint32_t q = 0;
-          for (int t = 0; t < b; ++t)
-            q |= static_cast<uint32_t>((codes[o0 + t * nw + w] >> lane) & 1u) << t;
-          const uint32_t p = pr[j / G];
-          const float s = f16_bits_to_f32(static_cast<uint16_t>(p & 0xffffu));
-          const float m = f16_bits_to_f32(static_cast<uint16_t>(p >> 16));
-          xh = fmaf(static_cast<float>(q), s, m);  // the value bitsmoe_unpack returns
+    for (int t = 0; t < T; ++t) {
+      xs[t] = 0.0f;
+      if (t < nt && seg < nseg) {
+        const float4* p4 = reinterpret_cast<const float4*>(xrow[t] + seg * kSeg);
+#pragma unroll
+        for (int q = 0; q < kSeg / 4; ++q) {
+          const float4 v = p4[q];
+          x[t][4 * q] = v.x;
+          x[t][4 * q + 1] = v.y;
+          x[t][4 * q + 2] = v.z;
+          x[t][4 * q + 3] = v.w;
         }
 #pragma unroll
-        for (int t = 0; t < kTok; ++t) acc[t] = fmaf(xh, xs[t][j], acc[t]);
+        for (int j = 0; j < kSeg; ++j) xs[t] += x[t][j];
+      } else {
+#pragma unroll
+        for (int j = 0; j < kSeg; ++j) x[t][j] = 0.0f;
+      }
+    }
+  };
+  // the descriptor of pass p for this lane's row group
+  auto row_of = [&](int p, RowFetch& f) {
+    const int src = sub * L + p;
+    f.b = __shfl(db, src, 64);
+    const int lo = __shfl(static_cast<int>(do0 & 0xffffffff), src, 64);
+    const int hi = __shfl(static_cast<int>(do0 >> 32), src, 64);
+    f.o0 = (static_cast<int64_t>(hi) << 32) | static_cast<uint32_t>(lo);
+  };
+  // plane words and parameter of segment seg (widths 1..8)
+  auto fetch_planes = [&](int k, int seg, RowFetch& f) {
+    if (f.b >= 1 && f.b <= BITSMOE_MAX_BITS && seg < nseg && k < r) {
+      const int64_t u = static_cast<int64_t>(e) * r + k;
+      const uint32_t* pw = codes32 + 2 * f.o0 + seg;
+#pragma unroll
+      for (int t = 0; t < BITSMOE_MAX_BITS; ++t)
+        if (t < f.b) f.pw[t] = pw[2 * t * nw];
+      f.prm = params[u * (d / G) + (seg * kSeg) / G];
+    }
+  };
+  // sum over the segment: acc[t] += sum_j c^_j x[t][j]
+  auto seg_dot = [&](const RowFetch& f, int seg, float (&acc)[T]) {
+    float dq[T];
+#pragma unroll
+    for (int t = 0; t < T; ++t) dq[t] = 0.0f;
+    if (f.b == 16) {
+      // fp16 row: entries 32 seg .. 32 seg + 31 at byte 8 o0 + 64 seg
+      const uint2* h = reinterpret_cast<const uint2*>(codes32 + 2 * f.o0) + 8 * seg;
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        const uint2 v = h[q];
+        const float c[4] = {f16_bits_to_f32(static_cast<uint16_t>(v.x & 0xffffu)),
+                            f16_bits_to_f32(static_cast<uint16_t>(v.x >> 16)),
+                            f16_bits_to_f32(static_cast<uint16_t>(v.y & 0xffffu)),
+                            f16_bits_to_f32(static_cast<uint16_t>(v.y >> 16))};
+#pragma unroll
+        for (int c4 = 0; c4 < 4; ++c4)
+#pragma unroll
+          for (int t = 0; t < T; ++t) dq[t] = fmaf(c[c4], x[t][4 * q + c4], dq[t]);
+      }
+#pragma unroll
+      for (int t = 0; t < T; ++t) acc[t] += dq[t];
+      return;
+    }
+    const float s = f16_bits_to_f32(static_cast<uint16_t>(f.prm & 0xffffu));
+    const float m = f16_bits_to_f32(static_cast<uint16_t>(f.prm >> 16));
+    uint32_t qb[kSeg / 4];
+#pragma unroll
+    for (int kk = 0; kk < kSeg / 4; ++kk) qb[kk] = spread4(f.pw[0] >> (4 * kk));
+#pragma unroll
+    for (int t = 1; t < BITSMOE_MAX_BITS; ++t)
+      if (t < f.b) {
+#pragma unroll
+        for (int kk = 0; kk < kSeg / 4; ++kk) qb[kk] |= spread4(f.pw[t] >> (4 * kk)) << t;
+      }
+#pragma unroll
+    for (int kk = 0; kk < kSeg / 4; ++kk) {
+#pragma unroll
+      for (int c4 = 0; c4 < 4; ++c4) {
+        const float q = static_cast<float>((qb[kk] >> (8 * c4)) & 0xffu);
+#pragma unroll
+        for (int t = 0; t < T; ++t) dq[t] = fmaf(q, x[t][4 * kk + c4], dq[t]);
       }
     }
 #pragma unroll
-    for (int t = 0; t < kTok; ++t) {
-      const float v = wave_sum(acc[t]);
-      if (t < nt && lane == 0) zp[(c0 + t) * r + k] = ew[c0 + t] * v;
+    for (int t = 0; t < T; ++t) acc[t] += fmaf(s, dq[t], m * xs[t]);
+  };
+  auto finish_row = [&](int k, float (&acc)[T]) {
+    // sum over the L lanes of each row (lane groups are aligned powers of two)
+    for (int mlane = L / 2; mlane >= 1; mlane >>= 1)
+#pragma unroll
+      for (int t = 0; t < T; ++t) acc[t] += __shfl_xor(acc[t], mlane, 64);
+    if (k < r && sl == 0) {
+#pragma unroll
+      for (int t = 0; t < T; ++t)
+        if (t < nt) zp[(i0 + t) * r + k] = dead ? 0.0f : ew[i0 + t] * acc[t];
+    }
+  };
+  if (ONE_SLICE) {
+    load_x(sl);
+    RowFetch cur, nxt;
+    nxt.b = 0;
+    nxt.o0 = 0;
+    row_of(0, cur);
+    fetch_planes(kbase + sub, sl, cur);
+    for (int pass = 0; pass < passes; ++pass) {
+      const int k = kbase + pass * R + sub;
+      if (pass + 1 < passes) {
+        row_of(pass + 1, nxt);
+        fetch_planes(k + R, sl, nxt);
+      }
+      float acc[T];
+#pragma unroll
+      for (int t = 0; t < T; ++t) acc[t] = 0.0f;
+      if (k < r && cur.b != 0 && sl < nseg) seg_dot(cur, sl, acc);
+      finish_row(k, acc);
+      cur = nxt;
+    }
+  } else {
+    for (int pass = 0; pass < passes; ++pass) {
+      const int k = kbase + pass * R + sub;
+      RowFetch f;
+      row_of(pass, f);
+      float acc[T];
+#pragma unroll
+      for (int t = 0; t < T; ++t) acc[t] = 0.0f;
+      if (k < r && f.b != 0) {
+        for (int sidx = 0; sidx < ns; ++sidx) {
+          const int seg = sidx * L + sl;
+          load_x(seg);
+          if (seg >= nseg) continue;
+          fetch_planes(k, seg, f);
+          seg_dot(f, seg, acc);
+        }
+      }
+      finish_row(k, acc);
     }
   }
 }
 
-// y[b][o] = sum_k Ut[k][o] z_b[k], z_b[k] = sum over token b's routing entries
-// (in the order given) of zp[i][k].
-__global__ __launch_bounds__(256) void decode_y_kernel(const float* __restrict__ zp,
-                                                       const int64_t* __restrict__ pidx, int kmax,
-                                                       int64_t r, const float* __restrict__ Ut,
-                                                       int64_t d_out, float* __restrict__ Y) {
-  extern __shared__ float z[];  // [r]
-  const int64_t b = blockIdx.y;
-  const int64_t* pb = pidx + b * kmax;
-  for (int64_t k = threadIdx.x; k < r; k += 256) {
-    float s = 0.0f;
-    for (int j = 0; j < kmax; ++j) {
-      const int64_t i = pb[j];
-      if (i >= 0) s += zp[i * r + k];
+// y[b][o] = sum_k Ut[k][o] z_b[k], z_b[k] = sum over token b's routing
+// entries (in the order given) of zp[i][k]: the entries pidx[b][0..kmax)
+// (-1 = none), or b kmax .. b kmax + kmax - 1 when pidx is null.  TB tokens per workgroup
+// (blockIdx.y), 64 output columns per workgroup (blockIdx.x); wave w takes
+// the contiguous rows [w nk, (w + 1) nk) (nk a multiple of 4), fetching U
+// 16 rows ahead, and the 16 partial sums are added in wave order.
+template <int TB>
+__global__ __launch_bounds__(1024) void decode_y_kernel(const float* __restrict__ zp,
+                                                        const int64_t* __restrict__ pidx, int kmax,
+                                                        int r, const float* __restrict__ Ut,
+                                                        int64_t d_out, int64_t B,
+                                                        float* __restrict__ Y) {
+  constexpr int KC = 16;
+  extern __shared__ float sm[];  // z [TB][rp], then partials [16][TB][64]
+  const int nk = ((r + kYWaves - 1) / kYWaves + 3) / 4 * 4;
+  const int rp = nk * kYWaves;  // r padded (z is 0 past r)
+  float* z = sm;
+  float* red = sm + TB * rp;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t o = static_cast<int64_t>(blockIdx.x) * 64 + lane;
+  const int k0 = wave * nk;
+  const bool col = o < d_out;
+  float ua[KC], ub[KC];
+  auto fetch = [&](int c, float (&u)[KC]) {
+#pragma unroll
+    for (int i = 0; i < KC; ++i) {
+      const int k = k0 + c * KC + i;
+      u[i] = (col && c * KC + i < nk && k < r) ? Ut[static_cast<int64_t>(k) * d_out + o] : 0.0f;
     }
-    z[k] = s;
+  };
+  fetch(0, ua);
+  const int64_t b0 = static_cast<int64_t>(blockIdx.y) * TB;
+  for (int idx = threadIdx.x; idx < TB * rp; idx += 64 * kYWaves) {
+    const int tb = idx / rp, k = idx - tb * rp;
+    const int64_t b = b0 + tb;
+    float s = 0.0f;
+    if (b < B && k < r) {
+      for (int j = 0; j < kmax; ++j) {
+        const int64_t i = pidx ? pidx[b * kmax + j] : b * kmax + j;
+        if (i >= 0) s += zp[i * r + k];
+      }
+    }
+    z[idx] = s;
   }
   __syncthreads();
-  const int64_t o = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
-  if (o >= d_out) return;
-  float acc = 0.0f;
-  for (int64_t k = 0; k < r; ++k) acc = fmaf(Ut[k * d_out + o], z[k], acc);
-  Y[b * d_out + o] = acc;
+  float acc[TB];
+#pragma unroll
+  for (int tb = 0; tb < TB; ++tb) acc[tb] = 0.0f;
+  const int nc = (nk + KC - 1) / KC;
+  for (int c = 0; c < nc; ++c) {
+    if (c + 1 < nc) fetch(c + 1, ub);
+#pragma unroll
+    for (int i4 = 0; i4 < KC / 4; ++i4) {
+      const int kk = k0 + c * KC + 4 * i4;  // < rp: nk is a multiple of 4
+      if (c * KC + 4 * i4 < nk) {
+#pragma unroll
+        for (int tb = 0; tb < TB; ++tb) {
+          const float4 zv = *reinterpret_cast<const float4*>(z + tb * rp + kk);
+          acc[tb] = fmaf(ua[4 * i4], zv.x, acc[tb]);
+          acc[tb] = fmaf(ua[4 * i4 + 1], zv.y, acc[tb]);
+          acc[tb] = fmaf(ua[4 * i4 + 2], zv.z, acc[tb]);
+          acc[tb] = fmaf(ua[4 * i4 + 3], zv.w, acc[tb]);
+        }
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < KC; ++i) ua[i] = ub[i];
+  }
+#pragma unroll
+  for (int tb = 0; tb < TB; ++tb) red[(wave * TB + tb) * 64 + lane] = acc[tb];
+  __syncthreads();
+  if (wave < TB) {
+    const int tb = wave;
+    float s = 0.0f;
+    for (int w = 0; w < kYWaves; ++w) s += red[(w * TB + tb) * 64 + lane];
+    const int64_t b = b0 + tb;
+    if (b < B && o < d_out) Y[b * d_out + o] = s;
+  }
+}
+
+}  // namespace
+}  // namespace bitsmoe
+
+namespace bitsmoe {
+namespace {
+
+bitsmoe_status check_decode(const char* who, const void* codes, const void* params,
+                            const void* bits, const void* offs, const void* Ut, const void* X,
+                            const void* Y, int64_t total_words, int64_t E, int64_t r, int64_t d_in,
+                            int group, int64_t d_out, int64_t B) {
+  const std::string w(who);
+  if (!codes || !params || !bits || !offs || !Ut || !X || !Y)
+    return fail(BITSMOE_ERR_ARG, w + ": null pointer");
+  if (!aligned16({codes, params, bits, offs, Ut, X, Y}))
+    return fail(BITSMOE_ERR_ARG, w + ": device pointers must be 16-byte aligned");
+  if (E <= 0 || r <= 0 || d_in <= 0 || d_out <= 0 || B <= 0 || total_words < 0)
+    return fail(BITSMOE_ERR_ARG, w + ": non-positive size");
+  if (E > 65535 || B > 65535) return fail(BITSMOE_ERR_SHAPE, w + ": at most 65535 experts and tokens");
+  if (!(group == 32 || group == 64 || group == 128 || group == 256))
+    return fail(BITSMOE_ERR_SHAPE, w + ": group must be 32, 64, 128 or 256");
+  if (d_in % 64 != 0 || d_in % group != 0)
+    return fail(BITSMOE_ERR_SHAPE, w + ": d_in must be a multiple of 64 and of the group");
+  if (r > 8192) return fail(BITSMOE_ERR_SHAPE, w + ": r above 8192");
+  if (d_in > (1 << 20)) return fail(BITSMOE_ERR_SHAPE, w + ": d_in above 2^20");
+  return ok();
+}
+
+// Launch shape of both kernels.
+struct DecodeGeom {
+  int L;            // lanes per unit row (power of two, <= 64)
+  bool one_slice;   // the row's segments fit in L lanes
+  int R;            // rows per wave pass
+  int passes;       // passes per wave
+  int64_t rows_wg;  // rows per decode_z workgroup
+  int64_t rp;       // r padded for decode_y
+  int TB;           // tokens per decode_y workgroup
+};
+
+DecodeGeom decode_geometry(int64_t njobs, int64_t r, int64_t d_in, int64_t B) {
+  DecodeGeom g;
+  // lanes per row: the row's segments rounded up to a power of two (up to 64)
+  const int nseg = static_cast<int>(d_in / 32);
+  g.L = 2;
+  while (g.L < nseg && g.L < 64) g.L *= 2;
+  g.one_slice = nseg <= g.L;
+  g.R = 64 / g.L;
+  // rows per wave: about 1024 waves or more, up to 8 (and L) passes of R
+  // rows; more passes reuse the token values held in registers
+  const int64_t total_rows = std::max<int64_t>(njobs, 1) * r;
+  g.passes = static_cast<int>(
+      std::clamp<int64_t>(total_rows / (g.R * 1024), 1, std::min(8, g.one_slice ? g.L : 8)));
+  g.rows_wg = static_cast<int64_t>(kWaves) * g.passes * g.R;
+  // decode_y: token tile TB with z [TB][rp] and the partials within 64 KiB
+  // of LDS (rp = r rounded up to 16 waves x a multiple of 4 rows)
+  g.rp = ((r + kYWaves - 1) / kYWaves + 3) / 4 * 4 * kYWaves;
+  g.TB = 8;
+  while (g.TB > 1 && static_cast<int64_t>(g.TB) * (g.rp + kYWaves * 64) * 4 > 65536) g.TB /= 2;
+  if (B == 1) g.TB = 1;
+  return g;
+}
+
+bitsmoe_status decode_launch(const DecodeGeom& g, int T, bool topk_jobs, int64_t njobs,
+                             const uint64_t* codes_dev, const uint16_t* params_dev,
+                             const uint8_t* bits_dev, const int64_t* offs_dev, int64_t total_words,
+                             int64_t E, int64_t r, int64_t d_in, int group, const float* Ut_dev,
+                             int64_t d_out, const float* X_dev, int64_t B, const int4* jobs_d,
+                             const int32_t* topk_d, int kk, const float* w_d, const int64_t* pidx_d,
+                             int kmax, float* zp, float* Y_dev, hipStream_t s) {
+  const uint32_t* pr = reinterpret_cast<const uint32_t*>(params_dev);
+  const uint32_t* c32 = reinterpret_cast<const uint32_t*>(codes_dev);
+  void* stream = s;
+  if (njobs > 0) {
+    KernelTimer timer("moe_decode_z", stream);
+    dim3 grid(static_cast<unsigned>((r + g.rows_wg - 1) / g.rows_wg), static_cast<unsigned>(njobs));
+#define BITSMOE_DEC(TT, OS, TK)                                                                    \
+  hipLaunchKernelGGL((decode_z_kernel<TT, OS, TK>), grid, dim3(64 * kWaves), 0, s, c32, pr,        \
+                     bits_dev, offs_dev, total_words, static_cast<int>(r), static_cast<int>(d_in), \
+                     group, g.L, g.passes, X_dev, jobs_d, topk_d, kk, static_cast<int>(E), w_d, zp)
+    if (topk_jobs) {
+      if (g.one_slice) BITSMOE_DEC(1, true, true); else BITSMOE_DEC(1, false, true);
+    } else if (T == 4) {
+      if (g.one_slice) BITSMOE_DEC(4, true, false); else BITSMOE_DEC(4, false, false);
+    } else {
+      if (g.one_slice) BITSMOE_DEC(1, true, false); else BITSMOE_DEC(1, false, false);
+    }
+#undef BITSMOE_DEC
+  }
+  BITSMOE_LAUNCH_CHECK("moe_decode: z launch");
+  {
+    KernelTimer timer("moe_decode_y", stream);
+    dim3 grid(static_cast<unsigned>((d_out + 63) / 64), static_cast<unsigned>((B + g.TB - 1) / g.TB));
+    const size_t lds = static_cast<size_t>(g.TB) * (g.rp + kYWaves * 64) * 4;
+#define BITSMOE_DECY(TT)                                                                   \
+  hipLaunchKernelGGL(decode_y_kernel<TT>, grid, dim3(64 * kYWaves), lds, s, zp, pidx_d,    \
+                     kmax, static_cast<int>(r), Ut_dev, d_out, B, Y_dev)
+    switch (g.TB) {
+      case 8: BITSMOE_DECY(8); break;
+      case 4: BITSMOE_DECY(4); break;
+      case 2: BITSMOE_DECY(2); break;
+      default: BITSMOE_DECY(1); break;
+    }
+#undef BITSMOE_DECY
+  }
+  BITSMOE_LAUNCH_CHECK("moe_decode: y launch");
+  return ok();
 }
 
 }  // namespace
@@ -125,24 +465,17 @@ extern "C" bitsmoe_status bitsmoe_moe_decode(const uint64_t* codes_dev, const ui
                                              int64_t B, const int64_t* offsets_host,
                                              const int32_t* tokens_host, const float* weights_host,
                                              float* Y_dev, void* stream) {
-  if (!codes_dev || !params_dev || !bits_dev || !word_offsets_dev || !Ut_dev || !X_dev || !Y_dev ||
-      !offsets_host || !tokens_host || !weights_host)
+  bitsmoe_status st = check_decode("moe_decode", codes_dev, params_dev, bits_dev, word_offsets_dev,
+                                   Ut_dev, X_dev, Y_dev, total_words, E, r, d_in, group, d_out, B);
+  if (st != BITSMOE_OK) return st;
+  if (!offsets_host || !tokens_host || !weights_host)
     return fail(BITSMOE_ERR_ARG, "moe_decode: null pointer");
-  if (!aligned16({codes_dev, params_dev, bits_dev, word_offsets_dev, Ut_dev, X_dev, Y_dev}))
-    return fail(BITSMOE_ERR_ARG, "moe_decode: device pointers must be 16-byte aligned");
-  if (E <= 0 || r <= 0 || d_in <= 0 || d_out <= 0 || B <= 0 || total_words < 0)
-    return fail(BITSMOE_ERR_ARG, "moe_decode: non-positive size");
-  if (E > 65535 || B > 65535) return fail(BITSMOE_ERR_SHAPE, "moe_decode: at most 65535 experts and tokens");
-  if (!(group == 32 || group == 64 || group == 128 || group == 256))
-    return fail(BITSMOE_ERR_SHAPE, "moe_decode: group must be 32, 64, 128 or 256");
-  if (d_in % 64 != 0 || d_in % group != 0)
-    return fail(BITSMOE_ERR_SHAPE, "moe_decode: d_in must be a multiple of 64 and of the group");
-  if (r > 8192) return fail(BITSMOE_ERR_SHAPE, "moe_decode: r above 8192");
   if (offsets_host[0] != 0) return fail(BITSMOE_ERR_ARG, "moe_decode: offsets[0] must be 0");
   for (int64_t e = 0; e < E; ++e)
     if (offsets_host[e + 1] < offsets_host[e])
       return fail(BITSMOE_ERR_ARG, "moe_decode: offsets must not decrease");
   const int64_t nnz = offsets_host[E];
+  if (nnz > INT32_MAX) return fail(BITSMOE_ERR_SHAPE, "moe_decode: too many routing entries");
   // routing entries of each token, in the order given (fixed summation order)
   std::vector<int64_t> cnt(static_cast<size_t>(B), 0);
   for (int64_t i = 0; i < nnz; ++i) {
@@ -153,55 +486,83 @@ extern "C" bitsmoe_status bitsmoe_moe_decode(const uint64_t* codes_dev, const ui
   }
   int64_t kmax = 1;
   for (int64_t c : cnt) kmax = std::max(kmax, c);
+  if (kmax > 65535) return fail(BITSMOE_ERR_SHAPE, "moe_decode: more than 65535 entries of one token");
   std::vector<int64_t> pidx(static_cast<size_t>(B * kmax), -1);
   std::fill(cnt.begin(), cnt.end(), 0);
   for (int64_t i = 0; i < nnz; ++i) {
     const int64_t b = tokens_host[i];
     pidx[static_cast<size_t>(b * kmax + cnt[static_cast<size_t>(b)]++)] = i;
   }
+  // jobs: every expert's routing entries in chunks of T (4 when some expert
+  // has several tokens, else 1, which needs fewer registers)
+  int64_t cmax = 0;
+  for (int64_t e = 0; e < E; ++e) cmax = std::max(cmax, offsets_host[e + 1] - offsets_host[e]);
+  const int T = cmax > 1 ? 4 : 1;
+  std::vector<int32_t> jobs;  // per job: {expert, first entry, entries, 0}, {tokens}
+  for (int64_t e = 0; e < E; ++e)
+    for (int64_t i = offsets_host[e]; i < offsets_host[e + 1]; i += T) {
+      const int64_t n = std::min<int64_t>(T, offsets_host[e + 1] - i);
+      jobs.push_back(static_cast<int32_t>(e));
+      jobs.push_back(static_cast<int32_t>(i));
+      jobs.push_back(static_cast<int32_t>(n));
+      jobs.push_back(0);
+      for (int t = 0; t < 4; ++t) jobs.push_back(t < n ? tokens_host[i + t] : 0);
+    }
+  const int64_t njobs = static_cast<int64_t>(jobs.size() / 8);
+  if (njobs > 65535) return fail(BITSMOE_ERR_SHAPE, "moe_decode: more than 65535 routing chunks");
+  const DecodeGeom g = decode_geometry(njobs, r, d_in, B);
   hipStream_t s = static_cast<hipStream_t>(stream);
-  bitsmoe_status st;
-  // device tables: expert offsets [E+1], tokens [nnz], weights [nnz], token
-  // entry lists [B][kmax]; partials zp [nnz][r]
-  const size_t tab_bytes = static_cast<size_t>(E + 1) * 8 + static_cast<size_t>(B * kmax) * 8 +
-                           static_cast<size_t>(nnz) * 8 + 64;
+  // device tables: jobs [njobs][8], routing weights [nnz], token entry
+  // lists [B][kmax]; partials zp [nnz][r]
+  const size_t job_bytes = static_cast<size_t>(std::max<int64_t>(njobs, 1)) * 32;
+  const size_t pidx_bytes = static_cast<size_t>(B * kmax) * 8;
+  const size_t w_bytes = (static_cast<size_t>(nnz) * 4 + 15) / 16 * 16;
+  const size_t tab_bytes = job_bytes + pidx_bytes + w_bytes + 64;
   char* tab = static_cast<char*>(scratch(kScratchMisc, tab_bytes, stream, &st));
   if (!tab) return st;
-  int64_t* eoff_d = reinterpret_cast<int64_t*>(tab);
-  int64_t* pidx_d = eoff_d + (E + 1);
-  int32_t* tok_d = reinterpret_cast<int32_t*>(pidx_d + B * kmax);
-  float* w_d = reinterpret_cast<float*>(tok_d + nnz + (nnz & 1));
-  hipError_t he = hipMemcpyAsync(eoff_d, offsets_host, (E + 1) * 8, hipMemcpyHostToDevice, s);
+  int4* jobs_d = reinterpret_cast<int4*>(tab);
+  int64_t* pidx_d = reinterpret_cast<int64_t*>(tab + job_bytes);
+  float* w_d = reinterpret_cast<float*>(tab + job_bytes + pidx_bytes);
+  hipError_t he = hipSuccess;
+  if (njobs > 0) he = hipMemcpyAsync(jobs_d, jobs.data(), njobs * 32, hipMemcpyHostToDevice, s);
   if (he == hipSuccess)
     he = hipMemcpyAsync(pidx_d, pidx.data(), B * kmax * 8, hipMemcpyHostToDevice, s);
-  if (he == hipSuccess && nnz > 0) he = hipMemcpyAsync(tok_d, tokens_host, nnz * 4, hipMemcpyHostToDevice, s);
   if (he == hipSuccess && nnz > 0) he = hipMemcpyAsync(w_d, weights_host, nnz * 4, hipMemcpyHostToDevice, s);
   if (he == hipSuccess) he = hipStreamSynchronize(s);  // host tables may go away after return
   if (he != hipSuccess) return device_error("moe_decode: routing table copy", he);
   float* zp = static_cast<float*>(scratch(kScratchPart, std::max<int64_t>(nnz, 1) * r * 4, stream, &st));
   if (!zp) return st;
-  const uint32_t* pr = reinterpret_cast<const uint32_t*>(params_dev);
-  {
-    KernelTimer timer("moe_decode_z", stream);
-    dim3 grid(static_cast<unsigned>((r + 3) / 4), static_cast<unsigned>(E));
-#define BITSMOE_DEC(GG)                                                                          \
-  hipLaunchKernelGGL(decode_z_kernel<GG>, grid, dim3(256), 0, s, codes_dev, pr, bits_dev,       \
-                     word_offsets_dev, total_words, r, d_in, X_dev, eoff_d, tok_d, w_d, zp)
-    switch (group) {
-      case 32: BITSMOE_DEC(32); break;
-      case 64: BITSMOE_DEC(64); break;
-      case 128: BITSMOE_DEC(128); break;
-      default: BITSMOE_DEC(256); break;
-    }
-#undef BITSMOE_DEC
-  }
-  BITSMOE_LAUNCH_CHECK("moe_decode: z launch");
-  {
-    KernelTimer timer("moe_decode_y", stream);
-    dim3 grid(static_cast<unsigned>((d_out + 255) / 256), static_cast<unsigned>(B));
-    hipLaunchKernelGGL(decode_y_kernel, grid, dim3(256), static_cast<size_t>(r) * 4, s, zp, pidx_d,
-                       static_cast<int>(kmax), r, Ut_dev, d_out, Y_dev);
-  }
-  BITSMOE_LAUNCH_CHECK("moe_decode: y launch");
-  return ok();
+  return decode_launch(g, T, false, njobs, codes_dev, params_dev, bits_dev, word_offsets_dev,
+                       total_words, E, r, d_in, group, Ut_dev, d_out, X_dev, B, jobs_d, nullptr, 1,
+                       w_d, pidx_d, static_cast<int>(kmax), zp, Y_dev, s);
+}
+
+extern "C" bitsmoe_status bitsmoe_moe_decode_topk(const uint64_t* codes_dev, const uint16_t* params_dev,
+                                                  const uint8_t* bits_dev,
+                                                  const int64_t* word_offsets_dev, int64_t total_words,
+                                                  int64_t E, int64_t r, int64_t d_in, int group,
+                                                  const float* Ut_dev, int64_t d_out,
+                                                  const float* X_dev, int64_t B, int64_t k,
+                                                  const int32_t* topk_experts_dev,
+                                                  const float* topk_weights_dev, float* Y_dev,
+                                                  void* stream) {
+  bitsmoe_status st = check_decode("moe_decode_topk", codes_dev, params_dev, bits_dev,
+                                   word_offsets_dev, Ut_dev, X_dev, Y_dev, total_words, E, r, d_in,
+                                   group, d_out, B);
+  if (st != BITSMOE_OK) return st;
+  if (!topk_experts_dev || !topk_weights_dev)
+    return fail(BITSMOE_ERR_ARG, "moe_decode_topk: null pointer");
+  if (!aligned16({topk_experts_dev, topk_weights_dev}))
+    return fail(BITSMOE_ERR_ARG, "moe_decode_topk: device pointers must be 16-byte aligned");
+  if (k <= 0) return fail(BITSMOE_ERR_ARG, "moe_decode_topk: non-positive k");
+  if (k > E || B * k > 65535)
+    return fail(BITSMOE_ERR_SHAPE, "moe_decode_topk: k above E, or more than 65535 routing slots");
+  const int64_t njobs = B * k;
+  const DecodeGeom g = decode_geometry(njobs, r, d_in, B);
+  float* zp = static_cast<float*>(scratch(kScratchPart, njobs * r * 4, stream, &st));
+  if (!zp) return st;
+  return decode_launch(g, 1, true, njobs, codes_dev, params_dev, bits_dev, word_offsets_dev,
+                       total_words, E, r, d_in, group, Ut_dev, d_out, X_dev, B, nullptr,
+                       topk_experts_dev, static_cast<int>(k), topk_weights_dev, nullptr,
+                       static_cast<int>(k), zp, Y_dev, static_cast<hipStream_t>(stream));
 }

@@ -248,6 +248,19 @@ def test_device_entry_points_validate_before_launch(lib):
     odd = ctypes.c_void_p(0x1008)
     assert lib.bitsmoe_moe_decode(fake, fake, fake, fake, 10, 2, 8, 128, 64, fake, 64, odd, 2,
                                   off, dtok, dw, fake, s) == 1
+    assert lib.bitsmoe_moe_decode_topk(fake, fake, fake, fake, 10, 2, 8, 128, 64, fake, 64, fake,
+                                       2, 2, odd, fake, fake, s) == 1
+    # top-k decode: k outside [1, E], B k above 65535, shape rules, nulls
+    assert lib.bitsmoe_moe_decode_topk(fake, fake, fake, fake, 10, 2, 8, 128, 64, fake, 64, fake,
+                                       2, 0, fake, fake, fake, s) == 1
+    assert lib.bitsmoe_moe_decode_topk(fake, fake, fake, fake, 10, 2, 8, 128, 64, fake, 64, fake,
+                                       2, 3, fake, fake, fake, s) == 2
+    assert lib.bitsmoe_moe_decode_topk(fake, fake, fake, fake, 10, 8, 8, 128, 64, fake, 64, fake,
+                                       10000, 8, fake, fake, fake, s) == 2
+    assert lib.bitsmoe_moe_decode_topk(fake, fake, fake, fake, 10, 2, 8, 100, 64, fake, 64, fake,
+                                       2, 2, fake, fake, fake, s) == 2
+    assert lib.bitsmoe_moe_decode_topk(fake, fake, fake, fake, 10, 2, 8, 128, 64, fake, 64, fake,
+                                       2, 2, null, fake, fake, s) == 1
     assert lib.bitsmoe_gram(odd, 1, 64, 64, fake, s) == 1
     assert "aligned" in pkg.last_error()
     assert lib.bitsmoe_gram_experts(fake, 1, 2, 64, 64, odd, s) == 1

@@ -80,6 +80,9 @@ def _run(E, r, d_in, d_out, B, k, G, widths, seed, drop_token=None):
     (6, 40, 192, 96, 17, 3, 32, (0, 1, 2, 4, 8, 16)),   # eviction and fp16 rows
     (3, 8, 768, 64, 1, 1, 128, (2, 3)),                 # one token, one expert
     (8, 33, 512, 256, 40, 8, 256, (1, 2, 3, 4, 6, 8)),  # every token on every expert
+    (5, 24, 2560, 128, 1, 2, 64, (0, 1, 2, 16)),        # rows in two slices, one token
+    (4, 20, 4096, 64, 9, 2, 128, (2, 3, 4, 16)),        # rows in two slices, chunks of four
+    (2, 70, 64, 96, 5, 1, 32, (1, 3, 5, 7)),            # 32 rows per wave pass
 ])
 def test_moe_decode_matches_oracle(E, r, d_in, d_out, B, k, G, widths):
     say("decode", E, r, d_in, d_out, B, k, G, widths)
@@ -102,3 +105,51 @@ def test_moe_decode_qwen_gate_rows():
     err = relfro(Y, ref)
     say("qwen rows rel fro", err)
     assert err <= REL
+
+
+def _topk_run(E, r, d_in, d_out, B, k, G, widths, seed, bad=()):
+    """Decode from a device top-k table; `bad` = (token, slot, expert) entries
+    with an expert outside [0, E), which must contribute nothing."""
+    C, bits_u, codes, params, off, Ut, X, _ = _case(E, r, d_in, d_out, B, k, G, widths, seed)
+    g = np.random.default_rng(seed + 1)
+    logits = g.standard_normal((B, E))
+    top = np.argsort(-logits, axis=1)[:, :k].astype(np.int32)
+    w = np.exp(np.take_along_axis(logits, top, 1))
+    w = (w / w.sum(1, keepdims=True)).astype(np.float32)
+    for b, j, e in bad:
+        top[b, j] = e
+    ok = (top >= 0) & (top < E)
+    ex, tok, wt = top[ok], np.nonzero(ok)[0].astype(np.int32), w[ok]
+    order = np.lexsort((tok, ex))
+    offs = np.r_[0, np.cumsum(np.bincount(ex, minlength=E))].astype(np.int64)
+    routing = (offs, tok[order], wt[order])
+    cd = torch.from_numpy(codes.view(np.int64).copy() if len(codes) else np.zeros(1, np.int64)).to(DEV)
+    pd = torch.from_numpy(params.view(np.int16).copy()).to(DEV)
+    bd = torch.from_numpy(bits_u).to(DEV)
+    od = torch.from_numpy(off).to(DEV)
+    Utd, Xd = torch.from_numpy(Ut).to(DEV), torch.from_numpy(X).to(DEV)
+    Y = bm.moe_decode_topk(cd, pd, bd, od, int(off[-1]), E, r, d_in, G, Utd, Xd,
+                           torch.from_numpy(top).to(DEV), torch.from_numpy(w).to(DEV)).cpu().numpy()
+    Yg = bm.moe_decode(cd, pd, bd, od, int(off[-1]), E, r, d_in, G, Utd, Xd, routing).cpu().numpy()
+    Chat = decode.dequantized_factors(codes, params, bits_u, d_in, G)
+    ref = decode.moe_decode(Chat, r, Ut, X, *routing)
+    return Y, Yg, ref
+
+
+@pytest.mark.parametrize("E,r,d_in,d_out,B,k,G,widths", [
+    (16, 384, 2048, 768, 1, 8, 128, (1, 2, 3, 4)),      # Qwen3-30B-A3B gate rows, one token
+    (16, 256, 768, 512, 3, 8, 128, (0, 1, 2, 3, 16)),   # down-projection row length
+    (6, 40, 2560, 96, 5, 2, 64, (1, 2, 4)),              # rows in two slices
+])
+def test_moe_decode_topk_matches_oracle(E, r, d_in, d_out, B, k, G, widths):
+    say("decode topk", E, r, d_in, d_out, B, k, G, widths)
+    Y, Yg, ref = _topk_run(E, r, d_in, d_out, B, k, G, widths, seed=E + B)
+    assert relfro(Y, ref) <= REL
+    assert relfro(Y, Yg) <= 1e-5
+
+
+def test_moe_decode_topk_skips_experts_out_of_range():
+    Y, Yg, ref = _topk_run(8, 32, 256, 64, 4, 3, 64, (2, 3), seed=5,
+                           bad=((0, 1, -1), (2, 0, 8), (3, 2, 1 << 30)))
+    assert relfro(Y, ref) <= REL
+    assert relfro(Y, Yg) <= 1e-5
