@@ -326,16 +326,54 @@ def _decode_case(p, r, inp, routing, Xdec, bm, reps):
     b.record()
     torch.cuda.synchronize()
     dense_ms = a.elapsed_time(b) / reps
+    a.record()
+    for _ in range(reps):
+        torch.bmm(Wt, Xpt)
+    b.record()
+    torch.cuda.synchronize()
+    bmm_ms = a.elapsed_time(b) / reps
     dense_bytes = len(touched) * d_out * d_in * W.element_size() + B * d_in * 2 + B * d_out * 4
     dev_ms = zms + yms
+    # the same tokens from a device top-k table (no host work per call),
+    # calls back to back as in a decode loop
+    top = np.full((B, 8 if nnz >= 8 * B else max(1, nnz // B)), -1, dtype=np.int32)
+    wt = np.zeros(top.shape, dtype=np.float32)
+    fill = np.zeros(B, dtype=np.int64)
+    for e in range(E):
+        for i in range(offs[e], offs[e + 1]):
+            b = tok[i]
+            if fill[b] < top.shape[1]:
+                top[b, fill[b]], wt[b, fill[b]] = e, w[i]
+                fill[b] += 1
+    topd, wtd = torch.from_numpy(top).cuda(), torch.from_numpy(wt).cuda()
+    Yk = torch.empty((B, d_out), dtype=torch.float32, device="cuda")
+    for _ in range(3):
+        bm.moe_decode_topk(r.codes, r.params, bits_d, off_d, int(r.offsets[-1]), E, p.r, d_in, G,
+                           r.Ut, Xdec, topd, wtd, out=Yk)
+    bm.timing(True)
+    bm.kernel_time("moe_decode_z")
+    bm.kernel_time("moe_decode_y")
+    a0, a1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a0.record()
+    for _ in range(reps):
+        bm.moe_decode_topk(r.codes, r.params, bits_d, off_d, int(r.offsets[-1]), E, p.r, d_in, G,
+                           r.Ut, Xdec, topd, wtd, out=Yk)
+    a1.record()
+    torch.cuda.synchronize()
+    topk_call_ms = a0.elapsed_time(a1) / reps
+    tz = bm.kernel_time("moe_decode_z")[0] / reps
+    ty = bm.kernel_time("moe_decode_y")[0] / reps
+    bm.timing(False)
     return {"tokens": B, "experts_touched": len(touched), "routing_entries": nnz,
             "z_kernel_ms": round(zms, 5), "y_kernel_ms": round(yms, 5),
             "device_ms": round(dev_ms, 5), "call_ms_incl_host_routing": round(call_ms, 4),
             "bytes": dec_bytes, "gbs": round(dec_bytes / (dev_ms * 1e-3) / 1e9, 1),
             "hbm_floor_ms": round(dec_bytes / (PEAK_HBM_GBS * 1e9) * 1e3, 5),
-            "dense_bf16_ms": round(dense_ms, 5), "dense_bf16_bytes": dense_bytes,
+            "dense_bf16_ms": round(dense_ms, 5), "dense_bf16_bmm_only_ms": round(bmm_ms, 5),
+            "dense_bf16_bytes": dense_bytes,
             "dense_bf16_gbs": round(dense_bytes / (dense_ms * 1e-3) / 1e9, 1),
-            "speedup_vs_dense_bf16": round(dense_ms / dev_ms, 2)}
+            "speedup_vs_dense_bf16": round(dense_ms / dev_ms, 2),
+            "topk_device_ms": round(tz + ty, 5), "topk_call_ms_back_to_back": round(topk_call_ms, 5)}
 
 
 def decode_report(cfg, layer, res, dev_inputs, bm, reps=50) -> dict:
