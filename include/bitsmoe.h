@@ -16,6 +16,7 @@
  *   bitsmoe_gram          H = X^T X / n                      (device)
  *   bitsmoe_gram_experts  M = sum_e W_e W_e^T                (device)
  *   bitsmoe_shared_basis  U = top-r eigenvectors of M        (host LAPACK)
+ *     or bitsmoe_shared_basis_gpu (tridiagonal reduction on the device)
  *   bitsmoe_project       C_e = U^T W_e                      (device)
  *   bitsmoe_score         L[u][j] = delta H delta^T          (device)
  *   bitsmoe_allocate      widths per unit under a budget     (host, exact)
@@ -143,6 +144,31 @@ bitsmoe_status bitsmoe_gram_experts(const void* W_dev, bitsmoe_dtype wt, int64_t
 bitsmoe_status bitsmoe_shared_basis(const double* M_dev, int64_t d_out, int64_t r,
                                     float* Ut_dev, double* eigvals_host, double* host_ms,
                                     void* stream);
+
+/*
+ * Step 2 on the GPU: the same outputs and conventions as
+ * bitsmoe_shared_basis (eigenvalues descending, each eigenvector's entry of
+ * largest magnitude positive), computed on the device:
+ *   1. a blocked Householder reduction of M to tridiagonal form Q^T M Q
+ *      (fp64, panels of 32 columns);
+ *   2. eigenvalues d_out-r+1..d_out of the tridiagonal matrix by bisection,
+ *      eigenvectors by inverse iteration (tridiagonal LU with partial
+ *      pivoting), eigenvectors of eigenvalues closer than 1e-7 ||T|| made
+ *      orthonormal by modified Gram-Schmidt;
+ *   3. the back-transformation U = Q Z.
+ * Only the two diagonals (for bounds and the finiteness check) and the r
+ * eigenvalues cross PCIe.  Inside clusters of (nearly) equal eigenvalues
+ * the eigenvectors are a valid orthonormal basis of the cluster but need not
+ * equal bitsmoe_shared_basis's.
+ *   Arguments as bitsmoe_shared_basis; host_ms is the wall time of the
+ *   whole call.
+ * Shape rules: 1 <= r <= d_out <= 65536.  Device scratch: (d_out + 6 r)
+ * d_out doubles.  The call waits for the stream.  A non-finite M gives
+ * BITSMOE_ERR_NUMERIC.
+ */
+bitsmoe_status bitsmoe_shared_basis_gpu(const double* M_dev, int64_t d_out, int64_t r,
+                                        float* Ut_dev, double* eigvals_host, double* host_ms,
+                                        void* stream);
 
 /*
  * Step 3 -- expert spectral factors.

@@ -42,7 +42,7 @@ EXPORTS = [
     "bitsmoe_surrogate", "bitsmoe_surrogate_budget", "bitsmoe_gram_experts_in",
     "bitsmoe_project_in", "bitsmoe_basis_importance", "bitsmoe_score_diag",
     "bitsmoe_gram_routed", "bitsmoe_score_routed", "bitsmoe_moe_decode",
-    "bitsmoe_moe_decode_topk",
+    "bitsmoe_moe_decode_topk", "bitsmoe_shared_basis_gpu",
 ]
 # Candidate widths of the surrogate table, in column order.
 SURROGATE_WIDTHS = (0, 1, 2, 3, 4, 6, 8, 16)
@@ -100,6 +100,7 @@ def lib() -> ctypes.CDLL:
     L.bitsmoe_score_routed.argtypes = [vp, i64, i64, vp, i64, vp, i32, i32, vp, vp]
     L.bitsmoe_moe_decode.argtypes = [vp, vp, vp, vp, i64, i64, i64, i64, i32, vp, i64, vp, i64,
                                      vp, vp, vp, vp, vp]
+    L.bitsmoe_shared_basis_gpu.argtypes = [vp, i64, i64, vp, vp, vp, vp]
     L.bitsmoe_moe_decode_topk.argtypes = [vp, vp, vp, vp, i64, i64, i64, i64, i32, vp, i64, vp,
                                           i64, i64, vp, vp, vp, vp]
     L.bitsmoe_set_lapack.argtypes = [ctypes.c_char_p]
@@ -193,6 +194,23 @@ def shared_basis(M, r: int, out=None) -> Tuple[object, np.ndarray, float]:
     _check(lib().bitsmoe_shared_basis(_dev(M, "M"), d, r, _dev(out, "Ut"),
                                       ev.ctypes.data_as(ctypes.c_void_p), ctypes.byref(ms),
                                       _stream()), "shared_basis")
+    return out, ev, ms.value
+
+
+def shared_basis_gpu(M, r: int, out=None) -> Tuple[object, np.ndarray, float]:
+    """Top-r eigenvectors of M, tridiagonal reduction on the device.
+    Returns (Ut [r][d_out] fp32, eigvals, wall ms of the call)."""
+    torch = _torch()
+    d = M.shape[0]
+    if M.dtype != torch.float64:
+        raise TypeError("M must be float64")
+    if out is None:
+        out = torch.empty((r, d), dtype=torch.float32, device=M.device)
+    ev = np.zeros(r, dtype=np.float64)
+    ms = ctypes.c_double(0.0)
+    _check(lib().bitsmoe_shared_basis_gpu(_dev(M, "M"), d, r, _dev(out, "Ut"),
+                                          ev.ctypes.data_as(ctypes.c_void_p), ctypes.byref(ms),
+                                          _stream()), "shared_basis_gpu")
     return out, ev, ms.value
 
 

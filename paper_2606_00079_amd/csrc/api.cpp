@@ -135,7 +135,6 @@ typedef void (*dsyevd32_t)(const char*, const char*, const int32_t*, double*, co
 typedef void (*dsyevd64_t)(const char*, const char*, const int64_t*, double*, const int64_t*,
                            double*, double*, const int64_t*, int64_t*, const int64_t*, int64_t*,
                            size_t, size_t);
-
 struct Lapack {
   void* handle = nullptr;
   dsyevd32_t f32 = nullptr;
@@ -219,6 +218,7 @@ bitsmoe_status eig_sym(double* A, int64_t n, double* w) {
   if (info != 0) return fail(BITSMOE_ERR_NUMERIC, "dsyevd failed (info=" + std::to_string(info) + ")");
   return BITSMOE_OK;
 }
+
 }  // namespace
 
 }  // namespace bitsmoe

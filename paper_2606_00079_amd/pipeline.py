@@ -26,7 +26,7 @@ import numpy as np
 
 from . import (SURROGATE_WIDTHS, allocate, basis_importance, gram, gram_experts, gram_experts_in,
                gram_routed, pack, pack_layout, project, project_in, score, score_diag,
-               score_routed, shared_basis, surrogate, surrogate_budget)
+               score_routed, shared_basis, shared_basis_gpu, surrogate, surrogate_budget)
 
 
 @dataclasses.dataclass
@@ -67,7 +67,10 @@ class _Seg:
 
 
 def quantize_projection(W, X, r: int, bits: Sequence[int], group: int, budget: int,
-                        H=None) -> ProjectionResult:
+                        H=None, eig: str = "host") -> ProjectionResult:
+    """The hot path on one projection.  eig = "host" (LAPACK on M copied to
+    the host) or "gpu" (tridiagonal reduction on the device); the eigensolve
+    is timed apart from the device segments either way (host_eig_ms)."""
     import torch
     times: Dict[str, float] = {}
     dev = W.device
@@ -83,7 +86,12 @@ def quantize_projection(W, X, r: int, bits: Sequence[int], group: int, budget: i
         if H is None:
             H = gram(X, out=Hbuf)
         gram_experts(W, out=M)
-    Ut, ev, eig_ms = shared_basis(M, r)      # synchronizes the stream first
+    if eig == "gpu":
+        Ut, ev, eig_ms = shared_basis_gpu(M, r)  # synchronizes the stream first
+    elif eig == "host":
+        Ut, ev, eig_ms = shared_basis(M, r)      # synchronizes the stream first
+    else:
+        raise ValueError("eig must be 'host' or 'gpu'")
     times["gpu_gram_ms"] = s1.ms()
     times["host_eig_ms"] = eig_ms
     C = torch.empty((E * r, d_in), dtype=torch.float32, device=dev)

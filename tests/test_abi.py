@@ -200,6 +200,10 @@ def test_device_entry_points_validate_before_launch(lib):
     assert lib.bitsmoe_shared_basis(fake, 64, 65, fake, null, null, s) == 2
     assert "r > d_out" in pkg.last_error()
     assert lib.bitsmoe_shared_basis(null, 64, 4, fake, null, null, s) == 1
+    assert lib.bitsmoe_shared_basis_gpu(fake, 64, 65, fake, null, null, s) == 2
+    assert lib.bitsmoe_shared_basis_gpu(fake, 70000, 4, fake, null, null, s) == 2
+    assert lib.bitsmoe_shared_basis_gpu(null, 64, 4, fake, null, null, s) == 1
+    assert lib.bitsmoe_shared_basis_gpu(fake, 64, 0, fake, null, null, s) == 1
     assert lib.bitsmoe_set_lapack(b"/nonexistent/liblapack.so") == 8
     kap = (ctypes.c_double * 3)(0.149492, 0.0406789, 0.01184786)
     badk = (ctypes.c_double * 3)(0.149492, -1.0, 0.01184786)
@@ -269,5 +273,6 @@ def test_device_entry_points_validate_before_launch(lib):
     assert lib.bitsmoe_pack(fake, 10, 256, 64, fake, odd, 10, fake, fake, s) == 1
     assert lib.bitsmoe_unpack(fake, fake, fake, fake, 10, 10, 256, 64, odd, s) == 1
     assert lib.bitsmoe_shared_basis(odd, 64, 4, fake, null, null, s) == 1
+    assert lib.bitsmoe_shared_basis_gpu(odd, 64, 4, fake, null, null, s) == 1
     assert lib.bitsmoe_surrogate(fake, 10, 256, fake, 0.7, kap, odd, null, s) == 1
     assert lib.bitsmoe_surrogate(fake, 10, 256, fake, 0.7, kap, fake, odd, s) == 1
