@@ -149,13 +149,16 @@ __global__ __launch_bounds__(256) void trsymv_kernel(const double* __restrict__ 
 // w for column c = i - j0 of the panel (rows j = i+1..n-1), stored in
 // Wp[c], and, when do_row, the rank-2 terms of panel columns 0..c applied to
 // row i+1 (entries j >= i+1).  ybv = trsymv's output: y [m], V^T v [c],
-// W^T v [c].  Every workgroup forms y.v (and w_{i+1}) itself.
+// W^T v [c].  Every workgroup forms y.v (and w_{i+1}) itself.  A workgroup
+// covers 64 entries j; its four waves take the panel columns c' = q mod 4
+// and their partial sums are added in wave order.
 __global__ __launch_bounds__(256) void trw_kernel(double* __restrict__ A, double* __restrict__ Wp,
                                                   int64_t n, int64_t i, int64_t j0, int c,
                                                   const double* __restrict__ ybv,
                                                   const double* __restrict__ tau, int do_row) {
   __shared__ double red[4];
   __shared__ double s_vtv[NB], s_wtv[NB], s_vi1[NB], s_wi1[NB];
+  __shared__ double part_w[4][64], part_r[4][64];
   const int64_t m = n - i - 1;
   const double t = tau[i];
   const double* v = A + i * n;
@@ -173,28 +176,33 @@ __global__ __launch_bounds__(256) void trw_kernel(double* __restrict__ A, double
   double q = 0.0;
   for (int cc = 0; cc < c; ++cc) q = fma(s_vtv[cc], s_wtv[cc], q);
   const double s = t * (yv - 2.0 * q);
-  const int64_t j = i + 1 + static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
-  double w = 0.0;
+  const int jl = threadIdx.x & 63, sl = threadIdx.x >> 6;
+  const int64_t j = i + 1 + static_cast<int64_t>(blockIdx.x) * 64 + jl;
+  double pw = 0.0, pr = 0.0;
   if (j < n) {
-    double acc = ybv[j - (i + 1)];
 #pragma unroll 8
-    for (int cc = 0; cc < c; ++cc)
-      acc -= A[(j0 + cc) * n + j] * s_wtv[cc] + Wp[cc * n + j] * s_vtv[cc];
-    w = t * acc - 0.5 * t * s * v[j];
-    Wp[static_cast<int64_t>(c) * n + j] = w;
+    for (int cc = sl; cc < c; cc += 4) {
+      const double vj = A[(j0 + cc) * n + j], wj = Wp[cc * n + j];
+      pw = fma(vj, s_wtv[cc], fma(wj, s_vtv[cc], pw));
+      pr = fma(vj, s_wi1[cc], fma(wj, s_vi1[cc], pr));
+    }
   }
+  part_w[sl][jl] = pw;
+  part_r[sl][jl] = pr;
+  __syncthreads();
+  if (sl != 0 || j >= n) return;
+  const double acc = ybv[j - (i + 1)] - (((part_w[0][jl] + part_w[1][jl]) + part_w[2][jl]) + part_w[3][jl]);
+  const double w = t * acc - 0.5 * t * s * v[j];
+  Wp[static_cast<int64_t>(c) * n + j] = w;
   if (!do_row) return;
   // w_{i+1} (v_{i+1} = 1), formed the same way in every workgroup
   double acc1 = ybv[0];
   for (int cc = 0; cc < c; ++cc) acc1 -= s_vi1[cc] * s_wtv[cc] + s_wi1[cc] * s_vtv[cc];
   const double w1 = t * acc1 - 0.5 * t * s;
-  if (j < n) {
-    double delta = v[j] * w1 + w;  // the current column: V[j][c] W[i+1][c] + W[j][c] V[i+1][c]
-#pragma unroll 8
-    for (int cc = 0; cc < c; ++cc)
-      delta += A[(j0 + cc) * n + j] * s_wi1[cc] + Wp[cc * n + j] * s_vi1[cc];
-    A[(i + 1) * n + j] -= delta;
-  }
+  // the current column: V[j][c] W[i+1][c] + W[j][c] V[i+1][c], then c' < c
+  const double delta =
+      v[j] * w1 + w + (((part_r[0][jl] + part_r[1][jl]) + part_r[2][jl]) + part_r[3][jl]);
+  A[(i + 1) * n + j] -= delta;
 }
 
 // A[r][q] -= sum_k Vp[k][r] Wp[k][q] + Wp[k][r] Vp[k][q] for r, q in [s, n),
@@ -245,15 +253,14 @@ __global__ __launch_bounds__(256) void trail_kernel(double* __restrict__ A,
 }
 
 // out[k][c] = sum_{j >= jlo} P[k][j] Vp[c][j] for k < rows, c < nbp (rows
-// of P with stride ldp, rows of Vp with stride n).  Two rows per wave; the
-// Vp columns of each 64-wide chunk are staged in LDS.
-__global__ __launch_bounds__(256) void rowdot_kernel(const double* __restrict__ P, int64_t ldp,
-                                                     int64_t rows, const double* __restrict__ Vp,
-                                                     int nbp, int64_t n, int64_t jlo,
-                                                     double* __restrict__ out) {
+// of P with stride ldp, rows of Vp with stride n), rows 8 bx .. 8 bx + 7.
+// Two rows per wave; the Vp columns of each 64-wide chunk are staged in LDS.
+__device__ void rowdot_rows(const double* __restrict__ P, int64_t ldp, int64_t rows,
+                            const double* __restrict__ Vp, int nbp, int64_t n, int64_t jlo,
+                            double* __restrict__ out, int64_t bx) {
   __shared__ double sV[NB][64];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int64_t k0 = (static_cast<int64_t>(blockIdx.x) * 4 + wave) * 2;
+  const int64_t k0 = (bx * 4 + wave) * 2;
   const bool ok0 = k0 < rows, ok1 = k0 + 1 < rows;
   double a0[NB], a1[NB];
 #pragma unroll
@@ -287,12 +294,35 @@ __global__ __launch_bounds__(256) void rowdot_kernel(const double* __restrict__ 
   }
 }
 
+__global__ __launch_bounds__(256) void rowdot_kernel(const double* __restrict__ P, int64_t ldp,
+                                                     int64_t rows, const double* __restrict__ Vp,
+                                                     int nbp, int64_t n, int64_t jlo,
+                                                     double* __restrict__ out) {
+  rowdot_rows(P, ldp, rows, Vp, nbp, n, jlo, out, blockIdx.x);
+}
+
+// G_p = Vp Vp^T of every panel p = blockIdx.y (Vp = the reflector rows
+// 32 p .. 32 p + nbp - 1 of A), into G + p NB NB.
+__global__ __launch_bounds__(256) void panel_gram_kernel(const double* __restrict__ A, int64_t n,
+                                                         double* __restrict__ G) {
+  const int64_t j0 = static_cast<int64_t>(blockIdx.y) * NB;
+  const int nbp = static_cast<int>(std::min<int64_t>(NB, n - 1 - j0));
+  const double* Vp = A + j0 * n;
+  rowdot_rows(Vp, n, nbp, Vp, nbp, n, j0 + 1, G + blockIdx.y * NB * NB, blockIdx.x);
+}
+
 // Upper-triangular T of the panel's compact form (forward, by columns):
 // T[c][c] = tau_c, T[0:c][c] = -tau_c T[0:c][0:c] G[0:c][c], G = Vp Vp^T.
-__global__ __launch_bounds__(64) void tfactor_kernel(const double* __restrict__ G,
-                                                     const double* __restrict__ tau, int nbp,
-                                                     double* __restrict__ T) {
+// One workgroup per panel p = blockIdx.x (G, tau and T offset by p).
+__global__ __launch_bounds__(64) void tfactor_kernel(const double* __restrict__ Gall,
+                                                     const double* __restrict__ tau_all, int64_t n,
+                                                     double* __restrict__ Tall) {
   __shared__ double sT[NB][NB], sG[NB][NB];
+  const int64_t j0 = static_cast<int64_t>(blockIdx.x) * NB;
+  const int nbp = static_cast<int>(std::min<int64_t>(NB, n - 1 - j0));
+  const double* G = Gall + blockIdx.x * NB * NB;
+  const double* tau = tau_all + j0;
+  double* T = Tall + blockIdx.x * NB * NB;
   const int r = threadIdx.x;
   for (int idx = r; idx < NB * NB; idx += 64) {
     const int a = idx / NB, b = idx % NB;
@@ -367,25 +397,35 @@ __device__ double sturm_below(const double* __restrict__ d, const double* __rest
   return q;
 }
 
-// w[k] = eigenvalue t0 + k (0-based, ascending) by bisection of [lo, hi]
-// until the midpoint is no longer inside the interval.
-__global__ __launch_bounds__(64) void bisect_kernel(const double* __restrict__ d,
-                                                    const double* __restrict__ e, int64_t n,
-                                                    int64_t r, int64_t t0, double lo0, double hi0,
-                                                    double pivmin, double* __restrict__ w) {
-  const int64_t k = static_cast<int64_t>(blockIdx.x) * 64 + threadIdx.x;
-  if (k >= r) return;
+// w[k] = eigenvalue t0 + k (0-based, ascending): one wave per eigenvalue
+// splits [lo, hi] at 64 interior points per step (lane l evaluates the
+// Sturm count at lo + (hi - lo)(l + 1)/65); the counts grow with x, so the
+// lanes whose count is <= t form a prefix and the new interval is the gap
+// after it.  Stops when the interval is atol wide or the points no longer
+// fall strictly inside.
+__global__ __launch_bounds__(256) void bisect_kernel(const double* __restrict__ d,
+                                                     const double* __restrict__ e, int64_t n,
+                                                     int64_t r, int64_t t0, double lo0, double hi0,
+                                                     double pivmin, double atol,
+                                                     double* __restrict__ w) {
+  const int lane = threadIdx.x & 63;
+  const int64_t k = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
+  if (k >= r) return;  // whole wave
   const int64_t t = t0 + k;
   double lo = lo0, hi = hi0;
-  for (int it = 0; it < 256; ++it) {
-    const double mid = 0.5 * (lo + hi);
-    if (!(mid > lo && mid < hi)) break;
-    int64_t c;
-    sturm_below(d, e, n, mid, pivmin, &c);
-    if (c <= t) lo = mid;
-    else hi = mid;
+  for (int it = 0; it < 64 && hi - lo > atol; ++it) {
+    const double x = lo + (hi - lo) * (static_cast<double>(lane + 1) / 65.0);
+    const bool inside = x > lo && x < hi;
+    if (__ballot(inside) != ~0ull) break;  // the interval is a few ulps wide
+    int64_t cnt;
+    sturm_below(d, e, n, x, pivmin, &cnt);
+    const int p = __popcll(__ballot(cnt <= t));  // lanes 0..p-1 have count <= t
+    const double xl = __shfl(x, p > 0 ? p - 1 : 0, 64);
+    const double xh = __shfl(x, p < 64 ? p : 63, 64);
+    lo = p > 0 ? xl : lo;
+    hi = p < 64 ? xh : hi;
   }
-  w[k] = 0.5 * (lo + hi);
+  if (lane == 0) w[k] = 0.5 * (lo + hi);
 }
 
 // Start vector entry j of eigenvector k: a counter hash (splitmix64 of the
@@ -579,17 +619,19 @@ extern "C" bitsmoe_status bitsmoe_shared_basis_gpu(const double* M_dev, int64_t 
   if (!A) return st;
   double* Zt = static_cast<double*>(scratch(kScratchB, static_cast<size_t>(r * n) * 8, stream, &st));
   if (!Zt) return st;
-  const size_t small =
-      static_cast<size_t>(NB * n + (n + 2 * NB) + 3 * n + 2 * NB * NB + r * NB + r) * 8;
+  const int64_t npan = (n - 1 + NB - 1) / NB;
+  const size_t small = static_cast<size_t>(NB * n + (n + 2 * NB) + 3 * n +
+                                           2 * std::max<int64_t>(npan, 1) * NB * NB + r * NB + r) *
+                       8;
   double* Wp = static_cast<double*>(scratch(kScratchPart, small, stream, &st));
   if (!Wp) return st;
   double* ybv = Wp + NB * n;
   double* dvec = ybv + n + 2 * NB;
   double* evec = dvec + n;
   double* tau = evec + n;
-  double* G = tau + n;
-  double* T = G + NB * NB;
-  double* X = T + NB * NB;
+  double* G = tau + n;                                  // [npan][NB][NB]
+  double* T = G + std::max<int64_t>(npan, 1) * NB * NB;  // [npan][NB][NB]
+  double* X = T + std::max<int64_t>(npan, 1) * NB * NB;
   hipError_t he = hipMemcpyAsync(A, M_dev, static_cast<size_t>(n * n) * 8, hipMemcpyDeviceToDevice, s);
   if (he != hipSuccess) return device_error("shared_basis_gpu: copy of M", he);
   // 1. tridiagonal reduction
@@ -606,7 +648,7 @@ extern "C" bitsmoe_status bitsmoe_shared_basis_gpu(const double* M_dev, int64_t 
         hipLaunchKernelGGL(trsymv_kernel, dim3(static_cast<unsigned>((R + 7) / 8)), dim3(256), 0, s,
                            A, Wp, n, i, j0, c, ybv);
         const int do_row = (full && c == NB - 1) ? 0 : 1;
-        hipLaunchKernelGGL(trw_kernel, dim3(static_cast<unsigned>((m + 255) / 256)), dim3(256), 0, s,
+        hipLaunchKernelGGL(trw_kernel, dim3(static_cast<unsigned>((m + 63) / 64)), dim3(256), 0, s,
                            A, Wp, n, i, j0, c, ybv, tau, do_row);
       }
       if (full) {
@@ -655,8 +697,8 @@ extern "C" bitsmoe_status bitsmoe_shared_basis_gpu(const double* M_dev, int64_t 
   {
     KernelTimer timer("eig_tri_solve", stream);
     const unsigned g = static_cast<unsigned>((r + 63) / 64);
-    hipLaunchKernelGGL(bisect_kernel, dim3(g), dim3(64), 0, s, dvec, evec, n, r, n - r, lo, hi,
-                       pivmin, wd);
+    hipLaunchKernelGGL(bisect_kernel, dim3(static_cast<unsigned>((r + 3) / 4)), dim3(256), 0, s, dvec,
+                       evec, n, r, n - r, lo, hi, pivmin, 2.0 * eps * tnorm, wd);
     hipLaunchKernelGGL(inviter_kernel, dim3(g), dim3(64), 0, s, dvec, evec, n, r, wd, pivmin, work,
                        Zn);
   }
@@ -692,21 +734,23 @@ extern "C" bitsmoe_status bitsmoe_shared_basis_gpu(const double* M_dev, int64_t 
   // 3. back-transformation, last panel first
   {
     KernelTimer timer("eig_backtransform", stream);
-    const int64_t npan = (n - 1 + NB - 1) / NB;
+    if (npan > 0) {
+      hipLaunchKernelGGL(panel_gram_kernel, dim3(NB / 8, static_cast<unsigned>(npan)), dim3(256), 0,
+                         s, A, n, G);
+      hipLaunchKernelGGL(tfactor_kernel, dim3(static_cast<unsigned>(npan)), dim3(64), 0, s, G, tau, n,
+                         T);
+    }
     for (int64_t p = npan - 1; p >= 0; --p) {
       const int64_t j0 = p * NB;
       const int nbp = static_cast<int>(std::min<int64_t>(j0 + NB, n - 1) - j0);
       const double* Vp = A + j0 * n;
       const int64_t jlo = j0 + 1;
-      hipLaunchKernelGGL(rowdot_kernel, dim3(static_cast<unsigned>((nbp + 7) / 8)), dim3(256), 0, s,
-                         Vp, n, static_cast<int64_t>(nbp), Vp, nbp, n, jlo, G);
-      hipLaunchKernelGGL(tfactor_kernel, dim3(1), dim3(64), 0, s, G, tau + j0, nbp, T);
       hipLaunchKernelGGL(rowdot_kernel, dim3(static_cast<unsigned>((r + 7) / 8)), dim3(256), 0, s,
                          Zt, n, r, Vp, nbp, n, jlo, X);
       hipLaunchKernelGGL(zupdate_kernel,
                          dim3(static_cast<unsigned>((n - jlo + 255) / 256),
                               static_cast<unsigned>((r + 31) / 32)),
-                         dim3(256), 0, s, Zt, r, X, T, Vp, nbp, n, jlo);
+                         dim3(256), 0, s, Zt, r, X, T + p * NB * NB, Vp, nbp, n, jlo);
     }
     // 4. order, sign, fp32
     hipLaunchKernelGGL(finish_kernel, dim3(static_cast<unsigned>(r)), dim3(256), 0, s, Zt, r, n, Ut_dev);
