@@ -399,6 +399,35 @@ def decode_report(cfg, layer, res, dev_inputs, bm, reps=50) -> dict:
             "cases": cases}
 
 
+def eig_report(cfg, layer, res, bm, reps=2) -> dict:
+    """The shared basis of each projection by the device eigensolver on the
+    step's own M, beside the step's host LAPACK solve: wall time of each, the
+    eigenvalues' largest difference (relative to the largest) and the
+    distance between the two bases of the planted shared directions
+    (projector norm over the leading k0 vectors, which are separated from the
+    noise bulk)."""
+    import numpy as np
+    parts = []
+    for p, r in zip(layer, res):
+        bm.shared_basis_gpu(r.M, p.r)  # warm
+        best = float("inf")
+        for _ in range(reps):
+            Ut, ev, ms = bm.shared_basis_gpu(r.M, p.r)
+            best = min(best, ms)
+        host_ms = r.times["host_eig_ms"]  # the step's own host solve of the same M
+        k0 = min(cfg.k0, p.r)
+        A = Ut.double().cpu().numpy()[:k0]
+        B = r.Ut.double().cpu().numpy()[:k0]
+        proj = float(np.linalg.norm(A.T @ A - B.T @ B) / np.sqrt(k0))
+        parts.append({"projection": p.spec.name, "d_out": p.spec.d_out, "r": p.r,
+                      "gpu_call_ms": round(best, 2), "host_call_ms": round(host_ms, 2),
+                      "eigval_max_rel_diff": float(np.max(np.abs(ev - r.eigvals)) / r.eigvals[0]),
+                      "shared_directions_projector_diff": proj})
+    return {"projections": parts,
+            "gpu_ms_per_layer": round(sum(q["gpu_call_ms"] for q in parts), 2),
+            "host_ms_per_layer": round(sum(q["host_call_ms"] for q in parts), 2)}
+
+
 def main(argv=None) -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -409,6 +438,9 @@ def main(argv=None) -> int:
     ap.add_argument("--device-inputs", action="store_true",
                     help="draw the layer's inputs directly in device memory (same recipes, "
                          "torch's RNG; for the configurations too large to draw on the host)")
+    ap.add_argument("--eig", choices=("host", "gpu"), default="host",
+                    help="shared-basis eigensolve inside the step: host LAPACK (default) or "
+                         "the device solver; timed apart from the device segments either way")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="run one elementwise copy of MIB MiB before timing (calibrates HBM "
                          "byte counters under rocprofv3 --pmc)")
@@ -459,12 +491,12 @@ def main(argv=None) -> int:
 
     def step():
         if not args.device_inputs:
-            return pipeline.quantize_layer(dev_inputs)
+            return pipeline.quantize_layer(dev_inputs, eig=args.eig)
         # large layers: the same as quantize_layer, with a progress line per projection
         res, hcache = [], {}
         for i, p in enumerate(dev_inputs):
             r = pipeline.quantize_projection(p["W"], p["X"], p["r"], p["bits"], p["group"],
-                                             p["budget"], H=hcache.get(id(p["X"])))
+                                             p["budget"], H=hcache.get(id(p["X"])), eig=args.eig)
             hcache[id(p["X"])] = r.H
             res.append(r)
             log(f"projection {i + 1}/{len(dev_inputs)}: gpu {r.times['gpu_ms']:.2f} ms, "
@@ -538,6 +570,7 @@ def main(argv=None) -> int:
     insp = inspace_report(layer, res, dev_inputs, bm, pipeline)
     rout = routed_report(cfg, layer, dev_inputs, bm, pipeline)
     dec = decode_report(cfg, layer, res, dev_inputs, bm)
+    eigr = eig_report(cfg, layer, res, bm) if args.eig == "host" else None
 
     value = float(np.median(gpu_ms))
     traffic = measured_traffic(args.config)
@@ -577,6 +610,9 @@ def main(argv=None) -> int:
     out["inspace"] = insp
     out["routed"] = rout
     out["decode"] = dec
+    out["eig"] = {"in_step": args.eig, "host_eig_ms_in_step": out["host_eig_ms"]}
+    if eigr is not None:
+        out["eig"]["device_solver"] = eigr
     if not args.no_cpu_baseline and not args.device_inputs:
         log("timing the fp64 oracle on a sample")
         out["cpu_baseline"] = cpu_baseline(cfg, layer)

@@ -216,7 +216,7 @@ def quantize_projection_routed(W, X, routing, r: int, bits: Sequence[int], group
     return ProjectionResult(Hs, M, Ut, ev, C, L, bits_u, obj, off, codes, params, times)
 
 
-def quantize_layer(projs: List[dict]) -> List[ProjectionResult]:
+def quantize_layer(projs: List[dict], eig: str = "host") -> List[ProjectionResult]:
     """projs: dicts with W, X, r, bits, group, budget.  X objects that are the
     same tensor share one H."""
     cache = {}
@@ -224,7 +224,7 @@ def quantize_layer(projs: List[dict]) -> List[ProjectionResult]:
     for p in projs:
         key = id(p["X"])
         res = quantize_projection(p["W"], p["X"], p["r"], p["bits"], p["group"], p["budget"],
-                                  H=cache.get(key))
+                                  H=cache.get(key), eig=eig)
         cache[key] = res.H
         out.append(res)
     return out
