@@ -438,6 +438,9 @@ def main(argv=None) -> int:
     ap.add_argument("--device-inputs", action="store_true",
                     help="draw the layer's inputs directly in device memory (same recipes, "
                          "torch's RNG; for the configurations too large to draw on the host)")
+    ap.add_argument("--core-only", action="store_true",
+                    help="time the step only: skip the side reports (surrogate, input-space, "
+                         "routed, decode, device eigensolver), e.g. under a profiler")
     ap.add_argument("--eig", choices=("host", "gpu"), default="host",
                     help="shared-basis eigensolve inside the step: host LAPACK (default) or "
                          "the device solver; timed apart from the device segments either way")
@@ -566,11 +569,12 @@ def main(argv=None) -> int:
     # The paper's own allocation (closed-form surrogate, widths 0..16, the
     # equivalent-bit budget) on the same units, outside the timed region;
     # reported beside the exact path with its agreement with the exact costs.
-    sur = surrogate_report(cfg, layer, res, dev_inputs, bm, pipeline)
-    insp = inspace_report(layer, res, dev_inputs, bm, pipeline)
-    rout = routed_report(cfg, layer, dev_inputs, bm, pipeline)
-    dec = decode_report(cfg, layer, res, dev_inputs, bm)
-    eigr = eig_report(cfg, layer, res, bm) if args.eig == "host" else None
+    side = not args.core_only
+    sur = surrogate_report(cfg, layer, res, dev_inputs, bm, pipeline) if side else None
+    insp = inspace_report(layer, res, dev_inputs, bm, pipeline) if side else None
+    rout = routed_report(cfg, layer, dev_inputs, bm, pipeline) if side else None
+    dec = decode_report(cfg, layer, res, dev_inputs, bm) if side else None
+    eigr = eig_report(cfg, layer, res, bm) if side and args.eig == "host" else None
 
     value = float(np.median(gpu_ms))
     traffic = measured_traffic(args.config)
@@ -606,10 +610,11 @@ def main(argv=None) -> int:
                      "executed_frac": round(score_exec_flops / (score_ms_step * 1e-3) / 1e12
                                             / PEAK_BF16_TFLOPS, 4)},
     }
-    out["surrogate"] = sur
-    out["inspace"] = insp
-    out["routed"] = rout
-    out["decode"] = dec
+    if side:
+        out["surrogate"] = sur
+        out["inspace"] = insp
+        out["routed"] = rout
+        out["decode"] = dec
     out["eig"] = {"in_step": args.eig, "host_eig_ms_in_step": out["host_eig_ms"]}
     if eigr is not None:
         out["eig"]["device_solver"] = eigr
