@@ -24,6 +24,7 @@ definition from the paper (arXiv 2606.00079, "BitsMoE"), in fp64:
 * ``routed``         routing-affinity-weighted calibration Grams H_e per expert
                      (App. B.2, Eq. app_affinity_gram) and their loss table
 * ``decode``         stage-3 inference from the packed factors: y = U sum_j g_j C^_e x
+                     (output space) and y = sum_j g_j C^_e^T Phi^T x (input space)
                      (Sec. 4.4)
 * ``surrogate``      the paper's piecewise surrogate cost alpha^2 beta^gamma E(b) over the
                      widths {0,1,2,3,4,6,8,16}, its quantizers and the equivalent-bit

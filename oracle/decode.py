@@ -10,7 +10,9 @@ routed to experts e_1..e_k with weights g_1..g_k gives
     y = sum_j g_j W_{e_j} x  ~  U z,   z = sum_j g_j C^_{e_j} x,
 
 with C^_e the dequantized rows of expert e (exactly what ``quant.unpack``
-returns) and the shared basis applied once per token.
+returns) and the shared basis applied once per token.  ``moe_decode_in`` is
+the input-space form of the gate/up projections, where the basis is applied
+first (z = Phi^T x) and each routed expert's units are combined with z.
 """
 from __future__ import annotations
 
@@ -55,4 +57,28 @@ def moe_dense(W, X, offsets, tokens, weights) -> np.ndarray:
         for i in range(int(offsets[e]), int(offsets[e + 1])):
             b = int(tokens[i])
             Y[b] += float(weights[i]) * (W[e] @ X[b])
+    return Y
+
+
+def moe_decode_in(Chat, r: int, Vt, X, offsets, tokens, weights) -> np.ndarray:
+    """The input-space form (the paper's gate/up projections, Sec. 3.2 and
+    Sec. 4.4): expert e is W_e ~ C^_e^T Phi_r^T with the units of C^_e the
+    columns W_e phi_k (length d_out), so the basis is applied first, once per
+    token, z_b = Phi_r^T x_b, and
+        y_b = sum over token b's routing entries i of weights[i] C^_e^T z_b,
+    fp64 [B][d_out].
+
+    Chat: [E*r][d_out] dequantized units (unit e*r + k is row k of C^_e);
+    Vt: [r][d_in] (rows phi_k^T); X: [B][d_in]; routing as ``moe_decode``.
+    """
+    Chat = np.asarray(Chat, dtype=np.float64)
+    Vt = np.asarray(Vt, dtype=np.float64)
+    X = np.asarray(X, dtype=np.float64)
+    Z = X @ Vt.T
+    Y = np.zeros((X.shape[0], Chat.shape[1]))
+    for e in range(len(offsets) - 1):
+        Ce = Chat[e * r:(e + 1) * r]
+        for i in range(int(offsets[e]), int(offsets[e + 1])):
+            b = int(tokens[i])
+            Y[b] += float(weights[i]) * (Z[b] @ Ce)
     return Y
