@@ -42,6 +42,7 @@
  * and serving a projection from its packed factors:
  *   bitsmoe_moe_decode        y = U sum_j g_j C^_{e_j} x           (device)
  *   bitsmoe_moe_decode_topk   the same from a device top-k table   (device)
+ *   bitsmoe_moe_decode_in     y = sum_j g_j C^_{e_j}^T Phi^T x      (device)
  *
  * Conventions shared by every call:
  *  - Pointers named *_dev are device memory on the current HIP device;
@@ -371,6 +372,33 @@ bitsmoe_status bitsmoe_moe_decode(const uint64_t* codes_dev, const uint16_t* par
                                   const float* Ut_dev, int64_t d_out, const float* X_dev, int64_t B,
                                   const int64_t* offsets_host, const int32_t* tokens_host,
                                   const float* weights_host, float* Y_dev, void* stream);
+
+/*
+ * Stage-3 inference of a gate/up projection built in input space
+ * (bitsmoe_gram_experts_in, bitsmoe_project_in; Sec. 3.2 and Sec. 4.4): the
+ * units of C^_e are the columns W_e phi_k (length d_out), so the basis is
+ * applied once per token before the experts,
+ *     z_b = Phi_r^T x_b,   y_b = sum over token b's routing entries i of
+ *                                 weights[i] C^_{e(i)}^T z_b.
+ *   codes_dev .. total_words   the packed units of all E * r units, of
+ *               length d_out (as from bitsmoe_pack)
+ *   Vt_dev      [r][d_in] fp32 basis rows phi_k^T
+ *   X_dev       [B][d_in] fp32 tokens
+ *   offsets_host, tokens_host, weights_host   as bitsmoe_moe_decode
+ *   Y_dev       [B][d_out] fp32 output (a token without entries gets 0)
+ * Shape rules: d_out % 64 == 0, d_out % group == 0, group in {32, 64, 128,
+ * 256}, d_out and d_in <= 2^20, r <= 8192, E and B <= 65535, at most 65535
+ * chunks of four routing entries of one expert.  Units with inconsistent
+ * widths or offsets contribute nothing.  The call waits for the stream once
+ * (after copying the routing tables).
+ */
+bitsmoe_status bitsmoe_moe_decode_in(const uint64_t* codes_dev, const uint16_t* params_dev,
+                                     const uint8_t* bits_dev, const int64_t* word_offsets_dev,
+                                     int64_t total_words, int64_t E, int64_t r, int64_t d_out,
+                                     int group, const float* Vt_dev, int64_t d_in,
+                                     const float* X_dev, int64_t B, const int64_t* offsets_host,
+                                     const int32_t* tokens_host, const float* weights_host,
+                                     float* Y_dev, void* stream);
 
 /*
  * bitsmoe_moe_decode with the router's top-k table on the device, for

@@ -42,7 +42,7 @@ EXPORTS = [
     "bitsmoe_surrogate", "bitsmoe_surrogate_budget", "bitsmoe_gram_experts_in",
     "bitsmoe_project_in", "bitsmoe_basis_importance", "bitsmoe_score_diag",
     "bitsmoe_gram_routed", "bitsmoe_score_routed", "bitsmoe_moe_decode",
-    "bitsmoe_moe_decode_topk", "bitsmoe_shared_basis_gpu",
+    "bitsmoe_moe_decode_topk", "bitsmoe_shared_basis_gpu", "bitsmoe_moe_decode_in",
 ]
 # Candidate widths of the surrogate table, in column order.
 SURROGATE_WIDTHS = (0, 1, 2, 3, 4, 6, 8, 16)
@@ -101,6 +101,8 @@ def lib() -> ctypes.CDLL:
     L.bitsmoe_moe_decode.argtypes = [vp, vp, vp, vp, i64, i64, i64, i64, i32, vp, i64, vp, i64,
                                      vp, vp, vp, vp, vp]
     L.bitsmoe_shared_basis_gpu.argtypes = [vp, i64, i64, vp, vp, vp, vp]
+    L.bitsmoe_moe_decode_in.argtypes = [vp, vp, vp, vp, i64, i64, i64, i64, i32, vp, i64, vp, i64,
+                                        vp, vp, vp, vp, vp]
     L.bitsmoe_moe_decode_topk.argtypes = [vp, vp, vp, vp, i64, i64, i64, i64, i32, vp, i64, vp,
                                           i64, i64, vp, vp, vp, vp]
     L.bitsmoe_set_lapack.argtypes = [ctypes.c_char_p]
@@ -364,6 +366,35 @@ def moe_decode(codes, params, bits_dev, offsets_dev, total_words: int, E: int, r
                                     tok.ctypes.data_as(ctypes.c_void_p),
                                     wt.ctypes.data_as(ctypes.c_void_p), _dev(out, "Y"), _stream()),
            "moe_decode")
+    return out
+
+
+def moe_decode_in(codes, params, bits_dev, offsets_dev, total_words: int, E: int, r: int,
+                  d_out: int, group: int, Vt, X, routing, out=None):
+    """Input-space (gate/up) decode: y = sum_j g_j C^_e^T (Vt x) for every token
+    of X [B][d_in] (fp32); Vt [r][d_in] fp32; units of length d_out ->
+    fp32 [B][d_out]."""
+    torch = _torch()
+    B = X.shape[0]
+    if X.dtype != torch.float32 or Vt.dtype != torch.float32:
+        raise TypeError("X and Vt must be float32")
+    if X.dim() != 2 or Vt.dim() != 2 or Vt.shape[0] != r or Vt.shape[1] != X.shape[1]:
+        raise ValueError("Vt must be [r][d_in] and X [B][d_in]")
+    off = np.ascontiguousarray(np.asarray(routing[0], dtype=np.int64))
+    tok = np.ascontiguousarray(np.asarray(routing[1], dtype=np.int32))
+    wt = np.ascontiguousarray(np.asarray(routing[2], dtype=np.float32))
+    if off.shape[0] != E + 1 or tok.shape[0] < off[-1] or wt.shape[0] < off[-1]:
+        raise ValueError("routing tables do not match E")
+    if out is None:
+        out = torch.empty((B, d_out), dtype=torch.float32, device=X.device)
+    _check(lib().bitsmoe_moe_decode_in(_dev(codes, "codes"), _dev(params, "params"),
+                                       _dev(bits_dev, "bits"), _dev(offsets_dev, "offsets"),
+                                       int(total_words), E, r, d_out, group, _dev(Vt, "Vt"),
+                                       X.shape[1], _dev(X, "X"), B,
+                                       off.ctypes.data_as(ctypes.c_void_p),
+                                       tok.ctypes.data_as(ctypes.c_void_p),
+                                       wt.ctypes.data_as(ctypes.c_void_p), _dev(out, "Y"), _stream()),
+           "moe_decode_in")
     return out
 
 

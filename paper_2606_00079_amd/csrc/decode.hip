@@ -345,6 +345,157 @@ __global__ __launch_bounds__(1024) void decode_y_kernel(const float* __restrict_
   }
 }
 
+// ---- input-space form (gate/up): y = sum_j g_j C^_e^T z, z = Phi_r^T x ----
+
+// z[b][k] = sum_i Vt[k][i] X[b][i]: one wave per (k, b).
+__global__ __launch_bounds__(256) void zin_kernel(const float* __restrict__ Vt, int r, int64_t d_in,
+                                                  const float* __restrict__ X, int64_t B,
+                                                  float* __restrict__ z) {
+  const int lane = threadIdx.x & 63;
+  const int64_t k = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
+  const int64_t b = blockIdx.y;
+  if (k >= r || b >= B) return;  // whole wave
+  const float* v = Vt + k * d_in;
+  const float* x = X + b * d_in;
+  float acc = 0.0f;
+#pragma unroll 4
+  for (int64_t i = lane; i < d_in; i += 64) acc = fmaf(v[i], x[i], acc);
+  acc = wave_sum(acc);
+  if (lane == 0) z[b * r + k] = acc;
+}
+
+// Partial outputs of the routing entries of one job (blockIdx.y; jobs[2j] =
+// {expert, first entry, entries 1..T, 0}, jobs[2j+1] = their tokens) over the
+// unit rows of row split blockIdx.z:
+//   yp[rz][i][o] = w_i sum_{k in split} z[tok_i][k] c^_{e,k}[o].
+// Thread (slice rs, segment sg) owns the 32 outputs 32 sg .. 32 sg + 31 of
+// segment block blockIdx.x and the rows k = rs, rs + RSL, ... of the split;
+// a unit row's 32 entries there are one word of each of its bit planes and
+// one group parameter, so c^ = q s + m is summed as (z s) q and z m.  The
+// RSL slices are added in slice order through LDS.
+template <int T>
+__global__ __launch_bounds__(256) void yin_kernel(
+    const uint32_t* __restrict__ codes32, const uint32_t* __restrict__ params,
+    const uint8_t* __restrict__ bits, const int64_t* __restrict__ off, int64_t total_words,
+    int r, int d, int G, int SEGW, int rows_split, const float* __restrict__ z,
+    const int4* __restrict__ jobs, const float* __restrict__ ew, int64_t nnz,
+    float* __restrict__ yp) {
+  __shared__ float red[256 * kSeg];
+  const int4 job = jobs[2 * blockIdx.y];
+  const int4 jt = jobs[2 * blockIdx.y + 1];
+  const int e = job.x;
+  const int64_t i0 = job.y;
+  const int nt = job.z;
+  const int tk[4] = {jt.x, jt.y, jt.z, jt.w};
+  const int RSL = 256 / SEGW;
+  const int sg_local = threadIdx.x % SEGW, rs = threadIdx.x / SEGW;
+  const int nseg = d / kSeg;
+  const int sg = static_cast<int>(blockIdx.x) * SEGW + sg_local;
+  const int64_t nw = d / 64;
+  const int kb = static_cast<int>(blockIdx.z) * rows_split;
+  const int ke = min(r, kb + rows_split);
+  float acc[T][kSeg], macc[T];
+#pragma unroll
+  for (int t = 0; t < T; ++t) {
+    macc[t] = 0.0f;
+#pragma unroll
+    for (int j = 0; j < kSeg; ++j) acc[t][j] = 0.0f;
+  }
+  if (sg < nseg) {
+    for (int k = kb + rs; k < ke; k += RSL) {
+      const int64_t u = static_cast<int64_t>(e) * r + k;
+      const int b = bits[u];
+      const int64_t o0 = off[u], o1 = off[u + 1];
+      // a unit whose width or offsets are inconsistent contributes nothing
+      if (!(width_ok(b) && b != 0 && o1 - o0 == b * nw && o0 >= 0 && o1 <= total_words)) continue;
+      float zk[T];
+#pragma unroll
+      for (int t = 0; t < T; ++t) zk[t] = t < nt ? z[static_cast<int64_t>(tk[t]) * r + k] : 0.0f;
+      if (b == 16) {
+        const uint2* h = reinterpret_cast<const uint2*>(codes32 + 2 * o0) + 8 * sg;
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+          const uint2 v = h[q];
+          const float c[4] = {f16_bits_to_f32(static_cast<uint16_t>(v.x & 0xffffu)),
+                              f16_bits_to_f32(static_cast<uint16_t>(v.x >> 16)),
+                              f16_bits_to_f32(static_cast<uint16_t>(v.y & 0xffffu)),
+                              f16_bits_to_f32(static_cast<uint16_t>(v.y >> 16))};
+#pragma unroll
+          for (int c4 = 0; c4 < 4; ++c4)
+#pragma unroll
+            for (int t = 0; t < T; ++t) acc[t][4 * q + c4] = fmaf(zk[t], c[c4], acc[t][4 * q + c4]);
+        }
+        continue;
+      }
+      const uint32_t prm = params[u * (d / G) + (sg * kSeg) / G];
+      const float s = f16_bits_to_f32(static_cast<uint16_t>(prm & 0xffffu));
+      const float m = f16_bits_to_f32(static_cast<uint16_t>(prm >> 16));
+      const uint32_t* pw = codes32 + 2 * o0 + sg;  // plane t: word 2 (o0 + t nw) + sg
+      uint32_t qb[kSeg / 4];
+      {
+        const uint32_t p0 = pw[0];
+#pragma unroll
+        for (int kk = 0; kk < kSeg / 4; ++kk) qb[kk] = spread4(p0 >> (4 * kk));
+      }
+      for (int t = 1; t < b; ++t) {
+        const uint32_t pt = pw[2 * t * nw];
+#pragma unroll
+        for (int kk = 0; kk < kSeg / 4; ++kk) qb[kk] |= spread4(pt >> (4 * kk)) << t;
+      }
+      float zs[T];
+#pragma unroll
+      for (int t = 0; t < T; ++t) {
+        zs[t] = zk[t] * s;
+        macc[t] = fmaf(zk[t], m, macc[t]);
+      }
+#pragma unroll
+      for (int kk = 0; kk < kSeg / 4; ++kk)
+#pragma unroll
+        for (int c4 = 0; c4 < 4; ++c4) {
+          const float q = static_cast<float>((qb[kk] >> (8 * c4)) & 0xffu);
+#pragma unroll
+          for (int t = 0; t < T; ++t) acc[t][4 * kk + c4] = fmaf(zs[t], q, acc[t][4 * kk + c4]);
+        }
+    }
+  }
+  // slices in order, one token at a time: red[rs][sg_local][j]
+  for (int t = 0; t < T; ++t) {
+    if (t >= nt) break;  // uniform over the workgroup
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < kSeg; ++j) red[(rs * SEGW + sg_local) * kSeg + j] = acc[t][j] + macc[t];
+    __syncthreads();
+    const float wt = ew[i0 + t];
+    for (int idx = threadIdx.x; idx < SEGW * kSeg; idx += 256) {
+      const int sgl = idx / kSeg, j = idx - sgl * kSeg;
+      const int sgo = static_cast<int>(blockIdx.x) * SEGW + sgl;
+      if (sgo >= nseg) continue;
+      float v = 0.0f;
+      for (int q = 0; q < RSL; ++q) v += red[(q * SEGW + sgl) * kSeg + j];
+      yp[(static_cast<int64_t>(blockIdx.z) * nnz + i0 + t) * d + static_cast<int64_t>(sgo) * kSeg + j] =
+          wt * v;
+    }
+  }
+}
+
+// y[b][o] = sum over row splits (in order) of the sum over token b's routing
+// entries (in the order given) of yp[rz][i][o].
+__global__ __launch_bounds__(256) void ysum_kernel(const float* __restrict__ yp, int nsplit,
+                                                   int64_t nnz, const int64_t* __restrict__ pidx,
+                                                   int kmax, int64_t d, int64_t B,
+                                                   float* __restrict__ Y) {
+  const int64_t o = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  const int64_t b = blockIdx.y;
+  if (o >= d || b >= B) return;
+  float s = 0.0f;
+  for (int q = 0; q < nsplit; ++q)
+    for (int j = 0; j < kmax; ++j) {
+      const int64_t i = pidx[b * kmax + j];
+      if (i >= 0) s += yp[(q * nnz + i) * d + o];
+    }
+  Y[b * d + o] = s;
+}
+
 }  // namespace
 }  // namespace bitsmoe
 
@@ -366,9 +517,93 @@ bitsmoe_status check_decode(const char* who, const void* codes, const void* para
   if (!(group == 32 || group == 64 || group == 128 || group == 256))
     return fail(BITSMOE_ERR_SHAPE, w + ": group must be 32, 64, 128 or 256");
   if (d_in % 64 != 0 || d_in % group != 0)
-    return fail(BITSMOE_ERR_SHAPE, w + ": d_in must be a multiple of 64 and of the group");
+    return fail(BITSMOE_ERR_SHAPE, w + ": the units' length must be a multiple of 64 and of the group");
   if (r > 8192) return fail(BITSMOE_ERR_SHAPE, w + ": r above 8192");
-  if (d_in > (1 << 20)) return fail(BITSMOE_ERR_SHAPE, w + ": d_in above 2^20");
+  if (d_in > (1 << 20)) return fail(BITSMOE_ERR_SHAPE, w + ": the units' length is above 2^20");
+  return ok();
+}
+
+// Host routing grouped by expert, checked, with each token's entries (in the
+// order given) and the experts' entries in jobs of up to T (4 when some
+// expert has several tokens, else 1).
+struct RoutingTables {
+  int64_t nnz = 0, kmax = 1, njobs = 0;
+  int T = 1;
+  std::vector<int64_t> pidx;   // [B][kmax], -1 = none
+  std::vector<int32_t> jobs;   // per job: {expert, first entry, entries, 0}, {tokens}
+};
+
+bitsmoe_status build_routing(const std::string& who, int64_t E, int64_t B,
+                             const int64_t* offsets_host, const int32_t* tokens_host,
+                             const float* weights_host, RoutingTables* rt) {
+  if (!offsets_host || !tokens_host || !weights_host) return fail(BITSMOE_ERR_ARG, who + ": null pointer");
+  if (offsets_host[0] != 0) return fail(BITSMOE_ERR_ARG, who + ": offsets[0] must be 0");
+  for (int64_t e = 0; e < E; ++e)
+    if (offsets_host[e + 1] < offsets_host[e])
+      return fail(BITSMOE_ERR_ARG, who + ": offsets must not decrease");
+  const int64_t nnz = offsets_host[E];
+  if (nnz > INT32_MAX) return fail(BITSMOE_ERR_SHAPE, who + ": too many routing entries");
+  std::vector<int64_t> cnt(static_cast<size_t>(B), 0);
+  for (int64_t i = 0; i < nnz; ++i) {
+    if (tokens_host[i] < 0 || tokens_host[i] >= B)
+      return fail(BITSMOE_ERR_ARG, who + ": token index outside [0, B)");
+    if (!std::isfinite(weights_host[i])) return fail(BITSMOE_ERR_ARG, who + ": non-finite weight");
+    ++cnt[static_cast<size_t>(tokens_host[i])];
+  }
+  int64_t kmax = 1;
+  for (int64_t c : cnt) kmax = std::max(kmax, c);
+  if (kmax > 65535) return fail(BITSMOE_ERR_SHAPE, who + ": more than 65535 entries of one token");
+  rt->pidx.assign(static_cast<size_t>(B * kmax), -1);
+  std::fill(cnt.begin(), cnt.end(), 0);
+  for (int64_t i = 0; i < nnz; ++i) {
+    const int64_t b = tokens_host[i];
+    rt->pidx[static_cast<size_t>(b * kmax + cnt[static_cast<size_t>(b)]++)] = i;
+  }
+  int64_t cmax = 0;
+  for (int64_t e = 0; e < E; ++e) cmax = std::max(cmax, offsets_host[e + 1] - offsets_host[e]);
+  const int T = cmax > 1 ? 4 : 1;
+  rt->jobs.clear();
+  for (int64_t e = 0; e < E; ++e)
+    for (int64_t i = offsets_host[e]; i < offsets_host[e + 1]; i += T) {
+      const int64_t n = std::min<int64_t>(T, offsets_host[e + 1] - i);
+      rt->jobs.push_back(static_cast<int32_t>(e));
+      rt->jobs.push_back(static_cast<int32_t>(i));
+      rt->jobs.push_back(static_cast<int32_t>(n));
+      rt->jobs.push_back(0);
+      for (int t = 0; t < 4; ++t) rt->jobs.push_back(t < n ? tokens_host[i + t] : 0);
+    }
+  rt->njobs = static_cast<int64_t>(rt->jobs.size() / 8);
+  if (rt->njobs > 65535) return fail(BITSMOE_ERR_SHAPE, who + ": more than 65535 routing chunks");
+  rt->nnz = nnz;
+  rt->kmax = kmax;
+  rt->T = T;
+  return ok();
+}
+
+// Device copies of the jobs [njobs][8], the weights [nnz] and the token entry
+// lists [B][kmax] in the small-table scratch; waits for the stream (the host
+// tables may go away after the call returns).
+bitsmoe_status upload_routing(const std::string& who, const RoutingTables& rt,
+                              const float* weights_host, int64_t B, void* stream, int4** jobs_d,
+                              int64_t** pidx_d, float** w_d) {
+  bitsmoe_status st;
+  const size_t job_bytes = static_cast<size_t>(std::max<int64_t>(rt.njobs, 1)) * 32;
+  const size_t pidx_bytes = static_cast<size_t>(B * rt.kmax) * 8;
+  const size_t w_bytes = (static_cast<size_t>(rt.nnz) * 4 + 15) / 16 * 16;
+  char* tab = static_cast<char*>(scratch(kScratchMisc, job_bytes + pidx_bytes + w_bytes + 64, stream, &st));
+  if (!tab) return st;
+  *jobs_d = reinterpret_cast<int4*>(tab);
+  *pidx_d = reinterpret_cast<int64_t*>(tab + job_bytes);
+  *w_d = reinterpret_cast<float*>(tab + job_bytes + pidx_bytes);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipError_t he = hipSuccess;
+  if (rt.njobs > 0) he = hipMemcpyAsync(*jobs_d, rt.jobs.data(), rt.njobs * 32, hipMemcpyHostToDevice, s);
+  if (he == hipSuccess)
+    he = hipMemcpyAsync(*pidx_d, rt.pidx.data(), B * rt.kmax * 8, hipMemcpyHostToDevice, s);
+  if (he == hipSuccess && rt.nnz > 0)
+    he = hipMemcpyAsync(*w_d, weights_host, rt.nnz * 4, hipMemcpyHostToDevice, s);
+  if (he == hipSuccess) he = hipStreamSynchronize(s);
+  if (he != hipSuccess) return device_error((who + ": routing table copy").c_str(), he);
   return ok();
 }
 
@@ -468,73 +703,22 @@ extern "C" bitsmoe_status bitsmoe_moe_decode(const uint64_t* codes_dev, const ui
   bitsmoe_status st = check_decode("moe_decode", codes_dev, params_dev, bits_dev, word_offsets_dev,
                                    Ut_dev, X_dev, Y_dev, total_words, E, r, d_in, group, d_out, B);
   if (st != BITSMOE_OK) return st;
-  if (!offsets_host || !tokens_host || !weights_host)
-    return fail(BITSMOE_ERR_ARG, "moe_decode: null pointer");
-  if (offsets_host[0] != 0) return fail(BITSMOE_ERR_ARG, "moe_decode: offsets[0] must be 0");
-  for (int64_t e = 0; e < E; ++e)
-    if (offsets_host[e + 1] < offsets_host[e])
-      return fail(BITSMOE_ERR_ARG, "moe_decode: offsets must not decrease");
-  const int64_t nnz = offsets_host[E];
-  if (nnz > INT32_MAX) return fail(BITSMOE_ERR_SHAPE, "moe_decode: too many routing entries");
-  // routing entries of each token, in the order given (fixed summation order)
-  std::vector<int64_t> cnt(static_cast<size_t>(B), 0);
-  for (int64_t i = 0; i < nnz; ++i) {
-    if (tokens_host[i] < 0 || tokens_host[i] >= B)
-      return fail(BITSMOE_ERR_ARG, "moe_decode: token index outside [0, B)");
-    if (!std::isfinite(weights_host[i])) return fail(BITSMOE_ERR_ARG, "moe_decode: non-finite weight");
-    ++cnt[static_cast<size_t>(tokens_host[i])];
-  }
-  int64_t kmax = 1;
-  for (int64_t c : cnt) kmax = std::max(kmax, c);
-  if (kmax > 65535) return fail(BITSMOE_ERR_SHAPE, "moe_decode: more than 65535 entries of one token");
-  std::vector<int64_t> pidx(static_cast<size_t>(B * kmax), -1);
-  std::fill(cnt.begin(), cnt.end(), 0);
-  for (int64_t i = 0; i < nnz; ++i) {
-    const int64_t b = tokens_host[i];
-    pidx[static_cast<size_t>(b * kmax + cnt[static_cast<size_t>(b)]++)] = i;
-  }
-  // jobs: every expert's routing entries in chunks of T (4 when some expert
-  // has several tokens, else 1, which needs fewer registers)
-  int64_t cmax = 0;
-  for (int64_t e = 0; e < E; ++e) cmax = std::max(cmax, offsets_host[e + 1] - offsets_host[e]);
-  const int T = cmax > 1 ? 4 : 1;
-  std::vector<int32_t> jobs;  // per job: {expert, first entry, entries, 0}, {tokens}
-  for (int64_t e = 0; e < E; ++e)
-    for (int64_t i = offsets_host[e]; i < offsets_host[e + 1]; i += T) {
-      const int64_t n = std::min<int64_t>(T, offsets_host[e + 1] - i);
-      jobs.push_back(static_cast<int32_t>(e));
-      jobs.push_back(static_cast<int32_t>(i));
-      jobs.push_back(static_cast<int32_t>(n));
-      jobs.push_back(0);
-      for (int t = 0; t < 4; ++t) jobs.push_back(t < n ? tokens_host[i + t] : 0);
-    }
-  const int64_t njobs = static_cast<int64_t>(jobs.size() / 8);
-  if (njobs > 65535) return fail(BITSMOE_ERR_SHAPE, "moe_decode: more than 65535 routing chunks");
-  const DecodeGeom g = decode_geometry(njobs, r, d_in, B);
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  // device tables: jobs [njobs][8], routing weights [nnz], token entry
-  // lists [B][kmax]; partials zp [nnz][r]
-  const size_t job_bytes = static_cast<size_t>(std::max<int64_t>(njobs, 1)) * 32;
-  const size_t pidx_bytes = static_cast<size_t>(B * kmax) * 8;
-  const size_t w_bytes = (static_cast<size_t>(nnz) * 4 + 15) / 16 * 16;
-  const size_t tab_bytes = job_bytes + pidx_bytes + w_bytes + 64;
-  char* tab = static_cast<char*>(scratch(kScratchMisc, tab_bytes, stream, &st));
-  if (!tab) return st;
-  int4* jobs_d = reinterpret_cast<int4*>(tab);
-  int64_t* pidx_d = reinterpret_cast<int64_t*>(tab + job_bytes);
-  float* w_d = reinterpret_cast<float*>(tab + job_bytes + pidx_bytes);
-  hipError_t he = hipSuccess;
-  if (njobs > 0) he = hipMemcpyAsync(jobs_d, jobs.data(), njobs * 32, hipMemcpyHostToDevice, s);
-  if (he == hipSuccess)
-    he = hipMemcpyAsync(pidx_d, pidx.data(), B * kmax * 8, hipMemcpyHostToDevice, s);
-  if (he == hipSuccess && nnz > 0) he = hipMemcpyAsync(w_d, weights_host, nnz * 4, hipMemcpyHostToDevice, s);
-  if (he == hipSuccess) he = hipStreamSynchronize(s);  // host tables may go away after return
-  if (he != hipSuccess) return device_error("moe_decode: routing table copy", he);
-  float* zp = static_cast<float*>(scratch(kScratchPart, std::max<int64_t>(nnz, 1) * r * 4, stream, &st));
+  RoutingTables rt;
+  st = build_routing("moe_decode", E, B, offsets_host, tokens_host, weights_host, &rt);
+  if (st != BITSMOE_OK) return st;
+  const DecodeGeom g = decode_geometry(rt.njobs, r, d_in, B);
+  int4* jobs_d;
+  int64_t* pidx_d;
+  float* w_d;
+  st = upload_routing("moe_decode", rt, weights_host, B, stream, &jobs_d, &pidx_d, &w_d);
+  if (st != BITSMOE_OK) return st;
+  // partials zp [nnz][r]
+  float* zp = static_cast<float*>(scratch(kScratchPart, std::max<int64_t>(rt.nnz, 1) * r * 4, stream, &st));
   if (!zp) return st;
-  return decode_launch(g, T, false, njobs, codes_dev, params_dev, bits_dev, word_offsets_dev,
+  return decode_launch(g, rt.T, false, rt.njobs, codes_dev, params_dev, bits_dev, word_offsets_dev,
                        total_words, E, r, d_in, group, Ut_dev, d_out, X_dev, B, jobs_d, nullptr, 1,
-                       w_d, pidx_d, static_cast<int>(kmax), zp, Y_dev, s);
+                       w_d, pidx_d, static_cast<int>(rt.kmax), zp, Y_dev,
+                       static_cast<hipStream_t>(stream));
 }
 
 extern "C" bitsmoe_status bitsmoe_moe_decode_topk(const uint64_t* codes_dev, const uint16_t* params_dev,
@@ -565,4 +749,81 @@ extern "C" bitsmoe_status bitsmoe_moe_decode_topk(const uint64_t* codes_dev, con
                        total_words, E, r, d_in, group, Ut_dev, d_out, X_dev, B, nullptr,
                        topk_experts_dev, static_cast<int>(k), topk_weights_dev, nullptr,
                        static_cast<int>(k), zp, Y_dev, static_cast<hipStream_t>(stream));
+}
+
+extern "C" bitsmoe_status bitsmoe_moe_decode_in(const uint64_t* codes_dev, const uint16_t* params_dev,
+                                                const uint8_t* bits_dev,
+                                                const int64_t* word_offsets_dev,
+                                                int64_t total_words, int64_t E, int64_t r,
+                                                int64_t d_out, int group, const float* Vt_dev,
+                                                int64_t d_in, const float* X_dev, int64_t B,
+                                                const int64_t* offsets_host,
+                                                const int32_t* tokens_host,
+                                                const float* weights_host, float* Y_dev,
+                                                void* stream) {
+  // the units have d_out entries here: the shape rules of the packed rows
+  // apply to d_out, the basis rows and tokens have d_in
+  bitsmoe_status st = check_decode("moe_decode_in", codes_dev, params_dev, bits_dev,
+                                   word_offsets_dev, Vt_dev, X_dev, Y_dev, total_words, E, r, d_out,
+                                   group, d_in, B);
+  if (st != BITSMOE_OK) return st;
+  if (d_in > (1 << 20)) return fail(BITSMOE_ERR_SHAPE, "moe_decode_in: d_in above 2^20");
+  RoutingTables rt;
+  st = build_routing("moe_decode_in", E, B, offsets_host, tokens_host, weights_host, &rt);
+  if (st != BITSMOE_OK) return st;
+  int4* jobs_d;
+  int64_t* pidx_d;
+  float* w_d;
+  st = upload_routing("moe_decode_in", rt, weights_host, B, stream, &jobs_d, &pidx_d, &w_d);
+  if (st != BITSMOE_OK) return st;
+  // segments of 32 outputs: SEGW per workgroup (a power of two up to 256),
+  // RSL = 256 / SEGW row slices; rows split over blockIdx.z for about 1024
+  // workgroups
+  const int64_t nseg = d_out / kSeg;
+  int SEGW = 2;
+  while (SEGW < nseg && SEGW < 256) SEGW *= 2;
+  const int RSL = 256 / SEGW;
+  const int64_t segblocks = (nseg + SEGW - 1) / SEGW;
+  const int64_t max_split = (r + RSL - 1) / RSL;
+  int64_t nsplit = std::clamp<int64_t>(1024 / std::max<int64_t>(rt.njobs * segblocks, 1), 1, max_split);
+  const int64_t rows_split = (r + nsplit - 1) / nsplit;
+  nsplit = (r + rows_split - 1) / rows_split;
+  if (nsplit > 65535 || segblocks > 65535) return fail(BITSMOE_ERR_SHAPE, "moe_decode_in: too large");
+  // z [B][r], partials yp [nsplit][nnz][d_out]
+  const size_t zbytes = (static_cast<size_t>(B * r) * 4 + 255) / 256 * 256;
+  char* part = static_cast<char*>(scratch(
+      kScratchPart, zbytes + static_cast<size_t>(nsplit * std::max<int64_t>(rt.nnz, 1) * d_out) * 4,
+      stream, &st));
+  if (!part) return st;
+  float* z = reinterpret_cast<float*>(part);
+  float* yp = reinterpret_cast<float*>(part + zbytes);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  {
+    KernelTimer timer("moe_decode_in_z", stream);
+    hipLaunchKernelGGL(zin_kernel, dim3(static_cast<unsigned>((r + 3) / 4), static_cast<unsigned>(B)),
+                       dim3(256), 0, s, Vt_dev, static_cast<int>(r), d_in, X_dev, B, z);
+  }
+  BITSMOE_LAUNCH_CHECK("moe_decode_in: z launch");
+  const uint32_t* pr = reinterpret_cast<const uint32_t*>(params_dev);
+  const uint32_t* c32 = reinterpret_cast<const uint32_t*>(codes_dev);
+  if (rt.njobs > 0) {
+    KernelTimer timer("moe_decode_in_y", stream);
+    dim3 grid(static_cast<unsigned>(segblocks), static_cast<unsigned>(rt.njobs),
+              static_cast<unsigned>(nsplit));
+#define BITSMOE_DECIN(TT)                                                                           \
+  hipLaunchKernelGGL(yin_kernel<TT>, grid, dim3(256), 0, s, c32, pr, bits_dev, word_offsets_dev,    \
+                     total_words, static_cast<int>(r), static_cast<int>(d_out), group, SEGW,        \
+                     static_cast<int>(rows_split), z, jobs_d, w_d, rt.nnz, yp)
+    if (rt.T == 4) BITSMOE_DECIN(4); else BITSMOE_DECIN(1);
+#undef BITSMOE_DECIN
+  }
+  BITSMOE_LAUNCH_CHECK("moe_decode_in: y launch");
+  {
+    KernelTimer timer("moe_decode_in_sum", stream);
+    hipLaunchKernelGGL(ysum_kernel, dim3(static_cast<unsigned>((d_out + 255) / 256), static_cast<unsigned>(B)),
+                       dim3(256), 0, s, yp, static_cast<int>(nsplit), rt.nnz, pidx_d,
+                       static_cast<int>(rt.kmax), d_out, B, Y_dev);
+  }
+  BITSMOE_LAUNCH_CHECK("moe_decode_in: sum launch");
+  return ok();
 }

@@ -254,6 +254,15 @@ def test_device_entry_points_validate_before_launch(lib):
                                   off, dtok, dw, fake, s) == 1
     assert lib.bitsmoe_moe_decode_topk(fake, fake, fake, fake, 10, 2, 8, 128, 64, fake, 64, fake,
                                        2, 2, odd, fake, fake, s) == 1
+    # input-space decode: the units' length (d_out) follows the pack rules
+    assert lib.bitsmoe_moe_decode_in(fake, fake, fake, fake, 10, 2, 8, 100, 64, fake, 64, fake, 2,
+                                     off, dtok, dw, fake, s) == 2
+    assert lib.bitsmoe_moe_decode_in(fake, fake, fake, fake, 10, 2, 8, 128, 64, fake, 64, fake, 2,
+                                     off, dbad, dw, fake, s) == 1
+    assert lib.bitsmoe_moe_decode_in(fake, fake, fake, fake, 10, 2, 8, 128, 64, fake, 0, fake, 2,
+                                     off, dtok, dw, fake, s) == 1
+    assert lib.bitsmoe_moe_decode_in(fake, fake, fake, fake, 10, 2, 8, 128, 64, fake, 64, odd, 2,
+                                     off, dtok, dw, fake, s) == 1
     # top-k decode: k outside [1, E], B k above 65535, shape rules, nulls
     assert lib.bitsmoe_moe_decode_topk(fake, fake, fake, fake, 10, 2, 8, 128, 64, fake, 64, fake,
                                        2, 0, fake, fake, fake, s) == 1

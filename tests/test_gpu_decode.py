@@ -153,3 +153,44 @@ def test_moe_decode_topk_skips_experts_out_of_range():
                            bad=((0, 1, -1), (2, 0, 8), (3, 2, 1 << 30)))
     assert relfro(Y, ref) <= REL
     assert relfro(Y, Yg) <= 1e-5
+
+
+# ---- input-space form (gate/up): y = sum_j g_j C^_e^T (Vt x) ----
+
+def _run_in(E, r, d_out, d_in, B, k, G, widths, seed):
+    g = np.random.default_rng(seed)
+    C = (g.standard_normal((E * r, d_out)) * np.exp(g.standard_normal((E * r, 1)))).astype(np.float32)
+    bits_u = g.choice(widths, size=E * r).astype(np.uint8)
+    codes, params, off = oracle.pack(C, bits_u, G)
+    Vt = np.ascontiguousarray(np.linalg.qr(g.standard_normal((d_in, r)))[0].T, dtype=np.float32)
+    X = g.standard_normal((B, d_in)).astype(np.float32)
+    logits = g.standard_normal((B, E))
+    top = np.argsort(-logits, axis=1)[:, :k]
+    wts = np.exp(np.take_along_axis(logits, top, 1))
+    wts = (wts / wts.sum(1, keepdims=True)).astype(np.float32)
+    tok = np.repeat(np.arange(B, dtype=np.int32), k)
+    ex = top.reshape(-1)
+    order = np.lexsort((tok, ex))
+    offs = np.r_[0, np.cumsum(np.bincount(ex, minlength=E))].astype(np.int64)
+    routing = (offs, tok[order], wts.reshape(-1)[order])
+    cd = torch.from_numpy(codes.view(np.int64).copy() if len(codes) else np.zeros(1, np.int64)).to(DEV)
+    pd = torch.from_numpy(params.view(np.int16).copy()).to(DEV)
+    Y = bm.moe_decode_in(cd, pd, torch.from_numpy(bits_u).to(DEV), torch.from_numpy(off).to(DEV),
+                         int(off[-1]), E, r, d_out, G, torch.from_numpy(Vt).to(DEV),
+                         torch.from_numpy(X).to(DEV), routing).cpu().numpy()
+    Chat = decode.dequantized_factors(codes, params, bits_u, d_out, G)
+    return Y, decode.moe_decode_in(Chat, r, Vt, X, *routing)
+
+
+@pytest.mark.parametrize("E,r,d_out,d_in,B,k,G,widths", [
+    (4, 64, 128, 256, 24, 2, 64, (1, 2, 3, 4)),
+    (6, 40, 192, 96, 17, 3, 32, (0, 1, 2, 4, 8, 16)),   # eviction and fp16 rows
+    (3, 8, 64, 768, 1, 1, 32, (2, 3)),                  # 64-entry units, one token
+    (4, 30, 9216, 64, 5, 2, 128, (1, 2, 16)),           # two segment blocks
+    (16, 384, 768, 2048, 1, 8, 128, (1, 2, 3, 4)),      # Qwen3-30B-A3B gate, one token
+    (16, 384, 768, 2048, 64, 8, 128, (1, 2, 3, 4)),     # the same, 64 tokens
+])
+def test_moe_decode_in_matches_oracle(E, r, d_out, d_in, B, k, G, widths):
+    say("decode_in", E, r, d_out, d_in, B, k, G, widths)
+    Y, ref = _run_in(E, r, d_out, d_in, B, k, G, widths, seed=E + r + B)
+    assert relfro(Y, ref) <= REL
