@@ -232,7 +232,7 @@ def routed_report(cfg, layer, dev_inputs, bm, pipeline) -> dict:
     return {"top_k": synth.TOP_K.get(cfg.name), "projections": parts, "kernel_ms": kt}
 
 
-def inspace_report(layer, res, dev_inputs, bm, pipeline) -> dict:
+def inspace_report(cfg, layer, res, dev_inputs, bm, pipeline) -> dict:
     """The paper's input-space construction of the gate/up projections (basis
     from M_in = sum W_e^T W_e, diagonal-approximation loss), once each, on the
     same weights, calibration Gram, r, widths and budget."""
@@ -241,26 +241,42 @@ def inspace_report(layer, res, dev_inputs, bm, pipeline) -> dict:
     for n in names:
         bm.kernel_time(n)
     bm.timing(True)
-    parts = []
+    parts, last = [], {}
     for p, r, inp in zip(layer, res, dev_inputs):
         if p.spec.name not in ("gate", "up"):
             continue
         ri = pipeline.quantize_projection_in(inp["W"], inp["X"], inp["r"], inp["bits"],
                                              inp["group"], inp["budget"], H=r.H)
         torch.cuda.synchronize()
+        last[p.spec.name] = ri
         parts.append({"projection": p.spec.name,
                       "gpu_ms": round(ri.times["gpu_ms"], 4),
                       "host_eig_ms": round(ri.times["host_eig_ms"], 2),
                       "host_ilp_ms": round(ri.times["host_ilp_ms"], 2)})
     bm.timing(False)
     kt = {n: round(bm.kernel_time(n)[0], 4) for n in names}
+    # stage-3 decode of the input-space gate projection (z = Phi^T x first)
+    import synth
+    dec = []
+    for p, inp in zip(layer, dev_inputs):
+        if p.spec.name != "gate":
+            continue
+        ri = last[p.spec.name]
+        for B in (1, 64):
+            Xh = inp["X"][:B].float().cpu().numpy()
+            routing = synth.routing(cfg, Xh if cfg.dtype == "f32" else synth.f32_to_bf16_bits(Xh))
+            c = _decode_case(p, ri, inp, routing, inp["X"][:B].float().contiguous(), bm, 50, form="in")
+            c["projection"] = p.spec.name
+            dec.append(c)
     return {"projections": parts, "kernel_ms": kt,
-            "gpu_ms_gate_up": round(sum(q["gpu_ms"] for q in parts), 4)}
+            "gpu_ms_gate_up": round(sum(q["gpu_ms"] for q in parts), 4), "decode": dec}
 
 
-def _decode_case(p, r, inp, routing, Xdec, bm, reps):
+def _decode_case(p, r, inp, routing, Xdec, bm, reps, form="out"):
     """One projection, one decode batch: the packed-factor decode and a dense
-    bf16 batched GEMV/GEMM over the same routed experts."""
+    bf16 batched GEMV/GEMM over the same routed experts.  form "out": the
+    output-space factors (y = U sum g C^ x); "in": the input-space ones of
+    gate/up (y = sum g C^^T Phi^T x; r.Ut holds Phi^T)."""
     import numpy as np
     import torch
     E, d_out, d_in, G = p.E, p.spec.d_out, p.spec.d_in, p.group
@@ -270,29 +286,39 @@ def _decode_case(p, r, inp, routing, Xdec, bm, reps):
     bits_d = torch.from_numpy(np.ascontiguousarray(r.bits_u)).cuda()
     off_d = torch.from_numpy(np.ascontiguousarray(r.offsets)).cuda()
     Y = torch.empty((B, d_out), dtype=torch.float32, device="cuda")
+    ulen = d_in if form == "out" else d_out  # length of the packed units
+    names = ("moe_decode_z", "moe_decode_y") if form == "out" else \
+        ("moe_decode_in_z", "moe_decode_in_y", "moe_decode_in_sum")
+
+    def run():
+        if form == "out":
+            bm.moe_decode(r.codes, r.params, bits_d, off_d, int(r.offsets[-1]), E, p.r, d_in, G,
+                          r.Ut, Xdec, routing, out=Y)
+        else:
+            bm.moe_decode_in(r.codes, r.params, bits_d, off_d, int(r.offsets[-1]), E, p.r, d_out, G,
+                             r.Ut, Xdec, routing, out=Y)
     for _ in range(3):
-        bm.moe_decode(r.codes, r.params, bits_d, off_d, int(r.offsets[-1]), E, p.r, d_in, G, r.Ut,
-                      Xdec, routing, out=Y)
+        run()
     torch.cuda.synchronize()
     bm.timing(True)
-    bm.kernel_time("moe_decode_z")
-    bm.kernel_time("moe_decode_y")
+    for n in names:
+        bm.kernel_time(n)
     t0 = time.perf_counter()
     for _ in range(reps):
-        bm.moe_decode(r.codes, r.params, bits_d, off_d, int(r.offsets[-1]), E, p.r, d_in, G, r.Ut,
-                      Xdec, routing, out=Y)
+        run()
     torch.cuda.synchronize()
     call_ms = (time.perf_counter() - t0) * 1e3 / reps
-    zms = bm.kernel_time("moe_decode_z")[0] / reps
-    yms = bm.kernel_time("moe_decode_y")[0] / reps
+    kms = [bm.kernel_time(n)[0] / reps for n in names]
+    zms, yms = kms[0], sum(kms[1:])
     bm.timing(False)
     # algorithmic bytes: the touched experts' packed units (bit planes, group
-    # parameters, fp16 rows), U^T in fp32, X and Y
+    # parameters, fp16 rows), the basis in fp32, X and Y
     touched = [e for e in range(E) if offs[e + 1] > offs[e]]
     bu = r.bits_u.reshape(E, p.r)[touched].astype(np.int64)
-    packed = int(np.sum(np.where(bu == 16, 2 * d_in,
-                                 np.where(bu == 0, 0, bu * d_in // 8 + 4 * (d_in // G)))))
-    dec_bytes = packed + p.r * d_out * 4 + B * d_in * 4 + B * d_out * 4
+    packed = int(np.sum(np.where(bu == 16, 2 * ulen,
+                                 np.where(bu == 0, 0, bu * ulen // 8 + 4 * (ulen // G)))))
+    basis = p.r * (d_out if form == "out" else d_in) * 4
+    dec_bytes = packed + basis + B * d_in * 4 + B * d_out * 4
     # dense bf16 baseline: the touched experts' weights gathered contiguous
     # (outside the timed region), one batched product, weighted combine
     W = inp["W"]
@@ -334,6 +360,13 @@ def _decode_case(p, r, inp, routing, Xdec, bm, reps):
     bmm_ms = a.elapsed_time(b) / reps
     dense_bytes = len(touched) * d_out * d_in * W.element_size() + B * d_in * 2 + B * d_out * 4
     dev_ms = zms + yms
+    if form == "in":
+        return {"tokens": B, "experts_touched": len(touched), "routing_entries": nnz,
+                "z_kernel_ms": round(zms, 5), "y_kernel_ms": round(yms, 5),
+                "device_ms": round(dev_ms, 5), "call_ms_incl_host_routing": round(call_ms, 4),
+                "bytes": dec_bytes, "gbs": round(dec_bytes / (dev_ms * 1e-3) / 1e9, 1),
+                "dense_bf16_bmm_only_ms": round(bmm_ms, 5),
+                "speedup_vs_dense_bf16_bmm": round(bmm_ms / dev_ms, 2)}
     # the same tokens from a device top-k table (no host work per call),
     # calls back to back as in a decode loop
     top = np.full((B, 8 if nnz >= 8 * B else max(1, nnz // B)), -1, dtype=np.int32)
@@ -571,7 +604,7 @@ def main(argv=None) -> int:
     # reported beside the exact path with its agreement with the exact costs.
     side = not args.core_only
     sur = surrogate_report(cfg, layer, res, dev_inputs, bm, pipeline) if side else None
-    insp = inspace_report(layer, res, dev_inputs, bm, pipeline) if side else None
+    insp = inspace_report(cfg, layer, res, dev_inputs, bm, pipeline) if side else None
     rout = routed_report(cfg, layer, dev_inputs, bm, pipeline) if side else None
     dec = decode_report(cfg, layer, res, dev_inputs, bm) if side else None
     eigr = eig_report(cfg, layer, res, bm) if side and args.eig == "host" else None

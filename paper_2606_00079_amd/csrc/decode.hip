@@ -459,8 +459,9 @@ __global__ __launch_bounds__(256) void yin_kernel(
     }
   }
   // slices in order, one token at a time: red[rs][sg_local][j]
+#pragma unroll
   for (int t = 0; t < T; ++t) {
-    if (t >= nt) break;  // uniform over the workgroup
+    if (t >= nt) continue;  // uniform over the workgroup
     __syncthreads();
 #pragma unroll
     for (int j = 0; j < kSeg; ++j) red[(rs * SEGW + sg_local) * kSeg + j] = acc[t][j] + macc[t];
@@ -478,22 +479,51 @@ __global__ __launch_bounds__(256) void yin_kernel(
   }
 }
 
-// y[b][o] = sum over row splits (in order) of the sum over token b's routing
-// entries (in the order given) of yp[rz][i][o].
+// y[b][o] = the sum of the partials yp[rz][i][o] over the row splits rz and
+// token b's routing entries i: P = nsplit kmax partials per output.  A
+// workgroup covers 64 outputs of one token; token b's entry list is staged
+// in LDS first, then its four waves take the partials p = w mod 4 with 16
+// accumulators each (16 independent loads in flight), combined in a fixed
+// order through LDS.
 __global__ __launch_bounds__(256) void ysum_kernel(const float* __restrict__ yp, int nsplit,
                                                    int64_t nnz, const int64_t* __restrict__ pidx,
                                                    int kmax, int64_t d, int64_t B,
                                                    float* __restrict__ Y) {
-  const int64_t o = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  constexpr int U = 16;
+  __shared__ float red[4][64];
+  __shared__ int64_t ent[1024];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int64_t o = static_cast<int64_t>(blockIdx.x) * 64 + lane;
   const int64_t b = blockIdx.y;
-  if (o >= d || b >= B) return;
-  float s = 0.0f;
-  for (int q = 0; q < nsplit; ++q)
-    for (int j = 0; j < kmax; ++j) {
-      const int64_t i = pidx[b * kmax + j];
-      if (i >= 0) s += yp[(q * nnz + i) * d + o];
+  float a[U];
+#pragma unroll
+  for (int q = 0; q < U; ++q) a[q] = 0.0f;
+  for (int j0 = 0; j0 < kmax; j0 += 1024) {  // entry lists longer than 1024: in pieces
+    const int nj = min(1024, kmax - j0);
+    __syncthreads();
+    for (int j = threadIdx.x; j < nj; j += 256) ent[j] = pidx[b * kmax + j0 + j];
+    __syncthreads();
+    const int P = nsplit * nj;
+    if (o < d) {
+      for (int p0 = wave; p0 < P; p0 += 4 * U) {
+#pragma unroll
+        for (int q = 0; q < U; ++q) {
+          const int p = p0 + 4 * q;
+          if (p < P) {
+            const int j = p / nsplit, sp = p - j * nsplit;
+            const int64_t i = ent[j];
+            if (i >= 0) a[q] += yp[(sp * nnz + i) * d + o];
+          }
+        }
+      }
     }
-  Y[b * d + o] = s;
+  }
+  float t = 0.0f;
+#pragma unroll
+  for (int q = 0; q < U; ++q) t += a[q];
+  red[wave][lane] = t;
+  __syncthreads();
+  if (wave == 0 && o < d) Y[b * d + o] = ((red[0][lane] + red[1][lane]) + red[2][lane]) + red[3][lane];
 }
 
 }  // namespace
@@ -778,14 +808,15 @@ extern "C" bitsmoe_status bitsmoe_moe_decode_in(const uint64_t* codes_dev, const
   if (st != BITSMOE_OK) return st;
   // segments of 32 outputs: SEGW per workgroup (a power of two up to 256),
   // RSL = 256 / SEGW row slices; rows split over blockIdx.z for about 1024
-  // workgroups
+  // workgroups but at least four rows per thread (each split adds a partial
+  // per output to the final sum)
   const int64_t nseg = d_out / kSeg;
   int SEGW = 2;
   while (SEGW < nseg && SEGW < 256) SEGW *= 2;
   const int RSL = 256 / SEGW;
   const int64_t segblocks = (nseg + SEGW - 1) / SEGW;
-  const int64_t max_split = (r + RSL - 1) / RSL;
-  int64_t nsplit = std::clamp<int64_t>(1024 / std::max<int64_t>(rt.njobs * segblocks, 1), 1, max_split);
+  int64_t nsplit = std::clamp<int64_t>(1024 / std::max<int64_t>(rt.njobs * segblocks, 1), 1,
+                                       std::max<int64_t>(1, (r + 4 * RSL - 1) / (4 * RSL)));
   const int64_t rows_split = (r + nsplit - 1) / nsplit;
   nsplit = (r + rows_split - 1) / rows_split;
   if (nsplit > 65535 || segblocks > 65535) return fail(BITSMOE_ERR_SHAPE, "moe_decode_in: too large");
@@ -820,7 +851,7 @@ extern "C" bitsmoe_status bitsmoe_moe_decode_in(const uint64_t* codes_dev, const
   BITSMOE_LAUNCH_CHECK("moe_decode_in: y launch");
   {
     KernelTimer timer("moe_decode_in_sum", stream);
-    hipLaunchKernelGGL(ysum_kernel, dim3(static_cast<unsigned>((d_out + 255) / 256), static_cast<unsigned>(B)),
+    hipLaunchKernelGGL(ysum_kernel, dim3(static_cast<unsigned>((d_out + 63) / 64), static_cast<unsigned>(B)),
                        dim3(256), 0, s, yp, static_cast<int>(nsplit), rt.nnz, pidx_d,
                        static_cast<int>(rt.kmax), d_out, B, Y_dev);
   }
