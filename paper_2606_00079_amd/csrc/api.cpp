@@ -37,6 +37,26 @@ bitsmoe_status device_error(const char* what, int hip_err) {
   return fail(BITSMOE_ERR_DEVICE, buf);
 }
 
+int device_cus() {
+  static std::mutex mu;
+  static std::map<int, int> cache;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) {
+    (void)hipGetLastError();
+    return 256;
+  }
+  std::lock_guard<std::mutex> lock(mu);
+  auto it = cache.find(dev);
+  if (it != cache.end()) return it->second;
+  int n = 0;
+  if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) {
+    (void)hipGetLastError();
+    n = 256;
+  }
+  cache[dev] = n;
+  return n;
+}
+
 // ----------------------------------------------------------------------------
 // scratch
 // ----------------------------------------------------------------------------

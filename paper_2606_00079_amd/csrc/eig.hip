@@ -9,16 +9,17 @@
 //   1. Householder reduction to tridiagonal form, T = Q^T M Q, in panels of
 //      NB columns (the blocked scheme of LAPACK's symmetric reduction, lower
 //      form, stored by rows since M is symmetric).  Per column i of a panel:
-//        house_kernel   one workgroup: the reflector H_i = I - tau v v^T that
-//                       zeroes row i right of its first off-diagonal entry;
-//                       row i of the work matrix is overwritten by v (zeros
-//                       up to i, 1 at i+1);
-//        trsymv_kernel  y = A_t v over the trailing rows, and V^T v, W^T v
+//        trsymv_kernel  the reflector H_i = I - tau v v^T that zeroes row i
+//                       right of its first off-diagonal entry (formed by
+//                       every wave from row i, recorded by one), and
+//                       y = A_t v over the trailing rows, and V^T v, W^T v
 //                       over the panel's earlier reflectors V and vectors W,
-//                       one wave per four rows;
+//                       one wave per two rows;
 //        trw_kernel     w = tau (y - V W^T v - W V^T v) - (tau/2)(w'^T v) v,
-//                       and row i+1 brought up to date with the panel's
-//                       rank-2 terms (it is the next column's row);
+//                       row i of the work matrix overwritten by v (zeros up
+//                       to i, 1 at i+1), and row i+1 brought up to date with
+//                       the panel's rank-2 terms (it is the next column's
+//                       row);
 //      then trail_kernel applies A_t -= V W^T + W V^T to the trailing block
 //      once per panel.
 //   2. The selected eigenpairs of T on the device: eigenvalues n-r+1..n by
@@ -72,58 +73,37 @@ __device__ double block_sum_f64(double v, double* red) {
   return s;
 }
 
-// Reflector of row i: x = A[i][i+1..n), alpha = x_0, sigma = sum_{j>=1} x_j^2,
-// beta = -sign(alpha) sqrt(alpha^2 + sigma), tau = (beta - alpha) / beta,
-// v = (1, x_1.. / (alpha - beta)); sigma = 0 gives tau = 0, beta = alpha.
-// Row n-1 only records its diagonal.
-__global__ __launch_bounds__(1024) void house_kernel(double* __restrict__ A, int64_t n, int64_t i,
-                                                     double* __restrict__ dvec,
-                                                     double* __restrict__ evec,
-                                                     double* __restrict__ tau) {
-  __shared__ double red[16];
-  double* row = A + i * n;
-  const int64_t m = n - i - 1;
-  const double diag = row[i];
-  if (m == 0) {
-    if (threadIdx.x == 0) dvec[i] = diag;
-    return;
-  }
-  const double alpha = row[i + 1];
-  double part = 0.0;
-  for (int64_t j = 1 + threadIdx.x; j < m; j += 1024) {
-    const double x = row[i + 1 + j];
-    part = fma(x, x, part);
-  }
-  const double sigma = block_sum_f64<1024>(part, red);
-  double beta = alpha, t = 0.0, sc = 0.0;
-  if (sigma != 0.0) {
-    beta = -copysign(sqrt(fma(alpha, alpha, sigma)), alpha);
-    t = (beta - alpha) / beta;
-    sc = 1.0 / (alpha - beta);
-  }
-  __syncthreads();  // every thread has read row i before it is rewritten
-  if (threadIdx.x == 0) {
-    dvec[i] = diag;
-    evec[i] = beta;
-    tau[i] = t;
-    row[i + 1] = 1.0;
-  }
-  for (int64_t j = threadIdx.x; j <= i; j += 1024) row[j] = 0.0;
-  for (int64_t j = 1 + threadIdx.x; j < m; j += 1024) row[i + 1 + j] *= sc;
+// The last diagonal entry of T (row n-1 has no reflector).
+__global__ void last_diag_kernel(const double* __restrict__ A, int64_t n, double* __restrict__ dvec) {
+  if (threadIdx.x == 0) dvec[n - 1] = A[(n - 1) * n + n - 1];
 }
 
-// out[rr] = row_rr . v over the columns i+1..n-1, v = A[i][i+1..n), for the
-// rows rr < m: A[i+1+rr]; m <= rr < m+c: A[j0 + rr - m] (the panel's earlier
-// reflectors); m+c <= rr < m+2c: Wp[rr - m - c].  Two rows per wave.
+// The reflector of row i, formed by every wave from the row as the previous
+// kernels left it: x = A[i][i+1..n), alpha = x_0, sigma = sum_{j>=1} x_j^2,
+// beta = -sign(alpha) sqrt(alpha^2 + sigma), tau = (beta - alpha) / beta,
+// v = (1, x_1.. / (alpha - beta)); sigma = 0 gives tau = 0, beta = alpha.
+// Then out[rr] = row_rr . v = row_rr[i+1] + (sum_{j>=1} row_rr[i+1+j] x_j)
+// / (alpha - beta) over the rows rr < m: A[i+1+rr]; m <= rr < m+c:
+// A[j0 + rr - m] (the panel's earlier reflectors); m+c <= rr < m+2c:
+// Wp[rr - m - c].  Two rows per wave; sigma and the dot products come from
+// the same pass over x (every wave sums sigma in the same order, so all
+// agree).  Wave 0 of workgroup 0 records d[i] = A[i][i], e[i] = beta,
+// tau[i] and v into vbuf[i+1..n); row i itself is rewritten by trw_kernel,
+// after every wave here has read it.
 __global__ __launch_bounds__(256) void trsymv_kernel(const double* __restrict__ A,
                                                      const double* __restrict__ Wp, int64_t n,
                                                      int64_t i, int64_t j0, int c,
-                                                     double* __restrict__ out) {
+                                                     double* __restrict__ out,
+                                                     double* __restrict__ dvec,
+                                                     double* __restrict__ evec,
+                                                     double* __restrict__ tau,
+                                                     double* __restrict__ vbuf) {
   const int lane = threadIdx.x & 63;
   const int64_t m = n - i - 1;
   const int64_t R = m + 2 * c;
   const int64_t rr0 = (static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6)) * 2;
   if (rr0 >= R) return;  // whole wave
+  const double* x = A + i * n;
   const double* src[2];
 #pragma unroll
   for (int q = 0; q < 2; ++q) {
@@ -131,40 +111,71 @@ __global__ __launch_bounds__(256) void trsymv_kernel(const double* __restrict__ 
     src[q] = rr < m ? A + (i + 1 + rr) * n
                     : (rr < m + c ? A + (j0 + rr - m) * n : Wp + (rr - m - c) * n);
   }
-  const double* v = A + i * n;
-  double acc[2] = {0.0, 0.0};
+  double acc[2] = {0.0, 0.0}, sig = 0.0;
 #pragma unroll 8
   for (int64_t col = i + 1 + lane; col < n; col += 64) {
-    const double vv = v[col];
+    const double xx = col == i + 1 ? 0.0 : x[col];
+    sig = fma(xx, xx, sig);
 #pragma unroll
-    for (int q = 0; q < 2; ++q) acc[q] = fma(src[q][col], vv, acc[q]);
+    for (int q = 0; q < 2; ++q) acc[q] = fma(src[q][col], xx, acc[q]);
+  }
+  const double sigma = wave_sum_f64(sig);
+  const double alpha = x[i + 1];
+  double beta = alpha, t = 0.0, sc = 0.0;
+  if (sigma != 0.0) {
+    beta = -copysign(sqrt(fma(alpha, alpha, sigma)), alpha);
+    t = (beta - alpha) / beta;
+    sc = 1.0 / (alpha - beta);
   }
 #pragma unroll
   for (int q = 0; q < 2; ++q) {
     const double s = wave_sum_f64(acc[q]);
-    if (lane == 0 && rr0 + q < R) out[rr0 + q] = s;
+    if (lane == 0 && rr0 + q < R) out[rr0 + q] = fma(s, sc, src[q][i + 1]);
+  }
+  if (blockIdx.x == 0 && threadIdx.x < 64) {
+    if (lane == 0) {
+      dvec[i] = x[i];
+      evec[i] = beta;
+      tau[i] = t;
+      vbuf[i + 1] = 1.0;
+    }
+    for (int64_t j = i + 2 + lane; j < n; j += 64) vbuf[j] = x[j] * sc;
   }
 }
 
 // w for column c = i - j0 of the panel (rows j = i+1..n-1), stored in
 // Wp[c], and, when do_row, the rank-2 terms of panel columns 0..c applied to
-// row i+1 (entries j >= i+1).  ybv = trsymv's output: y [m], V^T v [c],
-// W^T v [c].  Every workgroup forms y.v (and w_{i+1}) itself.  A workgroup
-// covers 64 entries j; its four waves take the panel columns c' = q mod 4
-// and their partial sums are added in wave order.
+// row i+1 (entries j >= i+1); row i is overwritten by its reflector v (zeros
+// up to i, then vbuf).  ybv = trsymv's output: y [m], V^T v [c], W^T v [c].
+// Every workgroup forms y.v (and w_{i+1}) itself.  A workgroup covers 64
+// entries j; its four waves take the panel columns c' = q mod 4 and their
+// partial sums are added in wave order.  Every load is issued before the
+// first barrier.
 __global__ __launch_bounds__(256) void trw_kernel(double* __restrict__ A, double* __restrict__ Wp,
                                                   int64_t n, int64_t i, int64_t j0, int c,
                                                   const double* __restrict__ ybv,
-                                                  const double* __restrict__ tau, int do_row) {
+                                                  const double* __restrict__ tau,
+                                                  const double* __restrict__ vbuf, int do_row) {
+  constexpr int KP = NB / 4;  // panel columns per wave
   __shared__ double red[4];
   __shared__ double s_vtv[NB], s_wtv[NB], s_vi1[NB], s_wi1[NB];
   __shared__ double part_w[4][64], part_r[4][64];
   const int64_t m = n - i - 1;
-  const double t = tau[i];
-  const double* v = A + i * n;
+  const int jl = threadIdx.x & 63, sl = threadIdx.x >> 6;
+  const int64_t j = i + 1 + static_cast<int64_t>(blockIdx.x) * 64 + jl;
+  const bool jin = j < n;
   double part = 0.0;
-  for (int64_t jj = threadIdx.x; jj < m; jj += 256) part = fma(ybv[jj], v[i + 1 + jj], part);
-  const double yv = block_sum_f64<256>(part, red);
+  for (int64_t jj = threadIdx.x; jj < m; jj += 256) part = fma(ybv[jj], vbuf[i + 1 + jj], part);
+  double vj[KP], wj[KP];
+#pragma unroll
+  for (int k = 0; k < KP; ++k) {
+    const int cc = sl + 4 * k;
+    vj[k] = wj[k] = 0.0;
+    if (jin && cc < c) {
+      vj[k] = A[(j0 + cc) * n + j];
+      wj[k] = Wp[cc * n + j];
+    }
+  }
   if (threadIdx.x < c) {
     const int cc = threadIdx.x;
     s_vtv[cc] = ybv[m + cc];
@@ -172,27 +183,31 @@ __global__ __launch_bounds__(256) void trw_kernel(double* __restrict__ A, double
     s_vi1[cc] = A[(j0 + cc) * n + i + 1];  // V[i+1][c'] for c' < c
     s_wi1[cc] = Wp[cc * n + i + 1];        // W[i+1][c']
   }
-  __syncthreads();
+  const double vjj = jin ? vbuf[j] : 0.0;
+  const double t = tau[i];
+  // nothing in this kernel reads row i
+  if (sl == 0 && jin) A[i * n + j] = vjj;
+  if (blockIdx.x == 0)
+    for (int64_t jz = threadIdx.x; jz <= i; jz += 256) A[i * n + jz] = 0.0;
+  const double yv = block_sum_f64<256>(part, red);  // its barriers publish s_*
   double q = 0.0;
   for (int cc = 0; cc < c; ++cc) q = fma(s_vtv[cc], s_wtv[cc], q);
   const double s = t * (yv - 2.0 * q);
-  const int jl = threadIdx.x & 63, sl = threadIdx.x >> 6;
-  const int64_t j = i + 1 + static_cast<int64_t>(blockIdx.x) * 64 + jl;
   double pw = 0.0, pr = 0.0;
-  if (j < n) {
-#pragma unroll 8
-    for (int cc = sl; cc < c; cc += 4) {
-      const double vj = A[(j0 + cc) * n + j], wj = Wp[cc * n + j];
-      pw = fma(vj, s_wtv[cc], fma(wj, s_vtv[cc], pw));
-      pr = fma(vj, s_wi1[cc], fma(wj, s_vi1[cc], pr));
+#pragma unroll
+  for (int k = 0; k < KP; ++k) {
+    const int cc = sl + 4 * k;
+    if (cc < c) {
+      pw = fma(vj[k], s_wtv[cc], fma(wj[k], s_vtv[cc], pw));
+      pr = fma(vj[k], s_wi1[cc], fma(wj[k], s_vi1[cc], pr));
     }
   }
   part_w[sl][jl] = pw;
   part_r[sl][jl] = pr;
   __syncthreads();
-  if (sl != 0 || j >= n) return;
+  if (sl != 0 || !jin) return;
   const double acc = ybv[j - (i + 1)] - (((part_w[0][jl] + part_w[1][jl]) + part_w[2][jl]) + part_w[3][jl]);
-  const double w = t * acc - 0.5 * t * s * v[j];
+  const double w = t * acc - 0.5 * t * s * vjj;
   Wp[static_cast<int64_t>(c) * n + j] = w;
   if (!do_row) return;
   // w_{i+1} (v_{i+1} = 1), formed the same way in every workgroup
@@ -201,7 +216,7 @@ __global__ __launch_bounds__(256) void trw_kernel(double* __restrict__ A, double
   const double w1 = t * acc1 - 0.5 * t * s;
   // the current column: V[j][c] W[i+1][c] + W[j][c] V[i+1][c], then c' < c
   const double delta =
-      v[j] * w1 + w + (((part_r[0][jl] + part_r[1][jl]) + part_r[2][jl]) + part_r[3][jl]);
+      vjj * w1 + w + (((part_r[0][jl] + part_r[1][jl]) + part_r[2][jl]) + part_r[3][jl]);
   A[(i + 1) * n + j] -= delta;
 }
 
@@ -613,14 +628,14 @@ extern "C" bitsmoe_status bitsmoe_shared_basis_gpu(const double* M_dev, int64_t 
   hipStream_t s = static_cast<hipStream_t>(stream);
   bitsmoe_status st;
   // work matrix (M, then the reflectors by rows), Z^T, and small buffers:
-  // Wp [NB][n], trsymv output [n + 2 NB], d, e, tau [n], G and T [NB][NB],
+  // Wp [NB][n], trsymv output [n + 2 NB], d, e, tau, v [n], G and T [NB][NB],
   // X [r][NB], eigenvalues [r]
   double* A = static_cast<double*>(scratch(kScratchA, static_cast<size_t>(n * n) * 8, stream, &st));
   if (!A) return st;
   double* Zt = static_cast<double*>(scratch(kScratchB, static_cast<size_t>(r * n) * 8, stream, &st));
   if (!Zt) return st;
   const int64_t npan = (n - 1 + NB - 1) / NB;
-  const size_t small = static_cast<size_t>(NB * n + (n + 2 * NB) + 3 * n +
+  const size_t small = static_cast<size_t>(NB * n + (n + 2 * NB) + 4 * n +
                                            2 * std::max<int64_t>(npan, 1) * NB * NB + r * NB + r) *
                        8;
   double* Wp = static_cast<double*>(scratch(kScratchPart, small, stream, &st));
@@ -629,7 +644,8 @@ extern "C" bitsmoe_status bitsmoe_shared_basis_gpu(const double* M_dev, int64_t 
   double* dvec = ybv + n + 2 * NB;
   double* evec = dvec + n;
   double* tau = evec + n;
-  double* G = tau + n;                                  // [npan][NB][NB]
+  double* vbuf = tau + n;  // the current column's reflector
+  double* G = vbuf + n;                                 // [npan][NB][NB]
   double* T = G + std::max<int64_t>(npan, 1) * NB * NB;  // [npan][NB][NB]
   double* X = T + std::max<int64_t>(npan, 1) * NB * NB;
   hipError_t he = hipMemcpyAsync(A, M_dev, static_cast<size_t>(n * n) * 8, hipMemcpyDeviceToDevice, s);
@@ -643,13 +659,12 @@ extern "C" bitsmoe_status bitsmoe_shared_basis_gpu(const double* M_dev, int64_t 
       for (int64_t i = j0; i < pe; ++i) {
         const int c = static_cast<int>(i - j0);
         const int64_t m = n - i - 1;
-        hipLaunchKernelGGL(house_kernel, dim3(1), dim3(1024), 0, s, A, n, i, dvec, evec, tau);
         const int64_t R = m + 2 * c;
         hipLaunchKernelGGL(trsymv_kernel, dim3(static_cast<unsigned>((R + 7) / 8)), dim3(256), 0, s,
-                           A, Wp, n, i, j0, c, ybv);
+                           A, Wp, n, i, j0, c, ybv, dvec, evec, tau, vbuf);
         const int do_row = (full && c == NB - 1) ? 0 : 1;
         hipLaunchKernelGGL(trw_kernel, dim3(static_cast<unsigned>((m + 63) / 64)), dim3(256), 0, s,
-                           A, Wp, n, i, j0, c, ybv, tau, do_row);
+                           A, Wp, n, i, j0, c, ybv, tau, vbuf, do_row);
       }
       if (full) {
         const int64_t sidx = j0 + NB;
@@ -658,7 +673,7 @@ extern "C" bitsmoe_status bitsmoe_shared_basis_gpu(const double* M_dev, int64_t 
                            sidx);
       }
     }
-    hipLaunchKernelGGL(house_kernel, dim3(1), dim3(1024), 0, s, A, n, n - 1, dvec, evec, tau);
+    hipLaunchKernelGGL(last_diag_kernel, dim3(1), dim3(64), 0, s, A, n, dvec);
   }
   BITSMOE_LAUNCH_CHECK("shared_basis_gpu: tridiagonal reduction");
   // 2. eigenpairs of T: bounds and clusters on the host, the rest on the device

@@ -239,12 +239,25 @@ bitsmoe_status run_symmetric(gemm::Problem p, int64_t d, double scale, OutT* out
   const int64_t ntiles = static_cast<int64_t>(T) * (T + 1) / 2;
   p.tiles_m = p.tiles_n = T;
   p.symmetric = 1;
-  // K chunks of at most 4096 terms, at least ~3 workgroups per CU, and at
-  // least four K tiles per workgroup.
+  // Split-K.  The engine keeps one workgroup per CU, so the GEMM takes about
+  // (rounds of workgroups over the CUs) x (K tiles per workgroup); each
+  // split also writes a 256 x 256 fp32 partial tile that the reduction reads
+  // back (about 0.14 K-tile times of the whole device per workgroup at HBM
+  // speed).  The split minimizing the sum, with at least four K tiles per
+  // workgroup.
   const int64_t kt = p.ktiles;  // in units of gemm::BK
-  int64_t splits = (kt * BK + 4095) / 4096;
-  splits = std::max<int64_t>(splits, (768 + ntiles * batches - 1) / (ntiles * batches));
-  splits = std::min<int64_t>(splits, std::max<int64_t>(1, kt / 4));
+  const int64_t cus = device_cus();
+  const int64_t wg1 = ntiles * batches;
+  int64_t splits = 1;
+  double best = 0.0;
+  for (int64_t sp = 1; sp <= std::max<int64_t>(1, kt / 4); ++sp) {
+    const int64_t rounds = (wg1 * sp + cus - 1) / cus;
+    const double cost = static_cast<double>(rounds * ((kt + sp - 1) / sp)) + 0.14 * wg1 * sp;
+    if (sp == 1 || cost < best) {
+      best = cost;
+      splits = sp;
+    }
+  }
   p.splits = static_cast<int>(splits);
   if (batches > 65535) return fail(BITSMOE_ERR_SHAPE, std::string(name) + ": too many batches");
   bitsmoe_status st;

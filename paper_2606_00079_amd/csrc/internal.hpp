@@ -34,6 +34,10 @@ void* scratch(int slot, size_t bytes, void* stream, bitsmoe_status* st);
 // HIP error -> status with a message naming `what`.
 bitsmoe_status device_error(const char* what, int hip_err);
 
+// Compute units of the current device (cached per device; 256 if the query
+// fails).
+int device_cus();
+
 // Records HIP events around a kernel launch when timing is enabled
 // (bitsmoe_timing); construct right before the launch, destroy right after.
 class KernelTimer {
