@@ -62,6 +62,11 @@ struct StaticFor<N, N> {
   template <class Fn>
   __device__ __forceinline__ static void run(Fn&&) {}
 };
+// A compile-time range [A, B) of a refill's direct loads.
+template <int A, int B>
+struct LoadRange {
+  static constexpr int first = A, second = B;
+};
 constexpr int kXcds = 8;
 
 // Operand layouts.  Row-major (kstep == 0): row r, column k at r * ld + k;
@@ -362,6 +367,12 @@ __device__ __forceinline__ void wait_vmcnt() {
   static_assert(N >= 0 && N < 64, "vmcnt");
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
+// The same, and every LDS read of this wave returned (lgkmcnt 0).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt_lds() {
+  static_assert(N >= 0 && N < 64, "vmcnt");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4));
+}
 
 // The K-loop stage buffers, free once the loop is done; epilogues may use
 // them as scratch: kStages A buffers then kStages B buffers.
@@ -554,16 +565,20 @@ void gemm_nt_kernel(Problem p, Epi epi) {
   // one K=16 step, the fragments of the next step are read into the other.
   using Op = Operand<F16>;
   typename Op::vec fa[2][F::FM], fb[2][F::FN];
-  auto read_frags = [&](auto set, int s, int kk) {
+  // Operand fragment q of the K=16 step kk of stage s into register set
+  // `set`, in the order the matrix-core ops of a step first use them: A0,
+  // then B0 .. B(FN-1), then A1 .. A(FM-1).
+  auto read_frag = [&](auto set, auto qq, int s, int kk) {
     constexpr int T = decltype(set)::value;
-    const uint16_t* la = As + s * ASZ;
-    const uint16_t* lb = Bs + s * BSZ;
+    constexpr int q = decltype(qq)::value;
     const int j = 2 * kk + jq;
-#pragma unroll
-    for (int mi = 0; mi < F::FM; ++mi)
+    if constexpr (q == 0 || q > F::FN) {
+      constexpr int mi = q == 0 ? 0 : q - F::FN;
+      const uint16_t* la = As + s * ASZ;
       fa[T][mi] = *reinterpret_cast<const typename Op::vec*>(&la[lds_off<KB>(arow + 32 * mi, j)]);
-#pragma unroll
-    for (int ni = 0; ni < F::FN; ++ni) {
+    } else {
+      constexpr int ni = q - 1;
+      const uint16_t* lb = Bs + s * BSZ;
       if constexpr (BKN) {
         // rows 16 kk + 8 (lane / 32) + 4 t + (lane % 16) / 4, column
         // n + 16 ((lane / 16) % 2) + 4 (lane % 4) of the [32][256] stage tile
@@ -581,47 +596,81 @@ void gemm_nt_kernel(Problem p, Epi epi) {
       }
     }
   };
-  // The matrix-core ops of one K=16 step from fragment set `set`; with a
-  // refill, its LPS loads are issued one after each of the first LPS ops.
-  // Scheduling barriers keep this order (the compiler would otherwise sink
-  // the fragment reads of the next step below the ops of this one).
-  static_assert(LPS <= F::FM * F::FN, "one load per matrix-core op at most");
-  auto mfmas = [&](auto set, const Issue* is) {
+  constexpr int NFR = F::FM + F::FN;  // fragment reads per step
+  auto read_frags = [&](auto set, int s, int kk) {
+    StaticFor<0, NFR>::run([&](auto qq) { read_frag(set, qq, s, kk); });
+  };
+  // The matrix-core ops of one K=16 step from fragment set `set`.  Between
+  // them go the other instructions of the step: the NFR fragment reads of
+  // the next step into the other set (`frs`: stage and step) and direct
+  // loads L0 .. L1-1 of a refill (`is`), alternating and spread evenly over
+  // all ops but the last two (so that the reads have returned by the end of
+  // the step).  A wave issues in order, so a burst of reads or loads ahead
+  // of the ops would leave the matrix cores idle while it is issued; spread
+  // out, each instruction issues while an op is executing.  Scheduling
+  // barriers keep this order (the compiler would otherwise sink the reads of
+  // the next step below the ops of this one).
+  struct FragSrc {
+    int s, kk;
+  };
+  auto mfmas = [&](auto set, auto has_fr, auto lrange, const FragSrc& frs, const Issue& is) {
     constexpr int T = decltype(set)::value;
+    using Other = std::integral_constant<int, 1 - T>;
+    constexpr int L0 = decltype(lrange)::first, L1 = decltype(lrange)::second;
+    constexpr int NF = decltype(has_fr)::value ? NFR : 0;
+    constexpr int NL = L1 - L0;
+    constexpr int M = NF + NL;
+    constexpr int Q = F::FM * F::FN;
+    constexpr int QS = Q > 4 ? Q - 2 : Q;  // ops followed by memory instructions
     __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-    for (int mi = 0; mi < F::FM; ++mi)
-#pragma unroll
-      for (int ni = 0; ni < F::FN; ++ni) {
-        f.acc[mi][ni] = Op::mfma(fa[T][mi], fb[T][ni], f.acc[mi][ni]);
-        const int q = mi * F::FN + ni;
-        if (is != nullptr && q < LPS) {
-          __builtin_amdgcn_sched_barrier(0);
-          issue_part(*is, q);
-          __builtin_amdgcn_sched_barrier(0);
-        }
-      }
+    StaticFor<0, Q>::run([&](auto qq) {
+      constexpr int q = decltype(qq)::value;
+      constexpr int mi = q / F::FN, ni = q % F::FN;
+      f.acc[mi][ni] = Op::mfma(fa[T][mi], fb[T][ni], f.acc[mi][ni]);
+      // memory instructions j0 .. j1-1 of the alternating sequence F0, L0,
+      // F1, L1, ... (the longer list continuing alone)
+      constexpr int j0 = q < QS ? q * M / QS : M, j1 = q < QS ? (q + 1) * M / QS : M;
+      StaticFor<j0, j1>::run([&](auto jj) {
+        constexpr int j = decltype(jj)::value;
+        constexpr int m = NF < NL ? NF : NL;  // pairs
+        constexpr bool frag = j < 2 * m ? (j % 2 == 0) : (NF > NL);
+        constexpr int idx = j < 2 * m ? j / 2 : j - m;
+        __builtin_amdgcn_sched_barrier(0);
+        if constexpr (frag)
+          read_frag(Other(), std::integral_constant<int, idx>(), frs.s, frs.kk);
+        else
+          issue_part(is, L0 + idx);
+        __builtin_amdgcn_sched_barrier(0);
+      });
+    });
     __builtin_amdgcn_sched_barrier(0);
   };
 
   int64_t nk = 0;      // K tiles of the current job
   int64_t issued = 0;  // K tiles whose loads have been issued
+  constexpr int KS = KB / 16;  // K=16 steps per tile (even)
+  // A refill's LPS loads are spread over the KS steps of the tile that
+  // issues them: step k issues loads k LPS / KS .. (k + 1) LPS / KS - 1, so
+  // PRE of them precede the barrier of the tile's last step.
+  constexpr int PRE = (KS - 1) * LPS / KS;
   // Makes K tile `next` visible to every wave: wait for this wave's loads of
-  // it (the STAGES - 3 tiles issued after it may stay in flight), then a bare
+  // it (the STAGES - 3 tiles issued after it, and the PRE loads of the
+  // current refill, may stay in flight) and for its LDS reads, then a bare
   // barrier (__syncthreads() would also wait for the loads still in flight).
-  // After the barrier every wave has also consumed the fragments of the
-  // buffer of tile next - 2, which is refilled with tile next + STAGES - 2.
+  // After the barrier every wave has read the last fragments of tile
+  // next - 1, so the buffer of tile next - 1 is free: the refill with tile
+  // next + STAGES - 1 that the next tile issues may start at once.
   static_assert(STAGES >= 3, "one buffer being read, one about to be read, one or more in flight");
-  static_assert((STAGES - 3) * LPS < 64, "vmcnt holds at most 63 outstanding loads");
+  static_assert((STAGES - 3) * LPS + PRE < 64, "vmcnt holds at most 63 outstanding loads");
   auto sync_tile = [&](int64_t next, auto tail) {
     if constexpr (decltype(tail)::value) {
       const int64_t after = issued - 1 - next;  // 0 .. STAGES - 3
       StaticFor<0, STAGES - 2>::run([&](auto q) {
         constexpr int n = decltype(q)::value;
-        if (after == n) wait_vmcnt<n * LPS>();
+        if (after == n) wait_vmcnt_lds<n * LPS>();
       });
     } else {
-      wait_vmcnt<(STAGES - 3) * LPS>();
+      wait_vmcnt_lds<(STAGES - 3) * LPS + PRE>();
     }
     asm volatile("" ::: "memory");
     __builtin_amdgcn_s_barrier();
@@ -630,30 +679,28 @@ void gemm_nt_kernel(Problem p, Epi epi) {
   using True = std::integral_constant<bool, true>;
   using False = std::integral_constant<bool, false>;
   using Set0 = std::integral_constant<int, 0>;
-  constexpr int KS = KB / 16;  // K=16 steps per tile (even)
   // K tile i (fragments of its first step already requested into set 0).
-  // has_next: tile i + 1 exists; refill: tile i + STAGES - 1 exists.
+  // has_next: tile i + 1 exists; refill: tile i + STAGES - 1 exists (into
+  // the buffer of tile i - 1, free since the barrier before this tile).
   auto tile = [&](int64_t i, auto has_next, auto refill, auto tail) {
     const int s = static_cast<int>(i % STAGES);
+    Issue is{};
+    if constexpr (decltype(refill)::value) {
+      is = issue_begin(static_cast<int>(issued % STAGES));
+      ++issued;
+    }
     StaticFor<0, KS>::run([&](auto kq) {
       constexpr int kk = decltype(kq)::value;
       using Cur = std::integral_constant<int, kk & 1>;
-      using Nxt = std::integral_constant<int, (kk + 1) & 1>;
+      constexpr int la = decltype(refill)::value ? kk * LPS / KS : 0;
+      constexpr int lb = decltype(refill)::value ? (kk + 1) * LPS / KS : 0;
       if constexpr (kk + 1 < KS) {
-        read_frags(Nxt(), s, kk + 1);
-        mfmas(Cur(), nullptr);
+        mfmas(Cur(), True(), LoadRange<la, lb>(), FragSrc{s, kk + 1}, is);
       } else if constexpr (decltype(has_next)::value) {
         sync_tile(i + 1, tail);
-        read_frags(Nxt(), static_cast<int>((i + 1) % STAGES), 0);
-        if constexpr (decltype(refill)::value) {
-          const Issue is = issue_begin(static_cast<int>(issued % STAGES));
-          ++issued;
-          mfmas(Cur(), &is);
-        } else {
-          mfmas(Cur(), nullptr);
-        }
+        mfmas(Cur(), True(), LoadRange<la, lb>(), FragSrc{static_cast<int>((i + 1) % STAGES), 0}, is);
       } else {
-        mfmas(Cur(), nullptr);
+        mfmas(Cur(), False(), LoadRange<la, lb>(), FragSrc{0, 0}, is);
       }
     });
   };
