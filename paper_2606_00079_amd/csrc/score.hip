@@ -139,15 +139,20 @@ struct QuantBits {
 // consecutive lanes.  Codes follow the fp64 rule exactly: the fp32 quotient
 // is used unless it lies within 1e-4 of a rounding boundary (its error is
 // below 6.1e-5 for codes up to 255), in which case fp64 decides.
-// The row is read twice: once for max |c|, once to quantize (the second read
-// mostly hits in the caches; holding the row in registers instead costs more
-// in occupancy than it saves); both passes keep several loads in flight.
+// The row is read twice: once for max |c|, once to quantize.  With ROWLDS
+// (rows of at most kRowLds entries) the first pass also keeps the row in
+// LDS (8 KiB per wave at 2048 entries) and the second reads it from there,
+// so C leaves HBM once; otherwise the second read goes to the caches again
+// (holding the row in registers instead costs more in occupancy than it
+// saves).  Both passes keep several loads in flight.
 //
 // NORM: only the error norms are wanted (the input-space table
 // beta_k ||delta||^2 of the diagonal approximation): no error rows are
 // written, H's diagonal is taken as 1, the errors are not rescaled (E = 0),
 // and diag[u * nb + j] = w[u % wperiod] * sum delta^2.
-template <int NB, bool NORM = false>
+constexpr int kRowLds = 2048;  // longest row dgen_kernel<..., ROWLDS> keeps in LDS
+
+template <int NB, bool NORM = false, bool ROWLDS = false>
 __global__ __launch_bounds__(256) void dgen_kernel(const float* __restrict__ C, int64_t units,
                                                    int64_t d, int G, QuantBits qb,
                                                    const float* __restrict__ hdiag,
@@ -179,6 +184,35 @@ __global__ __launch_bounds__(256) void dgen_kernel(const float* __restrict__ C, 
       for (int i = 0; i < 8; ++i) c[i] = 0.0f;
     }
   };
+  // ROWLDS: this wave's copy of its row
+  __shared__ float rowbuf[ROWLDS ? 4 * kRowLds : 1];
+  float* const myrow = rowbuf + (ROWLDS ? (threadIdx.x >> 6) * kRowLds : 0);
+  auto keep8 = [&](int64_t k0, const float (&c)[8]) {
+    if constexpr (ROWLDS) {
+      const int64_t k = k0 + 8 * lane;
+      if (k < d) {
+        *reinterpret_cast<float4*>(myrow + k) = make_float4(c[0], c[1], c[2], c[3]);
+        *reinterpret_cast<float4*>(myrow + k + 4) = make_float4(c[4], c[5], c[6], c[7]);
+      }
+    }
+  };
+  // the second pass's copy of the lane's 8 entries (zeros past the end)
+  auto reload8 = [&](int64_t k0, float (&c)[8]) {
+    if constexpr (ROWLDS) {
+      const int64_t k = k0 + 8 * lane;
+      if (k < d) {
+        const float4 v0 = *reinterpret_cast<const float4*>(myrow + k);
+        const float4 v1 = *reinterpret_cast<const float4*>(myrow + k + 4);
+        c[0] = v0.x; c[1] = v0.y; c[2] = v0.z; c[3] = v0.w;
+        c[4] = v1.x; c[5] = v1.y; c[6] = v1.z; c[7] = v1.w;
+      } else {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) c[i] = 0.0f;
+      }
+    } else {
+      load8(k0, c);
+    }
+  };
   auto absmax8 = [](const float (&c)[8]) {
     float m = 0.0f;
 #pragma unroll
@@ -198,12 +232,16 @@ __global__ __launch_bounds__(256) void dgen_kernel(const float* __restrict__ C, 
 #pragma unroll
       for (int x = 0; x < 4; ++x) load8(ka + 512 * x, c4[x]);
 #pragma unroll
-      for (int x = 0; x < 4; ++x) amax = fmaxf(amax, absmax8(c4[x]));
+      for (int x = 0; x < 4; ++x) {
+        amax = fmaxf(amax, absmax8(c4[x]));
+        keep8(ka + 512 * x, c4[x]);
+      }
     }
     for (; ka < d; ka += 512) {
       float cc[8];
       load8(ka, cc);
       amax = fmaxf(amax, absmax8(cc));
+      keep8(ka, cc);
     }
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) amax = fmaxf(amax, __shfl_xor(amax, o, 64));
@@ -296,10 +334,11 @@ __global__ __launch_bounds__(256) void dgen_kernel(const float* __restrict__ C, 
     }
   };
   // the loads of chunk c + 1 are issued before chunk c is quantized
+  static_assert(!(NORM && ROWLDS), "the norm-only form has no first pass");
   float cur[8], nxt[8];
-  load8(0, cur);
+  reload8(0, cur);
   for (int64_t k0 = 0; k0 < d; k0 += 512) {
-    if (k0 + 512 < d) load8(k0 + 512, nxt);
+    if (k0 + 512 < d) reload8(k0 + 512, nxt);
     chunk(k0, cur);
 #pragma unroll
     for (int i = 0; i < 8; ++i) cur[i] = nxt[i];
@@ -725,10 +764,14 @@ extern "C" bitsmoe_status bitsmoe_score(const float* C_dev, int64_t units, int64
   {
   KernelTimer dgen_timer("score_dgen", stream);
   switch (nbits) {
-#define BITSMOE_DGEN(NB)                                                                       \
-  case NB:                                                                                     \
-    hipLaunchKernelGGL(dgen_kernel<NB>, dim3(db), dim3(256), 0, s, C_dev, units, d, group, qb, \
-                       t.hdiag, t.D, t.diag, t.uexp);                                          \
+#define BITSMOE_DGEN(NB)                                                                         \
+  case NB:                                                                                       \
+    if (d <= kRowLds)                                                                            \
+      hipLaunchKernelGGL((dgen_kernel<NB, false, true>), dim3(db), dim3(256), 0, s, C_dev, units, \
+                         d, group, qb, t.hdiag, t.D, t.diag, t.uexp);                            \
+    else                                                                                         \
+      hipLaunchKernelGGL((dgen_kernel<NB, false, false>), dim3(db), dim3(256), 0, s, C_dev,      \
+                         units, d, group, qb, t.hdiag, t.D, t.diag, t.uexp);                     \
     break;
     BITSMOE_DGEN(1) BITSMOE_DGEN(2) BITSMOE_DGEN(3) BITSMOE_DGEN(4)
     BITSMOE_DGEN(5) BITSMOE_DGEN(6) BITSMOE_DGEN(7) BITSMOE_DGEN(8)
@@ -902,10 +945,15 @@ extern "C" bitsmoe_status bitsmoe_score_routed(const float* C_dev, int64_t units
   {
     KernelTimer dgen_timer("score_routed_dgen", stream);
     switch (nbits) {
-#define BITSMOE_DGEN_R(NB)                                                                        \
-  case NB:                                                                                        \
-    hipLaunchKernelGGL((dgen_kernel<NB, false>), dim3(db), dim3(256), 0, s, C_dev, units, d, group, \
-                       qb, t.hdiag, t.D, t.diag, t.uexp, nullptr, 1, units_per_h);             \
+#define BITSMOE_DGEN_R(NB)                                                                       \
+  case NB:                                                                                       \
+    if (d <= kRowLds)                                                                            \
+      hipLaunchKernelGGL((dgen_kernel<NB, false, true>), dim3(db), dim3(256), 0, s, C_dev, units, \
+                         d, group, qb, t.hdiag, t.D, t.diag, t.uexp, nullptr, 1, units_per_h);   \
+    else                                                                                         \
+      hipLaunchKernelGGL((dgen_kernel<NB, false, false>), dim3(db), dim3(256), 0, s, C_dev,      \
+                         units, d, group, qb, t.hdiag, t.D, t.diag, t.uexp, nullptr, 1,          \
+                         units_per_h);                                                           \
     break;
       BITSMOE_DGEN_R(1) BITSMOE_DGEN_R(2) BITSMOE_DGEN_R(3) BITSMOE_DGEN_R(4)
       BITSMOE_DGEN_R(5) BITSMOE_DGEN_R(6) BITSMOE_DGEN_R(7) BITSMOE_DGEN_R(8)
