@@ -412,6 +412,32 @@ struct Frag {
   __device__ __forceinline__ int col(int ni) const { return col0 + 32 * ni + (lane & 31); }
 };
 
+// For epilogues that store rows: lane k of each group of four lanes holds rows R .. R+3 of column c0 + k
+// on entry and row R + k of columns c0 .. c0+3 on exit (a 4 x 4 transpose
+// by two butterfly exchanges with DPP quad permutations).
+template <int CTRL>
+__device__ __forceinline__ float quad_dpp(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), CTRL, 0xF, 0xF, false));
+}
+__device__ __forceinline__ void quad_transpose(float (&a)[4], int k) {
+  constexpr int kSwap1 = 0xB1;  // quad_perm [1, 0, 3, 2]: lane k ^ 1
+  constexpr int kSwap2 = 0x4E;  // quad_perm [2, 3, 0, 1]: lane k ^ 2
+  const bool o1 = (k & 1) != 0;
+  float s0 = quad_dpp<kSwap1>(o1 ? a[0] : a[1]);
+  float s1 = quad_dpp<kSwap1>(o1 ? a[2] : a[3]);
+  a[0] = o1 ? s0 : a[0];
+  a[1] = o1 ? a[1] : s0;
+  a[2] = o1 ? s1 : a[2];
+  a[3] = o1 ? a[3] : s1;
+  const bool o2 = (k & 2) != 0;
+  s0 = quad_dpp<kSwap2>(o2 ? a[0] : a[2]);
+  s1 = quad_dpp<kSwap2>(o2 ? a[1] : a[3]);
+  a[0] = o2 ? s0 : a[0];
+  a[1] = o2 ? s1 : a[1];
+  a[2] = o2 ? a[2] : s0;
+  a[3] = o2 ? a[3] : s1;
+}
+
 // 16-bit operand element: bf16 (default) or fp16.
 template <bool F16>
 struct Operand {

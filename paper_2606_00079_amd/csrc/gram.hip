@@ -125,16 +125,23 @@ struct PartialStore {
   __device__ void operator()(F& f, const gemm::StageLds&) const {
     const int64_t t = (static_cast<int64_t>(f.tm) * (2 * ntiles_side - f.tm + 1)) / 2 + (f.tn - f.tm);
     float* base = part + f.z * zstride + (static_cast<int64_t>(f.ks) * ntiles + t) * GT * GT;
+    // four consecutive columns of one row per lane and 16-byte store (the
+    // fragment's columns transposed within each group of four lanes)
+    const int k = f.lane & 3;
 #pragma unroll
     for (int mi = 0; mi < F::FM; ++mi)
 #pragma unroll
-      for (int ni = 0; ni < F::FN; ++ni)
+      for (int ni = 0; ni < F::FN; ++ni) {
+        const int lc0 = f.col0 - f.tn * GT + 32 * ni + (f.lane & 28);
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int lr = f.row(mi, r) - f.tm * GT;
-          const int lc = f.col(ni) - f.tn * GT;
-          base[lr * GT + lc] = f.acc[mi][ni][r];
+        for (int j = 0; j < 4; ++j) {
+          float a[4] = {f.acc[mi][ni][4 * j], f.acc[mi][ni][4 * j + 1], f.acc[mi][ni][4 * j + 2],
+                        f.acc[mi][ni][4 * j + 3]};
+          gemm::quad_transpose(a, k);
+          const int lr = f.row0 - f.tm * GT + 32 * mi + 8 * j + 4 * (f.lane >> 5) + k;
+          *reinterpret_cast<float4*>(base + lr * GT + lc0) = make_float4(a[0], a[1], a[2], a[3]);
         }
+      }
   }
 };
 

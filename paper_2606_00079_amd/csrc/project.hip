@@ -91,32 +91,6 @@ __global__ __launch_bounds__(256) void split_rows_kernel(const float* __restrict
   }
 }
 
-// Lane k of each group of four lanes holds rows R .. R+3 of column c0 + k
-// on entry and row R + k of columns c0 .. c0+3 on exit (a 4 x 4 transpose
-// by two butterfly exchanges with DPP quad permutations).
-template <int CTRL>
-__device__ __forceinline__ float quad_dpp(float v) {
-  return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), CTRL, 0xF, 0xF, false));
-}
-__device__ __forceinline__ void quad_transpose(float (&a)[4], int k) {
-  constexpr int kSwap1 = 0xB1;  // quad_perm [1, 0, 3, 2]: lane k ^ 1
-  constexpr int kSwap2 = 0x4E;  // quad_perm [2, 3, 0, 1]: lane k ^ 2
-  const bool o1 = (k & 1) != 0;
-  float s0 = quad_dpp<kSwap1>(o1 ? a[0] : a[1]);
-  float s1 = quad_dpp<kSwap1>(o1 ? a[2] : a[3]);
-  a[0] = o1 ? s0 : a[0];
-  a[1] = o1 ? a[1] : s0;
-  a[2] = o1 ? s1 : a[2];
-  a[3] = o1 ? a[3] : s1;
-  const bool o2 = (k & 2) != 0;
-  s0 = quad_dpp<kSwap2>(o2 ? a[0] : a[2]);
-  s1 = quad_dpp<kSwap2>(o2 ? a[1] : a[3]);
-  a[0] = o2 ? s0 : a[0];
-  a[1] = o2 ? s1 : a[1];
-  a[2] = o2 ? a[2] : s0;
-  a[3] = o2 ? a[3] : s1;
-}
-
 // C[z][row][col] = acc for row < r, col < cols (cols a multiple of 4).  The
 // accumulators of a 32 x 32 fragment give each lane one column and 16 rows;
 // transposed within each group of four lanes, each lane stores four
@@ -139,7 +113,7 @@ struct FactorStore {
         for (int j = 0; j < 4; ++j) {
           float a[4] = {f.acc[mi][ni][4 * j], f.acc[mi][ni][4 * j + 1], f.acc[mi][ni][4 * j + 2],
                         f.acc[mi][ni][4 * j + 3]};
-          quad_transpose(a, k);  // every lane takes part (DPP reads its quad)
+          gemm::quad_transpose(a, k);  // every lane takes part (DPP reads its quad)
           const int row = f.row0 + 32 * mi + 8 * j + 4 * (f.lane >> 5) + k;
           if (row < r && c0 < cols)
             *reinterpret_cast<float4*>(base + static_cast<int64_t>(row) * cols + c0) =
