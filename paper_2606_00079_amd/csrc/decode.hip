@@ -554,7 +554,7 @@ bitsmoe_status check_decode(const char* who, const void* codes, const void* para
 }
 
 // Host routing grouped by expert, checked, with each token's entries (in the
-// order given) and the experts' entries in jobs of up to T (4 when some
+// order given) and the experts' entries in jobs of up to T (tmax when some
 // expert has several tokens, else 1).
 struct RoutingTables {
   int64_t nnz = 0, kmax = 1, njobs = 0;
@@ -565,7 +565,7 @@ struct RoutingTables {
 
 bitsmoe_status build_routing(const std::string& who, int64_t E, int64_t B,
                              const int64_t* offsets_host, const int32_t* tokens_host,
-                             const float* weights_host, RoutingTables* rt) {
+                             const float* weights_host, int tmax, RoutingTables* rt) {
   if (!offsets_host || !tokens_host || !weights_host) return fail(BITSMOE_ERR_ARG, who + ": null pointer");
   if (offsets_host[0] != 0) return fail(BITSMOE_ERR_ARG, who + ": offsets[0] must be 0");
   for (int64_t e = 0; e < E; ++e)
@@ -591,7 +591,7 @@ bitsmoe_status build_routing(const std::string& who, int64_t E, int64_t B,
   }
   int64_t cmax = 0;
   for (int64_t e = 0; e < E; ++e) cmax = std::max(cmax, offsets_host[e + 1] - offsets_host[e]);
-  const int T = cmax > 1 ? 4 : 1;
+  const int T = cmax > 1 ? tmax : 1;
   rt->jobs.clear();
   for (int64_t e = 0; e < E; ++e)
     for (int64_t i = offsets_host[e]; i < offsets_host[e + 1]; i += T) {
@@ -692,6 +692,8 @@ bitsmoe_status decode_launch(const DecodeGeom& g, int T, bool topk_jobs, int64_t
       if (g.one_slice) BITSMOE_DEC(1, true, true); else BITSMOE_DEC(1, false, true);
     } else if (T == 4) {
       if (g.one_slice) BITSMOE_DEC(4, true, false); else BITSMOE_DEC(4, false, false);
+    } else if (T == 2) {
+      if (g.one_slice) BITSMOE_DEC(2, true, false); else BITSMOE_DEC(2, false, false);
     } else {
       if (g.one_slice) BITSMOE_DEC(1, true, false); else BITSMOE_DEC(1, false, false);
     }
@@ -734,7 +736,9 @@ extern "C" bitsmoe_status bitsmoe_moe_decode(const uint64_t* codes_dev, const ui
                                    Ut_dev, X_dev, Y_dev, total_words, E, r, d_in, group, d_out, B);
   if (st != BITSMOE_OK) return st;
   RoutingTables rt;
-  st = build_routing("moe_decode", E, B, offsets_host, tokens_host, weights_host, &rt);
+  // two tokens per job: the token values a lane holds take 64 registers
+  // (four tokens' 128 left room for two waves per SIMD only)
+  st = build_routing("moe_decode", E, B, offsets_host, tokens_host, weights_host, 2, &rt);
   if (st != BITSMOE_OK) return st;
   const DecodeGeom g = decode_geometry(rt.njobs, r, d_in, B);
   int4* jobs_d;
@@ -799,7 +803,7 @@ extern "C" bitsmoe_status bitsmoe_moe_decode_in(const uint64_t* codes_dev, const
   if (st != BITSMOE_OK) return st;
   if (d_in > (1 << 20)) return fail(BITSMOE_ERR_SHAPE, "moe_decode_in: d_in above 2^20");
   RoutingTables rt;
-  st = build_routing("moe_decode_in", E, B, offsets_host, tokens_host, weights_host, &rt);
+  st = build_routing("moe_decode_in", E, B, offsets_host, tokens_host, weights_host, 4, &rt);
   if (st != BITSMOE_OK) return st;
   int4* jobs_d;
   int64_t* pidx_d;
