@@ -690,8 +690,6 @@ bitsmoe_status decode_launch(const DecodeGeom& g, int T, bool topk_jobs, int64_t
                      group, g.L, g.passes, X_dev, jobs_d, topk_d, kk, static_cast<int>(E), w_d, zp)
     if (topk_jobs) {
       if (g.one_slice) BITSMOE_DEC(1, true, true); else BITSMOE_DEC(1, false, true);
-    } else if (T == 4) {
-      if (g.one_slice) BITSMOE_DEC(4, true, false); else BITSMOE_DEC(4, false, false);
     } else if (T == 2) {
       if (g.one_slice) BITSMOE_DEC(2, true, false); else BITSMOE_DEC(2, false, false);
     } else {
