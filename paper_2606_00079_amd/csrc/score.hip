@@ -62,10 +62,18 @@ __global__ __launch_bounds__(256) void habsmax_kernel(const float* __restrict__ 
   partial += static_cast<int64_t>(blockIdx.y) * kAbsMaxBlocks;
   float m = 0.0f;
   const int64_t n4 = d * d / 4;
+  const int64_t stride = static_cast<int64_t>(gridDim.x) * 256;
+  // four 16-byte loads in flight per thread
   for (int64_t idx = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; idx < n4;
-       idx += static_cast<int64_t>(gridDim.x) * 256) {
-    const float4 v = reinterpret_cast<const float4*>(H)[idx];
-    m = fmaxf(m, fmaxf(fmaxf(fabsf(v.x), fabsf(v.y)), fmaxf(fabsf(v.z), fabsf(v.w))));
+       idx += 4 * stride) {
+    float4 v[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      v[q] = idx + q * stride < n4 ? reinterpret_cast<const float4*>(H)[idx + q * stride]
+                                   : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      m = fmaxf(m, fmaxf(fmaxf(fabsf(v[q].x), fabsf(v[q].y)), fmaxf(fabsf(v[q].z), fabsf(v[q].w))));
   }
   red[threadIdx.x] = m;
   __syncthreads();
@@ -108,24 +116,38 @@ __global__ __launch_bounds__(256) void hoff_kernel(const float* __restrict__ H, 
   }
   __syncthreads();
   const int F = sF;
-  const int64_t total = d_pad * d;
+  // eight consecutive outputs per thread: one row i, entries k .. k+7 of one
+  // K tile and one column block (d is a multiple of 32)
+  const int64_t total8 = d_pad * d / 8;
   const int64_t nkt = d / gemm::kTileK;
   constexpr int64_t TB = static_cast<int64_t>(SBM) * gemm::kTileK;  // elements per tiled block
-  for (int64_t idx = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; idx < total;
-       idx += static_cast<int64_t>(gridDim.x) * 256) {
+  for (int64_t c = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; c < total8;
+       c += static_cast<int64_t>(gridDim.x) * 256) {
+    const int64_t idx = 8 * c;
     const int64_t t = idx / TB, w = idx - t * TB;
     const int64_t rt = t / nkt, kt = t - rt * nkt;
     const int64_t i = rt * SBM + w / gemm::kTileK;
     const int64_t k = kt * gemm::kTileK + w % gemm::kTileK;
-    uint16_t v = 0;
-    if (i < d) {
-      const float h = H[i * d + k];
-      if (i == k)
-        hdiag[i] = h;
-      else if (k / SBM >= i / SBM)  // at or right of the diagonal block
-        v = f32_to_f16_bits(ldexpf(h, k / SBM > i / SBM ? F + 1 : F));
+    uint16_t v[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    if (i < d && k / SBM >= i / SBM) {  // at or right of the diagonal block
+      const float4 h0 = *reinterpret_cast<const float4*>(H + i * d + k);
+      const float4 h1 = *reinterpret_cast<const float4*>(H + i * d + k + 4);
+      const float h[8] = {h0.x, h0.y, h0.z, h0.w, h1.x, h1.y, h1.z, h1.w};
+      const int e = k / SBM > i / SBM ? F + 1 : F;
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        if (i == k + q)
+          hdiag[i] = h[q];
+        else
+          v[q] = f32_to_f16_bits(ldexpf(h[q], e));
+      }
     }
-    Hoff[idx] = v;
+    uint4 pk;
+    pk.x = static_cast<uint32_t>(v[0]) | (static_cast<uint32_t>(v[1]) << 16);
+    pk.y = static_cast<uint32_t>(v[2]) | (static_cast<uint32_t>(v[3]) << 16);
+    pk.z = static_cast<uint32_t>(v[4]) | (static_cast<uint32_t>(v[5]) << 16);
+    pk.w = static_cast<uint32_t>(v[6]) | (static_cast<uint32_t>(v[7]) << 16);
+    *reinterpret_cast<uint4*>(Hoff + idx) = pk;
   }
 }
 
@@ -669,7 +691,7 @@ bitsmoe_status loss_table_hoff(const float* H_dev, const LossTable& t, hipStream
   const unsigned nh = static_cast<unsigned>(t.nh);
   hipLaunchKernelGGL(habsmax_kernel, dim3(kAbsMaxBlocks, nh), dim3(256), 0, s, H_dev, t.d, t.hpart);
   BITSMOE_LAUNCH_CHECK(who);
-  const unsigned hb = static_cast<unsigned>(std::min<int64_t>((t.d_pad * t.d + 255) / 256, 16384));
+  const unsigned hb = static_cast<unsigned>(std::min<int64_t>((t.d_pad * t.d / 8 + 255) / 256, 16384));
   hipLaunchKernelGGL(hoff_kernel, dim3(hb, nh), dim3(256), 0, s, H_dev, t.d, t.d_pad, t.hpart, t.Hoff,
                      t.hdiag, t.hexp);
   BITSMOE_LAUNCH_CHECK(who);
