@@ -13,13 +13,14 @@
 // grid, each wave owning a (BM/2) x (BN/2) block of v_mfma_f32_32x32x16_bf16
 // (or _f16 when the operands are fp16)
 // accumulators.  K advances 32 at a time through four LDS stages filled by
-// direct global->LDS loads (global_load_lds_dwordx4), so three stages are in
-// flight while one is multiplied; the stages are distinct LDS arrays and the
-// K loop is unrolled by four, which lets the compiler see that reading one
-// stage does not wait for the loads into the others.  LDS rows are 64 bytes
-// and the four 16-byte chunks of row r are stored XOR-swizzled by
-// (r / 4) mod 4, so the fragment reads of the matrix-core operands are free
-// of bank conflicts.
+// direct global->LDS loads (global_load_lds_dwordx4): while K tile i is
+// multiplied, tile i+3 is loaded into the buffer tile i-1 used.  One wave
+// per SIMD issues in order, so the loads of a refill and the fragment reads
+// of the next K=16 step are interleaved one per matrix-core op and spread
+// over both steps of the tile (see `mfmas`); waits are explicit s_waitcnt
+// counts and barriers bare s_barrier.  LDS rows are 64 bytes and the four
+// 16-byte chunks of row r are stored XOR-swizzled by (r / 4) mod 4, so the
+// fragment reads of the matrix-core operands are free of bank conflicts.
 //
 // The K index is a flattened (pass, segment, k) triple:
 //   * passes   let one launch add up to 4 products A_p B_p^T into the same
