@@ -43,6 +43,23 @@ PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 / fp16 matrix-core peak
 SURROGATE_GAMMA = {"tiny": 0.7, "qwen_gate": 0.7, "qwen_layer": 0.7, "mixtral": 0.5, "dsv3": 0.2}
 KAPPA_PRINTED = (0.14949200, 0.04067890, 0.01184786)  # Table kappa_values, widths 2, 3, 4
 PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
+# The paper's own headline ratios, with the hardware it states; context only
+# (other GPUs, another pipeline: its surrogate cost and a MILP solver).
+PAPER_CONTEXT = {
+    "note": "context only: the paper's ratios over GPTQ on its own hardware, not a target "
+            "for this measurement",
+    "quantization_speedup_over_gptq": {
+        "value": 12.3, "hardware": "NVIDIA A100-PCIe-80GB",
+        "workload": "Qwen3-30B-A3B-Base, 2-bit; offline quantization end to end (calibration "
+                    "statistics, SVD, ILP by the Gurobi solver)",
+        "source": "abstract; Sec. 4.4 (Fig. time_breakdown); hardware in Sec. 4.1"},
+    "decode_speedup_over_gptq": {
+        "value": 1.76, "tokens_per_s": {"bitsmoe": 5.71, "gptq": 3.25, "fp16": 3.07},
+        "hardware": "NVIDIA A6000",
+        "workload": "Qwen3-30B-A3B-Base, 2-bit; batch 1, prefill 256, generate 128; GPTQ on its "
+                    "Triton backend",
+        "source": "abstract; Sec. 4.4 (Table efficiency_memory)"},
+}
 
 
 def log(*a):
@@ -95,7 +112,10 @@ class _LayerProj:
 
 
 def cpu_baseline(cfg, layer) -> dict:
-    """Times the fp64 oracle on a bounded sample of the layer; scales to the layer."""
+    """Times the fp64 oracle on the whole layer, every step measured in full
+    (no sampling, no scaling): per projection H (once per calibration input,
+    as the device path shares it), M over all experts, the eigensolve, C,
+    the loss table over every unit and width, the exact ILP DP and pack."""
     import numpy as np
     import oracle
     import synth
@@ -106,51 +126,37 @@ def cpu_baseline(cfg, layer) -> dict:
         threads = os.cpu_count() or 1
     total_s = 0.0
     parts = []
-    t_sample = time.perf_counter()
     H_cache = {}
     for proj in layer:
-        E = proj.E
-        e_s = min(E, 64)   # experts in the M sample
-        e_c = min(E, -(-16384 // proj.r))  # experts in the C sample (>= 16384 units)
-        W64 = synth.as_f64(proj.W[:e_s], proj.dtype)
+        steps = {}
+
+        def timed(name, fn):
+            t = time.perf_counter()
+            v = fn()
+            steps[name] = time.perf_counter() - t
+            log(f"oracle {proj.spec.name}: {name} {steps[name]:.2f}s")
+            return v
         key = id(proj.X)
-        t = time.perf_counter()
         if key not in H_cache:
-            H_cache[key] = oracle.gram(synth.as_f64(proj.X, proj.dtype))
+            H_cache[key] = timed("H", lambda: oracle.gram(synth.as_f64(proj.X, proj.dtype)))
+        else:
+            steps["H"] = 0.0
         H = H_cache[key]
-        t_h = time.perf_counter() - t
-        t = time.perf_counter()
-        M = oracle.gram_experts(W64)
-        t_m = (time.perf_counter() - t) * E / e_s
-        t = time.perf_counter()
-        Ut, _ = oracle.shared_basis(M, proj.r)
-        t_eig = time.perf_counter() - t
-        t = time.perf_counter()
-        C = oracle.project(Ut, synth.as_f64(proj.W[:e_c], proj.dtype))
-        t_c = (time.perf_counter() - t) * E / e_c
-        units = E * proj.r
-        rows = min(16384, C.shape[0])
-        t = time.perf_counter()
-        L = oracle.score(C[:rows].astype(np.float32), H, proj.bits, proj.group)
-        t_l = (time.perf_counter() - t) * units / rows
-        # ILP: the exact DP on a sample of units scales with units * budget
-        us = min(32768, units)
-        Ls = np.tile(L, (us // rows + 1, 1))[:us]
-        t = time.perf_counter()
-        oracle.allocate_dp(Ls, proj.bits, int(proj.cfg.budget * us))
-        t_ilp = (time.perf_counter() - t) * (units / us) ** 2
-        t = time.perf_counter()
-        bits_u = np.full(rows, proj.bits[1], dtype=np.uint8)
-        oracle.pack(C[:rows].astype(np.float32), bits_u, proj.group)
-        t_p = (time.perf_counter() - t) * units / rows
-        s = t_h + t_m + t_eig + t_c + t_l + t_ilp + t_p
-        total_s += s
-        parts.append(f"{proj.spec.name}: H {t_h:.2f}s M {t_m:.2f}s eig {t_eig:.2f}s C {t_c:.2f}s "
-                     f"L {t_l:.1f}s ILP {t_ilp:.1f}s pack {t_p:.1f}s")
-    spent = time.perf_counter() - t_sample
-    sample = (f"{spent:.1f} s of host time; fp64 numpy oracle per projection: full H and eigensolve; M on 64 experts, C on the first "
-              "16384 units' experts, L and pack on 16384 units, exact ILP DP on 32768 units; scaled to the layer "
-              "(linear in experts/units, quadratic for the DP). " + "; ".join(parts))
+        W64 = synth.as_f64(proj.W, proj.dtype)
+        M = timed("M", lambda: oracle.gram_experts(W64))
+        Ut, _ = timed("eig", lambda: oracle.shared_basis(M, proj.r))
+        C32 = timed("C", lambda: oracle.project(Ut, W64).astype(np.float32))
+        del W64, M
+        L = timed("L", lambda: oracle.score(C32, H, proj.bits, proj.group))
+        bits_u, _ = timed("ILP", lambda: oracle.allocate_dp(L, proj.bits, proj.budget_bits))
+        timed("pack", lambda: oracle.pack(C32, bits_u, proj.group))
+        del C32, L
+        total_s += sum(steps.values())
+        parts.append(f"{proj.spec.name}: " + " ".join(f"{k} {v:.2f}s" for k, v in steps.items()))
+    sample = ("the whole layer, every step measured in full (fp64 numpy oracle: H once per "
+              "calibration input, M over all experts, eigensolve, C, loss table over every unit "
+              "and width, exact ILP dynamic program, pack; no sampling or scaling). "
+              + "; ".join(parts))
     return {"value": round(total_s * 1e3, 1), "unit": "ms per layer", "cores": int(threads),
             "kind": "oracle", "sample": sample}
 
@@ -359,14 +365,28 @@ def _decode_case(p, r, inp, routing, Xdec, bm, reps, form="out"):
     torch.cuda.synchronize()
     bmm_ms = a.elapsed_time(b) / reps
     dense_bytes = len(touched) * d_out * d_in * W.element_size() + B * d_in * 2 + B * d_out * 4
-    dev_ms = zms + yms
+    common = {"tokens": B, "experts_touched": len(touched), "routing_entries": nnz,
+              "bytes": dec_bytes, "dense_bf16_bytes": dense_bytes,
+              "dense_bf16_window_ms": round(dense_ms, 5),
+              "dense_bf16_bmm_window_ms": round(bmm_ms, 5)}
     if form == "in":
-        return {"tokens": B, "experts_touched": len(touched), "routing_entries": nnz,
-                "z_kernel_ms": round(zms, 5), "y_kernel_ms": round(yms, 5),
-                "device_ms": round(dev_ms, 5), "call_ms_incl_host_routing": round(call_ms, 4),
-                "bytes": dec_bytes, "gbs": round(dec_bytes / (dev_ms * 1e-3) / 1e9, 1),
-                "dense_bf16_bmm_only_ms": round(bmm_ms, 5),
-                "speedup_vs_dense_bf16_bmm": round(bmm_ms / dev_ms, 2)}
+        # back-to-back calls in one event window, as the dense side is timed;
+        # each call prepares its routing tables on the host and waits for
+        # the stream once, and that is part of the window
+        a.record()
+        for _ in range(reps):
+            run()
+        b.record()
+        torch.cuda.synchronize()
+        win_ms = a.elapsed_time(b) / reps
+        common.update({
+            "decode_window_ms": round(win_ms, 5),
+            "decode_window_includes": "host routing preparation and one stream wait per call",
+            "speedup_vs_dense_bf16": round(dense_ms / win_ms, 2),
+            "speedup_vs_dense_bf16_bmm_only": round(bmm_ms / win_ms, 2),
+            "decode_kernel_ms": {"z": round(zms, 5), "y": round(yms, 5)},
+            "call_ms_wall": round(call_ms, 4)})
+        return common
     # the same tokens from a device top-k table (no host work per call),
     # calls back to back as in a decode loop
     top = np.full((B, 8 if nnz >= 8 * B else max(1, nnz // B)), -1, dtype=np.int32)
@@ -393,27 +413,40 @@ def _decode_case(p, r, inp, routing, Xdec, bm, reps, form="out"):
                            r.Ut, Xdec, topd, wtd, out=Yk)
     a1.record()
     torch.cuda.synchronize()
-    topk_call_ms = a0.elapsed_time(a1) / reps
+    topk_window_ms = a0.elapsed_time(a1) / reps
     tz = bm.kernel_time("moe_decode_z")[0] / reps
     ty = bm.kernel_time("moe_decode_y")[0] / reps
     bm.timing(False)
-    return {"tokens": B, "experts_touched": len(touched), "routing_entries": nnz,
-            "z_kernel_ms": round(zms, 5), "y_kernel_ms": round(yms, 5),
-            "device_ms": round(dev_ms, 5), "call_ms_incl_host_routing": round(call_ms, 4),
-            "bytes": dec_bytes, "gbs": round(dec_bytes / (dev_ms * 1e-3) / 1e9, 1),
-            "hbm_floor_ms": round(dec_bytes / (PEAK_HBM_GBS * 1e9) * 1e3, 5),
-            "dense_bf16_ms": round(dense_ms, 5), "dense_bf16_bmm_only_ms": round(bmm_ms, 5),
-            "dense_bf16_bytes": dense_bytes,
-            "dense_bf16_gbs": round(dense_bytes / (dense_ms * 1e-3) / 1e9, 1),
-            "speedup_vs_dense_bf16": round(dense_ms / dev_ms, 2),
-            "topk_device_ms": round(tz + ty, 5), "topk_call_ms_back_to_back": round(topk_call_ms, 5)}
+    # the same window without the per-kernel timing events
+    a0.record()
+    for _ in range(reps):
+        bm.moe_decode_topk(r.codes, r.params, bits_d, off_d, int(r.offsets[-1]), E, p.r, d_in, G,
+                           r.Ut, Xdec, topd, wtd, out=Yk)
+    a1.record()
+    torch.cuda.synchronize()
+    win_ms = a0.elapsed_time(a1) / reps
+    common.update({
+        "decode_window_ms": round(win_ms, 5),
+        "decode_window_includes": "the top-k form: z and y kernels, no host work",
+        "speedup_vs_dense_bf16": round(dense_ms / win_ms, 2),
+        "speedup_vs_dense_bf16_bmm_only": round(bmm_ms / win_ms, 2),
+        "decode_kernel_ms": {"z": round(tz, 5), "y": round(ty, 5)},
+        "decode_window_with_kernel_events_ms": round(topk_window_ms, 5),
+        "gbs_window": round(dec_bytes / (win_ms * 1e-3) / 1e9, 1),
+        "hbm_floor_ms": round(dec_bytes / (PEAK_HBM_GBS * 1e9) * 1e3, 5),
+        "dense_bf16_gbs_window": round(dense_bytes / (dense_ms * 1e-3) / 1e9, 1),
+        "grouped_form": {"z_kernel_ms": round(zms, 5), "y_kernel_ms": round(yms, 5),
+                         "call_ms_wall_incl_host_routing": round(call_ms, 4)}})
+    return common
 
 
 def decode_report(cfg, layer, res, dev_inputs, bm, reps=50) -> dict:
     """Stage-3 decode of every projection of the layer from its packed factors
     (y = U sum_j g_j C^_e x, output-space form) for a batch of 1 token and of
     64 tokens routed by the synthetic top-k router, beside a dense bf16
-    batched product over the same routed experts' weights."""
+    batched product over the same routed experts' weights.  Both sides are
+    timed the same way: one HIP-event window over back-to-back calls, divided
+    by the number of calls."""
     import numpy as np
     import torch
     import synth
@@ -633,6 +666,11 @@ def main(argv=None) -> int:
         "host_ilp_ms": round(float(np.median(ilp_ms)), 2),
         "kernels": kernels,
         "roofline": {"bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS,
+                     "achieved_basis": "algorithmic flops 2*units*nbits*d^2 per launch (dense "
+                                       "form) over the average launch time; the kernel uses the "
+                                       "symmetry of H and executes the upper block triangle only "
+                                       "(executed_tflops, executed_frac: the matrix cores' actual "
+                                       "rate)",
                      "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
                      "traffic": traffic, "kernel": "score_gemm",
                      "launches_per_step": n_gemm // max(steps, 1),
@@ -643,6 +681,7 @@ def main(argv=None) -> int:
                      "executed_frac": round(score_exec_flops / (score_ms_step * 1e-3) / 1e12
                                             / PEAK_BF16_TFLOPS, 4)},
     }
+    out["paper_context"] = PAPER_CONTEXT
     if side:
         out["surrogate"] = sur
         out["inspace"] = insp

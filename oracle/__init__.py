@@ -37,7 +37,7 @@ independent library routines (``tests/test_oracle_*.py``).
 from .spectral import gram, gram_experts, shared_basis, project, unit_energy, truncation_loss
 from .quant import (quant_group, fake_quant, score, score_rows, pack_layout, pack, unpack,
                     bit_planes)
-from .ilp import integerize, allocate_dp, allocate_exhaustive, objective, budget_from_avg
+from .ilp import integerize, allocate_dp, allocate_exhaustive, objective
 from . import surrogate, inspace, routed, decode
 from .surrogate import surrogate_table, budget_equivalent
 
@@ -45,5 +45,5 @@ __all__ = [
     "gram", "gram_experts", "shared_basis", "project", "unit_energy", "truncation_loss",
     "quant_group", "fake_quant", "score", "score_rows", "pack_layout", "pack", "unpack",
     "bit_planes", "integerize", "allocate_dp", "allocate_exhaustive", "objective",
-    "budget_from_avg", "surrogate", "surrogate_table", "budget_equivalent", "inspace", "routed", "decode",
+    "surrogate", "surrogate_table", "budget_equivalent", "inspace", "routed", "decode",
 ]

@@ -33,10 +33,6 @@ class Infeasible(ValueError):
     pass
 
 
-def budget_from_avg(avg_bits: float, units: int) -> int:
-    return int(math.floor(avg_bits * units))
-
-
 def integerize(L) -> np.ndarray:
     """Exact int64 costs: rint(L * 2^K / max|L|), K = 62 - ceil(log2(units+1))."""
     L = np.asarray(L, dtype=np.float64)
@@ -72,16 +68,25 @@ def _setup(L, bits, budget):
     return bits, Li, U, ex, cap
 
 
-def _backward_step(g_next: np.ndarray, row: np.ndarray, ex, cap: int) -> np.ndarray:
-    """g_i(c) = min_j row[j] + g_{i+1}(c - ex_j) over widths with ex_j <= c."""
-    g = g_next + row[0]
+def _backward_step(g_next: np.ndarray, row: np.ndarray, ex, cap: int,
+                   out: np.ndarray = None, tmp: np.ndarray = None) -> np.ndarray:
+    """g_i(c) = min_j row[j] + g_{i+1}(c - ex_j) over widths with ex_j <= c.
+
+    ``out`` and ``tmp`` (cap + 1 entries each, neither aliasing g_next) are
+    optional preallocated buffers; the result is written to ``out``."""
+    if out is None:
+        out = np.empty_like(g_next)
+    if tmp is None:
+        tmp = np.empty_like(g_next)
+    np.add(g_next, row[0], out=out)
     for j in range(1, len(ex)):
         e = ex[j]
         if e > cap:
             continue
-        cand = g_next[: cap + 1 - e] + row[j]
-        np.minimum(g[e:], cand, out=g[e:])
-    return g
+        cand = tmp[: cap + 1 - e]
+        np.add(g_next[: cap + 1 - e], row[j], out=cand)
+        np.minimum(out[e:], cand, out=out[e:])
+    return out
 
 
 def allocate_dp(L, bits, budget: int, block: int = 256, full_limit: int = 1 << 26):
@@ -124,12 +129,15 @@ def allocate_dp(L, bits, budget: int, block: int = 256, full_limit: int = 1 << 2
 
     ckpt = {U: zero}
     g = zero
+    bufs = [np.empty(cap + 1, dtype=np.int64) for _ in range(2)]
+    tmp = np.empty(cap + 1, dtype=np.int64)
     for i in range(U - 1, -1, -1):
-        g = _backward_step(g, Li[i], ex, cap)
+        g = _backward_step(g, Li[i], ex, cap, out=bufs[i % 2], tmp=tmp)
         if i % block == 0:
-            ckpt[i] = g
+            ckpt[i] = g.copy()
     best = int(ckpt[0][cap])
     c = cap
+    blk = [np.empty(cap + 1, dtype=np.int64) for _ in range(block)]  # reused per block
     for i0 in range(0, U, block):
         i1 = min(i0 + block, U)
         tables = [None] * (i1 - i0 + 1)
@@ -137,7 +145,8 @@ def allocate_dp(L, bits, budget: int, block: int = 256, full_limit: int = 1 << 2
         if tables[-1] is None:  # i1 == U is always checkpointed; others are block multiples
             raise AssertionError("missing checkpoint")
         for t in range(i1 - i0 - 1, 0, -1):
-            tables[t] = _backward_step(tables[t + 1], Li[i0 + t], ex, cap)
+            tables[t] = _backward_step(tables[t + 1], Li[i0 + t], ex, cap,
+                                       out=blk[t] if t < len(blk) else None, tmp=tmp)
         tables[0] = ckpt[i0]
         c = forward(i0, i1, tables, c)
     return out, best

@@ -116,28 +116,32 @@ def pack_layout(bits_u, d: int) -> np.ndarray:
 
 
 def bit_planes(q: np.ndarray, b: int) -> np.ndarray:
-    """Bit-plane words of one code row: [b][d/64] uint64.
+    """Bit-plane words of code rows: [..., b, d/64] uint64 for q [..., d].
 
-    Word w of plane t has bit j equal to bit t of q[64 w + j].
+    Word w of plane t has bit j equal to bit t of q[64 w + j] (one row: the
+    result is [b][d/64]).
     """
     q = np.asarray(q, dtype=np.uint64)
-    d = q.shape[0]
+    d = q.shape[-1]
+    lead = q.shape[:-1]
     shifts = np.arange(64, dtype=np.uint64)
-    out = np.empty((b, d // 64), dtype=np.uint64)
+    out = np.empty(lead + (b, d // 64), dtype=np.uint64)
     for t in range(b):
         bit = (q >> np.uint64(t)) & np.uint64(1)
-        out[t] = np.sum(bit.reshape(d // 64, 64) << shifts[None, :], axis=1, dtype=np.uint64)
+        out[..., t, :] = np.sum(bit.reshape(lead + (d // 64, 64)) << shifts, axis=-1,
+                                dtype=np.uint64)
     return out
 
 
-def pack(C, bits_u, G: int):
+def pack(C, bits_u, G: int, chunk: int = 8192):
     """Pack every unit at its assigned width.
 
     Widths 1..8 are codes of the group rule as bit planes.  The surrogate's
     two extra widths (Sec. 3.3, candidate set {16, 8, 6, 4, 3, 2, 1, 0}):
     16 stores the row itself in fp16 (round to nearest even), entry 4 w + i
     in bits 16 i .. 16 i + 15 of word w; 0 (eviction) stores nothing.  Their
-    group parameters are zero.
+    group parameters are zero.  Units of one width are packed together, in
+    blocks of ``chunk`` units.
 
     Returns (codes uint64 [total words], params uint16 [units][d/G][2] holding
     the fp16 bit patterns of (s16, m16), offsets int64 [units+1]).
@@ -149,21 +153,21 @@ def pack(C, bits_u, G: int):
     codes = np.zeros(int(off[-1]), dtype=np.uint64)
     params = np.zeros((units, d // G, 2), dtype=np.uint16)
     for b in np.unique(bits_u):
-        us = np.nonzero(bits_u == b)[0]
         if b == 0:
             continue
-        if b == 16:
-            for u in us:
-                codes[off[u]:off[u + 1]] = C32[u].astype(np.float16).view(np.uint64)
-            continue
-        if not 1 <= b <= 8:
+        if b != 16 and not 1 <= b <= 8:
             raise ValueError("pack: widths are 0, 1..8 or 16")
-        q, s16, m16 = quant_group(C32[us], int(b), G)
-        params[us, :, 0] = s16.view(np.uint16)
-        params[us, :, 1] = m16.view(np.uint16)
-        for i, u in enumerate(us):
-            words = bit_planes(q[i], int(b)).reshape(-1)
-            codes[off[u]:off[u + 1]] = words
+        for i0 in range(0, int(np.count_nonzero(bits_u == b)), chunk):
+            us = np.nonzero(bits_u == b)[0][i0:i0 + chunk]
+            words = int(b) * d // 64
+            where = off[us][:, None] + np.arange(words)[None, :]
+            if b == 16:
+                codes[where] = C32[us].astype(np.float16).view(np.uint64).reshape(len(us), words)
+                continue
+            q, s16, m16 = quant_group(C32[us], int(b), G)
+            params[us, :, 0] = s16.view(np.uint16)
+            params[us, :, 1] = m16.view(np.uint16)
+            codes[where] = bit_planes(q, int(b)).reshape(len(us), words)
     return codes, params, off
 
 

@@ -66,6 +66,29 @@ class _Seg:
         return float(self.a.elapsed_time(self.b))
 
 
+def _allocate_timed(seg: "_Seg", L, bits, budget: int, d: int, dev, times: Dict[str, float],
+                    seg_key: str):
+    """Waits for the device segment ``seg`` (its end event), copies L to the
+    host, then times the ILP alone (host_ilp_ms).  The L copy and the copy
+    of the widths and offsets back to the device are timed apart
+    (host_copy_ms), so that neither device time nor transfers are counted as
+    ILP time."""
+    import torch
+    times[seg_key] = seg.ms()              # synchronizes on the segment's end
+    t0 = time.perf_counter()
+    Lh = L.cpu().numpy()
+    t1 = time.perf_counter()
+    bits_u, obj = allocate(Lh, bits, budget)
+    off = pack_layout(bits_u, d)
+    t2 = time.perf_counter()
+    bits_d = torch.from_numpy(bits_u).to(dev, non_blocking=False)
+    off_d = torch.from_numpy(off).to(dev, non_blocking=False)
+    t3 = time.perf_counter()
+    times["host_ilp_ms"] = (t2 - t1) * 1e3
+    times["host_copy_ms"] = ((t1 - t0) + (t3 - t2)) * 1e3
+    return bits_u, obj, off, bits_d, off_d
+
+
 def quantize_projection(W, X, r: int, bits: Sequence[int], group: int, budget: int,
                         H=None, eig: str = "host") -> ProjectionResult:
     """The hot path on one projection.  eig = "host" (LAPACK on M copied to
@@ -100,14 +123,8 @@ def quantize_projection(W, X, r: int, bits: Sequence[int], group: int, budget: i
     with s2:
         project(Ut, W, out=C)
         score(C, H, bits, group, out=L)
-    t0 = time.perf_counter()
-    Lh = L.cpu().numpy()                     # waits for the score
-    bits_u, obj = allocate(Lh, bits, budget)
-    off = pack_layout(bits_u, C.shape[1])
-    times["gpu_score_ms"] = s2.ms()
-    bits_d = torch.from_numpy(bits_u).to(dev, non_blocking=False)
-    off_d = torch.from_numpy(off).to(dev, non_blocking=False)
-    times["host_ilp_ms"] = (time.perf_counter() - t0) * 1e3
+    bits_u, obj, off, bits_d, off_d = _allocate_timed(s2, L, bits, budget, C.shape[1], dev, times,
+                                                      "gpu_score_ms")
     codes = torch.empty((max(int(off[-1]), 1),), dtype=torch.int64, device=dev)
     params = torch.empty((C.shape[0], d_in // group, 2), dtype=torch.int16, device=dev)
     s3 = _Seg()
@@ -148,14 +165,8 @@ def quantize_projection_in(W, X, r: int, bits: Sequence[int], group: int, budget
         project_in(Vt, W, out=C)
         basis_importance(Vt, H, out=beta)
         score_diag(C, beta, bits, group, out=L)
-    t0 = time.perf_counter()
-    Lh = L.cpu().numpy()
-    bits_u, obj = allocate(Lh, bits, budget)
-    off = pack_layout(bits_u, d_out)
-    times["gpu_score_ms"] = s2.ms()
-    bits_d = torch.from_numpy(bits_u).to(dev, non_blocking=False)
-    off_d = torch.from_numpy(off).to(dev, non_blocking=False)
-    times["host_ilp_ms"] = (time.perf_counter() - t0) * 1e3
+    bits_u, obj, off, bits_d, off_d = _allocate_timed(s2, L, bits, budget, d_out, dev, times,
+                                                      "gpu_score_ms")
     codes = torch.empty((max(int(off[-1]), 1),), dtype=torch.int64, device=dev)
     params = torch.empty((C.shape[0], d_out // group, 2), dtype=torch.int16, device=dev)
     s3 = _Seg()
@@ -198,14 +209,8 @@ def quantize_projection_routed(W, X, routing, r: int, bits: Sequence[int], group
     with s2:
         project(Ut, W, out=C)
         score_routed(C, Hs, r, bits, group, out=L)
-    t0 = time.perf_counter()
-    Lh = L.cpu().numpy()
-    bits_u, obj = allocate(Lh, bits, budget)
-    off = pack_layout(bits_u, d_in)
-    times["gpu_score_ms"] = s2.ms()
-    bits_d = torch.from_numpy(bits_u).to(dev, non_blocking=False)
-    off_d = torch.from_numpy(off).to(dev, non_blocking=False)
-    times["host_ilp_ms"] = (time.perf_counter() - t0) * 1e3
+    bits_u, obj, off, bits_d, off_d = _allocate_timed(s2, L, bits, budget, d_in, dev, times,
+                                                      "gpu_score_ms")
     codes = torch.empty((max(int(off[-1]), 1),), dtype=torch.int64, device=dev)
     params = torch.empty((C.shape[0], d_in // group, 2), dtype=torch.int16, device=dev)
     s3 = _Seg()
@@ -256,14 +261,9 @@ def surrogate_allocation(C, H, gamma: float, kappa: Sequence[float], E: int, n_o
     seg = _Seg()
     with seg:
         surrogate(C, H, gamma, kappa, out=L, stats=st)
-    t0 = time.perf_counter()
-    Lh = L.cpu().numpy()
-    bits_u, obj = allocate(Lh, SURROGATE_WIDTHS, budget)
-    off = pack_layout(bits_u, d)
-    times = {"gpu_cost_ms": seg.ms()}
-    bits_d = torch.from_numpy(bits_u).to(dev)
-    off_d = torch.from_numpy(off).to(dev)
-    times["host_ilp_ms"] = (time.perf_counter() - t0) * 1e3
+    times: Dict[str, float] = {}
+    bits_u, obj, off, bits_d, off_d = _allocate_timed(seg, L, SURROGATE_WIDTHS, budget, d, dev,
+                                                      times, "gpu_cost_ms")
     codes = torch.empty((max(int(off[-1]), 1),), dtype=torch.int64, device=dev)
     params = torch.empty((units, d // group, 2), dtype=torch.int16, device=dev)
     sp = _Seg()

@@ -98,6 +98,45 @@ def test_allocate_core_path_mid_size(lib):
     assert core < U // 4
 
 
+def _layer_like_L(g, E, r, bits):
+    """Costs shaped like a loss table of E experts x r spectral units:
+    energy decaying along each expert's spectrum, error falling about 4x per
+    extra bit, log-normal spread; with forced ties (duplicated units, units
+    equal to another expert's, all-zero units, units whose widths all cost
+    the same) so that the lexicographic tie rule decides many of them."""
+    k = np.arange(r)
+    energy = (1.0 / (1.0 + k / 16.0))[None, :] * g.lognormal(0.0, 0.3, (E, r))
+    per_bit = np.power(4.0, -np.asarray(bits, np.float64))[None, :]
+    L = (energy.reshape(-1, 1) * per_bit * g.lognormal(0.0, 0.2, (E * r, len(bits))))
+    U = E * r
+    L = np.round(L * 2**14) / 2**14             # coarse values: many exact equalities
+    dup = g.integers(0, U, size=(U // 20, 2))
+    L[dup[:, 0]] = L[dup[:, 1]]
+    L[g.integers(0, U, size=U // 100)] = 0.0
+    flat = g.integers(0, U, size=U // 100)
+    L[flat] = L[flat, :1]
+    L[r:2 * r] = L[:r]                           # expert 1 repeats expert 0
+    return L.astype(np.float32)
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("E,r", [(128, 384), (128, 1024)], ids=["qwen_gate_49152", "qwen_down_131072"])
+def test_allocate_full_size_matches_oracle_dp(lib, E, r):
+    """The ILP at the Qwen3-30B-A3B-shaped layer's sizes (bits 1-4, 2.0 bits
+    per unit on average), as the benchmark runs it, against the oracle's
+    exact dynamic program: the same widths, bit for bit."""
+    g = np.random.default_rng(7000 + r)
+    bits = [1, 2, 3, 4]
+    L = _layer_like_L(g, E, r, bits)
+    U = E * r
+    budget = 2 * U
+    got, obj = pkg.allocate(L, bits, budget)
+    ref, _ = oracle.allocate_dp(L, bits, budget)
+    assert np.array_equal(got, ref)
+    assert int(got.astype(np.int64).sum()) <= budget
+    assert np.isclose(obj, oracle.objective(L, bits, ref), rtol=1e-12)
+
+
 def test_allocate_errors(lib):
     L = np.ones((4, 2), dtype=np.float32)
     with pytest.raises(pkg.BitsmoeError) as e:

@@ -5,8 +5,9 @@ The kernels run in the launch configuration bench.py uses, at the real
 shapes (several operands above 4 GB).  Inputs of the large layers are drawn
 on the device by ``synth.device`` (same recipes as the host generators); the
 oracle then checks what it can compute piece by piece: random principal
-submatrices of H and M, sampled blocks of C, sampled rows of L, and the
-codes and parameters of sampled units, bit for bit.  The bars are those of
+submatrices of H and M, sampled blocks of C, 4096 sampled rows of L, and the
+codes and parameters of 65536 units, bit for bit; the Qwen3-30B-A3B-shaped
+down projection is checked in full.  The bars are those of
 the other parity tests: 1e-3 relative Frobenius (H, M, C), 1e-3 relative per
 entry (L), bit-exact (codes, parameters, layouts).
 """
@@ -17,7 +18,7 @@ import pytest
 
 import oracle
 import synth
-from conftest import gpu_available
+from conftest import gpu_available, oracle_score_threaded
 
 pytestmark = pytest.mark.gpu
 
@@ -127,6 +128,7 @@ def test_project_full_size(case):
 
 # ------------------------------------------------------------------------- L
 SCORE_CASES = [("mixtral", "w2"), ("dsv3", "gate"), ("dsv3", "down")]
+SCORE_ROWS = 4096  # sampled rows of L per case (two of them degenerate)
 
 
 @pytest.mark.parametrize("case", SCORE_CASES, ids=lambda c: "_".join(c))
@@ -144,11 +146,12 @@ def test_score_full_size(case):
         f"error rows {units * len(cfg.bits) * d * 2 / 1e9:.1f} GB")
     L = bm.score(C, H, cfg.bits, cfg.group)
     torch.cuda.synchronize()
-    rows = np.r_[0, 1, np.sort(np.random.default_rng(16).choice(units - 2, size=62, replace=False)) + 2]
+    rows = np.r_[0, 1, np.sort(np.random.default_rng(16).choice(units - 2, size=SCORE_ROWS - 2,
+                                                                  replace=False)) + 2]
     ri = torch.from_numpy(rows).to(DEV)
     Cs = C.index_select(0, ri).cpu().numpy()
     Hh = H.cpu().numpy().astype(np.float64)
-    ref = oracle.score(Cs, Hh, cfg.bits, cfg.group)
+    ref = oracle_score_threaded(Cs, Hh, cfg.bits, cfg.group, chunk=256)
     got = L.index_select(0, ri).cpu().numpy()
     assert np.all(got[:2] == 0)
     err = l_rel(got[2:], ref[2:])
@@ -172,23 +175,31 @@ def test_pack_full_size_dsv3_down():
     off_d = torch.from_numpy(off).to(DEV)
     codes, params = bm.pack(C, bits_d, off_d, G, total)
     torch.cuda.synchronize()
-    sub = np.r_[0, units - 1, np.sort(np.random.default_rng(19).choice(units - 2, size=126,
-                                                                        replace=False)) + 1]
+    # every unit of a contiguous block of 32768, and 32768 sampled units
+    blk = np.arange(units // 2, units // 2 + 32768)
+    smp = np.sort(np.random.default_rng(19).choice(units - 2, size=32766, replace=False)) + 1
+    sub = np.unique(np.r_[0, units - 1, smp, blk])
     Cs = C.index_select(0, torch.from_numpy(sub).to(DEV)).cpu().numpy()
     rc, rp, ro = oracle.pack(Cs, bits_u[sub], G)
     codes_h = codes.cpu().numpy().view(np.uint64)
     params_h = params.cpu().numpy().view(np.uint16)
-    for i, u in enumerate(sub):
-        assert np.array_equal(codes_h[off[u]:off[u + 1]], rc[ro[i]:ro[i + 1]]), int(u)
+    # gather the device words of the sampled units into the oracle's layout
+    lens = off[sub + 1] - off[sub]
+    where = np.repeat(off[sub] - ro[:-1], lens) + np.arange(int(ro[-1]))
+    assert np.array_equal(codes_h[where], rc)
     assert np.array_equal(params_h[sub], rp)
+    say("pack", len(sub), "units bit-exact")
 
 
 # -------------------------------------------------------- end to end (down)
 def test_end_to_end_qwen_down_full_size():
     """The Qwen3-30B-A3B-shaped down projection as bench.py runs it (E=128,
-    2048x768, r=1024, SiLU-gated calibration rows), checked stage by stage.
-    The ILP's exactness is checked against the oracle DP on the full gate
-    projection and at mid sizes; here only its constraint is checked."""
+    2048x768, r=1024, SiLU-gated calibration rows), checked stage by stage:
+    every row of L (131072 units x 4 widths) and the codes and parameters of
+    every unit.  The ILP's widths at this size are checked for the budget
+    here; its exactness at 131072 units (against the oracle's dynamic
+    program) is a CPU test on costs of the same shape, and on the device's
+    own costs at the gate size."""
     layer = synth.make_layer("qwen_layer")
     proj = layer[2]
     say("end-to-end qwen down", proj.W.shape, "r", proj.r)
@@ -205,18 +216,16 @@ def test_end_to_end_qwen_down_full_size():
     C = res.C.cpu().numpy()
     assert relfro(C, oracle.project(Ut, W64)) <= REL
     H = res.H.cpu().numpy().astype(np.float64)
-    units = C.shape[0]
-    rows = np.sort(np.random.default_rng(20).choice(units, size=256, replace=False))
     L = res.L.cpu().numpy()
-    err = l_rel(L[rows], oracle.score_rows(C, H, proj.bits, proj.group, rows=rows))
-    say("L max rel", err)
+    err = l_rel(L, oracle_score_threaded(C, H, proj.bits, proj.group))
+    say("L max rel over all", C.shape[0], "units", err)
     assert err <= REL
     assert set(np.unique(res.bits_u)) <= set(proj.bits)
     assert int(res.bits_u.astype(np.int64).sum()) <= proj.budget_bits
-    sub = rows[:128]
-    rc, rp, ro = oracle.pack(C[sub], res.bits_u[sub], proj.group)
+    rc, rp, ro = oracle.pack(C, res.bits_u, proj.group)
+    assert np.array_equal(res.offsets, ro)
     codes = res.codes.cpu().numpy().view(np.uint64)
     params = res.params.cpu().numpy().view(np.uint16)
-    for i, u in enumerate(sub):
-        assert np.array_equal(codes[res.offsets[u]:res.offsets[u + 1]], rc[ro[i]:ro[i + 1]])
-    assert np.array_equal(params[sub], rp)
+    assert np.array_equal(codes[: len(rc)], rc)
+    assert np.array_equal(params, rp)
+    say("codes and params of all units bit-exact")
