@@ -42,6 +42,7 @@
  * and serving a projection from its packed factors:
  *   bitsmoe_moe_decode        y = U sum_j g_j C^_{e_j} x           (device)
  *   bitsmoe_moe_decode_topk   the same from a device top-k table   (device)
+ *   bitsmoe_moe_decode_topk_noalloc  the same, allocating nothing   (device)
  *   bitsmoe_moe_decode_in     y = sum_j g_j C^_{e_j}^T Phi^T x      (device)
  *
  * Conventions shared by every call:
@@ -421,6 +422,31 @@ bitsmoe_status bitsmoe_moe_decode_topk(const uint64_t* codes_dev, const uint16_t
                                        const float* X_dev, int64_t B, int64_t k,
                                        const int32_t* topk_experts_dev,
                                        const float* topk_weights_dev, float* Y_dev, void* stream);
+
+/*
+ * bitsmoe_moe_decode_topk for callers that cannot allocate device memory:
+ * code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc.  Same arguments, results and shape rules as
+ * bitsmoe_moe_decode_topk; it calls no hipMalloc, hipFree or other
+ * allocating routine, creates no events and does not wait.
+ * The partial sums ([B * k][r] fp32) live in a fixed device array of
+ * 4194304 floats (16 MiB) that every GPU the library runs on holds until
+ * the process ends; B * k * r above 4194304 gives BITSMOE_ERR_SHAPE.  The
+ * array's address on a device is looked up on the first call on that
+ * device.  Every call on one GPU shares that GPU's array: calls that
+ * overlap on one GPU (different streams, or several host threads) race on
+ * it and must be ordered by the caller.  Nothing in the array needs
+ * clearing between calls: each call writes every partial it reads.
+ */
+bitsmoe_status bitsmoe_moe_decode_topk_noalloc(const uint64_t* codes_dev,
+                                               const uint16_t* params_dev, const uint8_t* bits_dev,
+                                               const int64_t* word_offsets_dev,
+                                               int64_t total_words, int64_t E, int64_t r,
+                                               int64_t d_in, int group, const float* Ut_dev,
+                                               int64_t d_out, const float* X_dev, int64_t B,
+                                               int64_t k, const int32_t* topk_experts_dev,
+                                               const float* topk_weights_dev, float* Y_dev,
+                                               void* stream);
 
 /*
  * The paper's surrogate cost table (App. B.3-B.4, Theorem

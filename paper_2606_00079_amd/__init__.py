@@ -43,6 +43,7 @@ EXPORTS = [
     "bitsmoe_project_in", "bitsmoe_basis_importance", "bitsmoe_score_diag",
     "bitsmoe_gram_routed", "bitsmoe_score_routed", "bitsmoe_moe_decode",
     "bitsmoe_moe_decode_topk", "bitsmoe_shared_basis_gpu", "bitsmoe_moe_decode_in",
+    "bitsmoe_moe_decode_topk_noalloc",
 ]
 # Candidate widths of the surrogate table, in column order.
 SURROGATE_WIDTHS = (0, 1, 2, 3, 4, 6, 8, 16)
@@ -105,6 +106,7 @@ def lib() -> ctypes.CDLL:
                                         vp, vp, vp, vp, vp]
     L.bitsmoe_moe_decode_topk.argtypes = [vp, vp, vp, vp, i64, i64, i64, i64, i32, vp, i64, vp,
                                           i64, i64, vp, vp, vp, vp]
+    L.bitsmoe_moe_decode_topk_noalloc.argtypes = L.bitsmoe_moe_decode_topk.argtypes
     L.bitsmoe_set_lapack.argtypes = [ctypes.c_char_p]
     L.bitsmoe_timing.argtypes = [i32]
     L.bitsmoe_kernel_time.argtypes = [ctypes.c_char_p, vp, vp]
@@ -399,9 +401,12 @@ def moe_decode_in(codes, params, bits_dev, offsets_dev, total_words: int, E: int
 
 
 def moe_decode_topk(codes, params, bits_dev, offsets_dev, total_words: int, E: int, r: int,
-                    d_in: int, group: int, Ut, X, topk_experts, topk_weights, out=None):
+                    d_in: int, group: int, Ut, X, topk_experts, topk_weights, out=None,
+                    noalloc: bool = False):
     """moe_decode from the router's device top-k table: topk_experts int32
-    [B][k], topk_weights fp32 [B][k] (both on the device) -> fp32 [B][d_out]."""
+    [B][k], topk_weights fp32 [B][k] (both on the device) -> fp32 [B][d_out].
+    noalloc=True calls bitsmoe_moe_decode_topk_noalloc (no device allocation
+    in the library; pass ``out`` to allocate nothing here either)."""
     torch = _torch()
     B = X.shape[0]
     d_out = Ut.shape[1]
@@ -417,12 +422,12 @@ def moe_decode_topk(codes, params, bits_dev, offsets_dev, total_words: int, E: i
     k = topk_experts.shape[1]
     if out is None:
         out = torch.empty((B, d_out), dtype=torch.float32, device=X.device)
-    _check(lib().bitsmoe_moe_decode_topk(_dev(codes, "codes"), _dev(params, "params"),
-                                         _dev(bits_dev, "bits"), _dev(offsets_dev, "offsets"),
-                                         int(total_words), E, r, d_in, group, _dev(Ut, "Ut"), d_out,
-                                         _dev(X, "X"), B, k, _dev(topk_experts, "topk_experts"),
-                                         _dev(topk_weights, "topk_weights"), _dev(out, "Y"),
-                                         _stream()), "moe_decode_topk")
+    fn = lib().bitsmoe_moe_decode_topk_noalloc if noalloc else lib().bitsmoe_moe_decode_topk
+    _check(fn(_dev(codes, "codes"), _dev(params, "params"), _dev(bits_dev, "bits"),
+              _dev(offsets_dev, "offsets"), int(total_words), E, r, d_in, group, _dev(Ut, "Ut"),
+              d_out, _dev(X, "X"), B, k, _dev(topk_experts, "topk_experts"),
+              _dev(topk_weights, "topk_weights"), _dev(out, "Y"), _stream()),
+           "moe_decode_topk_noalloc" if noalloc else "moe_decode_topk")
     return out
 
 

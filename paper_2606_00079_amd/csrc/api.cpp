@@ -122,6 +122,7 @@ std::vector<TimedLaunch> g_launches;
 }  // namespace
 
 KernelTimer::KernelTimer(const char* name, void* stream) : name_(name), stream_(stream) {
+  if (!name) return;  // an untimed launch: no events
   std::lock_guard<std::mutex> lock(g_timing_mu);
   if (!g_timing) return;
   hipEvent_t e;

@@ -24,6 +24,7 @@
 //     sum_j (q_j s + m) x_j = s sum_j q_j x_j + m sum_j x_j.
 #include <algorithm>
 #include <cmath>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -536,20 +537,21 @@ bitsmoe_status check_decode(const char* who, const void* codes, const void* para
                             const void* bits, const void* offs, const void* Ut, const void* X,
                             const void* Y, int64_t total_words, int64_t E, int64_t r, int64_t d_in,
                             int group, int64_t d_out, int64_t B) {
-  const std::string w(who);
+  // the message text is only built on failure (no host allocation on success)
+  auto bad = [who](bitsmoe_status st, const char* msg) { return fail(st, std::string(who) + msg); };
   if (!codes || !params || !bits || !offs || !Ut || !X || !Y)
-    return fail(BITSMOE_ERR_ARG, w + ": null pointer");
+    return bad(BITSMOE_ERR_ARG, ": null pointer");
   if (!aligned16({codes, params, bits, offs, Ut, X, Y}))
-    return fail(BITSMOE_ERR_ARG, w + ": device pointers must be 16-byte aligned");
+    return bad(BITSMOE_ERR_ARG, ": device pointers must be 16-byte aligned");
   if (E <= 0 || r <= 0 || d_in <= 0 || d_out <= 0 || B <= 0 || total_words < 0)
-    return fail(BITSMOE_ERR_ARG, w + ": non-positive size");
-  if (E > 65535 || B > 65535) return fail(BITSMOE_ERR_SHAPE, w + ": at most 65535 experts and tokens");
+    return bad(BITSMOE_ERR_ARG, ": non-positive size");
+  if (E > 65535 || B > 65535) return bad(BITSMOE_ERR_SHAPE, ": at most 65535 experts and tokens");
   if (!(group == 32 || group == 64 || group == 128 || group == 256))
-    return fail(BITSMOE_ERR_SHAPE, w + ": group must be 32, 64, 128 or 256");
+    return bad(BITSMOE_ERR_SHAPE, ": group must be 32, 64, 128 or 256");
   if (d_in % 64 != 0 || d_in % group != 0)
-    return fail(BITSMOE_ERR_SHAPE, w + ": the units' length must be a multiple of 64 and of the group");
-  if (r > 8192) return fail(BITSMOE_ERR_SHAPE, w + ": r above 8192");
-  if (d_in > (1 << 20)) return fail(BITSMOE_ERR_SHAPE, w + ": the units' length is above 2^20");
+    return bad(BITSMOE_ERR_SHAPE, ": the units' length must be a multiple of 64 and of the group");
+  if (r > 8192) return bad(BITSMOE_ERR_SHAPE, ": r above 8192");
+  if (d_in > (1 << 20)) return bad(BITSMOE_ERR_SHAPE, ": the units' length is above 2^20");
   return ok();
 }
 
@@ -677,12 +679,16 @@ bitsmoe_status decode_launch(const DecodeGeom& g, int T, bool topk_jobs, int64_t
                              int64_t E, int64_t r, int64_t d_in, int group, const float* Ut_dev,
                              int64_t d_out, const float* X_dev, int64_t B, const int4* jobs_d,
                              const int32_t* topk_d, int kk, const float* w_d, const int64_t* pidx_d,
-                             int kmax, float* zp, float* Y_dev, hipStream_t s) {
+                             int kmax, float* zp, float* Y_dev, hipStream_t s,
+                             bool timed = true) {
   const uint32_t* pr = reinterpret_cast<const uint32_t*>(params_dev);
   const uint32_t* c32 = reinterpret_cast<const uint32_t*>(codes_dev);
+  // without timing the launches create no events
   void* stream = s;
+  const char* zname = timed ? "moe_decode_z" : nullptr;
+  const char* yname = timed ? "moe_decode_y" : nullptr;
   if (njobs > 0) {
-    KernelTimer timer("moe_decode_z", stream);
+    KernelTimer timer(zname, stream);
     dim3 grid(static_cast<unsigned>((r + g.rows_wg - 1) / g.rows_wg), static_cast<unsigned>(njobs));
 #define BITSMOE_DEC(TT, OS, TK)                                                                    \
   hipLaunchKernelGGL((decode_z_kernel<TT, OS, TK>), grid, dim3(64 * kWaves), 0, s, c32, pr,        \
@@ -699,7 +705,7 @@ bitsmoe_status decode_launch(const DecodeGeom& g, int T, bool topk_jobs, int64_t
   }
   BITSMOE_LAUNCH_CHECK("moe_decode: z launch");
   {
-    KernelTimer timer("moe_decode_y", stream);
+    KernelTimer timer(yname, stream);
     dim3 grid(static_cast<unsigned>((d_out + 63) / 64), static_cast<unsigned>((B + g.TB - 1) / g.TB));
     const size_t lds = static_cast<size_t>(g.TB) * (g.rp + kYWaves * 64) * 4;
 #define BITSMOE_DECY(TT)                                                                   \
@@ -715,6 +721,58 @@ bitsmoe_status decode_launch(const DecodeGeom& g, int T, bool topk_jobs, int64_t
   }
   BITSMOE_LAUNCH_CHECK("moe_decode: y launch");
   return ok();
+}
+
+// The top-k decode without allocation keeps its partial sums in a fixed
+// device array, decode_partials below: every GPU the library runs on holds
+// one copy (16 MiB) until the process ends.  Its address differs per device
+// and is looked up once per device, with that device current; host code
+// uses only that address (the array's name is a host-side stand-in).
+constexpr int64_t kNoAllocPartials = int64_t{1} << 22;  // floats: B * k * r at most
+constexpr int kNoAllocMaxDevices = 64;
+
+}  // namespace
+}  // namespace bitsmoe
+
+static __device__ __align__(256) float decode_partials[bitsmoe::kNoAllocPartials];
+
+namespace bitsmoe {
+namespace {
+
+std::mutex g_partials_mu;
+float* g_partials[kNoAllocMaxDevices];  // device address of decode_partials, per device
+
+// The current device's copy of decode_partials (looked up on the first call
+// on that device).  Allocates nothing.
+bitsmoe_status device_partials(float** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return device_error("moe_decode_topk_noalloc: hipGetDevice", e);
+  if (dev < 0 || dev >= kNoAllocMaxDevices)
+    return fail(BITSMOE_ERR_DEVICE, "moe_decode_topk_noalloc: device index above 63");
+  std::lock_guard<std::mutex> lock(g_partials_mu);
+  if (!g_partials[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(decode_partials));
+    if (e != hipSuccess || !p)
+      return device_error("moe_decode_topk_noalloc: hipGetSymbolAddress", e != hipSuccess ? e : hipErrorUnknown);
+    g_partials[dev] = static_cast<float*>(p);
+  }
+  *out = g_partials[dev];
+  return BITSMOE_OK;
+}
+
+// Checks of the top-k table shared by both top-k entry points.
+bitsmoe_status check_topk(const char* who, const void* topk_experts, const void* topk_weights,
+                          int64_t E, int64_t B, int64_t k) {
+  auto bad = [who](bitsmoe_status st, const char* msg) { return fail(st, std::string(who) + msg); };
+  if (!topk_experts || !topk_weights) return bad(BITSMOE_ERR_ARG, ": null pointer");
+  if (!aligned16({topk_experts, topk_weights}))
+    return bad(BITSMOE_ERR_ARG, ": device pointers must be 16-byte aligned");
+  if (k <= 0) return bad(BITSMOE_ERR_ARG, ": non-positive k");
+  if (k > E || B * k > 65535)
+    return bad(BITSMOE_ERR_SHAPE, ": k above E, or more than 65535 routing slots");
+  return BITSMOE_OK;
 }
 
 }  // namespace
@@ -766,13 +824,8 @@ extern "C" bitsmoe_status bitsmoe_moe_decode_topk(const uint64_t* codes_dev, con
                                    word_offsets_dev, Ut_dev, X_dev, Y_dev, total_words, E, r, d_in,
                                    group, d_out, B);
   if (st != BITSMOE_OK) return st;
-  if (!topk_experts_dev || !topk_weights_dev)
-    return fail(BITSMOE_ERR_ARG, "moe_decode_topk: null pointer");
-  if (!aligned16({topk_experts_dev, topk_weights_dev}))
-    return fail(BITSMOE_ERR_ARG, "moe_decode_topk: device pointers must be 16-byte aligned");
-  if (k <= 0) return fail(BITSMOE_ERR_ARG, "moe_decode_topk: non-positive k");
-  if (k > E || B * k > 65535)
-    return fail(BITSMOE_ERR_SHAPE, "moe_decode_topk: k above E, or more than 65535 routing slots");
+  st = check_topk("moe_decode_topk", topk_experts_dev, topk_weights_dev, E, B, k);
+  if (st != BITSMOE_OK) return st;
   const int64_t njobs = B * k;
   const DecodeGeom g = decode_geometry(njobs, r, d_in, B);
   float* zp = static_cast<float*>(scratch(kScratchPart, njobs * r * 4, stream, &st));
@@ -781,6 +834,34 @@ extern "C" bitsmoe_status bitsmoe_moe_decode_topk(const uint64_t* codes_dev, con
                        total_words, E, r, d_in, group, Ut_dev, d_out, X_dev, B, nullptr,
                        topk_experts_dev, static_cast<int>(k), topk_weights_dev, nullptr,
                        static_cast<int>(k), zp, Y_dev, static_cast<hipStream_t>(stream));
+}
+
+extern "C" bitsmoe_status bitsmoe_moe_decode_topk_noalloc(
+    const uint64_t* codes_dev, const uint16_t* params_dev, const uint8_t* bits_dev,
+    const int64_t* word_offsets_dev, int64_t total_words, int64_t E, int64_t r, int64_t d_in,
+    int group, const float* Ut_dev, int64_t d_out, const float* X_dev, int64_t B, int64_t k,
+    const int32_t* topk_experts_dev, const float* topk_weights_dev, float* Y_dev, void* stream) {
+  bitsmoe_status st = check_decode("moe_decode_topk_noalloc", codes_dev, params_dev, bits_dev,
+                                   word_offsets_dev, Ut_dev, X_dev, Y_dev, total_words, E, r, d_in,
+                                   group, d_out, B);
+  if (st != BITSMOE_OK) return st;
+  st = check_topk("moe_decode_topk_noalloc", topk_experts_dev, topk_weights_dev, E, B, k);
+  if (st != BITSMOE_OK) return st;
+  const int64_t njobs = B * k;
+  if (njobs * r > kNoAllocPartials)
+    return fail(BITSMOE_ERR_SHAPE,
+                "moe_decode_topk_noalloc: B * k * r is above the fixed partials buffer (4194304 floats)");
+  float* zp = nullptr;
+  st = device_partials(&zp);
+  if (st != BITSMOE_OK) return st;
+  // every partial [B k][r] is written by the z kernel before the y kernel
+  // reads it, so nothing needs clearing; no events, no scratch, no copies
+  const DecodeGeom g = decode_geometry(njobs, r, d_in, B);
+  return decode_launch(g, 1, true, njobs, codes_dev, params_dev, bits_dev, word_offsets_dev,
+                       total_words, E, r, d_in, group, Ut_dev, d_out, X_dev, B, nullptr,
+                       topk_experts_dev, static_cast<int>(k), topk_weights_dev, nullptr,
+                       static_cast<int>(k), zp, Y_dev, static_cast<hipStream_t>(stream),
+                       /*timed=*/false);
 }
 
 extern "C" bitsmoe_status bitsmoe_moe_decode_in(const uint64_t* codes_dev, const uint16_t* params_dev,

@@ -40,6 +40,7 @@ int device_cus();
 
 // Records HIP events around a kernel launch when timing is enabled
 // (bitsmoe_timing); construct right before the launch, destroy right after.
+// A null name records nothing.
 class KernelTimer {
  public:
   KernelTimer(const char* name, void* stream);

@@ -313,6 +313,14 @@ def test_device_entry_points_validate_before_launch(lib):
                                        2, 2, fake, fake, fake, s) == 2
     assert lib.bitsmoe_moe_decode_topk(fake, fake, fake, fake, 10, 2, 8, 128, 64, fake, 64, fake,
                                        2, 2, null, fake, fake, s) == 1
+    # the allocation-free top-k decode: the same checks, plus its buffer limit
+    assert lib.bitsmoe_moe_decode_topk_noalloc(fake, fake, fake, fake, 10, 2, 8, 128, 64, fake, 64,
+                                               fake, 2, 0, fake, fake, fake, s) == 1
+    assert lib.bitsmoe_moe_decode_topk_noalloc(fake, fake, fake, fake, 10, 2, 8, 128, 64, fake, 64,
+                                               fake, 2, 2, odd, fake, fake, s) == 1
+    assert lib.bitsmoe_moe_decode_topk_noalloc(fake, fake, fake, fake, 10, 8, 8192, 128, 64, fake,
+                                               64, fake, 520, 1, fake, fake, fake, s) == 2
+    assert "partials buffer" in pkg.last_error()
     assert lib.bitsmoe_gram(odd, 1, 64, 64, fake, s) == 1
     assert "aligned" in pkg.last_error()
     assert lib.bitsmoe_gram_experts(fake, 1, 2, 64, 64, odd, s) == 1
