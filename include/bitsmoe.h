@@ -88,9 +88,15 @@ typedef enum {
   BITSMOE_ERR_UNAVAILABLE = 8   /* no LAPACK library could be loaded            */
 } bitsmoe_status;
 
+/* The two sentinels are not element types: they make every int a valid
+ * value of the enum (in C++ an enum otherwise only spans its enumerators'
+ * bit range), so an unsupported code from a caller is rejected with
+ * BITSMOE_ERR_DTYPE instead of being undefined behaviour. */
 typedef enum {
   BITSMOE_F32 = 0,   /* IEEE fp32                                   */
-  BITSMOE_BF16 = 1   /* bfloat16, read as exact values              */
+  BITSMOE_BF16 = 1,  /* bfloat16, read as exact values              */
+  BITSMOE_DTYPE_RANGE_MIN_ = -2147483647 - 1,
+  BITSMOE_DTYPE_RANGE_MAX_ = 2147483647
 } bitsmoe_dtype;
 
 /* Largest candidate width and group sizes accepted by score and pack. */

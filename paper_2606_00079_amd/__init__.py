@@ -27,7 +27,9 @@ from typing import Optional, Sequence, Tuple
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libbitsmoe.so")
+# BITSMOE_LIB selects another build of the same library (e.g. the
+# host-sanitized libbitsmoe_san.so of ``build --sanitize``)
+LIB_PATH = os.environ.get("BITSMOE_LIB") or os.path.join(_HERE, "libbitsmoe.so")
 
 OK = 0
 _STATUS = {0: "OK", 1: "ERR_ARG", 2: "ERR_SHAPE", 3: "ERR_DTYPE", 4: "ERR_DEVICE",

@@ -1,7 +1,18 @@
 """Builds libbitsmoe.so in-tree: hipcc for the gfx950 kernels, g++ for the host
 code, one shared library next to this file.
 
-    python -m paper_2606_00079_amd.build          # build (always recompiles)
+    python -m paper_2606_00079_amd.build              # build (always recompiles)
+    python -m paper_2606_00079_amd.build --sanitize   # host-instrumented copy
+
+``--sanitize`` builds libbitsmoe_san.so: the same sources with the host code
+(every .cpp, and the host side of every .hip) instrumented by AddressSanitizer
+and UndefinedBehaviorSanitizer, all with the ROCm clang so that one sanitizer
+runtime serves both; device code is built as usual.  Load it in a process
+that preloads that runtime, e.g.
+
+    LD_PRELOAD=$(python -m paper_2606_00079_amd.build --asan-runtime) \
+    ASAN_OPTIONS=detect_leaks=0 BITSMOE_LIB=paper_2606_00079_amd/libbitsmoe_san.so \
+    python -m pytest tests/test_abi.py
 """
 from __future__ import annotations
 
@@ -49,20 +60,43 @@ def sources():
     return hip, cpp
 
 
-def build(verbose: bool = False, jobs: int = 8) -> str:
-    os.makedirs(BUILD, exist_ok=True)
+SAN_LIB = os.path.join(PKG, "libbitsmoe_san.so")
+SAN_BUILD = os.path.join(ROOT, "_build_san")
+# host-side sanitizers only: on hipcc lines each one follows -Xarch_host
+SAN_HOST = ["-fsanitize=address", "-fsanitize=undefined", "-fno-sanitize-recover=undefined"]
+
+
+def asan_runtime() -> str:
+    """The ROCm clang's shared AddressSanitizer runtime (to preload)."""
+    import glob
+    c = sorted(glob.glob(os.path.join(ROCM, "llvm", "lib", "clang", "*", "lib", "linux",
+                                      "libclang_rt.asan-x86_64.so")))
+    if not c:
+        raise FileNotFoundError("no libclang_rt.asan-x86_64.so under " + ROCM)
+    return c[-1]
+
+
+def build(verbose: bool = False, jobs: int = 8, sanitize: bool = False) -> str:
+    bdir, lib = (SAN_BUILD, SAN_LIB) if sanitize else (BUILD, LIB)
+    os.makedirs(bdir, exist_ok=True)
     hip, cpp = sources()
     cmds = []
     objs = []
+    hip_san = [x for f in SAN_HOST for x in ("-Xarch_host", f)] + ["-g"] if sanitize else []
     for f in hip:
-        o = os.path.join(BUILD, f + ".o")
-        cmds.append([_hipcc(), *HIP_FLAGS, f"-I{INCLUDE}", f"-I{CSRC}", "-c",
+        o = os.path.join(bdir, f + ".o")
+        cmds.append([_hipcc(), *HIP_FLAGS, *hip_san, f"-I{INCLUDE}", f"-I{CSRC}", "-c",
                      os.path.join(CSRC, f), "-o", o])
         objs.append(o)
-    cxx = shutil.which("g++") or "c++"
+    if sanitize:
+        cxx = os.path.join(ROCM, "llvm", "bin", "clang++")
+        cxx_flags = [*CXX_FLAGS, *SAN_HOST, "-g", "-fno-omit-frame-pointer"]
+    else:
+        cxx = shutil.which("g++") or "c++"
+        cxx_flags = CXX_FLAGS
     for f in cpp:
-        o = os.path.join(BUILD, f + ".o")
-        cmds.append([cxx, *CXX_FLAGS, f"-I{INCLUDE}", f"-I{CSRC}", "-c",
+        o = os.path.join(bdir, f + ".o")
+        cmds.append([cxx, *cxx_flags, f"-I{INCLUDE}", f"-I{CSRC}", "-c",
                      os.path.join(CSRC, f), "-o", o])
         objs.append(o)
     with ThreadPoolExecutor(max(1, min(jobs, len(cmds)))) as ex:
@@ -72,8 +106,9 @@ def build(verbose: bool = False, jobs: int = 8) -> str:
             print(" ".join(c))
             if o.strip():
                 print(o)
-    tmp = LIB + ".tmp"
-    _run([_hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs,
+    tmp = lib + ".tmp"
+    link_san = [x for f in SAN_HOST for x in ("-Xarch_host", f)] + ["-shared-libasan"] if sanitize else []
+    _run([_hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", *link_san, "-o", tmp, *objs,
           f"-L{ROCM}/lib", "-lamdhip64", "-ldl"])
     # A kernel whose host stub was dropped links fine but fails at load time.
     nm = shutil.which("nm")
@@ -82,9 +117,12 @@ def build(verbose: bool = False, jobs: int = 8) -> str:
         missing = [l for l in undef.splitlines() if "__device_stub__" in l]
         if missing:
             raise RuntimeError("kernel host stubs missing from the library:\n" + "\n".join(missing))
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, lib)
+    return lib
 
 
 if __name__ == "__main__":
-    print(build(verbose="-v" in sys.argv))
+    if "--asan-runtime" in sys.argv:
+        print(asan_runtime())
+    else:
+        print(build(verbose="-v" in sys.argv, sanitize="--sanitize" in sys.argv))
