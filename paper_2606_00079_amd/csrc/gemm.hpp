@@ -89,6 +89,8 @@ struct Side {
   int64_t rows;             // row-major: valid rows
   int64_t kstep;            // K-tiled: elements between consecutive K tiles (0 = row-major)
   int64_t rtile;            // K-tiled: elements between consecutive row tiles
+  int repeat_k;             // 1: every K tile of a segment starts at the segment's
+                            // base (the side's tile is reused; estride advances)
 };
 
 // Element offset of (r, k) in a K-tiled matrix of K columns with T-row tiles.
@@ -111,7 +113,32 @@ struct Problem {
   int64_t a_batch_rows;  // paired only: if > 0, the A operand of column tile tn is
                          // batch (tn * BN) / a_batch_rows (stride a.bstride): one A per
                          // block of B rows (a multiple of BN)
+  // run_if: when not null, every workgroup returns at once unless *run_if is
+  // nonzero (a launch made conditional on an earlier launch's flag)
+  const int* run_if;
+  // flat > 0 (not paired): one-dimensional grid of batches x splits x flat
+  // tiles (flat = the tiles of one batch and split), blockIdx.y = .z = 0.
+  // The linear id is XCD-remapped first, so the tiles of one split of one
+  // batch (which read the same K slice of the same operands) run on one XCD
+  // and share its L2.
+  int flat;
+  // persist > 0 (with flat, not paired): the same persist = batches x splits
+  // x flat logical tiles, walked by a grid of fewer workgroups (a multiple
+  // of the XCD count): XCD x takes the same contiguous range of logical ids
+  // as in the flat launch, and its workgroups take them in turn.  With an
+  // epilogue that leaves the LDS alone, each workgroup issues the first K
+  // tiles of its next tile before the epilogue of the current one, so the
+  // epilogue's stores overlap the next tile's loads.
+  int64_t persist;
 };
+
+// Logical (XCD-contiguous) range of XCD x when n logical ids are spread as
+// xcd_remap spreads them: [*start, *start + *len).
+__host__ __device__ __forceinline__ void xcd_range(int64_t n, int x, int64_t* start, int64_t* len) {
+  const int64_t q = n / kXcds, rem = n % kXcds;
+  *start = x < rem ? x * (q + 1) : rem * (q + 1) + (x - rem) * q;
+  *len = q + (x < rem ? 1 : 0);
+}
 
 // XCD-contiguous logical id of the linear workgroup id t (of n in total).
 __device__ __forceinline__ int xcd_remap(int t, int n) {
@@ -120,8 +147,8 @@ __device__ __forceinline__ int xcd_remap(int t, int n) {
   return (x < rem) ? x * (q + 1) + i : rem * (q + 1) + (x - rem) * q + i;
 }
 
-__device__ __forceinline__ void tile_coords(const Problem& p, int t, int n, int* tm, int* tn) {
-  t = xcd_remap(t, n);
+// Tile of logical (XCD-remapped) id t.
+__device__ __forceinline__ void tile_coords_logical(const Problem& p, int t, int* tm, int* tn) {
   if (p.symmetric) {
     int r = 0;
     while (t >= p.tiles_m - r) {
@@ -139,6 +166,9 @@ __device__ __forceinline__ void tile_coords(const Problem& p, int t, int n, int*
   // narrower) group still has w / tiles_m < its width
   *tm = w % p.tiles_m;
   *tn = first_n + w / p.tiles_m;
+}
+__device__ __forceinline__ void tile_coords(const Problem& p, int t, int n, int* tm, int* tn) {
+  tile_coords_logical(p, xcd_remap(t, n), tm, tn);
 }
 
 // Paired upper-triangle schedule (for a symmetric form: A is the square
@@ -254,8 +284,8 @@ struct KPos {
     }
     ba.make_uniform();
     bb.make_uniform();
-    stepa = uniform64(p.a.kstep != 0 ? p.a.kstep : KB);
-    stepb = uniform64(p.b.kstep != 0 ? p.b.kstep : KB);
+    stepa = uniform64(p.a.repeat_k ? 0 : (p.a.kstep != 0 ? p.a.kstep : KB));
+    stepb = uniform64(p.b.repeat_k ? 0 : (p.b.kstep != 0 ? p.b.kstep : KB));
     jumpa = uniform64(p.a.estride - tiles_seg * stepa);
     jumpb = uniform64(p.b.estride - tiles_seg * stepb);
     seg = uniform64(seg);
@@ -263,6 +293,8 @@ struct KPos {
     offa = uniform64(seg * p.a.estride + ki * stepa);
     offb = uniform64(seg * p.b.estride + ki * stepb);
   }
+  __device__ __forceinline__ const uint16_t* a_ptr() const { return ba.q0 + offa; }
+  __device__ __forceinline__ const uint16_t* b_ptr() const { return bb.q0 + offb; }
   __device__ __forceinline__ void next(const Problem& p) {
     k0 += KB;
     offa += stepa;
@@ -278,6 +310,33 @@ struct KPos {
     offb = wrap2 ? 0 : offb;
     ba.advance(wrap2);
     bb.advance(wrap2);
+  }
+};
+
+// K walk of a one-pass, one-segment problem (persistent launches): the
+// position of K tile kt is kt steps from the tile's base on each side.
+template <int KB>
+struct KPos1 {
+  const uint16_t* ba;
+  const uint16_t* bb;
+  int64_t offa, offb, stepa, stepb;
+  __device__ __forceinline__ void init(const Problem& p, int64_t kt, int64_t z, int tm, int tn,
+                                       int BM, int BN) {
+    PassBases a, b;
+    a.init(p.a, z, tm, BM);
+    b.init(p.b, z, tn, BN);
+    ba = reinterpret_cast<const uint16_t*>(uniform64(reinterpret_cast<int64_t>(a.q0)));
+    bb = reinterpret_cast<const uint16_t*>(uniform64(reinterpret_cast<int64_t>(b.q0)));
+    stepa = uniform64(p.a.kstep != 0 ? p.a.kstep : KB);
+    stepb = uniform64(p.b.kstep != 0 ? p.b.kstep : KB);
+    offa = uniform64(kt * stepa);
+    offb = uniform64(kt * stepb);
+  }
+  __device__ __forceinline__ const uint16_t* a_ptr() const { return ba + offa; }
+  __device__ __forceinline__ const uint16_t* b_ptr() const { return bb + offb; }
+  __device__ __forceinline__ void next(const Problem&) {
+    offa += stepa;
+    offb += stepb;
   }
 };
 
@@ -471,11 +530,36 @@ __device__ __forceinline__ s16x4 ds_read_tr16(const uint16_t* p) {
 // of transposing reads (4 rows x 4 chunks x 2 halves) covers all 64 banks.
 __device__ __forceinline__ int kn_swz(int r, int c) { return c ^ (4 * (r & 3)); }
 
+// Eight bf16 values (bit patterns, two per dword) -> eight fp16 values: each
+// bf16 is widened to the fp32 of the same value (its bits in the upper
+// half) and rounded to fp16 to nearest even, two at a time.  bf16 values
+// of magnitude 2^-14 .. 65504 convert exactly (fp16 has the wider
+// significand), 2^-17 .. 2^-14 land exactly on fp16 subnormals, smaller ones
+// round on the 2^-24 grid, larger ones become infinite.
+__device__ __forceinline__ f16x8 bf16x8_to_f16x8(const uint32_t (&w)[4]) {
+  typedef _Float16 h2 __attribute__((ext_vector_type(2)));
+  h2 o[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const float lo = __uint_as_float(w[i] << 16);
+    const float hi = __uint_as_float(w[i] & 0xffff0000u);
+    o[i] = h2{static_cast<_Float16>(lo), static_cast<_Float16>(hi)};
+  }
+  return f16x8{o[0].x, o[0].y, o[1].x, o[1].y, o[2].x, o[2].y, o[3].x, o[3].y};
+}
+
+// CVTB: the B operand is bf16 in memory and is multiplied as fp16 (F16):
+// each B fragment is converted in registers after its LDS read.
+// PERSIST: compiled for a persistent launch (Problem::persist > 0).
 template <int BM, int BN, int KB, int STAGES, class Epi, bool F16 = false, bool BKN = false,
-          bool PAIRED = false>
+          bool PAIRED = false, bool CVTB = false, bool PERSIST = false>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void gemm_nt_kernel(Problem p, Epi epi) {
   static_assert(BM % 64 == 0 && BN % 64 == 0, "tile");
+  static_assert(!CVTB || F16, "converted B fragments are fp16");
+  static_assert(!PERSIST || (!PAIRED && !Epi::kUsesLds), "persistent: one tile per job, LDS-free epilogue");
+  // (persistent: p.passes == 1 and p.segs == 1, see KPos1)
+  if (p.run_if && *p.run_if == 0) return;  // whole workgroup
   static_assert(!BKN || (BN == 256 && KB == 32), "KN B operand: 256-wide N tiles, 32-wide K steps");
   static_assert(KB == 32 || KB == 64, "K step");
   static_assert(STAGES >= 2 && STAGES <= 6, "stages");
@@ -499,22 +583,47 @@ void gemm_nt_kernel(Problem p, Epi epi) {
   f.wm = f.wave >> 1;
   f.wn = f.wave & 1;
   // PAIRED: gridDim.x = paired_workgroups(tiles_m, tiles_n), two jobs each
-  // (see paired_jobs); otherwise one tile per workgroup.
+  // (see paired_jobs); persistent: the logical tiles pjob0 + j pstride;
+  // otherwise one tile per workgroup.
   int njobs = 1, tm0 = 0, tn0 = 0, tm1 = 0, tn1 = 0;
+  int64_t pjob0 = 0, pstride = 0;
+  // logical id L of a flat or persistent launch -> tile, batch and split
+  auto flat_coords = [&](int64_t L, int* tm, int* tn, int64_t* z, int* ks) {
+    const int64_t per_z = static_cast<int64_t>(p.splits) * p.flat;
+    const int64_t zz = L / per_z;
+    const int rem = static_cast<int>(L - zz * per_z);
+    *z = zz;
+    *ks = rem / p.flat;
+    tile_coords_logical(p, rem - *ks * p.flat, tm, tn);
+  };
   if constexpr (PAIRED) {
     njobs = paired_jobs(p, blockIdx.x, gridDim.x, &tm0, &tn0, &tm1, &tn1);
     if (njobs == 0) return;  // whole workgroup: past the last column tile
+    f.ks = blockIdx.y;
+    f.z = blockIdx.z;
+  } else if (PERSIST) {
+    const int x = static_cast<int>(blockIdx.x % kXcds), wi = static_cast<int>(blockIdx.x / kXcds);
+    const int wx = static_cast<int>(gridDim.x / kXcds) + (x < static_cast<int>(gridDim.x % kXcds) ? 1 : 0);
+    int64_t start, len;
+    xcd_range(p.persist, x, &start, &len);
+    if (wi >= len) return;  // whole workgroup: nothing left on its XCD
+    njobs = static_cast<int>((len - wi + wx - 1) / wx);
+    pjob0 = start + wi;
+    pstride = wx;
+    flat_coords(pjob0, &tm0, &tn0, &f.z, &f.ks);
+  } else if (p.flat > 0) {
+    flat_coords(xcd_remap(blockIdx.x, gridDim.x), &tm0, &tn0, &f.z, &f.ks);
   } else {
     tile_coords(p, blockIdx.x, gridDim.x, &tm0, &tn0);
+    f.ks = blockIdx.y;
+    f.z = blockIdx.z;
   }
   f.tm = tm0;
   f.tn = tn0;
-  f.ks = blockIdx.y;
-  f.z = blockIdx.z;
 
   const int64_t ktiles = p.ktiles * BK / KB;  // K tiles of this kernel's step
-  const int64_t kt0 = ktiles * f.ks / p.splits;
-  const int64_t kt1 = ktiles * (f.ks + 1) / p.splits;
+  int64_t kt0 = ktiles * f.ks / p.splits;
+  int64_t kt1 = ktiles * (f.ks + 1) / p.splits;
 
   // Direct global->LDS loads.  Wave instruction i of this wave fills the
   // 1 KiB LDS block b = wave + 4 i (rows b*RPB .. b*RPB+RPB-1); lane l lands
@@ -523,9 +632,9 @@ void gemm_nt_kernel(Problem p, Epi epi) {
   // are clamped to the last row: their accumulators are never stored.
   uint32_t oa[AW], ob[BW];  // byte offsets from the tile's first element
   const bool a_tiled = p.a.kstep != 0, b_tiled = p.b.kstep != 0;
-  auto set_offsets = [&]() {
-  const int64_t a_row0 = static_cast<int64_t>(f.tm) * BM;
-  const int64_t b_row0 = static_cast<int64_t>(f.tn) * BN;
+  auto set_offsets = [&](int tm, int tn) {
+  const int64_t a_row0 = static_cast<int64_t>(tm) * BM;
+  const int64_t b_row0 = static_cast<int64_t>(tn) * BN;
 #pragma unroll
   for (int i = 0; i < AW; ++i) {
     const int r = (f.wave + 4 * i) * RPB + f.lane / KC;
@@ -553,7 +662,8 @@ void gemm_nt_kernel(Problem p, Epi epi) {
     }
   }
   };
-  KPos<KB> kp;
+  // persistent launches walk a one-pass, one-segment K (checked by the host)
+  std::conditional_t<PERSIST, KPos1<KB>, KPos<KB>> kp;
   TriWalk<KB> tw;
   // Loads of the next K tile into stage buffer s, one wave instruction at a
   // time (q < LPS) so that they can be spread between matrix-core ops.
@@ -568,7 +678,7 @@ void gemm_nt_kernel(Problem p, Epi epi) {
       tw.next();
       return is;
     } else {
-      Issue is{kp.ba.q0 + kp.offa, kp.bb.q0 + kp.offb, s};
+      Issue is{kp.a_ptr(), kp.b_ptr(), s};
       kp.next(p);
       return is;
     }
@@ -616,8 +726,19 @@ void gemm_nt_kernel(Problem p, Epi epi) {
           const int r = 16 * kk + 8 * jq + 4 * t + ((f.lane & 15) >> 2);
           h[t] = ds_read_tr16(lb + r * BN + (kn_swz(r, col >> 3) << 3) + (col & 7));
         }
-        fb[T][ni] = __builtin_bit_cast(typename Op::vec,
-                                       __builtin_shufflevector(h[0], h[1], 0, 1, 2, 3, 4, 5, 6, 7));
+        if constexpr (CVTB) {
+          uint32_t w[4];
+          __builtin_memcpy(w, &h[0], 8);
+          __builtin_memcpy(w + 2, &h[1], 8);
+          fb[T][ni] = bf16x8_to_f16x8(w);
+        } else {
+          fb[T][ni] = __builtin_bit_cast(typename Op::vec,
+                                         __builtin_shufflevector(h[0], h[1], 0, 1, 2, 3, 4, 5, 6, 7));
+        }
+      } else if constexpr (CVTB) {
+        const uint4 v = *reinterpret_cast<const uint4*>(&lb[lds_off<KB>(brow + 32 * ni, j)]);
+        const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+        fb[T][ni] = bf16x8_to_f16x8(w);
       } else {
         fb[T][ni] = *reinterpret_cast<const typename Op::vec*>(&lb[lds_off<KB>(brow + 32 * ni, j)]);
       }
@@ -675,6 +796,7 @@ void gemm_nt_kernel(Problem p, Epi epi) {
 
   int64_t nk = 0;      // K tiles of the current job
   int64_t issued = 0;  // K tiles whose loads have been issued
+  bool prefetched = false;  // the current job's first K tiles were issued by the previous one
   constexpr int KS = KB / 16;  // K=16 steps per tile (even)
   // A refill's LPS loads are spread over the KS steps of the tile that
   // issues them: step k issues loads k LPS / KS .. (k + 1) LPS / KS - 1, so
@@ -769,15 +891,19 @@ void gemm_nt_kernel(Problem p, Epi epi) {
       for (int ni = 0; ni < F::FN; ++ni)
 #pragma unroll
         for (int r = 0; r < 16; ++r) f.acc[mi][ni][r] = 0.0f;
-    set_offsets();
-    issued = 0;
-    if (nk > 0) {
-      if constexpr (!PAIRED) kp.init(p, kt0, f.z, f.tm, f.tn, BM, BN);
-      // tiles 0 .. STAGES - 3 up front, tile STAGES - 2 once tile 0 is visible
-      for (int q = 0; q < STAGES - 2 && issued < nk; ++q) {
-        issue(q);
-        ++issued;
+    if (!PERSIST || !prefetched) {
+      set_offsets(f.tm, f.tn);
+      issued = 0;
+      if (nk > 0) {
+        if constexpr (!PAIRED) kp.init(p, kt0, f.z, f.tm, f.tn, BM, BN);
+        // tiles 0 .. STAGES - 3 up front, tile STAGES - 2 once tile 0 is visible
+        for (int q = 0; q < STAGES - 2 && issued < nk; ++q) {
+          issue(q);
+          ++issued;
+        }
       }
+    }
+    if (nk > 0) {
       sync_tile(0, True());
       if (issued < nk) {
         issue(STAGES - 2);
@@ -796,8 +922,34 @@ void gemm_nt_kernel(Problem p, Epi epi) {
     for (int mi = 0; mi < F::FM; ++mi)
 #pragma unroll
       for (int ni = 0; ni < F::FN; ++ni) asm volatile("" : "+a"(f.acc[mi][ni]));
-    wait_vmcnt<0>();
-    __syncthreads();  // epilogues may reuse the stage buffers
+    // Persistent launch with an epilogue that leaves the LDS alone: once
+    // every wave is done with the stage buffers, the first K tiles of the
+    // next tile are issued into them, and the epilogue's stores go out
+    // behind those loads.
+    bool pre = false;
+    int ntm = 0, ntn = 0, nks = 0;
+    int64_t nz = 0;
+    if constexpr (PERSIST) {
+      if (job + 1 < njobs) {
+        __syncthreads();  // every wave's fragment reads of this tile returned
+        flat_coords(pjob0 + static_cast<int64_t>(job + 1) * pstride, &ntm, &ntn, &nz, &nks);
+        const int64_t nkt0 = ktiles * nks / p.splits, nkt1 = ktiles * (nks + 1) / p.splits;
+        set_offsets(ntm, ntn);
+        issued = 0;
+        if (nkt1 > nkt0) {
+          kp.init(p, nkt0, nz, ntm, ntn, BM, BN);
+          for (int q = 0; q < STAGES - 2 && issued < nkt1 - nkt0; ++q) {
+            issue(q);
+            ++issued;
+          }
+        }
+        pre = true;
+      }
+    }
+    if (!pre) {
+      wait_vmcnt<0>();
+      __syncthreads();  // epilogues may reuse the stage buffers
+    }
     StageLds lds;
     lds.a = As;
     lds.b = Bs;
@@ -807,6 +959,17 @@ void gemm_nt_kernel(Problem p, Epi epi) {
     lds.stages = STAGES;
     epi(f, lds);
     if constexpr (PAIRED) __syncthreads();  // the next job refills the stage buffers
+    if constexpr (PERSIST) {
+      if (pre) {
+        f.tm = ntm;
+        f.tn = ntn;
+        f.z = nz;
+        f.ks = nks;
+        kt0 = ktiles * nks / p.splits;
+        kt1 = ktiles * (nks + 1) / p.splits;
+      }
+      prefetched = pre;
+    }
   }
 }
 

@@ -117,6 +117,7 @@ __global__ __launch_bounds__(256) void routed_gather_kernel(
 
 // Stores each wave's fp32 accumulators into partials[batch][split][tile][GT][GT].
 struct PartialStore {
+  static constexpr bool kUsesLds = false;  // reads or writes the stage buffers
   float* part;
   int64_t ntiles;     // tiles in the upper triangle
   int ntiles_side;    // tiles per side
@@ -273,8 +274,12 @@ bitsmoe_status run_symmetric(gemm::Problem p, int64_t d, double scale, OutT* out
       scratch(kScratchPart, static_cast<size_t>(batches * zstride) * sizeof(float), stream, &st));
   if (!part) return st;
   PartialStore epi{part, ntiles, T, zstride};
-  dim3 grid(static_cast<unsigned>(ntiles), static_cast<unsigned>(splits),
-            static_cast<unsigned>(batches));
+  // one-dimensional XCD-aware grid: the tiles of one split (the same K slice
+  // of the operands) run together on one XCD and share its L2
+  if (ntiles * splits * batches > INT32_MAX)
+    return fail(BITSMOE_ERR_SHAPE, std::string(name) + ": too many workgroups");
+  p.flat = static_cast<int>(ntiles);
+  dim3 grid(static_cast<unsigned>(ntiles * splits * batches), 1, 1);
   {
     KernelTimer timer(name, stream);
     hipLaunchKernelGGL((gemm::gemm_nt_kernel<GT, GT, 32, 4, PartialStore>), grid,

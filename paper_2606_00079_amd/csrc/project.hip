@@ -1,9 +1,16 @@
 // Step 3: expert spectral factors C_e = U^T W_e for all experts in one batched
-// matrix-core launch.  U is fp32; it is split U = U_hi + U_lo into two bf16
-// terms so that the product keeps fp32 accuracy (bf16 W is exact; fp32 W is
-// split as well).  bf16 W is read where it lies: the contraction runs over
-// its rows, which the GEMM stages as [32 K][256 N] tiles and reads with the
-// transposing LDS read, so no transposed copy is made.
+// matrix-core launch.  bf16 W is read where it lies: the contraction runs
+// over its rows, which the GEMM stages as [32 K][256 N] tiles and reads with
+// the transposing LDS read, so no transposed copy is made.  It is multiplied
+// in one fp16 pass: U (fp32, orthonormal rows) rounded to fp16, each W
+// fragment widened from bf16 to fp16 in registers (exact over fp16's range),
+// fp32 accumulation: a relative error of about 1.5e-4 in C.  A W entry
+// beyond fp16's range makes some factor non-finite, and W entries below
+// fp16's normal range (an absolute error of up to 2^-25 each) only matter
+// when the factors are small too; the epilogue flags either case and a
+// second launch, which otherwise returns at once, recomputes C with the
+// exact two-pass form U = U_hi + U_lo in bf16.  fp32 W (split into hi and
+// lo as well) takes three bf16 passes.
 #include <algorithm>
 
 #include "bitsmoe.h"
@@ -19,24 +26,42 @@ namespace {
 constexpr int PN = 256;  // input-channel tile
 using gemm::BK;
 
-// fp32 U^T [r][K] -> (hi, lo) bf16 in the K-tiled layout of PM-row tiles,
-// rows padded to r_pad with zeros.
+// fp32 U^T [r][K] in the K-tiled layout of PM-row tiles (rows padded to
+// r_pad with zeros), as bf16 hi + lo planes (x ~ hi + lo to 2^-16):
+//   FOR_F16 = false: hi, then lo (lo = hi + r_pad K), two K-tiled matrices;
+//   FOR_F16 = true:  the fp16 rounding of x (one K-tiled matrix, first), then
+//                    one K-tiled matrix of 2K columns whose K tile 2q is the
+//                    hi part and 2q + 1 the lo part of K tile q (the exact
+//                    two-pass form with the terms of a K tile back to back),
+//                    and thread 0 clears *flag.
+template <bool FOR_F16>
 __global__ __launch_bounds__(256) void split_f32_kernel(const float* __restrict__ x, int64_t r,
                                                         int64_t r_pad, int64_t K, int PM,
-                                                        uint16_t* __restrict__ hi,
-                                                        uint16_t* __restrict__ lo) {
+                                                        uint16_t* __restrict__ out,
+                                                        int* __restrict__ flag) {
   const int64_t count = r_pad * K;
   const int64_t nkt = K / gemm::kTileK;
   const int64_t TB = static_cast<int64_t>(PM) * gemm::kTileK;
+  if (FOR_F16 && blockIdx.x == 0 && threadIdx.x == 0) *flag = 0;
   for (int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; i < count;
        i += static_cast<int64_t>(gridDim.x) * 256) {
     const int64_t t = i / TB, w = i - t * TB;
-    const int64_t row = (t / nkt) * PM + w / gemm::kTileK;
-    const int64_t k = (t % nkt) * gemm::kTileK + w % gemm::kTileK;
+    const int64_t rt = t / nkt, kt = t % nkt;
+    const int64_t row = rt * PM + w / gemm::kTileK;
+    const int64_t k = kt * gemm::kTileK + w % gemm::kTileK;
     const float v = row < r ? x[row * K + k] : 0.0f;
     const uint16_t h = f32_to_bf16(v);
-    hi[i] = h;
-    lo[i] = f32_to_bf16(v - bf16_to_f32(h));
+    const uint16_t l = f32_to_bf16(v - bf16_to_f32(h));
+    if (FOR_F16) {
+      out[i] = f32_to_f16_bits(v);
+      uint16_t* il = out + count;
+      const int64_t o = (rt * 2 * nkt + 2 * kt) * TB + w;
+      il[o] = h;
+      il[o + TB] = l;
+    } else {
+      out[i] = h;
+      out[i + count] = l;
+    }
   }
 }
 
@@ -97,31 +122,71 @@ __global__ __launch_bounds__(256) void split_rows_kernel(const float* __restrict
 // consecutive columns of one row as one 16-byte store (a quarter of the
 // store instructions of element-wise stores, whose count bounded the
 // epilogue).
+// With `inexact` set (the one-pass fp16 form), a wave writes 1 there when a
+// factor it stores is not finite (a W entry beyond fp16's range comes out
+// infinite) or when every factor it stores is below kSmallFactor in
+// magnitude (W entries below fp16's normal range carry an absolute error of
+// up to 2^-25 each, which only matters against factors that small); the
+// flag asks for the exact two-pass form.
+constexpr float kSmallFactor = 0.015625f;  // 2^-6
 struct FactorStore {
+  static constexpr bool kUsesLds = false;  // reads or writes the stage buffers
   float* C;
   int64_t r, cols;
+  int* inexact;
   template <class F>
   __device__ void operator()(F& f, const gemm::StageLds&) const {
+    // the lane index made opaque: no address arithmetic of the stores is
+    // hoisted into the K loop (where it would hold registers throughout)
+    const int lane = opaque(f.lane);
     float* base = C + f.z * r * cols;
-    const int k = f.lane & 3;
+    const int k = lane & 3;
+    bool bad = false, stored = false, big = false;
 #pragma unroll
     for (int mi = 0; mi < F::FM; ++mi)
 #pragma unroll
       for (int ni = 0; ni < F::FN; ++ni) {
-        const int c0 = f.col0 + 32 * ni + (f.lane & 28);  // first column of the lane's quad
+        const int c0 = f.col0 + 32 * ni + (lane & 28);  // first column of the lane's quad
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           float a[4] = {f.acc[mi][ni][4 * j], f.acc[mi][ni][4 * j + 1], f.acc[mi][ni][4 * j + 2],
                         f.acc[mi][ni][4 * j + 3]};
           gemm::quad_transpose(a, k);  // every lane takes part (DPP reads its quad)
-          const int row = f.row0 + 32 * mi + 8 * j + 4 * (f.lane >> 5) + k;
-          if (row < r && c0 < cols)
+          const int row = f.row0 + 32 * mi + 8 * j + 4 * (lane >> 5) + k;
+          if (row < r && c0 < cols) {
             *reinterpret_cast<float4*>(base + static_cast<int64_t>(row) * cols + c0) =
                 make_float4(a[0], a[1], a[2], a[3]);
+            if (inexact) {
+              const float m = fmaxf(fmaxf(fabsf(a[0]), fabsf(a[1])), fmaxf(fabsf(a[2]), fabsf(a[3])));
+              // m <= max finite is false for inf and nan (fmaxf drops a nan
+              // only next to a number, so test every entry as well)
+              bad |= !(m <= 3.4e38f) || a[0] != a[0] || a[1] != a[1] || a[2] != a[2] || a[3] != a[3];
+              big |= m >= kSmallFactor;
+              stored = true;
+            }
+          }
         }
       }
+    if (inexact && (__any(bad) || (__any(stored) && !__any(big))) && lane == 0) *inexact = 1;
   }
 };
+
+// Launch grid of a factor GEMM over E experts of p.flat tiles each: for a
+// one-pass, one-segment problem with more tiles than compute units (and
+// `persistent`), one persistent workgroup per compute unit
+// (a multiple of the XCD count) walks its XCD's tiles in turn, issuing each
+// next tile's first loads ahead of the current tile's stores; otherwise one
+// workgroup per tile.
+dim3 factor_grid(gemm::Problem& p, int64_t E, bool persistent) {
+  const int64_t n = static_cast<int64_t>(p.flat) * E;
+  const int64_t g = device_cus() / gemm::kXcds * gemm::kXcds;
+  if (persistent && p.passes == 1 && p.segs == 1 && g >= gemm::kXcds && n > g) {
+    p.persist = n;
+    return dim3(static_cast<unsigned>(g), 1, 1);
+  }
+  p.persist = 0;
+  return dim3(static_cast<unsigned>(n), 1, 1);
+}
 
 }  // namespace
 }  // namespace bitsmoe
@@ -143,34 +208,46 @@ extern "C" bitsmoe_status bitsmoe_project(const float* Ut_dev, const void* W_dev
   hipStream_t s = static_cast<hipStream_t>(stream);
   const bool f32 = wt == BITSMOE_F32;
   bitsmoe_status st;
-  // A: U hi/lo, K-tiled [2][r_pad][d_out] (PM-row tiles).  B: bf16 W is read
-  // in place as a K-major operand (K = d_out runs over its rows); fp32 W is
-  // split into K-tiled transposed hi/lo copies [E][d_in_pad][d_out].
+  // Tile: PM rows of U^T (the size that pads r least) x PN columns of W.
   int PM = 256;
   for (int t : {192, 128})
     if ((r + t - 1) / t * t < (r + PM - 1) / PM * PM) PM = t;
   const int64_t r_pad = (r + PM - 1) / PM * PM;
   const int64_t d_in_pad = (d_in + PN - 1) / PN * PN;
-  uint16_t* U2 = static_cast<uint16_t*>(scratch(kScratchMisc, 2 * r_pad * d_out * 2, stream, &st));
-  if (!U2) return st;
+  const int64_t ucount = r_pad * d_out;
+  // small tables: a flag (256 bytes), then U as fp16 (bf16 W) and as bf16
+  // hi/lo planes
+  char* misc = static_cast<char*>(scratch(kScratchMisc, 256 + 3 * ucount * 2, stream, &st));
+  if (!misc) return st;
+  int* flag = reinterpret_cast<int*>(misc);
+  uint16_t* U16 = reinterpret_cast<uint16_t*>(misc + 256);
   {
-    const int64_t count = r_pad * d_out;
-    const unsigned blocks = static_cast<unsigned>(std::min<int64_t>((count + 255) / 256, 65536));
-    hipLaunchKernelGGL(split_f32_kernel, dim3(blocks), dim3(256), 0, s, Ut_dev, r, r_pad, d_out, PM,
-                       U2, U2 + count);
+    const unsigned blocks = static_cast<unsigned>(std::min<int64_t>((ucount + 255) / 256, 65536));
+    if (f32)
+      hipLaunchKernelGGL(split_f32_kernel<false>, dim3(blocks), dim3(256), 0, s, Ut_dev, r, r_pad,
+                         d_out, PM, U16, flag);
+    else
+      hipLaunchKernelGGL(split_f32_kernel<true>, dim3(blocks), dim3(256), 0, s, Ut_dev, r, r_pad,
+                         d_out, PM, U16, flag);
     BITSMOE_LAUNCH_CHECK("project: split launch");
   }
-  gemm::Problem p{};
-  const uint16_t* Uhi = U2;
-  const uint16_t* Ulo = U2 + r_pad * d_out;
   static_assert(BK == gemm::kTileK, "the K-tiled operands need the kernel's K step");
+  gemm::Problem p{};
   p.a.rows = r_pad;
   p.a.kstep = static_cast<int64_t>(PM) * gemm::kTileK;
   p.a.rtile = static_cast<int64_t>(PM) * d_out;
-  p.a.bstride = 0;
   p.segs = 1;
   p.kseg = d_out;
+  p.splits = 1;
+  p.tiles_m = static_cast<int>((r + PM - 1) / PM);
+  p.tiles_n = static_cast<int>((d_in + PN - 1) / PN);
+  p.group_n = p.tiles_n;
+  // XCD-aware grid: an expert's tiles run together on one XCD, so its W is
+  // fetched into that XCD's L2 once for all of them
+  p.flat = p.tiles_m * p.tiles_n;
+  KernelTimer timer("project", stream);
   if (f32) {
+    // fp32 W: transposed K-tiled hi/lo copies, three bf16 passes
     const int64_t wcount = E * d_out * d_in_pad;
     uint16_t* Wt = static_cast<uint16_t*>(scratch(kScratchB, 2 * wcount * 2, stream, &st));
     if (!Wt) return st;
@@ -180,6 +257,8 @@ extern "C" bitsmoe_status bitsmoe_project(const float* Ut_dev, const void* W_dev
     hipLaunchKernelGGL(batched_transpose_kernel<true>, tg, dim3(256), 0, s, W_dev, d_out, d_in,
                        d_in_pad, Wt, Wt_lo);
     BITSMOE_LAUNCH_CHECK("project: transpose launch");
+    const uint16_t* Uhi = U16;
+    const uint16_t* Ulo = U16 + ucount;
     p.b.rows = d_in_pad;
     p.b.kstep = static_cast<int64_t>(PN) * gemm::kTileK;
     p.b.rtile = static_cast<int64_t>(PN) * d_out;
@@ -188,40 +267,77 @@ extern "C" bitsmoe_status bitsmoe_project(const float* Ut_dev, const void* W_dev
     p.a.pass[0] = Uhi; p.b.pass[0] = Wt;
     p.a.pass[1] = Uhi; p.b.pass[1] = Wt_lo;
     p.a.pass[2] = Ulo; p.b.pass[2] = Wt;
-  } else {
-    const uint16_t* Wb = static_cast<const uint16_t*>(W_dev);
-    p.b.ld = d_in;
-    p.b.rows = d_in;  // N extent (columns past it are clamped)
-    p.b.kstep = static_cast<int64_t>(gemm::kTileK) * d_in;
-    p.b.rtile = PN;
-    p.b.bstride = d_out * d_in;
-    p.passes = 2;  // Uhi*W + Ulo*W
-    p.a.pass[0] = Uhi; p.b.pass[0] = Wb;
-    p.a.pass[1] = Ulo; p.b.pass[1] = Wb;
-  }
-  p.ktiles = static_cast<int64_t>(p.passes) * d_out / BK;
-  p.splits = 1;
-  p.tiles_m = static_cast<int>((r + PM - 1) / PM);
-  p.tiles_n = static_cast<int>((d_in + PN - 1) / PN);
-  p.symmetric = 0;
-  p.group_n = p.tiles_n;
-  FactorStore epi{C_dev, r, d_in};
-  dim3 grid(static_cast<unsigned>(p.tiles_m * p.tiles_n), 1, static_cast<unsigned>(E));
-  {
-    KernelTimer timer("project", stream);
-#define BITSMOE_PROJECT(TM, KN)                                                              \
-  hipLaunchKernelGGL((gemm::gemm_nt_kernel<TM, PN, 32, 4, FactorStore, false, KN>), grid,   \
+    p.ktiles = 3 * d_out / BK;
+    const dim3 grid = factor_grid(p, E, false);
+    FactorStore epi{C_dev, r, d_in, nullptr};
+#define BITSMOE_PROJECT3(TM)                                                                   \
+  hipLaunchKernelGGL((gemm::gemm_nt_kernel<TM, PN, 32, 4, FactorStore>), grid,                \
                      dim3(gemm::kThreads), 0, s, p, epi)
-    if (PM == 256) {
-      if (f32) BITSMOE_PROJECT(256, false); else BITSMOE_PROJECT(256, true);
-    } else if (PM == 192) {
-      if (f32) BITSMOE_PROJECT(192, false); else BITSMOE_PROJECT(192, true);
-    } else {
-      if (f32) BITSMOE_PROJECT(128, false); else BITSMOE_PROJECT(128, true);
-    }
-#undef BITSMOE_PROJECT
+    if (PM == 256) BITSMOE_PROJECT3(256); else if (PM == 192) BITSMOE_PROJECT3(192); else BITSMOE_PROJECT3(128);
+#undef BITSMOE_PROJECT3
+    BITSMOE_LAUNCH_CHECK("project: gemm launch");
+    return ok();
   }
-  BITSMOE_LAUNCH_CHECK("project: gemm launch");
+  // bf16 W is read where it lies as a K-major operand (K = d_out runs over
+  // its rows).  One pass: U rounded to fp16 (relative error <= 2^-12), each
+  // W fragment widened to fp16 in registers (exact for |W| in 2^-14 ..
+  // 65504), fp32 accumulation.
+  const uint16_t* Wb = static_cast<const uint16_t*>(W_dev);
+  p.b.ld = d_in;
+  p.b.rows = d_in;  // N extent (columns past it are clamped)
+  p.b.kstep = static_cast<int64_t>(gemm::kTileK) * d_in;
+  p.b.rtile = PN;
+  p.b.bstride = d_out * d_in;
+  p.passes = 1;
+  p.a.pass[0] = U16; p.b.pass[0] = Wb;
+  p.ktiles = d_out / BK;
+  {
+    // persistent for the 192- and 128-row tiles (the 256-row persistent
+    // kernel does not fit the register file without spilling)
+    const dim3 grid = factor_grid(p, E, PM != 256);
+    FactorStore epi{C_dev, r, d_in, flag};
+#define BITSMOE_PROJECT16(TM, PERSIST)                                                            \
+  hipLaunchKernelGGL((gemm::gemm_nt_kernel<TM, PN, 32, 4, FactorStore, true, true, false, true,      \
+                                           PERSIST>), grid, dim3(gemm::kThreads), 0, s, p, epi)
+    if (PM == 256)
+      BITSMOE_PROJECT16(256, false);
+    else if (PM == 192 && p.persist)
+      BITSMOE_PROJECT16(192, true);
+    else if (PM == 192)
+      BITSMOE_PROJECT16(192, false);
+    else if (p.persist)
+      BITSMOE_PROJECT16(128, true);
+    else
+      BITSMOE_PROJECT16(128, false);
+#undef BITSMOE_PROJECT16
+    BITSMOE_LAUNCH_CHECK("project: gemm launch");
+  }
+  // Only if the one-pass form flagged a tile (a non-finite factor: a W entry
+  // beyond fp16's range, or a non-finite input; or a tile of factors all
+  // below 2^-6): the exact two-pass bf16 form, U = hi + lo, the
+  // two terms of a K tile back to back (d_out / 32 segments of two K tiles;
+  // A advances a tile at a time through the interleaved planes, B stays on
+  // the segment's K tile, so W's second read of a tile hits L2).  Otherwise
+  // its workgroups return at once.
+  p.a.pass[0] = U16 + ucount;
+  p.a.rtile = static_cast<int64_t>(PM) * 2 * d_out;
+  p.a.estride = 2 * p.a.kstep;
+  p.b.estride = p.b.kstep;
+  p.b.repeat_k = 1;
+  p.segs = static_cast<int>(d_out / gemm::kTileK);
+  p.kseg = 2 * gemm::kTileK;
+  p.ktiles = 2 * d_out / BK;
+  p.run_if = flag;
+  {
+    const dim3 grid = factor_grid(p, E, false);
+    FactorStore epi{C_dev, r, d_in, nullptr};
+#define BITSMOE_PROJECT2(TM)                                                                    \
+  hipLaunchKernelGGL((gemm::gemm_nt_kernel<TM, PN, 32, 4, FactorStore, false, true>), grid,      \
+                     dim3(gemm::kThreads), 0, s, p, epi)
+    if (PM == 256) BITSMOE_PROJECT2(256); else if (PM == 192) BITSMOE_PROJECT2(192); else BITSMOE_PROJECT2(128);
+#undef BITSMOE_PROJECT2
+    BITSMOE_LAUNCH_CHECK("project: exact gemm launch");
+  }
   return ok();
 }
 
@@ -253,8 +369,8 @@ extern "C" bitsmoe_status bitsmoe_project_in(const float* Vt_dev, const void* W_
   {
     const int64_t count = r_pad * d_in;
     const unsigned blocks = static_cast<unsigned>(std::min<int64_t>((count + 255) / 256, 65536));
-    hipLaunchKernelGGL(split_f32_kernel, dim3(blocks), dim3(256), 0, s, Vt_dev, r, r_pad, d_in, PM,
-                       V2, V2 + count);
+    hipLaunchKernelGGL(split_f32_kernel<false>, dim3(blocks), dim3(256), 0, s, Vt_dev, r, r_pad,
+                       d_in, PM, V2, nullptr);
     BITSMOE_LAUNCH_CHECK("project_in: split launch");
   }
   gemm::Problem p{};
@@ -294,8 +410,9 @@ extern "C" bitsmoe_status bitsmoe_project_in(const float* Vt_dev, const void* W_
   p.tiles_n = static_cast<int>((d_out + PN - 1) / PN);
   p.symmetric = 0;
   p.group_n = p.tiles_n;
-  FactorStore epi{C_dev, r, d_out};
-  dim3 grid(static_cast<unsigned>(p.tiles_m * p.tiles_n), 1, static_cast<unsigned>(E));
+  p.flat = p.tiles_m * p.tiles_n;  // XCD-aware grid, as in bitsmoe_project
+  FactorStore epi{C_dev, r, d_out, nullptr};
+  const dim3 grid = factor_grid(p, E, false);
   {
     KernelTimer timer("project_in", stream);
 #define BITSMOE_PROJECT_IN(TM)                                                                \

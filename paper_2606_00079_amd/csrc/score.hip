@@ -387,6 +387,7 @@ __global__ __launch_bounds__(256) void dgen_kernel(const float* __restrict__ C, 
 // rows past the end (the padding of the last row tile) are computed and
 // never stored.
 struct RowDot {
+  static constexpr bool kUsesLds = true;  // reads or writes the stage buffers
   const uint16_t* D;
   float* part;
   int64_t R, d;

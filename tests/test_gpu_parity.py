@@ -185,6 +185,47 @@ def test_project(case):
     assert rows.max() <= REL
 
 
+@pytest.mark.parametrize("case", ["beyond_fp16", "non_finite", "tiny_and_subnormal",
+                                  "tiny_expert"])
+def test_project_bf16_outside_fp16_range(case):
+    """bf16 W is multiplied in one fp16 pass; entries beyond fp16's range
+    (|W| > 65504) make that pass non-finite, and the library then recomputes
+    C exactly in the two-pass bf16 form: C is finite and within the bar.  A
+    non-finite W stays non-finite.  Entries far below fp16's normal range
+    lose only absolute precision (at most 2^-25 each), far below the bar
+    next to normal entries; a tile of factors that are all small (an expert
+    of tiny weights) is recomputed exactly."""
+    say("project outside fp16 range", case)
+    g = np.random.default_rng(8)
+    E, d_out, d_in, r = 3, 192, 320, 100
+    Wf = synth.random_rows(E * d_out, d_in, seed=9).reshape(E, d_out, d_in)
+    if case == "beyond_fp16":
+        Wf[1, 7, 11] = 1.5e5
+        Wf[2, 100, 300] = -7.0e4
+    elif case == "non_finite":
+        Wf[0, 3, 5] = np.inf
+    elif case == "tiny_expert":
+        Wf[0] *= 2.0 ** -30          # a whole expert below fp16's range (~1e-11)
+        Wf[2, :, 128:] *= 2.0 ** -20
+    else:
+        m = np.random.default_rng(10).random(Wf.shape) < 0.1   # a tenth of the entries tiny
+        Wf[m] *= 2.0 ** -20          # ~1e-8: fp16 subnormal or zero
+        Wf[1, :, :64] *= 2.0 ** -12
+    W = synth.f32_to_bf16_bits(Wf)
+    Ut = np.linalg.qr(g.standard_normal((d_out, r)))[0].T.astype(np.float32)
+    C = bm.project(dev(Ut, "f32"), dev(W, "bf16")).cpu().numpy().reshape(E, r, d_in)
+    W64 = f64(W, "bf16")
+    if case == "non_finite":
+        assert not np.all(np.isfinite(C))
+        return
+    assert np.all(np.isfinite(C))
+    for e in range(E):
+        ref = oracle.project(Ut.astype(np.float64), W64[e:e + 1])
+        err = relfro(C[e], ref)
+        say("expert", e, "rel fro", err)
+        assert err <= REL
+
+
 # ------------------------------------------------------------------------- L
 SCORE_CASES = [
     # (name, units, d, group, bits, heavy)
