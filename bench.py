@@ -96,6 +96,42 @@ def measured_traffic(config: str):
         return None
 
 
+def kernel_source_hash() -> str:
+    """sha256 (first 16 hex digits) of every kernel source, in name order."""
+    import glob
+    import hashlib
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2606_00079_amd", "csrc")
+    for f in sorted(glob.glob(os.path.join(csrc, "*.hip")) + glob.glob(os.path.join(csrc, "*.hpp"))):
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_counters(config: str):
+    """Per-kernel rocprofv3 counter figures (MfmaUtil, executed TFLOP/s, HBM
+    bytes and GB/s) from the committed summary of this workload, or None when
+    it is absent or any kernel source changed since it was taken."""
+    path = os.path.join(ROOT, "profiles", f"counters_{config}.md")
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    with open(path) as fh:
+        for line in fh:
+            if ":" in line and not line.startswith((" ", "|", "#", "*", "`")):
+                k, v = line.split(":", 1)
+                kv[k.strip()] = v.strip()
+    if kv.get("source_sha256_16") != kernel_source_hash():
+        return None
+    out = {}
+    for k, v in kv.items():
+        try:
+            out[k] = float(v)
+        except ValueError:
+            pass
+    return out
+
+
 def workload_name(cfg) -> str:
     parts = ", ".join(f"{p.name} {p.d_out}x{p.d_in} r={p.r}" for p in cfg.projs)
     return (f"{cfg.name}: E={cfg.E} experts x {{{parts}}}, calibration {cfg.n_tokens} rows, "
@@ -644,6 +680,21 @@ def main(argv=None) -> int:
 
     value = float(np.median(gpu_ms))
     traffic = measured_traffic(args.config)
+    counters = measured_counters(args.config)
+    if counters:
+        src = "rocprofv3 --pmc, profiles/counters_%s.md" % args.config
+        for kname, ckey in (("score_gemm", "score_gemm"), ("gram_experts", "symmetric_gram"),
+                            ("project", "project"), ("score_dgen", "score_dgen"), ("pack", "pack")):
+            c = {}
+            if f"{ckey}_mfma_util_pct" in counters and counters[f"{ckey}_mfma_util_pct"] > 0:
+                c["mfma_util"] = round(counters[f"{ckey}_mfma_util_pct"] / 100.0, 4)
+                c["exec_tflops"] = counters[f"{ckey}_exec_tflops"]
+            if f"{ckey}_hbm_gbs" in counters:
+                c["hbm_gbs"] = counters[f"{ckey}_hbm_gbs"]
+                c["hbm_bytes_per_launch"] = (counters[f"{ckey}_hbm_read_bytes_per_launch"]
+                                             + counters[f"{ckey}_hbm_write_bytes_per_launch"])
+            c["source"] = src + (" (H and M launches together)" if ckey == "symmetric_gram" else "")
+            kernels[kname]["counters"] = c
     out = {
         "metric": METRIC,
         "value": round(value, 3),
@@ -679,7 +730,9 @@ def main(argv=None) -> int:
                      "executed_flops_per_launch": score_exec_flops / max(n_gemm // max(steps, 1), 1),
                      "executed_tflops": round(score_exec_flops / (score_ms_step * 1e-3) / 1e12, 1),
                      "executed_frac": round(score_exec_flops / (score_ms_step * 1e-3) / 1e12
-                                            / PEAK_BF16_TFLOPS, 4)},
+                                            / PEAK_BF16_TFLOPS, 4),
+                     "mfma_util_counter": (kernels["score_gemm"].get("counters", {}).get("mfma_util")
+                                           if counters else None)},
     }
     out["paper_context"] = PAPER_CONTEXT
     if side:
