@@ -356,7 +356,12 @@ bitsmoe_status bitsmoe_score_routed(const float* C_dev, int64_t units, int64_t d
  * where e(i) is the expert whose range [offsets[e], offsets[e+1]) holds i and
  * C^_e is expert e's r packed units decoded exactly as bitsmoe_unpack does
  * (widths 0..8 and 16).  Each unit row is decoded once per chunk of its
- * expert's tokens; the basis is applied once per token.
+ * expert's tokens (below 16 tokens, or when d_in is not a multiple of 128,
+ * chunks of two on the vector units; otherwise chunks of 8, or 16 when the
+ * experts average more than 8 tokens, on the matrix cores: the codes as
+ * exact fp16 integers times the tokens as fp16 hi + lo, per group
+ * s sum q x + m sum x in fp32, and y = U z as an fp32 matrix product); the
+ * basis is applied once per token.
  *   codes_dev, params_dev, bits_dev, word_offsets_dev, total_words
  *               the packed units of all E * r units (as from bitsmoe_pack;
  *               bits and offsets must cover E * r units)
@@ -414,8 +419,10 @@ bitsmoe_status bitsmoe_moe_decode_in(const uint64_t* codes_dev, const uint16_t* 
  * in slot order.  Nothing is read back to the host and the call does not
  * wait for the stream (after the first call on a device, which allocates
  * the partial sums).  Each slot's expert row is decoded for that token
- * alone; bitsmoe_moe_decode, which groups each expert's tokens, suits
- * larger batches.
+ * alone below 16 tokens (or when d_in is not a multiple of 128); otherwise
+ * the slots are grouped by expert on the device (E <= 4096) and each
+ * expert's rows are decoded once per chunk of its tokens on the matrix
+ * cores (as in bitsmoe_moe_decode).
  *   topk_experts_dev  [B][k] int32; a slot whose expert is outside [0, E)
  *                     contributes nothing
  *   topk_weights_dev  [B][k] fp32, used as given
@@ -435,14 +442,18 @@ bitsmoe_status bitsmoe_moe_decode_topk(const uint64_t* codes_dev, const uint16_t
  * hipMalloc.  Same arguments, results and shape rules as
  * bitsmoe_moe_decode_topk; it calls no hipMalloc, hipFree or other
  * allocating routine, creates no events and does not wait.
- * The partial sums ([B * k][r] fp32) live in a fixed device array of
- * 4194304 floats (16 MiB) that every GPU the library runs on holds until
- * the process ends; B * k * r above 4194304 gives BITSMOE_ERR_SHAPE.  The
- * array's address on a device is looked up on the first call on that
- * device.  Every call on one GPU shares that GPU's array: calls that
- * overlap on one GPU (different streams, or several host threads) race on
- * it and must be ordered by the caller.  Nothing in the array needs
- * clearing between calls: each call writes every partial it reads.
+ * Its scratch (the partial sums, [B * k][r] fp32; on the matrix-core path
+ * also the tokens as fp16, their block sums, the routing tables and the
+ * token sums [B rounded up to 64][r], about 4 B d_in + 16 B k + 4 B r bytes
+ * more) lives in a fixed 16 MiB device
+ * array that every GPU the library runs on holds until the process ends; a
+ * call that needs more (B * k * r near 4194304 floats or above) gives
+ * BITSMOE_ERR_SHAPE.  The array's address on a device is looked up on the
+ * first call on that device.  Every call on one GPU shares that GPU's
+ * array: calls that overlap on one GPU (different streams, or several host
+ * threads) race on it and must be ordered by the caller.  Nothing in the
+ * array needs clearing between calls: each call writes every value it
+ * reads.
  */
 bitsmoe_status bitsmoe_moe_decode_topk_noalloc(const uint64_t* codes_dev,
                                                const uint16_t* params_dev, const uint8_t* bits_dev,

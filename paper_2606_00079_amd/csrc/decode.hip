@@ -43,9 +43,20 @@ __device__ __forceinline__ bool width_ok(int b) {
   return b == 0 || b == 16 || (b >= 1 && b <= BITSMOE_MAX_BITS);
 }
 
+// s_waitcnt vmcnt(0) alone (expcnt and lgkmcnt left at their maxima), in
+// the gfx9 encoding.
+__device__ __forceinline__ void wait_vmcnt0() { __builtin_amdgcn_s_waitcnt(0x0f70); }
+
 // bits 0..3 of v -> bit 0 of bytes 0..3
 __device__ __forceinline__ uint32_t spread4(uint32_t v) {
   return __umul24(v & 15u, 0x204081u) & 0x01010101u;
+}
+// nibble n (< 16) -> its bits at bit t of bytes 0..3.  The shift goes into
+// the multiplier while that stays within 24 bits (a full-rate v_mul_u32_u24);
+// past that the nibble is shifted first.
+__device__ __forceinline__ uint32_t spread4_at(uint32_t n, int t) {
+  return t <= 2 ? __umul24(n, 0x204081u << t) & (0x01010101u << t)
+                : __umul24(n << t, 0x204081u) & (0x01010101u << t);
 }
 
 // A row's packed state as one lane sees it: width (0 when the unit is
@@ -344,6 +355,533 @@ __global__ __launch_bounds__(1024) void decode_y_kernel(const float* __restrict_
     const int64_t b = b0 + tb;
     if (b < B && o < d_out) Y[b * d_out + o] = s;
   }
+}
+
+// ---- batches: z and y on the matrix cores ----
+//
+// Each expert's routing entries are taken in jobs of up to 16 tokens and
+// its unit rows in blocks of 16 (one wave each), so that
+//     Z[t][k] = sum_g s_{k,g} sum_{i in g} q_{k,i} x_t[i] + m_{k,g} sum_{i in g} x_t[i]
+// runs as v_mfma_f32_16x16x32_f16: A = the tokens' x as fp16 hi + lo (two
+// products; x = hi + lo to about 2^-22), B = the codes q of 16 rows (small
+// integers, exact in fp16), one fresh accumulator per group of G entries,
+// scaled by s and shifted by m times the token's group sum in fp32.  An
+// expert's codes are decoded once per job instead of once per routing
+// entry.  The token sums of the partial rows then go through the shared
+// basis as an fp32 matrix product (v_mfma_f32_16x16x4_f32).
+
+constexpr int kMmaWaves = 4;    // waves per z workgroup (16 unit rows each)
+constexpr int kMmaStages = 4;   // LDS ring of the z step: stages loaded 3 ahead
+
+typedef _Float16 half8 __attribute__((ext_vector_type(8)));
+typedef float float4v __attribute__((ext_vector_type(4)));
+
+// x [B][d] fp32 -> xh, xl [B][d] fp16 (x ~ xh + xl) and xs [B][d / G] fp32
+// (the sum of each block of G entries; the z step passes min(group, 128)),
+// for block index idx = token * (d / G) + block, by one wave: each lane
+// converts up to four entries and the block sum is a wave reduction.
+__device__ __forceinline__ void xprep_wave(const float* __restrict__ X, int64_t idx, int d, int G,
+                                           _Float16* __restrict__ xh, _Float16* __restrict__ xl,
+                                           float* __restrict__ xs) {
+  const int ng = d / G;
+  const int lane = threadIdx.x & 63;
+  const int64_t b = idx / ng;
+  const int g = static_cast<int>(idx - b * ng);
+  const int64_t base = b * d + static_cast<int64_t>(g) * G;
+  float sum = 0.0f;
+  for (int i = 4 * lane; i < G; i += 256) {
+    const float4 v = *reinterpret_cast<const float4*>(X + base + i);
+    const float vv[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const _Float16 hh = static_cast<_Float16>(vv[j]);
+      xh[base + i + j] = hh;
+      xl[base + i + j] = static_cast<_Float16>(vv[j] - static_cast<float>(hh));
+      sum += vv[j];
+    }
+  }
+  sum = wave_sum(sum);
+  if (lane == 0) xs[idx] = sum;
+}
+
+// Exclusive prefix sum over the 1024 threads of a workgroup (in thread
+// order) of one int each; `sh` is 16 ints of LDS.  Returns the thread's
+// exclusive sum and sets *total.
+__device__ __forceinline__ int block_scan_1024(int v, int* sh, int* total) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  int incl = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int u = __shfl_up(incl, o, 64);
+    if (lane >= o) incl += u;
+  }
+  if (lane == 63) sh[wave] = incl;
+  __syncthreads();
+  int before = 0, all = 0;
+#pragma unroll
+  for (int w = 0; w < 16; ++w) {
+    const int t = sh[w];
+    before += w < wave ? t : 0;
+    all += t;
+  }
+  __syncthreads();  // sh may be reused by the caller
+  *total = all;
+  return before + incl - v;
+}
+
+// Groups a device top-k table [B][kk] by expert: jobs {expert, first sorted
+// position, entries (1..jt), 0}, the number of jobs, and per sorted position
+// the entry (b kk + j), its token and weight.  A slot whose expert is
+// outside [0, E) has its partial row zp[entry][0..r) set to zero instead.
+// The order of an expert's entries among its positions is not fixed
+// (atomics), which changes nothing: each token's column of the product is
+// computed on its own.  Workgroup 0 does the routing (when topk is set);
+// the others, 16 waves each, run xprep_wave over the B (d / G) blocks.
+constexpr int kRouteThreads = 1024;
+constexpr int kRouteMaxExperts = 4096;  // four per thread in the scan
+__global__ __launch_bounds__(kRouteThreads) void prep_kernel(
+    const int32_t* __restrict__ topk, const float* __restrict__ topw, int64_t BK, int kk, int E,
+    int r, int jt, int4* __restrict__ jobs, int* __restrict__ njobs, int32_t* __restrict__ ent,
+    int32_t* __restrict__ tok, float* __restrict__ wgt, float* __restrict__ zp,
+    const float* __restrict__ X, int64_t nblk, int d, int G, _Float16* __restrict__ xh,
+    _Float16* __restrict__ xl, float* __restrict__ xs) {
+  const int route = topk ? 1 : 0;
+  if (static_cast<int>(blockIdx.x) >= route) {
+    const int64_t idx = (static_cast<int64_t>(blockIdx.x) - route) * 16 + (threadIdx.x >> 6);
+    if (idx < nblk) xprep_wave(X, idx, d, G, xh, xl, xs);
+    return;
+  }
+  __shared__ int cnt[kRouteMaxExperts];
+  __shared__ int start[kRouteMaxExperts];
+  __shared__ int jstart[kRouteMaxExperts];
+  __shared__ int sh[16];
+  for (int e = threadIdx.x; e < E; e += kRouteThreads) cnt[e] = 0;
+  __syncthreads();
+  for (int64_t i = threadIdx.x; i < BK; i += kRouteThreads) {
+    const int e = topk[i];
+    if (e >= 0 && e < E) {
+      atomicAdd(&cnt[e], 1);
+    } else {
+      for (int k = 0; k < r; ++k) zp[i * r + k] = 0.0f;
+    }
+  }
+  __syncthreads();
+  // positions and jobs: thread t owns experts 4t .. 4t + 3
+  int c4[4], n4 = 0, j4 = 0;
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const int e = 4 * static_cast<int>(threadIdx.x) + u;
+    c4[u] = e < E ? cnt[e] : 0;
+    n4 += c4[u];
+    j4 += (c4[u] + jt - 1) / jt;
+  }
+  int ntot, jtot;
+  int pos = block_scan_1024(n4, sh, &ntot);
+  int jb = block_scan_1024(j4, sh, &jtot);
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const int e = 4 * static_cast<int>(threadIdx.x) + u;
+    if (e < E) {
+      start[e] = pos;
+      jstart[e] = jb;
+      for (int j = 0; j * jt < c4[u]; ++j)
+        jobs[jb + j] = make_int4(e, pos + j * jt, min(jt, c4[u] - j * jt), 0);
+      cnt[e] = 0;  // reused as the fill count below
+    }
+    pos += c4[u];
+    jb += (c4[u] + jt - 1) / jt;
+  }
+  if (threadIdx.x == 0) *njobs = jtot;
+  __syncthreads();
+  for (int64_t i = threadIdx.x; i < BK; i += kRouteThreads) {
+    const int e = topk[i];
+    if (e >= 0 && e < E) {
+      const int p = start[e] + atomicAdd(&cnt[e], 1);
+      ent[p] = static_cast<int32_t>(i);
+      tok[p] = static_cast<int32_t>(i / kk);
+      wgt[p] = topw[i];
+    }
+  }
+}
+
+// The fp16 codes of 8 consecutive entries from their bit-plane bytes
+// (byte t holds bit t of the 8 codes, entry j in bit j; bytes of planes the
+// row does not have are zero): each byte's bits are spread to one byte per
+// entry, and byte q becomes the fp16 of 1024 + q (0x6400 | q), minus 1024:
+// exact.  Planes from bw on are skipped; bw is the same in every lane of the
+// wave, so that the loop has no divergent branch.
+__device__ __forceinline__ half8 codes8(const uint32_t (&byte)[BITSMOE_MAX_BITS], int bw) {
+  uint32_t qlo = 0, qhi = 0;
+#pragma unroll
+  for (int t = 0; t < BITSMOE_MAX_BITS; ++t) {
+    if (t < bw) {
+      qlo |= spread4_at(byte[t] & 15u, t);
+      qhi |= spread4_at(byte[t] >> 4, t);
+    }
+  }
+  // bytes 2i, 2i + 1 of q and 0x64 above each: v_perm_b32 selector bytes 0-3
+  // pick q, 4 picks 0x64
+  const uint32_t hi8 = 0x64646464u;
+  const uint32_t h[4] = {__builtin_amdgcn_perm(hi8, qlo, 0x04010400u),
+                         __builtin_amdgcn_perm(hi8, qlo, 0x04030402u),
+                         __builtin_amdgcn_perm(hi8, qhi, 0x04010400u),
+                         __builtin_amdgcn_perm(hi8, qhi, 0x04030402u)};
+  const half8 k1024 = {1024, 1024, 1024, 1024, 1024, 1024, 1024, 1024};
+  return __builtin_bit_cast(half8, h) - k1024;
+}
+
+// One wave-wide direct global->LDS load: lane l reads 16 (4) bytes at its
+// own address g and they land at LDS byte address lds + 16 l (+ 4 l); `lds`
+// is wave-uniform.  Issued through inline assembly so that the compiler
+// neither tracks the load nor inserts waits for it: the caller waits with
+// s_waitcnt vmcnt and synchronizes the workgroup before reading.  M0 carries
+// the LDS address; nothing else in the kernel uses M0.
+__device__ __forceinline__ void lds_dma16(const void* g, const void* lds) {
+  const uint32_t l = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(reinterpret_cast<uintptr_t>(lds)));
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" : : "v"(g), "s"(l) : "memory");
+}
+__device__ __forceinline__ void lds_dma4(const void* g, const void* lds) {
+  const uint32_t l = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(reinterpret_cast<uintptr_t>(lds)));
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dword %0, off" : : "v"(g), "s"(l) : "memory");
+}
+// s_waitcnt vmcnt(N) alone, in the gfx9 encoding (vmcnt[3:0] in bits 3:0,
+// vmcnt[5:4] in bits 15:14).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt_n() {
+  static_assert(N >= 0 && N < 64, "vmcnt");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// zp[ent[p]][k] = wgt[p] (c^_{e,k} . x_{tok[p]}) for the positions p of job
+// blockIdx.y (jobs[j] = {e, first, n <= TS, 0}; ent null: the position is
+// the entry) and the 16 WV unit rows of block blockIdx.x, 16 per wave, as
+// v_mfma_f32_16x16x32_f16 with the job's tokens as A (M; rows past TS are
+// zero) and the codes as B (N): lane l holds row l % 16 and, of every
+// 32-entry step, the 8 entries of chunk l / 16, and ends with the sums of
+// that row for tokens 4 (l / 16) + i.
+//
+// The entries go by stages of 128 (four steps).  Within a stage a group (or
+// the stage's half of a 256-entry group: a sub-group of GB = min(G, 128)
+// entries) is dealt to its steps so that chunk c is GB / 4 consecutive
+// entries; the stage's bits of a row's bit plane are 16 bytes, and chunk c of
+// a step is one byte of them.  Every stage is fetched straight into LDS by
+// the workgroup NS - 1 stages ahead (a ring of NS buffers): the tokens' x
+// (fp16 hi and lo, in the order the lanes read them), their sub-group sums,
+// and per wave the 16 rows' planes 0..3 and parameter words.  Every lane
+// issues every load of a stage (a lane without a row or token reads a valid
+// stand-in whose value goes unused, and the tail reloads the last stage), so
+// a wave has a fixed number of loads per stage and the wait before a stage
+// is exact.  Rows of 5 to 8 bits load their planes 4 and up, and fp16 rows
+// their values, when the stage is summed.  With njobs set, jobs at or past
+// *njobs return at once (the grid covers a bound).
+constexpr int kRingPlanes = 4;  // bit planes fetched ahead
+
+template <int G, int TS, int WV, int NS>
+__global__ __launch_bounds__(64 * WV) void decode_zmma_kernel(
+    const uint32_t* __restrict__ codes32, const uint32_t* __restrict__ params,
+    const uint8_t* __restrict__ bits, const int64_t* __restrict__ off, int64_t total_words, int r,
+    int d, const _Float16* __restrict__ xh, const _Float16* __restrict__ xl,
+    const float* __restrict__ xs, const int4* __restrict__ jobs, const int* __restrict__ njobs,
+    const int32_t* __restrict__ ent, const int32_t* __restrict__ tok,
+    const float* __restrict__ wgt, float* __restrict__ zp) {
+  constexpr int GB = G < 128 ? G : 128;  // sub-group: the part of a group within a stage
+  constexpr int SG = GB / 32;            // MFMA steps per sub-group
+  constexpr int NSUB = 128 / GB;         // sub-groups per stage
+  constexpr int CH = GB / 4;             // entries of a sub-group per chunk
+  constexpr int XSLOT = 16 * TS;         // 16-byte x slots of a stage (hi; lo alike)
+  constexpr int XI = 2 * XSLOT / 64;     // x loads per stage (64 lanes each)
+  constexpr int XPW = XI > WV ? XI / WV : 1;  // x loads per wave (waves past XI repeat one)
+  constexpr int PER = XPW + 3;           // loads per wave per stage: x, planes, params, sums
+  constexpr int RP = kRingPlanes;
+  static_assert(XI % WV == 0 || WV % XI == 0, "x loads spread evenly over the waves");
+  static_assert((NS - 2) * PER < 64, "vmcnt holds at most 63 loads");
+  struct Stage {
+    uint4 x[2][XSLOT];          // [hi, lo][(step * 4 + chunk) * TS + token]
+    uint4 w[WV][RP][16];        // [wave][plane][row]: the row's 128 bits of the stage
+    uint32_t prm[WV][4][16];    // [wave][sub-group][row]
+    float4 sum[4][4];           // [sub-group][token / 4]
+  };
+  __shared__ Stage st[NS];
+  if (njobs && static_cast<int>(blockIdx.y) >= *njobs) return;  // whole workgroup
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int4 jb = jobs[blockIdx.y];
+  const int e = jb.x, first = jb.y, n = jb.z;
+  const int64_t nw = d / 64;
+  const int ng = d / G;
+  const int nsb = d / GB;    // sub-groups of a unit row
+  const int nst = d / 128;   // stages
+
+  // this lane's unit row (lane % 16 of the wave's 16) and its width (0:
+  // evicted, inconsistent or past r)
+  const int rho = lane & 15, c = lane >> 4;
+  const int k = static_cast<int>(blockIdx.x) * (16 * WV) + 16 * wave + rho;
+  int ba = 0;
+  int64_t oa = 0;
+  if (k < r) {
+    const int64_t u = static_cast<int64_t>(e) * r + k;
+    const int b = bits[u];
+    const int64_t o0 = off[u], o1 = off[u + 1];
+    const bool valid = width_ok(b) && b != 0 && o1 - o0 == b * nw && o0 >= 0 && o1 <= total_words;
+    ba = valid ? b : 0;
+    oa = valid ? o0 : 0;
+  }
+  const bool packed = ba >= 1 && ba <= BITSMOE_MAX_BITS;
+  const uint32_t* pw = codes32 + 2 * oa;  // plane t starts at word 2 t nw
+  const void* standin = xh;               // a valid address for unused lanes
+
+  // load addresses of this lane, all but the stage offset
+  // x: slot xs0 + lane of load m = wave + WV i, part m / (XI / 2)
+  const _Float16* xsrc[XPW];
+#pragma unroll
+  for (int i = 0; i < XPW; ++i) {
+    const int m = (wave + WV * i) % XI;
+    const int part = m / (XI / 2);
+    const int slot = (m % (XI / 2)) * 64 + lane;
+    const int tt = slot % TS, cc = (slot / TS) % 4, q = slot / (4 * TS);
+    const int sg = q / SG, qq = q % SG;
+    const int tk = tok[first + min(tt, n - 1)];
+    xsrc[i] = (part ? xl : xh) + static_cast<int64_t>(tk) * d + sg * GB + cc * CH + 8 * qq;
+  }
+  // sums: sub-group c (lane / 16) of token rho, stand-in past NSUB or n
+  const float* ssrc;
+  {
+    const int tk = tok[first + min(rho, n - 1)];
+    ssrc = c < NSUB ? xs + static_cast<int64_t>(tk) * nsb + c : static_cast<const float*>(standin);
+  }
+  // planes: plane c of row rho (the 64 lanes cover 16 rows x 4 planes)
+  const uint32_t* wsrc = (packed && c < min(ba, RP)) ? pw + 2 * c * nw
+                                                     : static_cast<const uint32_t*>(standin);
+  // parameters: sub-group c of row rho
+  const uint32_t* psrc = (packed && c < NSUB)
+                             ? params + (static_cast<int64_t>(e) * r + k) * ng
+                             : static_cast<const uint32_t*>(standin);
+  auto issue = [&](int s, int buf) {
+    s = min(s, nst - 1);
+    Stage& S = st[buf];
+#pragma unroll
+    for (int i = 0; i < XPW; ++i) {
+      const int m = (wave + WV * i) % XI;
+      lds_dma16(xsrc[i] + 128 * static_cast<int64_t>(s),
+                &S.x[m / (XI / 2)][(m % (XI / 2)) * 64]);
+    }
+    lds_dma16(wsrc == standin ? wsrc : wsrc + 4 * s, &S.w[wave][0][0]);
+    // the parameter word of sub-group c of stage s: group (128 s + GB c) / G
+    lds_dma4(psrc == standin ? psrc : psrc + (128 * s + GB * c) / G, &S.prm[wave][0][0]);
+    lds_dma4(ssrc == standin ? ssrc : ssrc + static_cast<int64_t>(NSUB) * s, &S.sum[0][0]);
+  };
+  // the entries and weights of this lane's output tokens 4 c + i
+  int64_t eo[4];
+  float wo[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int sl = 4 * c + i;
+    eo[i] = -1;
+    wo[i] = 0.0f;
+    if (sl < n && k < r) {
+      const int p = first + sl;
+      eo[i] = ent ? ent[p] : p;
+      wo[i] = wgt[p];
+    }
+  }
+
+  // wave-uniform shape of the wave's rows: planes of the widest packed row,
+  // and whether any row is wider than the ring or stored as fp16
+  int bw = 0;
+#pragma unroll
+  for (int t = 0; t < BITSMOE_MAX_BITS; ++t)
+    if (__builtin_amdgcn_ballot_w64(packed && ba > t) != 0) bw = t + 1;
+  const bool any_raw = __builtin_amdgcn_ballot_w64(ba == 16) != 0;
+  // the group's affine step: s and m from the parameter word (packed rows),
+  // s = 1, m = 0 for fp16 rows, 0 for rows that contribute nothing
+  const float sc_raw = ba == 16 ? 1.0f : 0.0f;
+
+  float z[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+  // BW: planes decoded, a compile-time bound on the wave's widest packed row
+  auto sum_stage = [&]<int BW>(int s, const Stage& S) {
+    // the row's plane words of the stage: for sub-group sg, the 32-bit word
+    // holding its chunk c (word (sg GB + c CH) / 32 of the stage's four),
+    // read at a per-lane LDS address; words of planes the row lacks (or of
+    // rows that are not packed) are zeroed here
+    uint32_t wd[BITSMOE_MAX_BITS][NSUB];
+#pragma unroll
+    for (int t = 0; t < BITSMOE_MAX_BITS; ++t)
+#pragma unroll
+      for (int sg = 0; sg < NSUB; ++sg) wd[t][sg] = 0u;
+#pragma unroll
+    for (int t = 0; t < RP; ++t) {
+      if (t < BW) {
+        const uint32_t* row = reinterpret_cast<const uint32_t*>(&S.w[wave][t][rho]);
+        const bool has = packed && t < ba;
+#pragma unroll
+        for (int sg = 0; sg < NSUB; ++sg) {
+          const uint32_t v = row[(sg * GB + c * CH) >> 5];
+          wd[t][sg] = has ? v : 0u;
+        }
+      }
+    }
+    if (BW > RP) {
+      // rows of 5..8 bits: the planes past the ring, waited for here
+#pragma unroll
+      for (int t = RP; t < BITSMOE_MAX_BITS; ++t)
+        if (t < BW && packed && t < ba)
+#pragma unroll
+          for (int sg = 0; sg < NSUB; ++sg)
+            wd[t][sg] = pw[2 * t * nw + 4 * s + ((sg * GB + c * CH) >> 5)];
+      wait_vmcnt0();
+    }
+    uint4 raw[4];
+    if (any_raw) {
+      // fp16 rows: the values (the row starts at a 64-bit word: 8-byte loads)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        raw[q] = make_uint4(0, 0, 0, 0);
+        if (ba == 16) {
+          const int sg = q / SG, qq = q % SG;
+          const uint2* p2 = reinterpret_cast<const uint2*>(pw) +
+                            ((128 * static_cast<int64_t>(s) + sg * GB + c * CH + 8 * qq) >> 2);
+          const uint2 v0 = p2[0], v1 = p2[1];
+          raw[q] = make_uint4(v0.x, v0.y, v1.x, v1.y);
+        }
+      }
+      wait_vmcnt0();
+    }
+#pragma unroll
+    for (int sg = 0; sg < NSUB; ++sg) {
+      float4v acc = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+      for (int qq = 0; qq < SG; ++qq) {
+        const int q = sg * SG + qq;
+        // chunk c of step q: bits ((c CH + 8 qq) mod 32) .. +7 of its word
+        const int sh = (c * CH + 8 * qq) & 31;
+        uint32_t byte[BITSMOE_MAX_BITS];
+#pragma unroll
+        for (int t = 0; t < BITSMOE_MAX_BITS; ++t) byte[t] = (wd[t][sg] >> sh) & 0xffu;
+        half8 a = codes8(byte, BW);
+        if (any_raw && ba == 16) a = __builtin_bit_cast(half8, raw[q]);
+        // token rows past TS repeat rows below TS (their sums go unused)
+        const int slot = (q * 4 + c) * TS + (rho % TS);
+        const half8 h = __builtin_bit_cast(half8, S.x[0][slot]);
+        const half8 lo = __builtin_bit_cast(half8, S.x[1][slot]);
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(h, a, acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(lo, a, acc, 0, 0, 0);
+      }
+      const uint32_t prm = S.prm[wave][sg][rho];
+      const float sc = packed ? f16_bits_to_f32(static_cast<uint16_t>(prm & 0xffffu)) : sc_raw;
+      const float mn = packed ? f16_bits_to_f32(static_cast<uint16_t>(prm >> 16)) : 0.0f;
+      const float4 s4 = S.sum[sg][c];
+      const float sv[4] = {s4.x, s4.y, s4.z, s4.w};
+#pragma unroll
+      for (int i = 0; i < 4; ++i) z[i] = fmaf(sc, acc[i], fmaf(mn, sv[i], z[i]));
+    }
+  };
+
+#pragma unroll
+  for (int j = 0; j < NS - 1; ++j) issue(j, j);
+  for (int s0 = 0; s0 < nst; s0 += NS) {
+#pragma unroll
+    for (int j = 0; j < NS; ++j) {
+      const int s = s0 + j;
+      if (s < nst) {
+        wait_vmcnt_n<(NS - 2) * PER>();  // this wave's loads of stage s are in
+        __syncthreads();                  // everyone's are; stage s - 1 is read
+        issue(s + NS - 1, (j + NS - 1) % NS);
+        switch (bw) {
+          case 0:
+          case 1: sum_stage.template operator()<1>(s, st[j]); break;
+          case 2: sum_stage.template operator()<2>(s, st[j]); break;
+          case 3: sum_stage.template operator()<3>(s, st[j]); break;
+          case 4: sum_stage.template operator()<4>(s, st[j]); break;
+          default: sum_stage.template operator()<BITSMOE_MAX_BITS>(s, st[j]); break;
+        }
+      }
+    }
+  }
+  wait_vmcnt0();  // no load may land in LDS after the workgroup ends
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+    if (eo[i] >= 0) zp[eo[i] * r + k] = wo[i] * z[i];
+}
+
+// Z[b][k] for b < Bp, k < rp (zero past B and r) = the sum, in slot order,
+// of the token's partial rows zp[slot][k]: slots b kmax + j (pidx null) or
+// pidx[b kmax + j] (-1: none).
+__global__ __launch_bounds__(256) void zsum_kernel(const float* __restrict__ zp,
+                                                   const int64_t* __restrict__ pidx, int kmax,
+                                                   int r, int rp, int64_t B, int64_t Bp,
+                                                   float* __restrict__ Z) {
+  const int64_t idx = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (idx >= Bp * rp) return;
+  const int64_t b = idx / rp;
+  const int k = static_cast<int>(idx - b * rp);
+  float s = 0.0f;
+  if (b < B && k < r) {
+    for (int j = 0; j < kmax; ++j) {
+      const int64_t i = pidx ? pidx[b * kmax + j] : b * kmax + j;
+      if (i >= 0) s += zp[i * r + k];
+    }
+  }
+  Z[idx] = s;
+}
+
+// Y[b][o] = sum_k Z[b][k] U^T[k][o] for the 64 tokens of blockIdx.y and the
+// 16 columns of blockIdx.x as v_mfma_f32_16x16x4_f32 (A = Z, tokens as M;
+// B = U^T, columns as N), the 16 waves splitting k into ranges of kw (a
+// multiple of 16; Z [Bp][rp] is zero past r) and their sums added in wave
+// order through LDS.  Within 16 k's, lane l supplies k = 4 (l / 16) + i at
+// sub-step i, so that its four Z values are one float4.
+constexpr int kYmmaWaves = 16;
+__global__ __launch_bounds__(64 * kYmmaWaves) void decode_ymma_kernel(
+    const float* __restrict__ Z, int rp, int r, int kw, const float* __restrict__ Ut,
+    int64_t d_out, int64_t B, float* __restrict__ Y) {
+  __shared__ float red[kYmmaWaves][16][64];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int tau = lane & 15, c = lane >> 4;
+  const int64_t o = static_cast<int64_t>(blockIdx.x) * 16 + tau;
+  const int64_t b0 = static_cast<int64_t>(blockIdx.y) * 64;
+  const int k0 = wave * kw, k1 = min(k0 + kw, rp);
+  float4v acc[4];
+#pragma unroll
+  for (int m = 0; m < 4; ++m) acc[m] = float4v{0.0f, 0.0f, 0.0f, 0.0f};
+  // 64 k's at a time: every load of the four 16-k chunks before their MFMAs
+  for (int kb0 = k0; kb0 < k1; kb0 += 64) {
+    float4 a[4][4];
+    float bv[4][4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int kb = kb0 + 16 * u;
+#pragma unroll
+      for (int m = 0; m < 4; ++m)
+        a[u][m] = kb < k1 ? *reinterpret_cast<const float4*>(Z + (b0 + 16 * m + tau) * rp + kb + 4 * c)
+                          : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int kk = kb + 4 * c + i;
+        bv[u][i] = (kb < k1 && kk < r && o < d_out) ? Ut[static_cast<int64_t>(kk) * d_out + o] : 0.0f;
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int m = 0; m < 4; ++m) {
+          const float4 am = a[u][m];
+          const float av = i == 0 ? am.x : i == 1 ? am.y : i == 2 ? am.z : am.w;
+          acc[m] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bv[u][i], acc[m], 0, 0, 0);
+        }
+  }
+#pragma unroll
+  for (int m = 0; m < 4; ++m)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) red[wave][4 * m + i][lane] = acc[m][i];
+  __syncthreads();
+  const int j = threadIdx.x >> 6, ln = threadIdx.x & 63;
+  float sum = 0.0f;
+#pragma unroll
+  for (int w = 0; w < kYmmaWaves; ++w) sum += red[w][j][ln];
+  const int64_t b = b0 + 16 * (j >> 2) + 4 * (ln >> 4) + (j & 3);
+  const int64_t col = static_cast<int64_t>(blockIdx.x) * 16 + (ln & 15);
+  if (b < B && col < d_out) Y[b * d_out + col] = sum;
 }
 
 // ---- input-space form (gate/up): y = sum_j g_j C^_e^T z, z = Phi_r^T x ----
@@ -723,12 +1261,136 @@ bitsmoe_status decode_launch(const DecodeGeom& g, int T, bool topk_jobs, int64_t
   return ok();
 }
 
-// The top-k decode without allocation keeps its partial sums in a fixed
-// device array, decode_partials below: every GPU the library runs on holds
-// one copy (16 MiB) until the process ends.  Its address differs per device
+// Batches from this many tokens take the matrix-core z step (at one token
+// the VALU form, which waits on fewer dependent loads, is faster), when the
+// units' length is a multiple of its 128-entry stages.
+constexpr int64_t kMmaMinTokens = 16;
+bool mma_path(int64_t B, int64_t d_in) { return B >= kMmaMinTokens && d_in % 128 == 0; }
+
+// Tokens per job of the z step: 8 while the experts average at most 8
+// routing entries (the ring's x stage is then half the size, which leaves
+// room for three workgroups per CU), else 16.
+int mma_job_tokens(int64_t E, int64_t nnz) {
+  const int64_t busy = std::max<int64_t>(std::min(E, nnz), 1);
+  return nnz <= 8 * busy ? 8 : 16;
+}
+
+// Bytes of scratch decode_mma needs: x as fp16 hi/lo, the block sums, the
+// job table and its count, the sorted entries, tokens and weights, the
+// partials and the token sums Z [Bp][rp] (each region 256-byte aligned).
+struct MmaScratch {
+  size_t xb, sb, jb, eb, zb, Zb;
+  int64_t max_jobs, Bp, rp;
+  size_t total() const { return 2 * xb + sb + jb + 3 * eb + zb + Zb; }
+};
+MmaScratch mma_scratch(int64_t E, int64_t r, int64_t d_in, int group, int64_t B, bool topk,
+                       int64_t nnz, int64_t njobs_host) {
+  auto up = [](size_t b) { return (b + 255) / 256 * 256; };
+  MmaScratch m;
+  // jobs: one per expert with routing entries, plus one per further jt
+  const int jt = mma_job_tokens(E, nnz);
+  m.max_jobs = topk ? std::min<int64_t>(E, nnz) + (nnz + jt - 1) / jt : njobs_host;
+  m.Bp = (B + 63) / 64 * 64;
+  m.rp = (r + 15) / 16 * 16;
+  m.xb = up(static_cast<size_t>(B * d_in) * 2);
+  m.sb = up(static_cast<size_t>(B * (d_in / std::min(group, 128))) * 4);
+  m.jb = up(static_cast<size_t>(std::max<int64_t>(m.max_jobs, 1)) * 16 + 16);
+  m.eb = up(static_cast<size_t>(std::max<int64_t>(nnz, 1)) * 4);
+  m.zb = up(static_cast<size_t>(std::max<int64_t>(nnz, 1) * r) * 4);
+  m.Zb = up(static_cast<size_t>(m.Bp * m.rp) * 4);
+  return m;
+}
+
+// The matrix-core z step and the y step for B tokens, routing already in
+// device tables (jobs, ent, tok, wgt; njobs on the device when not null) or
+// produced from a device top-k table (topk set: prep_kernel).  The
+// scratch of mma_scratch is `base` when given (the caller checked its size),
+// else the library's scratch cache; `timed` records kernel events.
+bitsmoe_status decode_mma(const uint32_t* c32, const uint32_t* pr, const uint8_t* bits_dev,
+                          const int64_t* offs_dev, int64_t total_words, int64_t E, int64_t r,
+                          int64_t d_in, int group, const float* Ut_dev, int64_t d_out,
+                          const float* X_dev, int64_t B, const int32_t* topk, const float* topw,
+                          int kk, int64_t nnz, const int4* jobs_in, int64_t njobs_host,
+                          const int32_t* tok_in, const float* wgt_in, const int64_t* pidx_d,
+                          int kmax, float* Y_dev, void* stream, char* base = nullptr,
+                          bool timed = true) {
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int ng = static_cast<int>(d_in / group);
+  const MmaScratch m = mma_scratch(E, r, d_in, group, B, topk != nullptr, nnz, njobs_host);
+  const int64_t max_jobs = m.max_jobs;
+  const size_t xb = m.xb, sb = m.sb, jb = m.jb, eb = m.eb;
+  bitsmoe_status st;
+  char* sp = base;
+  if (!sp) {
+    sp = static_cast<char*>(scratch(kScratchPart, m.total(), stream, &st));
+    if (!sp) return st;
+  }
+  _Float16* xh = reinterpret_cast<_Float16*>(sp);
+  _Float16* xl = reinterpret_cast<_Float16*>(sp + xb);
+  float* xs = reinterpret_cast<float*>(sp + 2 * xb);
+  int4* jobs = reinterpret_cast<int4*>(sp + 2 * xb + sb);
+  int* njobs = reinterpret_cast<int*>(sp + 2 * xb + sb + jb - 16);
+  int32_t* ent = reinterpret_cast<int32_t*>(sp + 2 * xb + sb + jb);
+  int32_t* tok = reinterpret_cast<int32_t*>(sp + 2 * xb + sb + jb + eb);
+  float* wgt = reinterpret_cast<float*>(sp + 2 * xb + sb + jb + 2 * eb);
+  float* zp = reinterpret_cast<float*>(sp + 2 * xb + sb + jb + 3 * eb);
+  float* Zs = reinterpret_cast<float*>(sp + 2 * xb + sb + jb + 3 * eb + m.zb);
+  const int gb = std::min(group, 128);
+  const int jt = mma_job_tokens(E, nnz);
+  {
+    // one launch: routing (top-k form) in workgroup 0, x prep in the others
+    KernelTimer timer(timed ? "moe_decode_prep" : nullptr, stream);
+    const int64_t nblk = B * (d_in / gb);
+    const unsigned nwg = static_cast<unsigned>((nblk + 15) / 16) + (topk ? 1u : 0u);
+    hipLaunchKernelGGL(prep_kernel, dim3(nwg), dim3(kRouteThreads), 0, s, topk, topw, nnz, kk,
+                       static_cast<int>(E), static_cast<int>(r), jt, jobs, njobs, ent, tok, wgt, zp,
+                       X_dev, nblk, static_cast<int>(d_in), gb, xh, xl, xs);
+  }
+  BITSMOE_LAUNCH_CHECK("moe_decode: prep launch");
+  if (max_jobs > 0) {
+    KernelTimer timer(timed ? "moe_decode_z" : nullptr, stream);
+    constexpr int kRows = 16 * kMmaWaves;
+    dim3 grid(static_cast<unsigned>((r + kRows - 1) / kRows), static_cast<unsigned>(max_jobs));
+#define BITSMOE_DECZ(GG, TT)                                                                     \
+  hipLaunchKernelGGL((decode_zmma_kernel<GG, TT, kMmaWaves, kMmaStages>), grid, dim3(64 * kMmaWaves), \
+                     0, s, c32, pr, bits_dev, offs_dev, total_words, static_cast<int>(r),         \
+                     static_cast<int>(d_in), xh, xl, xs, topk ? jobs : jobs_in,                   \
+                     topk ? njobs : nullptr, topk ? ent : nullptr, topk ? tok : tok_in,           \
+                     topk ? wgt : wgt_in, zp)
+#define BITSMOE_DECZ_G(GG) \
+  if (jt == 8) BITSMOE_DECZ(GG, 8); else BITSMOE_DECZ(GG, 16);
+    switch (group) {
+      case 32: BITSMOE_DECZ_G(32); break;
+      case 64: BITSMOE_DECZ_G(64); break;
+      case 128: BITSMOE_DECZ_G(128); break;
+      default: BITSMOE_DECZ_G(256); break;
+    }
+#undef BITSMOE_DECZ_G
+#undef BITSMOE_DECZ
+  }
+  BITSMOE_LAUNCH_CHECK("moe_decode: z launch");
+  {
+    // the y step: token sums (zsum), then y = U z (decode_ymma)
+    KernelTimer timer(timed ? "moe_decode_y" : nullptr, stream);
+    const int64_t nz = m.Bp * m.rp;
+    hipLaunchKernelGGL(zsum_kernel, dim3(static_cast<unsigned>((nz + 255) / 256)), dim3(256), 0, s,
+                       zp, pidx_d, kmax, static_cast<int>(r), static_cast<int>(m.rp), B, m.Bp, Zs);
+    const int kw = static_cast<int>((m.rp / 16 + kYmmaWaves - 1) / kYmmaWaves * 16);
+    dim3 grid(static_cast<unsigned>((d_out + 15) / 16), static_cast<unsigned>(m.Bp / 64));
+    hipLaunchKernelGGL(decode_ymma_kernel, grid, dim3(64 * kYmmaWaves), 0, s, Zs,
+                       static_cast<int>(m.rp), static_cast<int>(r), kw, Ut_dev, d_out, B, Y_dev);
+  }
+  BITSMOE_LAUNCH_CHECK("moe_decode: y launch");
+  return ok();
+}
+
+// The top-k decode without allocation keeps its scratch (the partial sums;
+// on the matrix-core path also x as fp16, the group sums and the routing
+// tables) in a fixed device array, decode_partials below: every GPU the
+// library runs on holds one copy (16 MiB) until the process ends.  Its address differs per device
 // and is looked up once per device, with that device current; host code
 // uses only that address (the array's name is a host-side stand-in).
-constexpr int64_t kNoAllocPartials = int64_t{1} << 22;  // floats: B * k * r at most
+constexpr int64_t kNoAllocPartials = int64_t{1} << 22;  // floats (16 MiB)
 constexpr int kNoAllocMaxDevices = 64;
 
 }  // namespace
@@ -796,6 +1458,40 @@ extern "C" bitsmoe_status bitsmoe_moe_decode(const uint64_t* codes_dev, const ui
   // (four tokens' 128 left room for two waves per SIMD only)
   st = build_routing("moe_decode", E, B, offsets_host, tokens_host, weights_host, 2, &rt);
   if (st != BITSMOE_OK) return st;
+  if (mma_path(B, d_in)) {
+    // matrix-core z step: jobs of up to jt consecutive entries of an expert
+    // (the entries are grouped by expert, so a position is its entry)
+    const int jt = mma_job_tokens(E, rt.nnz);
+    std::vector<int4> jobs4;
+    for (int64_t e = 0; e < E; ++e)
+      for (int64_t i = offsets_host[e]; i < offsets_host[e + 1]; i += jt)
+        jobs4.push_back(make_int4(static_cast<int>(e), static_cast<int>(i),
+                                  static_cast<int>(std::min<int64_t>(jt, offsets_host[e + 1] - i)), 0));
+    const size_t jbytes = (jobs4.size() * 16 + 255) / 256 * 256;
+    const size_t ebytes = (static_cast<size_t>(std::max<int64_t>(rt.nnz, 1)) * 4 + 255) / 256 * 256;
+    const size_t pbytes = static_cast<size_t>(B * rt.kmax) * 8;
+    char* tab = static_cast<char*>(scratch(kScratchMisc, jbytes + 2 * ebytes + pbytes + 256, stream, &st));
+    if (!tab) return st;
+    int4* jobs_d = reinterpret_cast<int4*>(tab);
+    int32_t* tok_d = reinterpret_cast<int32_t*>(tab + jbytes);
+    float* w_d = reinterpret_cast<float*>(tab + jbytes + ebytes);
+    int64_t* pidx_d = reinterpret_cast<int64_t*>(tab + jbytes + 2 * ebytes);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    hipError_t he = hipSuccess;
+    if (!jobs4.empty()) he = hipMemcpyAsync(jobs_d, jobs4.data(), jobs4.size() * 16, hipMemcpyHostToDevice, s);
+    if (he == hipSuccess && rt.nnz > 0)
+      he = hipMemcpyAsync(tok_d, tokens_host, rt.nnz * 4, hipMemcpyHostToDevice, s);
+    if (he == hipSuccess && rt.nnz > 0)
+      he = hipMemcpyAsync(w_d, weights_host, rt.nnz * 4, hipMemcpyHostToDevice, s);
+    if (he == hipSuccess) he = hipMemcpyAsync(pidx_d, rt.pidx.data(), pbytes, hipMemcpyHostToDevice, s);
+    if (he == hipSuccess) he = hipStreamSynchronize(s);  // the host tables go away on return
+    if (he != hipSuccess) return device_error("moe_decode: routing table copy", he);
+    return decode_mma(reinterpret_cast<const uint32_t*>(codes_dev),
+                      reinterpret_cast<const uint32_t*>(params_dev), bits_dev, word_offsets_dev,
+                      total_words, E, r, d_in, group, Ut_dev, d_out, X_dev, B, nullptr, nullptr, 1,
+                      rt.nnz, jobs_d, static_cast<int64_t>(jobs4.size()), tok_d, w_d, pidx_d,
+                      static_cast<int>(rt.kmax), Y_dev, stream);
+  }
   const DecodeGeom g = decode_geometry(rt.njobs, r, d_in, B);
   int4* jobs_d;
   int64_t* pidx_d;
@@ -826,6 +1522,12 @@ extern "C" bitsmoe_status bitsmoe_moe_decode_topk(const uint64_t* codes_dev, con
   if (st != BITSMOE_OK) return st;
   st = check_topk("moe_decode_topk", topk_experts_dev, topk_weights_dev, E, B, k);
   if (st != BITSMOE_OK) return st;
+  if (mma_path(B, d_in) && E <= kRouteMaxExperts)
+    return decode_mma(reinterpret_cast<const uint32_t*>(codes_dev),
+                      reinterpret_cast<const uint32_t*>(params_dev), bits_dev, word_offsets_dev,
+                      total_words, E, r, d_in, group, Ut_dev, d_out, X_dev, B, topk_experts_dev,
+                      topk_weights_dev, static_cast<int>(k), B * k, nullptr, 0, nullptr, nullptr,
+                      nullptr, static_cast<int>(k), Y_dev, stream);
   const int64_t njobs = B * k;
   const DecodeGeom g = decode_geometry(njobs, r, d_in, B);
   float* zp = static_cast<float*>(scratch(kScratchPart, njobs * r * 4, stream, &st));
@@ -848,14 +1550,28 @@ extern "C" bitsmoe_status bitsmoe_moe_decode_topk_noalloc(
   st = check_topk("moe_decode_topk_noalloc", topk_experts_dev, topk_weights_dev, E, B, k);
   if (st != BITSMOE_OK) return st;
   const int64_t njobs = B * k;
-  if (njobs * r > kNoAllocPartials)
+  const bool mma = mma_path(B, d_in) && E <= kRouteMaxExperts;
+  // the same path as bitsmoe_moe_decode_topk, with every scratch region in
+  // the fixed array
+  const size_t need = mma ? mma_scratch(E, r, d_in, group, B, true, njobs, 0).total()
+                          : static_cast<size_t>(njobs * r) * sizeof(float);
+  if (need > static_cast<size_t>(kNoAllocPartials) * sizeof(float))
     return fail(BITSMOE_ERR_SHAPE,
-                "moe_decode_topk_noalloc: B * k * r is above the fixed partials buffer (4194304 floats)");
+                "moe_decode_topk_noalloc: the call needs more than the fixed scratch buffer (16 MiB)");
   float* zp = nullptr;
   st = device_partials(&zp);
   if (st != BITSMOE_OK) return st;
+  if (mma)
+    return decode_mma(reinterpret_cast<const uint32_t*>(codes_dev),
+                      reinterpret_cast<const uint32_t*>(params_dev), bits_dev, word_offsets_dev,
+                      total_words, E, r, d_in, group, Ut_dev, d_out, X_dev, B, topk_experts_dev,
+                      topk_weights_dev, static_cast<int>(k), njobs, nullptr, 0, nullptr, nullptr,
+                      nullptr, static_cast<int>(k), Y_dev, stream, reinterpret_cast<char*>(zp),
+                      /*timed=*/false);
   // every partial [B k][r] is written by the z kernel before the y kernel
-  // reads it, so nothing needs clearing; no events, no scratch, no copies
+  // reads it, so nothing needs clearing (on the matrix-core path the routing
+  // kernel writes the job count and zeroes the rows of unused slots); no
+  // events, no library scratch, no copies
   const DecodeGeom g = decode_geometry(njobs, r, d_in, B);
   return decode_launch(g, 1, true, njobs, codes_dev, params_dev, bits_dev, word_offsets_dev,
                        total_words, E, r, d_in, group, Ut_dev, d_out, X_dev, B, nullptr,

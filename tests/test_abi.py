@@ -320,7 +320,7 @@ def test_device_entry_points_validate_before_launch(lib):
                                                fake, 2, 2, odd, fake, fake, s) == 1
     assert lib.bitsmoe_moe_decode_topk_noalloc(fake, fake, fake, fake, 10, 8, 8192, 128, 64, fake,
                                                64, fake, 520, 1, fake, fake, fake, s) == 2
-    assert "partials buffer" in pkg.last_error()
+    assert "fixed scratch" in pkg.last_error()
     assert lib.bitsmoe_gram(odd, 1, 64, 64, fake, s) == 1
     assert "aligned" in pkg.last_error()
     assert lib.bitsmoe_gram_experts(fake, 1, 2, 64, 64, odd, s) == 1

@@ -1,10 +1,10 @@
 """The top-k decode entry point that allocates nothing
 (bitsmoe_moe_decode_topk_noalloc), called through the C ABI, against the
-allocating entry point (bitsmoe_moe_decode_topk) on the same inputs: two
-calls in a row, the second smaller than the first (the fixed partials
-buffer keeps the first call's contents), both bit-identical to the
-allocating call and within the decode bar (1e-4 relative Frobenius) of the
-fp64 oracle."""
+allocating entry point (bitsmoe_moe_decode_topk) on the same inputs: calls
+in a row, each smaller than the one before (the fixed scratch buffer keeps
+the previous call's contents), every one bit-identical to the allocating
+call and within the decode bar (1e-4 relative Frobenius) of the fp64
+oracle."""
 import ctypes
 import sys
 
@@ -26,7 +26,6 @@ import paper_2606_00079_amd as bm  # noqa: E402
 
 DEV = "cuda:0"
 REL = 1e-4
-CAPACITY = 1 << 22  # floats of the fixed partials buffer
 
 
 def say(*a):
@@ -81,14 +80,17 @@ def _call(fn, t, words, E, r, d_in, d_out, G, Y):
 @pytest.mark.parametrize("order", ["large_then_small"])
 def test_noalloc_matches_allocating_entry_point(order):
     L = bm.lib()
-    # first call: B * k * r at the buffer's capacity (down-projection rows);
-    # second: a smaller gate-shaped call that reuses (and overwrites only the
-    # start of) the same buffer
-    cases = [dict(E=16, r=1024, d_in=768, d_out=2048, B=512, k=8, G=128, widths=(1, 2, 3, 4, 16),
+    # first call: a large batch (matrix-core path, about 9 MiB of the fixed
+    # buffer: down-projection rows, 256 tokens, top-8); then smaller calls
+    # that reuse (and overwrite only part of) the same buffer: a gate-shaped
+    # batch of 20 tokens (matrix-core path, other layout) and 3 tokens (the
+    # one-token-per-slot path)
+    cases = [dict(E=16, r=1024, d_in=768, d_out=2048, B=256, k=8, G=128, widths=(1, 2, 3, 4, 16),
                   seed=31),
-             dict(E=8, r=384, d_in=2048, d_out=768, B=3, k=2, G=128, widths=(0, 1, 2, 3, 4),
-                  seed=32)]
-    assert cases[0]["B"] * cases[0]["k"] * cases[0]["r"] == CAPACITY
+             dict(E=8, r=384, d_in=2048, d_out=768, B=20, k=2, G=128, widths=(0, 1, 2, 3, 4),
+                  seed=32),
+             dict(E=8, r=384, d_in=2048, d_out=768, B=3, k=2, G=64, widths=(0, 1, 2, 3, 16),
+                  seed=33)]
     for c in cases:
         say("case", {k: v for k, v in c.items() if k != "widths"})
         t, words, ref = _case(**c)
@@ -111,7 +113,7 @@ def test_noalloc_rejects_sizes_above_the_buffer():
     L = bm.lib()
     t, words, _ = _case(E=4, r=64, d_in=128, d_out=64, B=2, k=2, G=64, widths=(1, 2), seed=33)
     Y = torch.empty((2, 64), dtype=torch.float32, device=DEV)
-    # r = 8192 and B * k = 520: B * k * r = 4259840, above the 4194304 floats
+    # r = 8192, B * k = 520: the partials alone (17 MB) exceed the 16 MiB
     big_B = 520
     bt = dict(t)
     bt["top"] = torch.zeros((big_B, 1), dtype=torch.int32, device=DEV)
@@ -119,7 +121,7 @@ def test_noalloc_rejects_sizes_above_the_buffer():
     bt["X"] = torch.zeros((big_B, 128), dtype=torch.float32, device=DEV)
     Yb = torch.empty((big_B, 64), dtype=torch.float32, device=DEV)
     st = _call(L.bitsmoe_moe_decode_topk_noalloc, bt, words, 4, 8192, 128, 64, 64, Yb)
-    assert st == 2 and "partials buffer" in bm.last_error()
+    assert st == 2 and "fixed scratch" in bm.last_error()
     # a call that fits still works afterwards
     assert _call(L.bitsmoe_moe_decode_topk_noalloc, t, words, 4, 64, 128, 64, 64, Y) == 0
     torch.cuda.synchronize()
