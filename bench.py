@@ -96,14 +96,21 @@ def measured_traffic(config: str):
         return None
 
 
+# The sources the core step's kernels are compiled from (the Grams, the
+# factor GEMM, the loss table and pack, with the headers they include); the
+# counter summaries of the core step are valid while these are unchanged.
+CORE_KERNEL_SOURCES = ("common.hpp", "gemm.hpp", "internal.hpp", "gram.hip", "project.hip",
+                       "score.hip", "pack.hip")
+
+
 def kernel_source_hash() -> str:
-    """sha256 (first 16 hex digits) of every kernel source, in name order."""
-    import glob
+    """sha256 (first 16 hex digits) of the core step's kernel sources, in the
+    order of CORE_KERNEL_SOURCES."""
     import hashlib
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2606_00079_amd", "csrc")
-    for f in sorted(glob.glob(os.path.join(csrc, "*.hip")) + glob.glob(os.path.join(csrc, "*.hpp"))):
-        with open(f, "rb") as fh:
+    for f in CORE_KERNEL_SOURCES:
+        with open(os.path.join(csrc, f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
 
@@ -111,7 +118,7 @@ def kernel_source_hash() -> str:
 def measured_counters(config: str):
     """Per-kernel rocprofv3 counter figures (MfmaUtil, executed TFLOP/s, HBM
     bytes and GB/s) from the committed summary of this workload, or None when
-    it is absent or any kernel source changed since it was taken."""
+    it is absent or a core kernel source changed since it was taken."""
     path = os.path.join(ROOT, "profiles", f"counters_{config}.md")
     if not os.path.exists(path):
         return None
