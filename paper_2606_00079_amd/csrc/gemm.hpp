@@ -551,13 +551,16 @@ __device__ __forceinline__ f16x8 bf16x8_to_f16x8(const uint32_t (&w)[4]) {
 // CVTB: the B operand is bf16 in memory and is multiplied as fp16 (F16):
 // each B fragment is converted in registers after its LDS read.
 // PERSIST: compiled for a persistent launch (Problem::persist > 0).
+// ONEK: compiled for a one-pass, one-segment problem without repeat_k (the
+// K walk is a fixed step per tile; persistent launches always are).
 template <int BM, int BN, int KB, int STAGES, class Epi, bool F16 = false, bool BKN = false,
-          bool PAIRED = false, bool CVTB = false, bool PERSIST = false>
+          bool PAIRED = false, bool CVTB = false, bool PERSIST = false, bool ONEK = false>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void gemm_nt_kernel(Problem p, Epi epi) {
   static_assert(BM % 64 == 0 && BN % 64 == 0, "tile");
   static_assert(!CVTB || F16, "converted B fragments are fp16");
   static_assert(!PERSIST || (!PAIRED && !Epi::kUsesLds), "persistent: one tile per job, LDS-free epilogue");
+  static_assert(!ONEK || !PAIRED, "the paired schedule has its own K walk");
   // (persistent: p.passes == 1 and p.segs == 1, see KPos1)
   if (p.run_if && *p.run_if == 0) return;  // whole workgroup
   static_assert(!BKN || (BN == 256 && KB == 32), "KN B operand: 256-wide N tiles, 32-wide K steps");
@@ -663,7 +666,7 @@ void gemm_nt_kernel(Problem p, Epi epi) {
   }
   };
   // persistent launches walk a one-pass, one-segment K (checked by the host)
-  std::conditional_t<PERSIST, KPos1<KB>, KPos<KB>> kp;
+  std::conditional_t<PERSIST || ONEK, KPos1<KB>, KPos<KB>> kp;
   TriWalk<KB> tw;
   // Loads of the next K tile into stage buffer s, one wave instruction at a
   // time (q < LPS) so that they can be spread between matrix-core ops.

@@ -296,9 +296,10 @@ extern "C" bitsmoe_status bitsmoe_project(const float* Ut_dev, const void* W_dev
     // kernel does not fit the register file without spilling)
     const dim3 grid = factor_grid(p, E, PM != 256);
     FactorStore epi{C_dev, r, d_in, flag};
+    // one pass, one segment: the minimal K walk (ONEK)
 #define BITSMOE_PROJECT16(TM, PERSIST)                                                            \
   hipLaunchKernelGGL((gemm::gemm_nt_kernel<TM, PN, 32, 4, FactorStore, true, true, false, true,      \
-                                           PERSIST>), grid, dim3(gemm::kThreads), 0, s, p, epi)
+                                           PERSIST, true>), grid, dim3(gemm::kThreads), 0, s, p, epi)
     if (PM == 256)
       BITSMOE_PROJECT16(256, false);
     else if (PM == 192 && p.persist)
