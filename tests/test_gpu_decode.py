@@ -168,10 +168,19 @@ def test_moe_decode_topk_skips_experts_out_of_range():
 
 
 # Batches of 16 tokens or more take the matrix-core z step, the top-k form
-# with its routing grouped by expert on the device.
+# with its routing grouped by expert on the device.  Jobs hold up to 8
+# routing entries of an expert while the experts average at most 8, else 16:
+# the first cases below have 16 per job, the 8-entry cases follow.
 @pytest.mark.parametrize("E,r,d_in,d_out,B,k,G,widths", [
     (16, 384, 2048, 768, 64, 8, 128, (1, 2, 3, 4)),     # Qwen3-30B-A3B gate units, 64 tokens, top-8
     (16, 1024, 768, 2048, 64, 8, 128, (1, 2, 3, 4)),    # down units
+    # 8-entry jobs: the benchmarked routing (128 experts, 64 tokens, top-8)
+    # and row lengths (gate 2048, down 768), fewer rows per expert
+    (128, 32, 2048, 256, 64, 8, 128, (1, 2, 3, 4)),
+    (128, 80, 768, 512, 64, 8, 128, (1, 2, 3, 4)),
+    (64, 96, 768, 128, 32, 6, 64, (1, 2, 3, 4, 5)),     # group 64, a 5-bit row past the prefetched planes
+    (48, 64, 512, 64, 24, 4, 256, (2, 3, 16)),          # group 256, fp16 rows
+    (40, 48, 256, 96, 20, 3, 32, (0, 1, 4, 8)),         # group 32, eviction, 8-bit rows
     (12, 40, 256, 96, 33, 5, 32, (0, 1, 2, 4, 8, 16)),  # ragged row blocks, eviction, fp16 rows
     (5, 17, 512, 64, 16, 5, 256, (3, 5, 7, 8)),         # every token on every expert, group 256
     (3, 64, 64, 64, 40, 2, 64, (1, 2)),                 # one group per row, many tokens per expert
