@@ -504,19 +504,20 @@ __global__ __launch_bounds__(kRouteThreads) void prep_kernel(
   }
 }
 
-// The fp16 codes of 8 consecutive entries from their bit-plane bytes
-// (byte t holds bit t of the 8 codes, entry j in bit j; bytes of planes the
-// row does not have are zero): each byte's bits are spread to one byte per
-// entry, and byte q becomes the fp16 of 1024 + q (0x6400 | q), minus 1024:
-// exact.  Planes from bw on are skipped; bw is the same in every lane of the
-// wave, so that the loop has no divergent branch.
-__device__ __forceinline__ half8 codes8(const uint32_t (&byte)[BITSMOE_MAX_BITS], int bw) {
+// The fp16 codes of 8 consecutive entries from their bit planes: bits
+// sh .. sh + 7 of plane word w[t] are bit t of the 8 codes (entry j at bit
+// sh + j; words of planes the row does not have are zero).  Each nibble's
+// bits are spread to one byte per entry, and byte q becomes the fp16 of
+// 1024 + q (0x6400 | q), minus 1024: exact.  Planes from bw on are skipped;
+// bw is the same in every lane of the wave, so that the loop has no
+// divergent branch.
+__device__ __forceinline__ half8 codes8(const uint32_t (&w)[BITSMOE_MAX_BITS], int sh, int bw) {
   uint32_t qlo = 0, qhi = 0;
 #pragma unroll
   for (int t = 0; t < BITSMOE_MAX_BITS; ++t) {
     if (t < bw) {
-      qlo |= spread4_at(byte[t] & 15u, t);
-      qhi |= spread4_at(byte[t] >> 4, t);
+      qlo |= spread4_at((w[t] >> sh) & 15u, t);
+      qhi |= spread4_at((w[t] >> (sh + 4)) & 15u, t);
     }
   }
   // bytes 2i, 2i + 1 of q and 0x64 above each: v_perm_b32 selector bytes 0-3
@@ -696,8 +697,9 @@ __global__ __launch_bounds__(64 * WV) void decode_zmma_kernel(
   const float sc_raw = ba == 16 ? 1.0f : 0.0f;
 
   float z[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-  // BW: planes decoded, a compile-time bound on the wave's widest packed row
-  auto sum_stage = [&]<int BW>(int s, const Stage& S) {
+  // BW: planes decoded, a compile-time bound on the wave's widest packed row;
+  // RAW: the wave has fp16 rows
+  auto sum_stage = [&]<int BW, bool RAW>(int s, const Stage& S) {
     // the row's plane words of the stage: for sub-group sg, the 32-bit word
     // holding its chunk c (word (sg GB + c CH) / 32 of the stage's four),
     // read at a per-lane LDS address; words of planes the row lacks (or of
@@ -730,7 +732,7 @@ __global__ __launch_bounds__(64 * WV) void decode_zmma_kernel(
       wait_vmcnt0();
     }
     uint4 raw[4];
-    if (any_raw) {
+    if (RAW) {
       // fp16 rows: the values (the row starts at a 64-bit word: 8-byte loads)
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
@@ -753,11 +755,11 @@ __global__ __launch_bounds__(64 * WV) void decode_zmma_kernel(
         const int q = sg * SG + qq;
         // chunk c of step q: bits ((c CH + 8 qq) mod 32) .. +7 of its word
         const int sh = (c * CH + 8 * qq) & 31;
-        uint32_t byte[BITSMOE_MAX_BITS];
+        uint32_t w[BITSMOE_MAX_BITS];
 #pragma unroll
-        for (int t = 0; t < BITSMOE_MAX_BITS; ++t) byte[t] = (wd[t][sg] >> sh) & 0xffu;
-        half8 a = codes8(byte, BW);
-        if (any_raw && ba == 16) a = __builtin_bit_cast(half8, raw[q]);
+        for (int t = 0; t < BITSMOE_MAX_BITS; ++t) w[t] = wd[t][sg];
+        half8 a = codes8(w, sh, BW);
+        if (RAW && ba == 16) a = __builtin_bit_cast(half8, raw[q]);
         // token rows past TS repeat rows below TS (their sums go unused)
         const int slot = (q * 4 + c) * TS + (rho % TS);
         const half8 h = __builtin_bit_cast(half8, S.x[0][slot]);
@@ -785,13 +787,16 @@ __global__ __launch_bounds__(64 * WV) void decode_zmma_kernel(
         wait_vmcnt_n<(NS - 2) * PER>();  // this wave's loads of stage s are in
         __syncthreads();                  // everyone's are; stage s - 1 is read
         issue(s + NS - 1, (j + NS - 1) % NS);
-        switch (bw) {
-          case 0:
-          case 1: sum_stage.template operator()<1>(s, st[j]); break;
-          case 2: sum_stage.template operator()<2>(s, st[j]); break;
-          case 3: sum_stage.template operator()<3>(s, st[j]); break;
-          case 4: sum_stage.template operator()<4>(s, st[j]); break;
-          default: sum_stage.template operator()<BITSMOE_MAX_BITS>(s, st[j]); break;
+        if (any_raw || bw > RP) {
+          sum_stage.template operator()<BITSMOE_MAX_BITS, true>(s, st[j]);
+        } else {
+          switch (bw) {
+            case 0:
+            case 1: sum_stage.template operator()<1, false>(s, st[j]); break;
+            case 2: sum_stage.template operator()<2, false>(s, st[j]); break;
+            case 3: sum_stage.template operator()<3, false>(s, st[j]); break;
+            default: sum_stage.template operator()<4, false>(s, st[j]); break;
+          }
         }
       }
     }
