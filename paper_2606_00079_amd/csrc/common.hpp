@@ -43,6 +43,10 @@ __device__ __forceinline__ int opaque(int v) {
   asm volatile("" : "+v"(v));
   return v;
 }
+__device__ __forceinline__ float opaque(float v) {
+  asm volatile("" : "+v"(v));
+  return v;
+}
 
 template <typename T>
 __device__ __forceinline__ T wave_sum(T v) {

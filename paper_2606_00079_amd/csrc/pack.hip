@@ -60,6 +60,7 @@ __global__ __launch_bounds__(256) void pack_kernel(const float* __restrict__ C, 
   }
   const double qmax = static_cast<double>((1 << b) - 1);
   const float qmaxf = static_cast<float>((1 << b) - 1);
+  const float near_at = 0.5f - ldexpf(1.0f, b - 21);  // the fp64 fallback's trigger
   uint8_t* ubytes = reinterpret_cast<uint8_t*>(codes + o0);  // plane t at byte t * d / 8
 
   // lane's 8 entries of the chunk at k0 (zeros past the end)
@@ -98,19 +99,19 @@ __global__ __launch_bounds__(256) void pack_kernel(const float* __restrict__ C, 
       const uint16_t s16 = f32_to_f16_bits((mx - mn) / qmaxf);
       const float mf = f16_bits_to_f32(m16);
       const float sf = f16_bits_to_f32(s16);
-      // hardware reciprocal (<= 1 ulp): the quotient stays within 6.1e-5 of
-      // the fp64 one for codes up to 255, inside the 1e-4 fallback margin
-      const float inv = sf > 0.0f ? __builtin_amdgcn_rcpf(sf) : 0.0f;
-      // codes from the fp32 quotient: it rounds the same way as the fp64 one
-      // unless it lies within 1e-4 of a rounding boundary, and those (rare)
+      // hardware reciprocal (<= 1 ulp): the fp32 quotient below is within
+      // 2^-22 |t| of the fp64 one, and only |t| < 2^b decides a code (further
+      // out it is clamped), so it rounds the same way as the fp64 quotient
+      // unless it lies within 2^(b-21) of a rounding boundary; those (rare)
       // lanes decide in fp64
+      const float inv = sf > 0.0f ? __builtin_amdgcn_rcpf(sf) : 0.0f;
       uint32_t q[8];
       bool near = false;
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
         const float t = (cur[i] - mf) * inv;
         const float r = rintf(t);
-        near |= fabsf(t - r) > 0.4999f;
+        near |= fabsf(t - r) > near_at;
         q[i] = static_cast<uint32_t>(__builtin_amdgcn_fmed3f(r, 0.0f, qmaxf));
       }
       if (near && sf > 0.0f) {

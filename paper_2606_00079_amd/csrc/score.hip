@@ -151,16 +151,84 @@ __global__ __launch_bounds__(256) void hoff_kernel(const float* __restrict__ H, 
   }
 }
 
+// The candidate widths, with 2^b - 1, its fp32 reciprocal (the host's
+// correctly rounded division) and the fp64 fallback's trigger for each, so
+// the kernels read them as arguments instead of deriving them per wave.
+//
+// The trigger: the fp32 quotient t = (c - m16) * rcp(s16) carries a
+// relative error below 2^-22 (fp32 subtraction and product, 2^-24 each, and
+// the hardware reciprocal's 1 ulp), and only |t| < 2^b matters (further out
+// the code is clamped whatever the rounding), so |t - t_fp64| < 2^(b-22).
+// Where t is more than twice that from every half-integer it rounds as the
+// fp64 quotient does; closer (|t - rint(t)| > 0.5 - 2^(b-21)) fp64 decides.
 struct QuantBits {
   int nb;
   int b[BITSMOE_MAX_NBITS];
+  float qmax[BITSMOE_MAX_NBITS];
+  float rq[BITSMOE_MAX_NBITS];
+  float near[BITSMOE_MAX_NBITS];
+  void set(int j, int bits) {
+    b[j] = bits;
+    qmax[j] = static_cast<float>((1 << bits) - 1);
+    rq[j] = 1.0f / qmax[j];
+    near[j] = 0.5f - std::ldexp(1.0f, bits - 21);
+  }
 };
+
+// Min and max over each aligned block of glanes lanes (a power of two, at
+// most 64); every lane of a block gets both.  Inside a row of 16 lanes each
+// step takes the partner value by DPP inside the min / max instruction:
+// lane ^ 1 and lane ^ 2 (quad permutations), then the half-row mirror (lane
+// i of 8 reads 7 - i, which holds the other quad's result) and the row
+// mirror (15 - i: the other half row's).  The s_nop ahead of the first step
+// covers the wait states a DPP read needs after a VALU write of its operand
+// or a write of EXEC; the ones between steps cover the operand written two
+// instructions earlier.  Lane ^ 16 is a swizzle, lane ^ 32 a shuffle.
+#define BITSMOE_DPP_MM(ctrl)                                                       \
+  "v_min_f32_dpp %0, %0, %0 " ctrl " row_mask:0xf bank_mask:0xf\n\t"               \
+  "v_max_f32_dpp %1, %1, %1 " ctrl " row_mask:0xf bank_mask:0xf\n\t"
+__device__ __forceinline__ void block_minmax(float& mn, float& mx, int glanes) {
+  if (glanes == 16) {  // groups of 128 entries at 8 per lane
+    asm("s_nop 4\n\t" BITSMOE_DPP_MM("quad_perm:[1,0,3,2]") "s_nop 1\n\t"
+        BITSMOE_DPP_MM("quad_perm:[2,3,0,1]") "s_nop 1\n\t" BITSMOE_DPP_MM("row_half_mirror")
+        "s_nop 1\n\t" BITSMOE_DPP_MM("row_mirror")
+        : "+v"(mn), "+v"(mx));
+    return;
+  }
+  if (glanes > 1) asm("s_nop 4\n\t" BITSMOE_DPP_MM("quad_perm:[1,0,3,2]") : "+v"(mn), "+v"(mx));
+  if (glanes > 2) asm("s_nop 4\n\t" BITSMOE_DPP_MM("quad_perm:[2,3,0,1]") : "+v"(mn), "+v"(mx));
+  if (glanes > 4) asm("s_nop 4\n\t" BITSMOE_DPP_MM("row_half_mirror") : "+v"(mn), "+v"(mx));
+  if (glanes > 8) asm("s_nop 4\n\t" BITSMOE_DPP_MM("row_mirror") : "+v"(mn), "+v"(mx));
+  if (glanes > 16) {  // swizzle in bit-mask mode: and 0x1f, xor 0x10
+    mn = fminf(mn, __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, mn), 0x401F)));
+    mx = fmaxf(mx, __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, mx), 0x401F)));
+  }
+  if (glanes > 32) {
+    mn = fminf(mn, __shfl_xor(mn, 32, 64));
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+  }
+}
+#undef BITSMOE_DPP_MM
+
+// x / qmax rounded to nearest-even in fp32, for qmax = 2^b - 1 (b <= 8) and
+// finite x >= 0, given rq = fp32(1 / qmax): the product x rq is corrected
+// once by its residual x - q0 qmax, which the fma forms exactly (a multiple
+// of ulp(q0) below 2^9 ulp(q0)).  Equal to the IEEE quotient for every such
+// x and qmax (checked exhaustively over the binades where scaling does not
+// apply and over whole binades elsewhere); three instructions instead of
+// the division's ten.
+__device__ __forceinline__ float div_qmax(float x, float qmax, float rq) {
+  const float q0 = x * rq;
+  return fmaf(fmaf(-q0, qmax, x), rq, q0);
+}
 
 // Group-wise fake quantization of one unit per wave.  Lane l covers entries
 // [512 c + 8 l, 512 c + 8 l + 8) of chunk c; a group of G entries spans G/8
-// consecutive lanes.  Codes follow the fp64 rule exactly: the fp32 quotient
-// is used unless it lies within 1e-4 of a rounding boundary (its error is
-// below 6.1e-5 for codes up to 255), in which case fp64 decides.
+// consecutive lanes (with a last chunk of 256 entries at 4 per lane, and G/4
+// lanes per group, where the row length is an odd multiple of 256).  Codes
+// follow the fp64 rule exactly: the fp32 quotient is used unless it lies
+// within 2^(b-21) of a rounding boundary (twice its error bound), in which
+// case fp64 decides.
 // The row is read twice: once for max |c|, once to quantize.  With ROWLDS
 // (rows of at most kRowLds entries) the first pass also keeps the row in
 // LDS (8 KiB per wave at 2048 entries) and the second reads it from there,
@@ -186,84 +254,89 @@ __global__ __launch_bounds__(256) void dgen_kernel(const float* __restrict__ C, 
   const int64_t u = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
   if (u >= units) return;  // whole wave exits together
   constexpr int nb = NB;
-  const int glanes = G / 8;
   float dacc[NB];
 #pragma unroll
   for (int j = 0; j < NB; ++j) dacc[j] = 0.0f;
   const float* crow = C + u * d;
   if (hd_upe > 0) hdiag += (u / hd_upe) * d;  // one H per block of hd_upe units
+  // A row kept in LDS whose length is an odd multiple of 256 ends with a
+  // chunk of 256 entries, 4 per lane, instead of a half-empty 512-entry one
+  // (d = 768: three quarters of the quantizing work of two full chunks).
+  const bool tail4 = ROWLDS && d % 512 == 256;
+  const int64_t d8 = tail4 ? d - 256 : d;  // the entries of 8-per-lane chunks
 
-  // lane's 8 entries of the 512-entry chunk at k0 (zeros past the end)
-  auto load8 = [&](int64_t k0, float (&c)[8]) {
-    const int64_t k = k0 + 8 * lane;
-    if (k < d) {
-      const float4 v0 = *reinterpret_cast<const float4*>(crow + k);
-      const float4 v1 = *reinterpret_cast<const float4*>(crow + k + 4);
-      c[0] = v0.x; c[1] = v0.y; c[2] = v0.z; c[3] = v0.w;
-      c[4] = v1.x; c[5] = v1.y; c[6] = v1.z; c[7] = v1.w;
+  // lane's EPL entries of the chunk at k0 (EPL * 64 entries; zeros at or past lim)
+  auto load = [&]<int EPL>(const float* src, int64_t k0, int64_t lim, float (&c)[EPL]) {
+    const int64_t k = k0 + EPL * lane;
+    if (k < lim) {
+#pragma unroll
+      for (int i = 0; i < EPL; i += 4) {
+        const float4 v = *reinterpret_cast<const float4*>(src + k + i);
+        c[i] = v.x; c[i + 1] = v.y; c[i + 2] = v.z; c[i + 3] = v.w;
+      }
     } else {
 #pragma unroll
-      for (int i = 0; i < 8; ++i) c[i] = 0.0f;
+      for (int i = 0; i < EPL; ++i) c[i] = 0.0f;
     }
   };
   // ROWLDS: this wave's copy of its row
   __shared__ float rowbuf[ROWLDS ? 4 * kRowLds : 1];
   float* const myrow = rowbuf + (ROWLDS ? (threadIdx.x >> 6) * kRowLds : 0);
-  auto keep8 = [&](int64_t k0, const float (&c)[8]) {
+  auto keep = [&]<int EPL>(int64_t k0, int64_t lim, const float (&c)[EPL]) {
     if constexpr (ROWLDS) {
-      const int64_t k = k0 + 8 * lane;
-      if (k < d) {
-        *reinterpret_cast<float4*>(myrow + k) = make_float4(c[0], c[1], c[2], c[3]);
-        *reinterpret_cast<float4*>(myrow + k + 4) = make_float4(c[4], c[5], c[6], c[7]);
-      }
-    }
-  };
-  // the second pass's copy of the lane's 8 entries (zeros past the end)
-  auto reload8 = [&](int64_t k0, float (&c)[8]) {
-    if constexpr (ROWLDS) {
-      const int64_t k = k0 + 8 * lane;
-      if (k < d) {
-        const float4 v0 = *reinterpret_cast<const float4*>(myrow + k);
-        const float4 v1 = *reinterpret_cast<const float4*>(myrow + k + 4);
-        c[0] = v0.x; c[1] = v0.y; c[2] = v0.z; c[3] = v0.w;
-        c[4] = v1.x; c[5] = v1.y; c[6] = v1.z; c[7] = v1.w;
-      } else {
+      const int64_t k = k0 + EPL * lane;
+      if (k < lim) {
 #pragma unroll
-        for (int i = 0; i < 8; ++i) c[i] = 0.0f;
+        for (int i = 0; i < EPL; i += 4)
+          *reinterpret_cast<float4*>(myrow + k + i) = make_float4(c[i], c[i + 1], c[i + 2], c[i + 3]);
       }
-    } else {
-      load8(k0, c);
     }
   };
-  auto absmax8 = [](const float (&c)[8]) {
+  // the second pass's copy of the lane's entries
+  auto reload = [&]<int EPL>(int64_t k0, int64_t lim, float (&c)[EPL]) {
+    load.template operator()<EPL>(ROWLDS ? myrow : crow, k0, lim, c);
+  };
+  auto absmax = []<int EPL>(const float (&c)[EPL]) {
     float m = 0.0f;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) m = fmaxf(m, fabsf(c[i]));
+    for (int i = 0; i < EPL; ++i) m = fmaxf(m, fabsf(c[i]));
     return m;
   };
 
   // |delta| <= max - min <= 2 max |c| < 2^(e + 1): the error rows are stored
-  // as fp16(delta * 2^E) with E = kF16Top - 1 - e.  Four chunks' loads are
-  // issued before any is reduced.
+  // as fp16(delta * 2^E) with E = kF16Top - 1 - e.  Every load of a group of
+  // chunks (four 8-entry chunks, or what is left of the row) is issued
+  // before any is reduced.
   int E = 0;
   if constexpr (!NORM) {
     float amax = 0.0f;
     int64_t ka = 0;
-    for (; ka + 4 * 512 <= d; ka += 4 * 512) {
+    for (; ka + 4 * 512 <= d8; ka += 4 * 512) {
       float c4[4][8];
 #pragma unroll
-      for (int x = 0; x < 4; ++x) load8(ka + 512 * x, c4[x]);
+      for (int x = 0; x < 4; ++x) load.template operator()<8>(crow, ka + 512 * x, d8, c4[x]);
 #pragma unroll
       for (int x = 0; x < 4; ++x) {
-        amax = fmaxf(amax, absmax8(c4[x]));
-        keep8(ka + 512 * x, c4[x]);
+        amax = fmaxf(amax, absmax.template operator()<8>(c4[x]));
+        keep.template operator()<8>(ka + 512 * x, d8, c4[x]);
       }
     }
-    for (; ka < d; ka += 512) {
-      float cc[8];
-      load8(ka, cc);
-      amax = fmaxf(amax, absmax8(cc));
-      keep8(ka, cc);
+    {
+      float c4[4][8], t[4];
+#pragma unroll
+      for (int x = 0; x < 4; ++x)
+        if (ka + 512 * x < d8) load.template operator()<8>(crow, ka + 512 * x, d8, c4[x]);
+      if (tail4) load.template operator()<4>(crow, d8, d, t);
+#pragma unroll
+      for (int x = 0; x < 4; ++x)
+        if (ka + 512 * x < d8) {
+          amax = fmaxf(amax, absmax.template operator()<8>(c4[x]));
+          keep.template operator()<8>(ka + 512 * x, d8, c4[x]);
+        }
+      if (tail4) {
+        amax = fmaxf(amax, absmax.template operator()<4>(t));
+        keep.template operator()<4>(d8, d, t);
+      }
     }
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) amax = fmaxf(amax, __shfl_xor(amax, o, 64));
@@ -271,99 +344,118 @@ __global__ __launch_bounds__(256) void dgen_kernel(const float* __restrict__ C, 
     if (lane == 0) uexp[u] = E;
   }
 
-  // quantize one 512-entry chunk at every width
-  auto chunk = [&](int64_t k0, const float (&c)[8]) {
-    const int64_t k = k0 + 8 * lane;
-    const bool active = k < d;
+  // quantize one chunk (EPL entries per lane) at every width
+  auto chunk = [&]<int EPL>(int64_t k0, int64_t lim, const float (&c)[EPL]) {
+    const int64_t k = k0 + EPL * lane;
+    const bool active = k < lim;
     float mn = c[0], mx = c[0];
 #pragma unroll
-    for (int i = 1; i < 8; ++i) {
+    for (int i = 1; i < EPL; ++i) {
       mn = fminf(mn, c[i]);
       mx = fmaxf(mx, c[i]);
     }
-    for (int o = 1; o < glanes; o <<= 1) {
-      mn = fminf(mn, __shfl_xor(mn, o, 64));
-      mx = fmaxf(mx, __shfl_xor(mx, o, 64));
-    }
+    block_minmax(mn, mx, G / EPL);
     if (!active) return;
-    float hd[8];
+    float hd[EPL];
     if constexpr (NORM) {
 #pragma unroll
-      for (int i = 0; i < 8; ++i) hd[i] = 1.0f;
+      for (int i = 0; i < EPL; ++i) hd[i] = 1.0f;
     } else {
-      const float4 h0 = *reinterpret_cast<const float4*>(hdiag + k);
-      const float4 h1 = *reinterpret_cast<const float4*>(hdiag + k + 4);
-      hd[0] = h0.x; hd[1] = h0.y; hd[2] = h0.z; hd[3] = h0.w;
-      hd[4] = h1.x; hd[5] = h1.y; hd[6] = h1.z; hd[7] = h1.w;
+      load.template operator()<EPL>(hdiag, k0, lim, hd);
     }
     const float mf = f16_bits_to_f32(f32_to_f16_bits(mn));
     const float range = mx - mn;
     // c - m16 once per entry, and its image scaled by 2^E (exact)
-    float cm[8], cms[8];
+    float cm[EPL], cms[EPL];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
+    for (int i = 0; i < EPL; ++i) {
       cm[i] = c[i] - mf;
       cms[i] = ldexpf(cm[i], E);
     }
 #pragma unroll
     for (int j = 0; j < NB; ++j) {
-      const int b = qb.b[j];
-      const float qmax = static_cast<float>((1 << b) - 1);
-      const float s32 = range / qmax;
+      const float qmax = qb.qmax[j];
+      // opaque(): the fp16 rounding below must apply to the fp32 quotient,
+      // not be fused into its last fma (which would round the exact sum once)
+      const float s32 = opaque(div_qmax(range, qmax, qb.rq[j]));
       const float sf = f16_bits_to_f32(f32_to_f16_bits(s32));
-      // hardware reciprocal (<= 1 ulp): the quotient below stays within
-      // 2^-22 |t| <= 6.1e-5 of the fp64 one for |t| <= 255.5, inside the
-      // 1e-4 margin of the fallback
+      // hardware reciprocal (<= 1 ulp)
       const float inv = sf > 0.0f ? __builtin_amdgcn_rcpf(sf) : 0.0f;
       const float sfs = ldexpf(sf, E);
       // codes from the fp32 quotient (inv = 0 gives q = 0 for a constant
-      // group); a quotient within 1e-4 of a rounding boundary is decided in
-      // fp64 instead, for the whole lane, in one rarely taken branch
-      float q[8];
+      // group); a quotient within 2^(b-21) of a rounding boundary is decided
+      // in fp64 instead, for the whole lane, in one rarely taken branch
+      const float near_at = qb.near[j];
+      float q[EPL];
       bool near = false;
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
+      for (int i = 0; i < EPL; ++i) {
         const float t = cm[i] * inv;
         const float r = rintf(t);
-        near |= fabsf(t - r) > 0.4999f;
+        near |= fabsf(t - r) > near_at;
         q[i] = __builtin_amdgcn_fmed3f(r, 0.0f, qmax);
       }
       if (near && sf > 0.0f) {
+        // The entries are read again (from the LDS copy, or through the
+        // caches) rather than kept in registers through every width.  Each
+        // entry's operand passes through an empty asm that also takes the
+        // previous entry's code: the fp64 work stays inside this branch and
+        // runs one entry at a time, so its registers do not add up over the
+        // entries (they would set the kernel's register count).
+        const float* src = (ROWLDS ? myrow : crow) + k;
+        const double md = static_cast<double>(mf);
+        const double sd = static_cast<double>(sf);
+        float prev = 0.0f;
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          const double td = (static_cast<double>(c[i]) - static_cast<double>(mf)) /
-                            static_cast<double>(sf);
+        for (int i = 0; i < EPL; ++i) {
+          float x = src[i];
+          asm volatile("" : "+v"(x) : "v"(prev));
+          const double td = (static_cast<double>(x) - md) / sd;
           q[i] = static_cast<float>(fmin(fmax(rint(td), 0.0), static_cast<double>(qmax)));
+          prev = q[i];
         }
       }
       // delta * 2^E = (c - m16) 2^E - q s16 2^E; the diagonal term is summed
       // from the scaled error and scaled back once at the end
-      uint16_t out[8];
+      uint16_t out[EPL];
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
+      for (int i = 0; i < EPL; ++i) {
         const float dls = fmaf(-q[i], sfs, cms[i]);
         out[i] = f32_to_f16_bits(dls);
         dacc[j] = fmaf(hd[i] * dls, dls, dacc[j]);
       }
       if constexpr (!NORM) {
-        uint4 pk;
-        pk.x = static_cast<uint32_t>(out[0]) | (static_cast<uint32_t>(out[1]) << 16);
-        pk.y = static_cast<uint32_t>(out[2]) | (static_cast<uint32_t>(out[3]) << 16);
-        pk.z = static_cast<uint32_t>(out[4]) | (static_cast<uint32_t>(out[5]) << 16);
-        pk.w = static_cast<uint32_t>(out[6]) | (static_cast<uint32_t>(out[7]) << 16);
-        *reinterpret_cast<uint4*>(D + gemm::tiled_offset(u * nb + j, k, d, SBN)) = pk;
+        uint16_t* dst = D + gemm::tiled_offset(u * nb + j, k, d, SBN);
+        if constexpr (EPL == 8) {
+          uint4 pk;
+          pk.x = static_cast<uint32_t>(out[0]) | (static_cast<uint32_t>(out[1]) << 16);
+          pk.y = static_cast<uint32_t>(out[2]) | (static_cast<uint32_t>(out[3]) << 16);
+          pk.z = static_cast<uint32_t>(out[4]) | (static_cast<uint32_t>(out[5]) << 16);
+          pk.w = static_cast<uint32_t>(out[6]) | (static_cast<uint32_t>(out[7]) << 16);
+          *reinterpret_cast<uint4*>(dst) = pk;
+        } else {
+          uint2 pk;
+          pk.x = static_cast<uint32_t>(out[0]) | (static_cast<uint32_t>(out[1]) << 16);
+          pk.y = static_cast<uint32_t>(out[2]) | (static_cast<uint32_t>(out[3]) << 16);
+          *reinterpret_cast<uint2*>(dst) = pk;
+        }
       }
     }
   };
   // the loads of chunk c + 1 are issued before chunk c is quantized
   static_assert(!(NORM && ROWLDS), "the norm-only form has no first pass");
   float cur[8], nxt[8];
-  reload8(0, cur);
-  for (int64_t k0 = 0; k0 < d; k0 += 512) {
-    if (k0 + 512 < d) reload8(k0 + 512, nxt);
-    chunk(k0, cur);
+  reload.template operator()<8>(0, d8, cur);
+  for (int64_t k0 = 0; k0 < d8; k0 += 512) {
+    if (k0 + 512 < d8) reload.template operator()<8>(k0 + 512, d8, nxt);
+    chunk.template operator()<8>(k0, d8, cur);
 #pragma unroll
     for (int i = 0; i < 8; ++i) cur[i] = nxt[i];
+  }
+  if (tail4) {
+    float t[4];
+    reload.template operator()<4>(d8, d, t);
+    chunk.template operator()<4>(d8, d, t);
   }
   const float wu = NORM ? w[u % wperiod] : 1.0f;
 #pragma unroll
@@ -771,7 +863,7 @@ extern "C" bitsmoe_status bitsmoe_score(const float* C_dev, int64_t units, int64
       return fail(BITSMOE_ERR_ARG, "score: width outside 1..8");
     if (j > 0 && bits_host[j] <= bits_host[j - 1])
       return fail(BITSMOE_ERR_ARG, "score: widths must be strictly ascending");
-    qb.b[j] = bits_host[j];
+    qb.set(j, bits_host[j]);
   }
   if (!(group == 32 || group == 64 || group == 128 || group == 256))
     return fail(BITSMOE_ERR_SHAPE, "score: group must be 32, 64, 128 or 256");
@@ -904,7 +996,7 @@ extern "C" bitsmoe_status bitsmoe_score_diag(const float* C_dev, int64_t units, 
       return fail(BITSMOE_ERR_ARG, "score_diag: width outside 1..8");
     if (j > 0 && bits_host[j] <= bits_host[j - 1])
       return fail(BITSMOE_ERR_ARG, "score_diag: widths must be strictly ascending");
-    qb.b[j] = bits_host[j];
+    qb.set(j, bits_host[j]);
   }
   if (!(group == 32 || group == 64 || group == 128 || group == 256))
     return fail(BITSMOE_ERR_SHAPE, "score_diag: group must be 32, 64, 128 or 256");
@@ -946,7 +1038,7 @@ extern "C" bitsmoe_status bitsmoe_score_routed(const float* C_dev, int64_t units
       return fail(BITSMOE_ERR_ARG, "score_routed: width outside 1..8");
     if (j > 0 && bits_host[j] <= bits_host[j - 1])
       return fail(BITSMOE_ERR_ARG, "score_routed: widths must be strictly ascending");
-    qb.b[j] = bits_host[j];
+    qb.set(j, bits_host[j]);
   }
   if (!(group == 32 || group == 64 || group == 128 || group == 256))
     return fail(BITSMOE_ERR_SHAPE, "score_routed: group must be 32, 64, 128 or 256");

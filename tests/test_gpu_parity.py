@@ -240,6 +240,10 @@ SCORE_CASES = [
     ("odd_row_tiles", 130, 704, 64, (1, 2, 3, 4), True),
     ("five_row_tiles", 70, 1280, 128, (2, 3, 4), False),
     ("four_row_tiles_ragged", 64, 960, 64, (1, 2, 3, 4), False),
+    # rows ending in a 256-entry chunk of 4 entries per lane (d % 512 == 256):
+    # groups of 32 lanes (lane ^ 16 by swizzle) and of 64 (lane ^ 32 too)
+    ("tail_chunk_768", 90, 768, 128, (1, 2, 3, 4), False),
+    ("tail_chunk_group256", 40, 768, 256, (2, 4), True),
 ]
 
 
