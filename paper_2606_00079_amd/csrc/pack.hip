@@ -7,8 +7,10 @@
 // byte: bit i of it is bit t of entry 8 l + i, which is exactly byte l of the
 // plane's 64-bit words 8 c .. 8 c + 7 (word w holds entries 64 w .. 64 w + 63,
 // bit j = entry 64 w + j, little-endian), so a plane of a chunk is one
-// coalesced 64-byte store.  The loads of chunk c + 1 are issued before chunk
-// c is packed.  Codes follow the fp64 quotient rule of the quantizer (decided
+// coalesced 64-byte store.  A row whose length is an odd multiple of 256 ends
+// with a 256-entry chunk at 4 entries per lane, each pair of lanes forming
+// one byte per plane.  The loads of chunk c + 1 are issued before chunk c is
+// packed.  Codes follow the fp64 quotient rule of the quantizer (decided
 // in fp32 where that provably gives the same integer), so they match an fp64
 // reference bit for bit given the same fp32 row.
 #include <algorithm>
@@ -60,79 +62,102 @@ __global__ __launch_bounds__(256) void pack_kernel(const float* __restrict__ C, 
   }
   const double qmax = static_cast<double>((1 << b) - 1);
   const float qmaxf = static_cast<float>((1 << b) - 1);
+  const float rq = 1.0f / qmaxf;
   const float near_at = 0.5f - ldexpf(1.0f, b - 21);  // the fp64 fallback's trigger
   uint8_t* ubytes = reinterpret_cast<uint8_t*>(codes + o0);  // plane t at byte t * d / 8
+  // A row whose length is an odd multiple of 256 ends with a chunk of 256
+  // entries at 4 per lane (two lanes' nibbles make a byte) instead of a
+  // half-empty 512-entry chunk.
+  const bool tail4 = d % 512 == 256;
+  const int64_t d8 = tail4 ? d - 256 : d;  // the entries of 8-per-lane chunks
 
-  // lane's 8 entries of the chunk at k0 (zeros past the end)
-  auto load8 = [&](int64_t k0, float (&c)[8]) {
-    const int64_t k = k0 + 8 * lane;
-    if (k < d) {
-      const float4 v0 = *reinterpret_cast<const float4*>(crow + k);
-      const float4 v1 = *reinterpret_cast<const float4*>(crow + k + 4);
-      c[0] = v0.x; c[1] = v0.y; c[2] = v0.z; c[3] = v0.w;
-      c[4] = v1.x; c[5] = v1.y; c[6] = v1.z; c[7] = v1.w;
+  // lane's EPL entries of the chunk at k0 (zeros at or past lim)
+  auto load = [&]<int EPL>(int64_t k0, int64_t lim, float (&c)[EPL]) {
+    const int64_t k = k0 + EPL * lane;
+    if (k < lim) {
+#pragma unroll
+      for (int i = 0; i < EPL; i += 4) {
+        const float4 v = *reinterpret_cast<const float4*>(crow + k + i);
+        c[i] = v.x; c[i + 1] = v.y; c[i + 2] = v.z; c[i + 3] = v.w;
+      }
     } else {
 #pragma unroll
-      for (int i = 0; i < 8; ++i) c[i] = 0.0f;
+      for (int i = 0; i < EPL; ++i) c[i] = 0.0f;
     }
   };
-  float cur[8], nxt[8];
-  load8(0, cur);
-  for (int64_t k0 = 0; k0 < d; k0 += 512) {
-    if (k0 + 512 < d) load8(k0 + 512, nxt);
-    const int64_t k = k0 + 8 * lane;
-    float mn = cur[0], mx = cur[0];
+  // codes, group parameters and plane bytes of one chunk
+  auto chunk = [&]<int EPL>(int64_t k0, int64_t lim, const float (&c)[EPL]) {
+    constexpr int GLE = G / EPL;  // lanes per group
+    const int64_t k = k0 + EPL * lane;
+    float mn = c[0], mx = c[0];
 #pragma unroll
-    for (int i = 1; i < 8; ++i) {
-      mn = fminf(mn, cur[i]);
-      mx = fmaxf(mx, cur[i]);
+    for (int i = 1; i < EPL; ++i) {
+      mn = fminf(mn, c[i]);
+      mx = fmaxf(mx, c[i]);
     }
-#pragma unroll
-    for (int o = 1; o < GL; o <<= 1) {
-      mn = fminf(mn, __shfl_xor(mn, o, 64));
-      mx = fmaxf(mx, __shfl_xor(mx, o, 64));
-    }
+    block_minmax(mn, mx, GLE);
     // d is a multiple of G, so a group is either wholly inside the row or
-    // wholly past its end
-    if (k < d) {
-      const uint16_t m16 = f32_to_f16_bits(mn);
-      const uint16_t s16 = f32_to_f16_bits((mx - mn) / qmaxf);
-      const float mf = f16_bits_to_f32(m16);
-      const float sf = f16_bits_to_f32(s16);
-      // hardware reciprocal (<= 1 ulp): the fp32 quotient below is within
-      // 2^-22 |t| of the fp64 one, and only |t| < 2^b decides a code (further
-      // out it is clamped), so it rounds the same way as the fp64 quotient
-      // unless it lies within 2^(b-21) of a rounding boundary; those (rare)
-      // lanes decide in fp64
-      const float inv = sf > 0.0f ? __builtin_amdgcn_rcpf(sf) : 0.0f;
-      uint32_t q[8];
-      bool near = false;
+    // wholly past its end (a 4-entry chunk is always whole)
+    if (EPL == 8 && k >= lim) return;
+    const uint16_t m16 = f32_to_f16_bits(mn);
+    // opaque(): fp16 rounding of the fp32 quotient, not fused into its fma
+    const uint16_t s16 = f32_to_f16_bits(opaque(div_qmax(mx - mn, qmaxf, rq)));
+    const float mf = f16_bits_to_f32(m16);
+    const float sf = f16_bits_to_f32(s16);
+    // hardware reciprocal (<= 1 ulp): the fp32 quotient below is within
+    // 2^-22 |t| of the fp64 one, and only |t| < 2^b decides a code (further
+    // out it is clamped), so it rounds the same way as the fp64 quotient
+    // unless it lies within 2^(b-21) of a rounding boundary; those (rare)
+    // lanes decide in fp64
+    const float inv = sf > 0.0f ? __builtin_amdgcn_rcpf(sf) : 0.0f;
+    uint32_t q[EPL];
+    bool near = false;
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const float t = (cur[i] - mf) * inv;
-        const float r = rintf(t);
-        near |= fabsf(t - r) > near_at;
-        q[i] = static_cast<uint32_t>(__builtin_amdgcn_fmed3f(r, 0.0f, qmaxf));
-      }
-      if (near && sf > 0.0f) {
-        const double md = static_cast<double>(mf), sd = static_cast<double>(sf);
+    for (int i = 0; i < EPL; ++i) {
+      const float t = (c[i] - mf) * inv;
+      const float r = rintf(t);
+      near |= fabsf(t - r) > near_at;
+      q[i] = static_cast<uint32_t>(__builtin_amdgcn_fmed3f(r, 0.0f, qmaxf));
+    }
+    if (near && sf > 0.0f) {
+      // opaque(): the fp64 forms are made inside this branch
+      const double md = static_cast<double>(opaque(mf)), sd = static_cast<double>(sf);
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          const double t = (static_cast<double>(cur[i]) - md) / sd;
-          q[i] = static_cast<uint32_t>(fmin(fmax(rint(t), 0.0), qmax));
-        }
-      }
-      if ((lane % GL) == 0)
-        uparams[k / G] = static_cast<uint32_t>(s16) | (static_cast<uint32_t>(m16) << 16);
-      for (int t = 0; t < b; ++t) {
-        uint32_t byte = 0;
-#pragma unroll
-        for (int i = 0; i < 8; ++i) byte |= ((q[i] >> t) & 1u) << i;
-        ubytes[t * (d / 8) + k / 8] = static_cast<uint8_t>(byte);
+      for (int i = 0; i < EPL; ++i) {
+        const double t = (static_cast<double>(opaque(c[i])) - md) / sd;
+        q[i] = static_cast<uint32_t>(fmin(fmax(rint(t), 0.0), qmax));
       }
     }
+    if ((lane % GLE) == 0)
+      uparams[k / G] = static_cast<uint32_t>(s16) | (static_cast<uint32_t>(m16) << 16);
+    for (int t = 0; t < b; ++t) {
+      uint32_t bb = 0;
+#pragma unroll
+      for (int i = 0; i < EPL; ++i) bb |= ((q[i] >> t) & 1u) << i;
+      if constexpr (EPL == 8) {
+        ubytes[t * (d / 8) + k / 8] = static_cast<uint8_t>(bb);
+      } else {
+        // the odd lane's nibble (entries 4 l + 4 .. 4 l + 7) is the high half
+        // of the even lane's byte: lane ^ 1 by a DPP quad permutation
+        const uint32_t hi = static_cast<uint32_t>(
+            __builtin_amdgcn_mov_dpp(static_cast<int>(bb), 0xB1, 0xF, 0xF, false));
+        if ((lane & 1) == 0) ubytes[t * (d / 8) + k / 8] = static_cast<uint8_t>(bb | (hi << 4));
+      }
+    }
+  };
+  // the loads of chunk c + 1 are issued before chunk c is packed
+  float cur[8], nxt[8];
+  load.template operator()<8>(0, d8, cur);
+  for (int64_t k0 = 0; k0 < d8; k0 += 512) {
+    if (k0 + 512 < d8) load.template operator()<8>(k0 + 512, d8, nxt);
+    chunk.template operator()<8>(k0, d8, cur);
 #pragma unroll
     for (int i = 0; i < 8; ++i) cur[i] = nxt[i];
+  }
+  if (tail4) {
+    float t[4];
+    load.template operator()<4>(d8, d, t);
+    chunk.template operator()<4>(d8, d, t);
   }
 }
 

@@ -297,7 +297,7 @@ def test_score_deterministic_and_degenerate_rows():
 
 # ---------------------------------------------------------------------- pack
 @pytest.mark.parametrize("group,d,units", [(64, 256, 300), (128, 2048, 97), (32, 192, 65),
-                                           (256, 768, 40)])
+                                           (256, 768, 40), (128, 768, 90), (32, 1280, 33)])
 def test_pack_bit_exact(group, d, units):
     say("pack", group, d, units)
     g = np.random.default_rng(group + d)
