@@ -700,6 +700,11 @@ def main(argv=None) -> int:
                 c["hbm_gbs"] = counters[f"{ckey}_hbm_gbs"]
                 c["hbm_bytes_per_launch"] = (counters[f"{ckey}_hbm_read_bytes_per_launch"]
                                              + counters[f"{ckey}_hbm_write_bytes_per_launch"])
+            if f"{ckey}_valu_busy_pct" in counters:
+                # vector-ALU busy time (rocprofv3 VALUBusy): the error-row and
+                # pack kernels are bound by it rather than by HBM bytes
+                c["valu_busy"] = round(counters[f"{ckey}_valu_busy_pct"] / 100.0, 4)
+                c["valu_insts_per_wave"] = counters[f"{ckey}_valu_insts_per_wave"]
             c["source"] = src + (" (H and M launches together)" if ckey == "symmetric_gram" else "")
             kernels[kname]["counters"] = c
     out = {
