@@ -27,6 +27,27 @@ __host__ __device__ __forceinline__ bool width_ok(int b) {
   return b == 0 || b == 16 || (b >= 1 && b <= BITSMOE_MAX_BITS);
 }
 
+// The bit planes of up to eight codes (each below 256): byte t of the result
+// holds bit t of code i in its bit i.  The codes are the rows of an 8 x 8
+// bit matrix (code i in byte i of one 64-bit word) and the planes its
+// columns, so three rounds of masked swaps (bits one, two and four places
+// off the diagonal) transpose it: a few dozen instructions for all eight
+// planes instead of three per bit.
+template <int N>
+__device__ __forceinline__ uint64_t bit_planes(const uint32_t (&q)[N]) {
+  static_assert(N <= 8, "eight codes per word");
+  uint64_t x = 0;
+#pragma unroll
+  for (int i = 0; i < N; ++i) x |= static_cast<uint64_t>(q[i]) << (8 * i);
+  uint64_t t = (x ^ (x >> 7)) & 0x00AA00AA00AA00AAull;
+  x ^= t ^ (t << 7);
+  t = (x ^ (x >> 14)) & 0x0000CCCC0000CCCCull;
+  x ^= t ^ (t << 14);
+  t = (x ^ (x >> 28)) & 0x00000000F0F0F0F0ull;
+  x ^= t ^ (t << 28);
+  return x;
+}
+
 template <int G>
 __global__ __launch_bounds__(256) void pack_kernel(const float* __restrict__ C, int64_t units,
                                                    int64_t d, const uint8_t* __restrict__ bits,
@@ -130,10 +151,9 @@ __global__ __launch_bounds__(256) void pack_kernel(const float* __restrict__ C, 
     }
     if ((lane % GLE) == 0)
       uparams[k / G] = static_cast<uint32_t>(s16) | (static_cast<uint32_t>(m16) << 16);
+    const uint64_t planes = bit_planes(q);
     for (int t = 0; t < b; ++t) {
-      uint32_t bb = 0;
-#pragma unroll
-      for (int i = 0; i < EPL; ++i) bb |= ((q[i] >> t) & 1u) << i;
+      const uint32_t bb = static_cast<uint32_t>(planes >> (8 * t)) & 0xFFu;
       if constexpr (EPL == 8) {
         ubytes[t * (d / 8) + k / 8] = static_cast<uint8_t>(bb);
       } else {
