@@ -557,8 +557,12 @@ bitsmoe_status bitsmoe_set_lapack(const char* path);
  * "pack".  bitsmoe_kernel_time waits for the recorded events of `name`,
  * returns their summed duration in ms and the number of launches, and
  * forgets them.  Enabling costs two event records per kernel and no
- * synchronization. */
+ * synchronization; each record also holds the stream for a few microseconds
+ * between kernels.  bitsmoe_timing_only(name) restricts the records to the
+ * kernels timed under `name` (NULL or "": all of them), so that one kernel
+ * can be timed inside a measured region without the others' records. */
 bitsmoe_status bitsmoe_timing(int enable);
+bitsmoe_status bitsmoe_timing_only(const char* name);
 bitsmoe_status bitsmoe_kernel_time(const char* name, double* total_ms, int64_t* launches);
 
 /* Text of the last non-OK status on the calling thread ("" if none). */

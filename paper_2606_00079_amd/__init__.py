@@ -40,7 +40,8 @@ EXPORTS = [
     "bitsmoe_gram", "bitsmoe_gram_experts", "bitsmoe_shared_basis", "bitsmoe_project",
     "bitsmoe_score", "bitsmoe_allocate", "bitsmoe_allocate_ex", "bitsmoe_pack_layout",
     "bitsmoe_pack", "bitsmoe_unpack", "bitsmoe_set_lapack", "bitsmoe_last_error",
-    "bitsmoe_release", "bitsmoe_version", "bitsmoe_timing", "bitsmoe_kernel_time",
+    "bitsmoe_release", "bitsmoe_version", "bitsmoe_timing", "bitsmoe_timing_only",
+    "bitsmoe_kernel_time",
     "bitsmoe_surrogate", "bitsmoe_surrogate_budget", "bitsmoe_gram_experts_in",
     "bitsmoe_project_in", "bitsmoe_basis_importance", "bitsmoe_score_diag",
     "bitsmoe_gram_routed", "bitsmoe_score_routed", "bitsmoe_moe_decode",
@@ -111,6 +112,7 @@ def lib() -> ctypes.CDLL:
     L.bitsmoe_moe_decode_topk_noalloc.argtypes = L.bitsmoe_moe_decode_topk.argtypes
     L.bitsmoe_set_lapack.argtypes = [ctypes.c_char_p]
     L.bitsmoe_timing.argtypes = [i32]
+    L.bitsmoe_timing_only.argtypes = [ctypes.c_char_p]
     L.bitsmoe_kernel_time.argtypes = [ctypes.c_char_p, vp, vp]
     L.bitsmoe_last_error.restype = ctypes.c_char_p
     L.bitsmoe_version.restype = ctypes.c_char_p
@@ -514,8 +516,10 @@ def unpack(codes, params, bits_dev, offsets_dev, units: int, d: int, group: int,
     return out
 
 
-def timing(enable: bool) -> None:
-    """Records HIP events around every main kernel while enabled."""
+def timing(enable: bool, only: Optional[str] = None) -> None:
+    """Records HIP events around every main kernel while enabled (``only``:
+    just around the kernels timed under that name)."""
+    _check(lib().bitsmoe_timing_only((only or "").encode()), "timing")
     _check(lib().bitsmoe_timing(1 if enable else 0), "timing")
 
 

@@ -118,15 +118,42 @@ struct TimedLaunch {
 };
 std::mutex g_timing_mu;
 bool g_timing = false;
+std::string g_timing_only;  // empty: every timed launch
 std::vector<TimedLaunch> g_launches;
+// Events read back by bitsmoe_kernel_time are kept for reuse, per device:
+// creating an event costs the host more than recording one, and between two
+// short kernels that cost shows up on the device as idle time.
+std::map<int, std::vector<hipEvent_t>> g_event_pool;
+
+// (with g_timing_mu held)
+hipError_t take_event(hipEvent_t* e) {
+  int dev = 0;
+  hipError_t st = hipGetDevice(&dev);
+  if (st != hipSuccess) return st;
+  std::vector<hipEvent_t>& pool = g_event_pool[dev];
+  if (!pool.empty()) {
+    *e = pool.back();
+    pool.pop_back();
+    return hipSuccess;
+  }
+  return hipEventCreate(e);
+}
+void give_event(hipEvent_t e) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) {
+    (void)hipEventDestroy(e);
+    return;
+  }
+  g_event_pool[dev].push_back(e);
+}
 }  // namespace
 
 KernelTimer::KernelTimer(const char* name, void* stream) : name_(name), stream_(stream) {
   if (!name) return;  // an untimed launch: no events
   std::lock_guard<std::mutex> lock(g_timing_mu);
-  if (!g_timing) return;
+  if (!g_timing || (!g_timing_only.empty() && g_timing_only != name)) return;
   hipEvent_t e;
-  if (hipEventCreate(&e) != hipSuccess) return;
+  if (take_event(&e) != hipSuccess) return;
   if (hipEventRecord(e, static_cast<hipStream_t>(stream)) != hipSuccess) {
     (void)hipEventDestroy(e);
     return;
@@ -138,8 +165,12 @@ KernelTimer::~KernelTimer() {
   if (!start_) return;
   std::lock_guard<std::mutex> lock(g_timing_mu);
   hipEvent_t e;
-  if (hipEventCreate(&e) != hipSuccess ||
-      hipEventRecord(e, static_cast<hipStream_t>(stream_)) != hipSuccess) {
+  if (take_event(&e) != hipSuccess) {
+    (void)hipEventDestroy(static_cast<hipEvent_t>(start_));
+    return;
+  }
+  if (hipEventRecord(e, static_cast<hipStream_t>(stream_)) != hipSuccess) {
+    (void)hipEventDestroy(e);
     (void)hipEventDestroy(static_cast<hipEvent_t>(start_));
     return;
   }
@@ -256,6 +287,12 @@ bitsmoe_status bitsmoe_timing(int enable) {
   return ok();
 }
 
+bitsmoe_status bitsmoe_timing_only(const char* name) {
+  std::lock_guard<std::mutex> lock(g_timing_mu);
+  g_timing_only = name ? name : "";
+  return ok();
+}
+
 bitsmoe_status bitsmoe_kernel_time(const char* name, double* total_ms, int64_t* launches) {
   if (!name || !total_ms) return fail(BITSMOE_ERR_ARG, "kernel_time: null pointer");
   std::lock_guard<std::mutex> lock(g_timing_mu);
@@ -274,8 +311,8 @@ bitsmoe_status bitsmoe_kernel_time(const char* name, double* total_ms, int64_t* 
     if (e != hipSuccess && st == BITSMOE_OK) st = device_error("kernel_time", e);
     sum += ms;
     ++count;
-    (void)hipEventDestroy(t.start);
-    (void)hipEventDestroy(t.stop);
+    give_event(t.start);
+    give_event(t.stop);
   }
   g_launches.swap(keep);
   *total_ms = sum;
@@ -286,6 +323,12 @@ bitsmoe_status bitsmoe_kernel_time(const char* name, double* total_ms, int64_t* 
 const char* bitsmoe_version(void) { return "bitsmoe-mi355x 0.1 (gfx950)"; }
 
 void bitsmoe_release(void) {
+  {
+    std::lock_guard<std::mutex> lock(g_timing_mu);
+    for (auto& kv : g_event_pool)
+      for (hipEvent_t e : kv.second) (void)hipEventDestroy(e);
+    g_event_pool.clear();
+  }
   std::lock_guard<std::mutex> lock(g_scratch_mu);
   int cur = 0;
   (void)hipGetDevice(&cur);
