@@ -151,6 +151,9 @@ __global__ __launch_bounds__(256) void hoff_kernel(const float* __restrict__ H, 
   }
 }
 
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
+
 // The candidate widths, with 2^b - 1, its fp32 reciprocal (the host's
 // correctly rounded division) and the fp64 fallback's trigger for each, so
 // the kernels read them as arguments instead of deriving them per wave.
@@ -370,28 +373,23 @@ __global__ __launch_bounds__(256) void dgen_kernel(const float* __restrict__ C, 
       }
       // delta * 2^E = (c - m16) 2^E - q s16 2^E; the diagonal term is summed
       // from the scaled error and scaled back once at the end
-      uint16_t out[EPL];
+      float dls[EPL];
 #pragma unroll
       for (int i = 0; i < EPL; ++i) {
-        const float dls = fmaf(-q[i], sfs, cms[i]);
-        out[i] = f32_to_f16_bits(dls);
-        dacc[j] = fmaf(hd[i] * dls, dls, dacc[j]);
+        dls[i] = fmaf(-q[i], sfs, cms[i]);
+        dacc[j] = fmaf(hd[i] * dls[i], dls[i], dacc[j]);
       }
       if constexpr (!NORM) {
+        // two fp16 per instruction (the fp32 value rounded to nearest even)
+        uint32_t pk[EPL / 2];
+#pragma unroll
+        for (int i = 0; i < EPL; i += 2)
+          pk[i / 2] = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{dls[i], dls[i + 1]}, f16x2));
         uint16_t* dst = D + gemm::tiled_offset(u * nb + j, k, d, SBN);
-        if constexpr (EPL == 8) {
-          uint4 pk;
-          pk.x = static_cast<uint32_t>(out[0]) | (static_cast<uint32_t>(out[1]) << 16);
-          pk.y = static_cast<uint32_t>(out[2]) | (static_cast<uint32_t>(out[3]) << 16);
-          pk.z = static_cast<uint32_t>(out[4]) | (static_cast<uint32_t>(out[5]) << 16);
-          pk.w = static_cast<uint32_t>(out[6]) | (static_cast<uint32_t>(out[7]) << 16);
-          *reinterpret_cast<uint4*>(dst) = pk;
-        } else {
-          uint2 pk;
-          pk.x = static_cast<uint32_t>(out[0]) | (static_cast<uint32_t>(out[1]) << 16);
-          pk.y = static_cast<uint32_t>(out[2]) | (static_cast<uint32_t>(out[3]) << 16);
-          *reinterpret_cast<uint2*>(dst) = pk;
-        }
+        if constexpr (EPL == 8)
+          *reinterpret_cast<uint4*>(dst) = make_uint4(pk[0], pk[1], pk[2], pk[3]);
+        else
+          *reinterpret_cast<uint2*>(dst) = make_uint2(pk[0], pk[1]);
       }
     }
   };
