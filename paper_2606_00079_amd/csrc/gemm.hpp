@@ -452,10 +452,13 @@ struct StageLds {
   }
 };
 
-// Accumulator fragment bookkeeping handed to epilogues.
-template <int BM, int BN>
+// Accumulator fragment bookkeeping handed to epilogues: the four waves as
+// NWM x NWN, wave (wm, wn) owning rows wm * WM .. and columns wn * WN .. of
+// the tile.
+template <int BM, int BN, int NWM = 2, int NWN = 2>
 struct Frag {
-  static constexpr int WM = BM / 2, WN = BN / 2;
+  static_assert(NWM * NWN == 4, "four waves");
+  static constexpr int WM = BM / NWM, WN = BN / NWN;
   static constexpr int FM = WM / 32;
   static constexpr int FN = WN / 32;
   f32x16 acc[FM][FN];
@@ -554,7 +557,8 @@ __device__ __forceinline__ f16x8 bf16x8_to_f16x8(const uint32_t (&w)[4]) {
 // ONEK: compiled for a one-pass, one-segment problem without repeat_k (the
 // K walk is a fixed step per tile; persistent launches always are).
 template <int BM, int BN, int KB, int STAGES, class Epi, bool F16 = false, bool BKN = false,
-          bool PAIRED = false, bool CVTB = false, bool PERSIST = false, bool ONEK = false>
+          bool PAIRED = false, bool CVTB = false, bool PERSIST = false, bool ONEK = false,
+          int NWN = 2>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void gemm_nt_kernel(Problem p, Epi epi) {
   static_assert(BM % 64 == 0 && BN % 64 == 0, "tile");
@@ -573,7 +577,10 @@ void gemm_nt_kernel(Problem p, Epi epi) {
   constexpr int LPS = AW + BW;      // vector-memory instructions per wave per stage
   constexpr int ASZ = BM * KB, BSZ = BN * KB;  // elements per stage
   static_assert(AW >= 1 && BW >= 1, "tile too small");
-  using F = Frag<BM, BN>;
+  // NWN = 4 (waves side by side along N, each all BM rows): every B fragment
+  // is read, and with CVTB widened, by one wave instead of two
+  using F = Frag<BM, BN, 4 / NWN, NWN>;
+  static_assert(F::WM % 32 == 0 && F::WN % 32 == 0, "32 x 32 fragments per wave");
 
   __shared__ __align__(1024) uint16_t As[STAGES * ASZ];
   __shared__ __align__(1024) uint16_t Bs[STAGES * BSZ];
@@ -583,8 +590,8 @@ void gemm_nt_kernel(Problem p, Epi epi) {
   f.lane = tid & 63;
   // wave-uniform: keeps everything derived from it in scalar registers
   f.wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  f.wm = f.wave >> 1;
-  f.wn = f.wave & 1;
+  f.wm = f.wave / NWN;
+  f.wn = f.wave % NWN;
   // PAIRED: gridDim.x = paired_workgroups(tiles_m, tiles_n), two jobs each
   // (see paired_jobs); persistent: the logical tiles pjob0 + j pstride;
   // otherwise one tile per workgroup.

@@ -297,9 +297,12 @@ extern "C" bitsmoe_status bitsmoe_project(const float* Ut_dev, const void* W_dev
     const dim3 grid = factor_grid(p, E, PM != 256);
     FactorStore epi{C_dev, r, d_in, flag};
     // one pass, one segment: the minimal K walk (ONEK)
+    // the four waves side by side along N (each all TM rows of U^T and 64
+    // columns of W): every W fragment is read and widened by one wave, not
+    // two as with 2 x 2 waves, for a quarter more fragment reads of U^T
 #define BITSMOE_PROJECT16(TM, PERSIST)                                                            \
   hipLaunchKernelGGL((gemm::gemm_nt_kernel<TM, PN, 32, 4, FactorStore, true, true, false, true,      \
-                                           PERSIST, true>), grid, dim3(gemm::kThreads), 0, s, p, epi)
+                                           PERSIST, true, 4>), grid, dim3(gemm::kThreads), 0, s, p, epi)
     if (PM == 256)
       BITSMOE_PROJECT16(256, false);
     else if (PM == 192 && p.persist)
