@@ -48,6 +48,12 @@ namespace gemm {
 constexpr int BK = 32;             // unit in which Problem::ktiles counts K
 constexpr int kKAlign = 64;        // every K segment (Problem::kseg) is a multiple of this
 constexpr int kThreads = 256;
+#ifndef BITSMOE_CVT_LAG
+#define BITSMOE_CVT_LAG 4
+#endif
+// Matrix-core ops between the LDS read of a bf16 B fragment and its widening
+// (each op runs 32 cycles: about the LDS read's latency under load at four).
+constexpr int kCvtLag = BITSMOE_CVT_LAG;
 
 // Compile-time loop: calls f(std::integral_constant<int, I>) for I = 0..N-1.
 template <int I, int N>
@@ -712,6 +718,10 @@ void gemm_nt_kernel(Problem p, Epi epi) {
   // one K=16 step, the fragments of the next step are read into the other.
   using Op = Operand<F16>;
   typename Op::vec fa[2][F::FM], fb[2][F::FN];
+  // CVTB: the raw bf16 B fragments of the step being read; each is widened
+  // into fb a few matrix-core ops after its read (cvt_frag), once the read
+  // has returned, so that the wave does not wait on the LDS.
+  uint32_t rawb[CVTB ? F::FN : 1][4];
   // Operand fragment q of the K=16 step kk of stage s into register set
   // `set`, in the order the matrix-core ops of a step first use them: A0,
   // then B0 .. B(FN-1), then A1 .. A(FM-1).
@@ -737,26 +747,32 @@ void gemm_nt_kernel(Problem p, Epi epi) {
           h[t] = ds_read_tr16(lb + r * BN + (kn_swz(r, col >> 3) << 3) + (col & 7));
         }
         if constexpr (CVTB) {
-          uint32_t w[4];
-          __builtin_memcpy(w, &h[0], 8);
-          __builtin_memcpy(w + 2, &h[1], 8);
-          fb[T][ni] = bf16x8_to_f16x8(w);
+          __builtin_memcpy(rawb[ni], &h[0], 8);
+          __builtin_memcpy(rawb[ni] + 2, &h[1], 8);
         } else {
           fb[T][ni] = __builtin_bit_cast(typename Op::vec,
                                          __builtin_shufflevector(h[0], h[1], 0, 1, 2, 3, 4, 5, 6, 7));
         }
       } else if constexpr (CVTB) {
         const uint4 v = *reinterpret_cast<const uint4*>(&lb[lds_off<KB>(brow + 32 * ni, j)]);
-        const uint32_t w[4] = {v.x, v.y, v.z, v.w};
-        fb[T][ni] = bf16x8_to_f16x8(w);
+        rawb[ni][0] = v.x;
+        rawb[ni][1] = v.y;
+        rawb[ni][2] = v.z;
+        rawb[ni][3] = v.w;
       } else {
         fb[T][ni] = *reinterpret_cast<const typename Op::vec*>(&lb[lds_off<KB>(brow + 32 * ni, j)]);
       }
     }
   };
+  auto cvt_frag = [&](auto set, auto nn) {
+    constexpr int T = decltype(set)::value;
+    constexpr int ni = decltype(nn)::value;
+    if constexpr (CVTB) fb[T][ni] = bf16x8_to_f16x8(rawb[ni]);
+  };
   constexpr int NFR = F::FM + F::FN;  // fragment reads per step
   auto read_frags = [&](auto set, int s, int kk) {
     StaticFor<0, NFR>::run([&](auto qq) { read_frag(set, qq, s, kk); });
+    StaticFor<0, F::FN>::run([&](auto nn) { cvt_frag(set, nn); });
   };
   // The matrix-core ops of one K=16 step from fragment set `set`.  Between
   // them go the other instructions of the step: the NFR fragment reads of
@@ -780,6 +796,17 @@ void gemm_nt_kernel(Problem p, Epi epi) {
     constexpr int M = NF + NL;
     constexpr int Q = F::FM * F::FN;
     constexpr int QS = Q > 4 ? Q - 2 : Q;  // ops followed by memory instructions
+    constexpr int m = NF < NL ? NF : NL;   // pairs
+    // CVTB: B fragment ni (read F(1 + ni)) is widened after op
+    // min(qr + kCvtLag, Q - 1), qr being the op its read follows
+    constexpr auto cvt_op = [](int ni) {
+      const int idx = 1 + ni;
+      const int j = idx < m ? 2 * idx : idx + m;  // its place in the sequence
+      int qr = QS - 1;
+      for (int q = 0; q < QS; ++q)
+        if (q * M / QS <= j && j < (q + 1) * M / QS) qr = q;
+      return qr + kCvtLag < Q - 1 ? qr + kCvtLag : Q - 1;
+    };
     __builtin_amdgcn_sched_barrier(0);
     StaticFor<0, Q>::run([&](auto qq) {
       constexpr int q = decltype(qq)::value;
@@ -790,7 +817,6 @@ void gemm_nt_kernel(Problem p, Epi epi) {
       constexpr int j0 = q < QS ? q * M / QS : M, j1 = q < QS ? (q + 1) * M / QS : M;
       StaticFor<j0, j1>::run([&](auto jj) {
         constexpr int j = decltype(jj)::value;
-        constexpr int m = NF < NL ? NF : NL;  // pairs
         constexpr bool frag = j < 2 * m ? (j % 2 == 0) : (NF > NL);
         constexpr int idx = j < 2 * m ? j / 2 : j - m;
         __builtin_amdgcn_sched_barrier(0);
@@ -800,6 +826,15 @@ void gemm_nt_kernel(Problem p, Epi epi) {
           issue_part(is, L0 + idx);
         __builtin_amdgcn_sched_barrier(0);
       });
+      if constexpr (CVTB && NF > 0) {
+        StaticFor<0, F::FN>::run([&](auto nn) {
+          if constexpr (cvt_op(decltype(nn)::value) == q) {
+            __builtin_amdgcn_sched_barrier(0);
+            cvt_frag(Other(), nn);
+            __builtin_amdgcn_sched_barrier(0);
+          }
+        });
+      }
     });
     __builtin_amdgcn_sched_barrier(0);
   };

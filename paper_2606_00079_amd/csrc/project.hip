@@ -140,6 +140,15 @@ struct FactorStore {
     // hoisted into the K loop (where it would hold registers throughout)
     const int lane = opaque(f.lane);
     float* base = C + f.z * r * cols;
+#ifndef BITSMOE_FULL_TILE_STORE
+#define BITSMOE_FULL_TILE_STORE 1
+#endif
+    // (rows of at most 2^20 columns: the block's byte offsets fit 31 bits)
+    if (BITSMOE_FULL_TILE_STORE && f.row0 + F::WM <= r && f.col0 + F::WN <= cols &&
+        cols <= (int64_t{1} << 20)) {
+      store_full(f, lane, base);
+      return;
+    }
     const int k = lane & 3;
     bool bad = false, stored = false, big = false;
 #pragma unroll
@@ -168,6 +177,43 @@ struct FactorStore {
         }
       }
     if (inexact && (__any(bad) || (__any(stored) && !__any(big))) && lane == 0) *inexact = 1;
+  }
+
+  // The wave's whole WM x WN block lies inside C (wave-uniform test): every
+  // accumulator goes out as one 4-byte store, those of one register of the
+  // 64 lanes covering 32 columns of two rows (two whole 128-byte lines).
+  // Through a buffer resource at the block's origin the lane's offset stays
+  // fixed and the row is the scalar offset: no address arithmetic, bounds
+  // test or lane exchange per store.  The inexact test runs on the largest
+  // magnitude, taken with NaN-propagating maxima.
+  template <class F>
+  __device__ void store_full(F& f, int lane, float* base) const {
+    float* wbase = base + static_cast<int64_t>(f.row0) * cols + f.col0;
+    const int64_t left = (r - f.row0) * cols - f.col0;  // elements from wbase to the end of C_z
+    const int nrec = static_cast<int>(left < (int64_t{1} << 29) ? left * 4 : (int64_t{1} << 31) - 4);
+    const auto rs = __builtin_amdgcn_make_buffer_rsrc(wbase, static_cast<short>(0), nrec, 0x00020000);
+    const int vo = ((4 * (lane >> 5)) * static_cast<int>(cols) + (lane & 31)) * 4;
+    const int rowb = static_cast<int>(cols) * 4;  // bytes per row
+    float m = 0.0f;
+#pragma unroll
+    for (int mi = 0; mi < F::FM; ++mi)
+#pragma unroll
+      for (int ni = 0; ni < F::FN; ++ni)
+#pragma unroll
+        for (int q = 0; q < 16; q += 2) {
+          const float v0 = f.acc[mi][ni][q], v1 = f.acc[mi][ni][q + 1];
+          const int row = 32 * mi + 8 * (q >> 2) + (q & 3);
+          __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v0), rs, vo + 128 * ni, row * rowb, 0);
+          __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v1), rs, vo + 128 * ni, (row + 1) * rowb, 0);
+          if (inexact)
+            m = __builtin_elementwise_maximum(
+                m, __builtin_elementwise_maximum(__builtin_fabsf(v0), __builtin_fabsf(v1)));
+        }
+    if (inexact) {
+      const bool bad = !(m <= 3.4e38f);  // NaN or infinity
+      const bool big = m >= kSmallFactor;
+      if ((__any(bad) || !__any(big)) && lane == 0) *inexact = 1;
+    }
   }
 };
 

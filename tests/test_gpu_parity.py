@@ -187,7 +187,8 @@ def test_project(case):
 
 @pytest.mark.parametrize("case", ["beyond_fp16", "non_finite", "tiny_and_subnormal",
                                   "tiny_expert"])
-def test_project_bf16_outside_fp16_range(case):
+@pytest.mark.parametrize("shape", ["ragged", "whole_tiles"])
+def test_project_bf16_outside_fp16_range(case, shape):
     """bf16 W is multiplied in one fp16 pass; entries beyond fp16's range
     (|W| > 65504) make that pass non-finite, and the library then recomputes
     C exactly in the two-pass bf16 form: C is finite and within the bar.  A
@@ -195,9 +196,11 @@ def test_project_bf16_outside_fp16_range(case):
     lose only absolute precision (at most 2^-25 each), far below the bar
     next to normal entries; a tile of factors that are all small (an expert
     of tiny weights) is recomputed exactly."""
-    say("project outside fp16 range", case)
+    say("project outside fp16 range", case, shape)
     g = np.random.default_rng(8)
-    E, d_out, d_in, r = 3, 192, 320, 100
+    # ragged: partial row and column tiles (bounds-tested stores);
+    # whole_tiles: r = 128 rows and d_in = 512 columns fill the tiles exactly
+    E, d_out, d_in, r = (3, 192, 320, 100) if shape == "ragged" else (3, 192, 512, 128)
     Wf = synth.random_rows(E * d_out, d_in, seed=9).reshape(E, d_out, d_in)
     if case == "beyond_fp16":
         Wf[1, 7, 11] = 1.5e5
