@@ -48,12 +48,10 @@ namespace gemm {
 constexpr int BK = 32;             // unit in which Problem::ktiles counts K
 constexpr int kKAlign = 64;        // every K segment (Problem::kseg) is a multiple of this
 constexpr int kThreads = 256;
-#ifndef BITSMOE_CVT_LAG
-#define BITSMOE_CVT_LAG 4
-#endif
 // Matrix-core ops between the LDS read of a bf16 B fragment and its widening
-// (each op runs 32 cycles: about the LDS read's latency under load at four).
-constexpr int kCvtLag = BITSMOE_CVT_LAG;
+// (each op runs 32 cycles: about the LDS read's latency under load at four;
+// two to six measured the same).
+constexpr int kCvtLag = 4;
 
 // Compile-time loop: calls f(std::integral_constant<int, I>) for I = 0..N-1.
 template <int I, int N>

@@ -117,11 +117,11 @@ __global__ __launch_bounds__(256) void split_rows_kernel(const float* __restrict
 }
 
 // C[z][row][col] = acc for row < r, col < cols (cols a multiple of 4).  The
-// accumulators of a 32 x 32 fragment give each lane one column and 16 rows;
-// transposed within each group of four lanes, each lane stores four
-// consecutive columns of one row as one 16-byte store (a quarter of the
-// store instructions of element-wise stores, whose count bounded the
-// epilogue).
+// accumulators of a 32 x 32 fragment give each lane one column and 16 rows.
+// A wave whose block lies wholly inside C stores them element by element
+// through a buffer resource (store_full); one partly outside transposes them
+// within each group of four lanes, so that each lane stores four consecutive
+// columns of one row as one bounds-tested 16-byte store.
 // With `inexact` set (the one-pass fp16 form), a wave writes 1 there when a
 // factor it stores is not finite (a W entry beyond fp16's range comes out
 // infinite) or when every factor it stores is below kSmallFactor in
@@ -140,11 +140,8 @@ struct FactorStore {
     // hoisted into the K loop (where it would hold registers throughout)
     const int lane = opaque(f.lane);
     float* base = C + f.z * r * cols;
-#ifndef BITSMOE_FULL_TILE_STORE
-#define BITSMOE_FULL_TILE_STORE 1
-#endif
     // (rows of at most 2^20 columns: the block's byte offsets fit 31 bits)
-    if (BITSMOE_FULL_TILE_STORE && f.row0 + F::WM <= r && f.col0 + F::WN <= cols &&
+    if (f.row0 + F::WM <= r && f.col0 + F::WN <= cols &&
         cols <= (int64_t{1} << 20)) {
       store_full(f, lane, base);
       return;
