@@ -187,7 +187,7 @@ def test_project(case):
 
 @pytest.mark.parametrize("case", ["beyond_fp16", "non_finite", "tiny_and_subnormal",
                                   "tiny_expert"])
-@pytest.mark.parametrize("shape", ["ragged", "whole_tiles"])
+@pytest.mark.parametrize("shape", ["ragged", "whole_tiles", "persistent"])
 def test_project_bf16_outside_fp16_range(case, shape):
     """bf16 W is multiplied in one fp16 pass; entries beyond fp16's range
     (|W| > 65504) make that pass non-finite, and the library then recomputes
@@ -199,8 +199,11 @@ def test_project_bf16_outside_fp16_range(case, shape):
     say("project outside fp16 range", case, shape)
     g = np.random.default_rng(8)
     # ragged: partial row and column tiles (bounds-tested stores);
-    # whole_tiles: r = 128 rows and d_in = 512 columns fill the tiles exactly
-    E, d_out, d_in, r = (3, 192, 320, 100) if shape == "ragged" else (3, 192, 512, 128)
+    # whole_tiles: r = 128 rows and d_in = 512 columns fill the tiles exactly;
+    # persistent: the same tiles over 160 experts, more tiles (320) than
+    # compute units, so one persistent workgroup per CU walks several
+    E, d_out, d_in, r = {"ragged": (3, 192, 320, 100), "whole_tiles": (3, 192, 512, 128),
+                         "persistent": (160, 192, 512, 128)}[shape]
     Wf = synth.random_rows(E * d_out, d_in, seed=9).reshape(E, d_out, d_in)
     if case == "beyond_fp16":
         Wf[1, 7, 11] = 1.5e5
