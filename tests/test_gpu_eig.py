@@ -64,6 +64,23 @@ def test_separated_spectrum_matches_oracle(n, r):
     _check_invariants(M, Ut, ev, r)
 
 
+@pytest.mark.parametrize("n,r", [(4133, 200)])
+def test_large_separated_spectrum_matches_oracle(n, r):
+    """A larger, ragged size (4133: no panel or tile boundary lines up with
+    the end of the matrix) against numpy eigh, element by element."""
+    say("separated, large", n, r)
+    M = _separated(n, seed=11)
+    Ut, ev, ms = bm.shared_basis_gpu(torch.from_numpy(M).to(DEV), r)
+    say("gpu eigensolve ms", round(ms, 1))
+    Ut = Ut.cpu().numpy()
+    Uref, lref = oracle.shared_basis(M, r)
+    assert np.max(np.abs(ev - lref)) <= 1e-11 * n
+    assert np.max(np.abs(Ut - Uref)) <= 2e-6
+    U = Ut.astype(np.float64).T
+    assert np.linalg.norm(M @ U - U * ev) <= 2e-6 * np.linalg.norm(M) * max(1.0, np.sqrt(r) / 8)
+    assert np.linalg.norm(U.T @ U - np.eye(r)) <= 2e-6 * max(1.0, np.sqrt(r))
+
+
 def test_rank_deficient_and_repeated():
     """A rank-5 M of size 96 (the zero eigenvalue repeated 91 times) and a
     doubly repeated leading eigenvalue: invariants only."""
