@@ -188,6 +188,9 @@ struct FactorStore {
     float* wbase = base + static_cast<int64_t>(f.row0) * cols + f.col0;
     const int64_t left = (r - f.row0) * cols - f.col0;  // elements from wbase to the end of C_z
     const int nrec = static_cast<int>(left < (int64_t{1} << 29) ? left * 4 : (int64_t{1} << 31) - 4);
+    // raw buffer (stride 0: num_records counts bytes, accesses past it are
+    // dropped); word 3 0x00020000 = 32-bit data format, the value for plain
+    // dword buffer loads and stores on this architecture
     const auto rs = __builtin_amdgcn_make_buffer_rsrc(wbase, static_cast<short>(0), nrec, 0x00020000);
     const int vo = ((4 * (lane >> 5)) * static_cast<int>(cols) + (lane & 31)) * 4;
     const int rowb = static_cast<int>(cols) * 4;  // bytes per row
